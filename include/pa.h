@@ -1,0 +1,197 @@
+/*
+ * pa.h -- C ABI of the MI355X (gfx950) Physics-Attention hot path.
+ *
+ * One Transolver++ Physics-Attention layer ("Transolver++: An Accurate Neural
+ * Solver for PDEs on Million-Scale Geometries", arXiv 2502.02414), forward and
+ * backward, for N mesh points with C channels, M slices and H heads:
+ *
+ *   t_i   = tau0 + a.x_i + b_t,  tau_i = max(t_i, tau_min)      Eq. 3 (Ada-Temp)
+ *   w_i   = softmax_j((x_i A + b + g_i) / tau_i)                Eq. 4 (Rep-Slice)
+ *   num_j = sum_i w_ij x_i,  den_j = sum_i w_ij,
+ *   s_j   = num_j / max(den_j, eps)                              Eq. 1, as the
+ *           partial sums of Section 4.2 (Algorithm 1, states step)
+ *   s'    = multi-head attention among the M states              Eq. 2
+ *   y_i   = sum_j w_ij s'_j                                      deslice, Section 3
+ *
+ * The backward calls are the chain rule of the above (the paper gives none).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Every tensor argument is a DEVICE pointer owned by the caller, row-major
+ *   and contiguous, 16-byte aligned.  Structs and scalars are host memory.
+ * - `dims->dtype` (pa_dtype) is the storage type of the point-side tensors
+ *   x [N,C], G [N,M], y [N,C], dY [N,C], dx [N,C] and of the slice
+ *   projection A [C,M] and a [C].  Everything else -- b [M], tokens [M,C],
+ *   num, den, attention parameters and every parameter gradient -- is fp32.
+ *   Arithmetic accumulates in fp32 (MFMA with fp32 accumulation).
+ * - Weights use the x*W ("in, out") layout: A is [C,M], W_q is [C,C].
+ * - G is the Gumbel sample g = -log(-log U), passed in as data so runs are
+ *   reproducible; NULL means no noise.  a = NULL means t_i = tau0 + b_t
+ *   (Transolver's constant temperature when b_t = 0).  b = NULL means 0.
+ * - Outputs are overwritten, never accumulated, and must not alias inputs.
+ * - Calls are asynchronous on `stream` (a hipStream_t; NULL = the default
+ *   stream).  The library never allocates, frees or synchronises device
+ *   memory.  Calls that take a workspace need at least
+ *   pa_workspace_size(dims) bytes of device memory; a workspace must not be
+ *   shared by calls that may run concurrently.
+ * - Results are deterministic: identical inputs give bitwise identical
+ *   outputs (fixed point partition that depends on N only, fixed-order
+ *   reductions, no floating-point atomics).
+ * - Arguments are validated on the host before anything is launched:
+ *   N >= 1; 1 <= M <= 64; C in {32, 64, 128, 256}; H >= 1 and C % H == 0;
+ *   tau_min > 0; eps > 0; required pointers non-NULL; workspace large
+ *   enough.  Failures return PA_ERR_INVALID, PA_ERR_UNSUPPORTED or
+ *   PA_ERR_WORKSPACE and set the thread-local message of pa_last_error().
+ *   A failed HIP launch returns PA_ERR_HIP with HIP's message.  Non-finite
+ *   input values propagate; there are no device-side checks.
+ */
+#ifndef PA_H
+#define PA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define PA_VERSION 1
+
+typedef enum { PA_F32 = 0, PA_BF16 = 1 } pa_dtype;
+
+typedef enum {
+  PA_OK = 0,
+  PA_ERR_INVALID = -1,     /* bad argument value or NULL pointer           */
+  PA_ERR_UNSUPPORTED = -2, /* valid, but a shape this build does not serve */
+  PA_ERR_WORKSPACE = -3,   /* workspace smaller than pa_workspace_size     */
+  PA_ERR_HIP = -4          /* a HIP runtime call or launch failed          */
+} pa_status;
+
+/* Layer dimensions and scalars (host struct). */
+typedef struct {
+  int64_t N;      /* mesh points                                  */
+  int32_t C;      /* channels                                     */
+  int32_t H;      /* heads of the token attention (D = C / H)     */
+  int32_t M;      /* slices (physical states)                     */
+  float tau0;     /* temperature constant of Eq. 3                */
+  float tau_min;  /* temperature floor: tau = max(t, tau_min)     */
+  float eps;      /* denominator floor: s = num / max(den, eps)   */
+  int32_t dtype;  /* pa_dtype of the point-side tensors and A, a  */
+} pa_dims;
+
+/* Slice projection (Eq. 4 Linear) and Ada-Temp projection (Eq. 3 Linear). */
+typedef struct {
+  const void* A;  /* [C,M] dtype, required                        */
+  const float* b; /* [M] fp32, nullable (0)                       */
+  const void* a;  /* [C] dtype, nullable (0)                      */
+  float b_t;      /* scalar bias of the Ada-Temp projection       */
+} pa_slice_params;
+
+/* Token attention parameters (Eq. 2), all fp32 [C,C] / [C]. */
+typedef struct {
+  const float *Wq, *bq; /* W required, b nullable */
+  const float *Wk, *bk;
+  const float *Wv, *bv;
+  const float *Wo, *bo; /* Wo NULL: no output projection (s' = heads) */
+} pa_attn_params;
+
+/* Gradients of the slice and Ada-Temp projections; fp32; each nullable. */
+typedef struct {
+  float* dA;    /* [C,M] */
+  float* db;    /* [M]   */
+  float* da;    /* [C]   */
+  float* db_t;  /* [1]   */
+  float* dtau0; /* [1], equal to db_t */
+} pa_slice_grads;
+
+/* Gradients of the token attention parameters; fp32; each nullable. */
+typedef struct {
+  float *dWq, *dbq;
+  float *dWk, *dbk;
+  float *dWv, *dbv;
+  float *dWo, *dbo; /* only written when the forward had Wo */
+} pa_attn_grads;
+
+/* Library version (PA_VERSION). */
+int pa_version(void);
+
+/* Thread-local message of the last failed call on this thread ("" if none). */
+const char* pa_last_error(void);
+
+/* Bytes of device workspace that every call below needs at these dims. */
+pa_status pa_workspace_size(const pa_dims* dims, size_t* bytes);
+
+/* Eq. 3 + Eq. 4 written out: W [N,M] fp32 (rows sum to 1) and, if tau is
+ * not NULL, the clamped temperature tau [N] fp32.  For tests and
+ * diagnostics; the fused calls below never write W. */
+pa_status pa_slice_weights(const pa_dims* dims, const void* x, const void* G,
+                           const pa_slice_params* sp, float* W, float* tau,
+                           void* ws, size_t ws_bytes, void* stream);
+
+/* Eq. 3 + Eq. 4 + Eq. 1 fused in one streaming pass over x and G (the
+ * weights stay on chip), reduced over fixed point chunks in a fixed order
+ * (the partial-sum form of Section 4.2): num [M,C], den [M], S [M,C], all
+ * fp32. */
+pa_status pa_slice_aggregate(const pa_dims* dims, const void* x, const void* G,
+                             const pa_slice_params* sp, float* num, float* den,
+                             float* S, void* ws, size_t ws_bytes, void* stream);
+
+/* Eq. 2: Q,K,V = S W_q + b_q, ...; per head h (channels [hD, hD+D)),
+ * softmax(Q_h K_h^T / sqrt(D)) V_h; heads concatenated; then, if Wo is
+ * given, Sp = O W_o + b_o.  S, Sp [M,C] fp32. */
+pa_status pa_token_attention(const pa_dims* dims, const float* S,
+                             const pa_attn_params* ap, float* Sp, void* ws,
+                             size_t ws_bytes, void* stream);
+
+/* Deslice (Section 3) with the weights recomputed from x and G exactly as
+ * in pa_slice_aggregate: y [N,C] (dtype) = W Sp. */
+pa_status pa_deslice(const pa_dims* dims, const void* x, const void* G,
+                     const pa_slice_params* sp, const float* Sp, void* y,
+                     void* ws, size_t ws_bytes, void* stream);
+
+/* Backward of the deslice, token half: dSp [M,C] fp32 = W^T dY, with the
+ * weights recomputed.  (The weight half, dY Sp^T, is folded into
+ * pa_slice_aggregate_backward.) */
+pa_status pa_deslice_backward(const pa_dims* dims, const void* x,
+                              const void* G, const pa_slice_params* sp,
+                              const void* dY, float* dSp, void* ws,
+                              size_t ws_bytes, void* stream);
+
+/* Backward of Eq. 2 (recomputes the forward from S): dS [M,C] fp32 and the
+ * parameter gradients requested in *ag (ag may be NULL). */
+pa_status pa_token_attention_backward(const pa_dims* dims, const float* S,
+                                      const pa_attn_params* ap,
+                                      const float* dSp, float* dS,
+                                      const pa_attn_grads* ag, void* ws,
+                                      size_t ws_bytes, void* stream);
+
+/* Backward of the slice side of the layer, in one streaming pass with the
+ * weights recomputed.  With dw_ij = <dY_i, Sp_j> + <x_i, dnum_j> + dden_j
+ * (dnum_j = dS_j / max(den_j, eps); dden_j = -<dS_j, S_j>/den_j when
+ * den_j >= eps, else 0), it writes
+ *   dx_i = sum_j w_ij dnum_j + A dl_i + a dt_i        (dx [N,C] dtype)
+ * and the projection gradients in *gr (gr may be NULL), where dl, dt are
+ * the chain rule of Eq. 4 and Eq. 3.  num, den are pa_slice_aggregate's
+ * outputs.  dS may be NULL (no states term); Sp and dY must both be NULL
+ * (no deslice term) or both be given. */
+pa_status pa_slice_aggregate_backward(const pa_dims* dims, const void* x,
+                                      const void* G, const pa_slice_params* sp,
+                                      const float* num, const float* den,
+                                      const float* dS, const float* Sp,
+                                      const void* dY, void* dx,
+                                      const pa_slice_grads* gr, void* ws,
+                                      size_t ws_bytes, void* stream);
+
+/* Backward of pa_slice_weights: from dW [N,M] fp32 and optional dtau [N]
+ * fp32 (the gradient of the clamped temperature), dx [N,C] dtype =
+ * A dl + a dt and the projection gradients in *gr (nullable). */
+pa_status pa_slice_weights_backward(const pa_dims* dims, const void* x,
+                                    const void* G, const pa_slice_params* sp,
+                                    const float* dW, const float* dtau,
+                                    void* dx, const pa_slice_grads* gr,
+                                    void* ws, size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PA_H */

@@ -1,0 +1,210 @@
+"""Thin Python binding of the C ABI in include/pa.h (``libpa.so``).
+
+Same entry-point names as the C library; each wrapper only checks and
+marshals arguments (torch device tensors -> device pointers, the current
+HIP stream) and raises ``PAError`` on a non-zero status.  Every step of the
+layer runs in the library's HIP kernels; there is no fallback of any kind:
+if ``libpa.so`` is missing or no GPU is present, calls fail loudly.
+
+Tensors: row-major contiguous CUDA (HIP) tensors.  Point-side tensors
+(x, G, y, dY, dx) and the slice projection (A, a) are ``torch.float32`` or
+``torch.bfloat16`` (matching ``dims.dtype``); tokens, b, attention
+parameters and every gradient of a parameter are float32.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libpa.so")
+
+PA_F32, PA_BF16 = 0, 1
+PA_OK, PA_ERR_INVALID, PA_ERR_UNSUPPORTED, PA_ERR_WORKSPACE, PA_ERR_HIP = 0, -1, -2, -3, -4
+
+# every exported symbol declared in include/pa.h
+SYMBOLS = (
+    "pa_version", "pa_last_error", "pa_workspace_size", "pa_slice_weights",
+    "pa_slice_aggregate", "pa_token_attention", "pa_deslice", "pa_deslice_backward",
+    "pa_token_attention_backward", "pa_slice_aggregate_backward",
+    "pa_slice_weights_backward",
+)
+
+
+class PAError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"pa status {status}: {msg}")
+        self.status = status
+
+
+class pa_dims(ctypes.Structure):
+    _fields_ = [("N", ctypes.c_int64), ("C", ctypes.c_int32), ("H", ctypes.c_int32),
+                ("M", ctypes.c_int32), ("tau0", ctypes.c_float), ("tau_min", ctypes.c_float),
+                ("eps", ctypes.c_float), ("dtype", ctypes.c_int32)]
+
+
+class pa_slice_params(ctypes.Structure):
+    _fields_ = [("A", ctypes.c_void_p), ("b", ctypes.c_void_p), ("a", ctypes.c_void_p),
+                ("b_t", ctypes.c_float)]
+
+
+class pa_attn_params(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("Wq", "bq", "Wk", "bk", "Wv", "bv", "Wo", "bo")]
+
+
+class pa_slice_grads(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("dA", "db", "da", "db_t", "dtau0")]
+
+
+class pa_attn_grads(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p)
+                for n in ("dWq", "dbq", "dWk", "dbk", "dWv", "dbv", "dWo", "dbo")]
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH):
+    """Load libpa.so (built by ``paper_2502_02414_amd.build``); raises if absent."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"HIP library {path} is not built; run __graft_entry__.build()")
+    lib = ctypes.CDLL(path)
+    P, S = ctypes.c_void_p, ctypes.c_size_t
+    D = ctypes.POINTER(pa_dims)
+    lib.pa_version.restype = ctypes.c_int
+    lib.pa_last_error.restype = ctypes.c_char_p
+    lib.pa_workspace_size.argtypes = [D, ctypes.POINTER(ctypes.c_size_t)]
+    SPp = ctypes.POINTER(pa_slice_params)
+    APp = ctypes.POINTER(pa_attn_params)
+    SGp = ctypes.POINTER(pa_slice_grads)
+    AGp = ctypes.POINTER(pa_attn_grads)
+    lib.pa_slice_weights.argtypes = [D, P, P, SPp, P, P, P, S, P]
+    lib.pa_slice_aggregate.argtypes = [D, P, P, SPp, P, P, P, P, S, P]
+    lib.pa_token_attention.argtypes = [D, P, APp, P, P, S, P]
+    lib.pa_deslice.argtypes = [D, P, P, SPp, P, P, P, S, P]
+    lib.pa_deslice_backward.argtypes = [D, P, P, SPp, P, P, P, S, P]
+    lib.pa_token_attention_backward.argtypes = [D, P, APp, P, P, AGp, P, S, P]
+    lib.pa_slice_aggregate_backward.argtypes = [D, P, P, SPp, P, P, P, P, P, P, SGp, P, S, P]
+    lib.pa_slice_weights_backward.argtypes = [D, P, P, SPp, P, P, P, SGp, P, S, P]
+    for name in SYMBOLS:
+        if name not in ("pa_version", "pa_last_error"):
+            getattr(lib, name).restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _check(status: int):
+    if status != PA_OK:
+        raise PAError(status, load().pa_last_error().decode())
+
+
+def _ptr(t) -> Optional[int]:
+    """Device pointer of a contiguous CUDA tensor (or None)."""
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("tensor must be on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("tensor must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream=None) -> Optional[int]:
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def make_dims(N: int, C: int, H: int, M: int, tau0: float, tau_min: float, eps: float,
+              dtype: int) -> pa_dims:
+    return pa_dims(int(N), int(C), int(H), int(M), float(tau0), float(tau_min), float(eps),
+                   int(dtype))
+
+
+def make_slice_params(A, b=None, a=None, b_t: float = 0.0) -> pa_slice_params:
+    return pa_slice_params(_ptr(A), _ptr(b), _ptr(a), float(b_t))
+
+
+def make_attn_params(Wq, Wk, Wv, bq=None, bk=None, bv=None, Wo=None, bo=None) -> pa_attn_params:
+    return pa_attn_params(_ptr(Wq), _ptr(bq), _ptr(Wk), _ptr(bk), _ptr(Wv), _ptr(bv), _ptr(Wo),
+                          _ptr(bo))
+
+
+def make_slice_grads(dA=None, db=None, da=None, db_t=None, dtau0=None) -> pa_slice_grads:
+    return pa_slice_grads(_ptr(dA), _ptr(db), _ptr(da), _ptr(db_t), _ptr(dtau0))
+
+
+def make_attn_grads(dWq=None, dbq=None, dWk=None, dbk=None, dWv=None, dbv=None, dWo=None,
+                    dbo=None) -> pa_attn_grads:
+    return pa_attn_grads(_ptr(dWq), _ptr(dbq), _ptr(dWk), _ptr(dbk), _ptr(dWv), _ptr(dbv),
+                         _ptr(dWo), _ptr(dbo))
+
+
+def pa_version() -> int:
+    return load().pa_version()
+
+
+def pa_last_error() -> str:
+    return load().pa_last_error().decode()
+
+
+def pa_workspace_size(dims: pa_dims) -> int:
+    n = ctypes.c_size_t(0)
+    _check(load().pa_workspace_size(ctypes.byref(dims), ctypes.byref(n)))
+    return n.value
+
+
+def workspace(dims: pa_dims, device="cuda"):
+    """A uint8 device tensor of pa_workspace_size bytes (torch allocates)."""
+    import torch
+    return torch.empty(pa_workspace_size(dims), dtype=torch.uint8, device=device)
+
+
+def pa_slice_weights(dims, x, G, sp, W, tau, ws, stream=None):
+    _check(load().pa_slice_weights(ctypes.byref(dims), _ptr(x), _ptr(G), ctypes.byref(sp),
+                                   _ptr(W), _ptr(tau), _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def pa_slice_aggregate(dims, x, G, sp, num, den, S, ws, stream=None):
+    _check(load().pa_slice_aggregate(ctypes.byref(dims), _ptr(x), _ptr(G), ctypes.byref(sp),
+                                     _ptr(num), _ptr(den), _ptr(S), _ptr(ws), ws.numel(),
+                                     _stream(stream)))
+
+
+def pa_token_attention(dims, S, ap, Sp, ws, stream=None):
+    _check(load().pa_token_attention(ctypes.byref(dims), _ptr(S), ctypes.byref(ap), _ptr(Sp),
+                                     _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def pa_deslice(dims, x, G, sp, Sp, y, ws, stream=None):
+    _check(load().pa_deslice(ctypes.byref(dims), _ptr(x), _ptr(G), ctypes.byref(sp), _ptr(Sp),
+                             _ptr(y), _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def pa_deslice_backward(dims, x, G, sp, dY, dSp, ws, stream=None):
+    _check(load().pa_deslice_backward(ctypes.byref(dims), _ptr(x), _ptr(G), ctypes.byref(sp),
+                                      _ptr(dY), _ptr(dSp), _ptr(ws), ws.numel(),
+                                      _stream(stream)))
+
+
+def pa_token_attention_backward(dims, S, ap, dSp, dS, ag, ws, stream=None):
+    _check(load().pa_token_attention_backward(
+        ctypes.byref(dims), _ptr(S), ctypes.byref(ap), _ptr(dSp), _ptr(dS),
+        ctypes.byref(ag) if ag is not None else None, _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def pa_slice_aggregate_backward(dims, x, G, sp, num, den, dS, Sp, dY, dx, gr, ws, stream=None):
+    _check(load().pa_slice_aggregate_backward(
+        ctypes.byref(dims), _ptr(x), _ptr(G), ctypes.byref(sp), _ptr(num), _ptr(den), _ptr(dS),
+        _ptr(Sp), _ptr(dY), _ptr(dx), ctypes.byref(gr) if gr is not None else None, _ptr(ws),
+        ws.numel(), _stream(stream)))
+
+
+def pa_slice_weights_backward(dims, x, G, sp, dW, dtau, dx, gr, ws, stream=None):
+    _check(load().pa_slice_weights_backward(
+        ctypes.byref(dims), _ptr(x), _ptr(G), ctypes.byref(sp), _ptr(dW), _ptr(dtau), _ptr(dx),
+        ctypes.byref(gr) if gr is not None else None, _ptr(ws), ws.numel(), _stream(stream)))

@@ -1,0 +1,485 @@
+// C ABI of the Physics-Attention hot path (see include/pa.h): host-side
+// validation, workspace carving and the launch sequence of every call.  No
+// arithmetic of the layer happens here; it all runs in the HIP kernels.
+#include "pa.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+
+#include "pa_internal.h"
+#include "pa_layout.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+pa_status fail(pa_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+pa_status fail(pa_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+pa_status hip_fail(hipError_t e, const char* what) {
+  return fail(PA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define PA_HIP(call, what)                      \
+  do {                                          \
+    hipError_t e_ = (call);                     \
+    if (e_ != hipSuccess) return hip_fail(e_, what); \
+  } while (0)
+
+constexpr size_t kAlign = 256;
+size_t up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+int mblocks(int M) { return (M + 15) / 16; }
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+// Workspace carve-up (offsets in bytes).
+struct Layout {
+  size_t img, parts, attn, total;
+  int P;          // point chunks (the largest over the streaming passes)
+};
+
+Layout layout_of(const pa_dims& d) {
+  Layout L{};
+  const int MB = mblocks(d.M);
+  size_t img = 0;
+  for (int pass = pa::kAggregate; pass <= pa::kWeightsBwd; ++pass) {
+    size_t b = pa::image_bytes(pass, d.dtype, d.C, MB);
+    if (b > img) img = b;
+  }
+  // chunks: every pass uses at most kPartialsMax blocks
+  const int64_t rec = (int64_t)d.C * d.M + d.M + d.C + 1;  // the largest record
+  const int P = pa::kPartialsMax;
+  const size_t mc = (size_t)d.M * d.C;
+  const size_t attn = (8 * mc + (size_t)d.H * d.M * d.M) * sizeof(float);
+  L.img = 0;
+  L.parts = up(img);
+  L.attn = L.parts + up((size_t)P * rec * sizeof(float));
+  L.total = L.attn + up(attn);
+  L.P = P;
+  return L;
+}
+
+pa_status check_dims(const pa_dims* d) {
+  if (!d) return fail(PA_ERR_INVALID, "dims is NULL");
+  if (d->N < 1) return fail(PA_ERR_INVALID, "N must be >= 1 (got %lld)", (long long)d->N);
+  if (d->M < 1 || d->M > 64) return fail(PA_ERR_INVALID, "M must be in [1, 64] (got %d)", d->M);
+  if (d->C < 1) return fail(PA_ERR_INVALID, "C must be >= 1 (got %d)", d->C);
+  if (d->H < 1 || d->C % d->H != 0)
+    return fail(PA_ERR_INVALID, "H must be >= 1 and divide C (C=%d, H=%d)", d->C, d->H);
+  if (!(d->tau_min > 0.f) || !std::isfinite(d->tau_min))
+    return fail(PA_ERR_INVALID, "tau_min must be finite and > 0");
+  if (!(d->eps > 0.f) || !std::isfinite(d->eps))
+    return fail(PA_ERR_INVALID, "eps must be finite and > 0");
+  if (!std::isfinite(d->tau0)) return fail(PA_ERR_INVALID, "tau0 must be finite");
+  if (d->dtype != PA_F32 && d->dtype != PA_BF16)
+    return fail(PA_ERR_INVALID, "dtype must be PA_F32 or PA_BF16 (got %d)", d->dtype);
+  if (d->C != 32 && d->C != 64 && d->C != 128 && d->C != 256)
+    return fail(PA_ERR_UNSUPPORTED, "C must be one of 32, 64, 128, 256 (got %d)", d->C);
+  return PA_OK;
+}
+
+pa_status check_pass(const pa_dims& d, int pass) {
+  if (pa::stream_waves(pass, d.dtype, d.C, mblocks(d.M)) <= 0)
+    return fail(PA_ERR_UNSUPPORTED,
+                "shape C=%d M=%d dtype=%d does not fit the on-chip tables of this pass", d.C,
+                d.M, d.dtype);
+  return PA_OK;
+}
+
+pa_status check_ptr(const void* p, const char* name, bool required) {
+  if (!p) return required ? fail(PA_ERR_INVALID, "%s is NULL", name) : PA_OK;
+  if (!aligned16(p)) return fail(PA_ERR_INVALID, "%s is not 16-byte aligned", name);
+  return PA_OK;
+}
+
+pa_status check_ws(const pa_dims& d, const void* ws, size_t ws_bytes) {
+  const Layout L = layout_of(d);
+  if (!ws) return fail(PA_ERR_WORKSPACE, "workspace is NULL (need %zu bytes)", L.total);
+  if (ws_bytes < L.total)
+    return fail(PA_ERR_WORKSPACE, "workspace too small: %zu < %zu bytes", ws_bytes, L.total);
+  if (((uintptr_t)ws & (kAlign - 1)) != 0)
+    return fail(PA_ERR_INVALID, "workspace is not %zu-byte aligned", kAlign);
+  return PA_OK;
+}
+
+#define PA_TRY(x)                \
+  do {                           \
+    pa_status s_ = (x);          \
+    if (s_ != PA_OK) return s_;  \
+  } while (0)
+
+char* wsb(void* ws) { return reinterpret_cast<char*>(ws); }
+
+int chunks(const pa_dims& d, int pass) {
+  return pa::num_chunks(d.N, pa::stream_waves(pass, d.dtype, d.C, mblocks(d.M)));
+}
+
+pa::PrepArgs prep_of(const pa_dims& d, int pass, const pa_slice_params* sp, void* ws) {
+  pa::PrepArgs p;
+  p.pass = pass;
+  p.dtype = d.dtype;
+  p.C = d.C;
+  p.M = d.M;
+  p.MB = mblocks(d.M);
+  p.eps = d.eps;
+  p.A = sp->A;
+  p.b = sp->b;
+  p.a = sp->a;
+  p.img = wsb(ws) + layout_of(d).img;
+  return p;
+}
+
+pa::StreamLaunch stream_of(const pa_dims& d, int pass, const void* x, const void* G,
+                           const pa_slice_params* sp, void* ws) {
+  pa::StreamLaunch L;
+  const Layout lay = layout_of(d);
+  L.x = x;
+  L.G = G;
+  L.img = wsb(ws) + lay.img;
+  L.partials = reinterpret_cast<float*>(wsb(ws) + lay.parts);
+  L.N = d.N;
+  L.M = d.M;
+  L.rec = (int)pa::record_floats(pass, d.C, d.M);
+  L.P = chunks(d, pass);
+  L.tb = (double)d.tau0 + (double)sp->b_t;
+  L.tau_min = d.tau_min;
+  return L;
+}
+
+pa_status check_slice(const pa_dims* dims, const void* x, const void* G,
+                      const pa_slice_params* sp) {
+  PA_TRY(check_dims(dims));
+  if (!sp) return fail(PA_ERR_INVALID, "slice params are NULL");
+  PA_TRY(check_ptr(x, "x", true));
+  PA_TRY(check_ptr(G, "G", false));
+  PA_TRY(check_ptr(sp->A, "A", true));
+  PA_TRY(check_ptr(sp->b, "b", false));
+  PA_TRY(check_ptr(sp->a, "a", false));
+  if (!std::isfinite(sp->b_t)) return fail(PA_ERR_INVALID, "b_t must be finite");
+  return PA_OK;
+}
+
+hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+}  // namespace
+
+extern "C" {
+
+int pa_version(void) { return PA_VERSION; }
+
+const char* pa_last_error(void) { return g_err.c_str(); }
+
+pa_status pa_workspace_size(const pa_dims* dims, size_t* bytes) {
+  PA_TRY(check_dims(dims));
+  if (!bytes) return fail(PA_ERR_INVALID, "bytes is NULL");
+  *bytes = layout_of(*dims).total;
+  return PA_OK;
+}
+
+pa_status pa_slice_weights(const pa_dims* dims, const void* x, const void* G,
+                           const pa_slice_params* sp, float* W, float* tau, void* ws,
+                           size_t ws_bytes, void* stream) {
+  PA_TRY(check_slice(dims, x, G, sp));
+  PA_TRY(check_ptr(W, "W", true));
+  PA_TRY(check_ptr(tau, "tau", false));
+  PA_TRY(check_pass(*dims, pa::kWeights));
+  PA_TRY(check_ws(*dims, ws, ws_bytes));
+  hipStream_t st = as_stream(stream);
+  PA_HIP(pa::launch_prep(prep_of(*dims, pa::kWeights, sp, ws), st), "prep");
+  pa::StreamLaunch L = stream_of(*dims, pa::kWeights, x, G, sp, ws);
+  L.out = W;
+  L.tau_out = tau;
+  PA_HIP(pa::launch_stream(pa::kWeights, dims->dtype, dims->C, mblocks(dims->M), L, st),
+         "slice weights");
+  return PA_OK;
+}
+
+pa_status pa_slice_aggregate(const pa_dims* dims, const void* x, const void* G,
+                             const pa_slice_params* sp, float* num, float* den, float* S,
+                             void* ws, size_t ws_bytes, void* stream) {
+  PA_TRY(check_slice(dims, x, G, sp));
+  PA_TRY(check_ptr(num, "num", true));
+  PA_TRY(check_ptr(den, "den", true));
+  PA_TRY(check_ptr(S, "S", true));
+  PA_TRY(check_pass(*dims, pa::kAggregate));
+  PA_TRY(check_ws(*dims, ws, ws_bytes));
+  hipStream_t st = as_stream(stream);
+  PA_HIP(pa::launch_prep(prep_of(*dims, pa::kAggregate, sp, ws), st), "prep");
+  pa::StreamLaunch L = stream_of(*dims, pa::kAggregate, x, G, sp, ws);
+  PA_HIP(pa::launch_stream(pa::kAggregate, dims->dtype, dims->C, mblocks(dims->M), L, st),
+         "slice aggregate");
+  pa::Segments seg{};
+  seg.dst[0] = num; seg.len[0] = (int64_t)dims->M * dims->C;
+  seg.dst[1] = den; seg.len[1] = dims->M;
+  seg.n = 2;
+  PA_HIP(pa::launch_reduce(L.partials, L.P, L.rec, seg, st), "reduce");
+  PA_HIP(pa::launch_states(num, den, S, dims->M, dims->C, dims->eps, st), "states");
+  return PA_OK;
+}
+
+static pa_status check_attn(const pa_dims* dims, const float* S, const pa_attn_params* ap) {
+  PA_TRY(check_dims(dims));
+  if (!ap) return fail(PA_ERR_INVALID, "attention params are NULL");
+  PA_TRY(check_ptr(S, "S", true));
+  PA_TRY(check_ptr(ap->Wq, "Wq", true));
+  PA_TRY(check_ptr(ap->Wk, "Wk", true));
+  PA_TRY(check_ptr(ap->Wv, "Wv", true));
+  PA_TRY(check_ptr(ap->bq, "bq", false));
+  PA_TRY(check_ptr(ap->bk, "bk", false));
+  PA_TRY(check_ptr(ap->bv, "bv", false));
+  PA_TRY(check_ptr(ap->Wo, "Wo", false));
+  PA_TRY(check_ptr(ap->bo, "bo", false));
+  if (ap->bo && !ap->Wo) return fail(PA_ERR_INVALID, "bo given without Wo");
+  return PA_OK;
+}
+
+namespace {
+struct AttnWs {
+  float *Q, *K, *V, *O, *dO, *dQ, *dK, *dV, *P;
+};
+AttnWs attn_ws(const pa_dims& d, void* ws) {
+  const size_t mc = (size_t)d.M * d.C;
+  float* base = reinterpret_cast<float*>(wsb(ws) + layout_of(d).attn);
+  AttnWs a;
+  a.Q = base; a.K = base + mc; a.V = base + 2 * mc; a.O = base + 3 * mc;
+  a.dO = base + 4 * mc; a.dQ = base + 5 * mc; a.dK = base + 6 * mc; a.dV = base + 7 * mc;
+  a.P = base + 8 * mc;
+  return a;
+}
+
+// out [M,C] = in [M,C] W [C,C] + b
+pa::Gemm affine(const float* in, const float* W, const float* b, float* out, int M, int C) {
+  pa::Gemm g{};
+  g.A = in; g.sai = C; g.sak = 1;
+  g.B = W; g.sbk = C; g.sbj = 1;
+  g.bias = b; g.out = out; g.ldo = C;
+  g.rows = M; g.cols = C; g.K = C;
+  return g;
+}
+// out [M,C] (+)= in [M,C] W^T
+pa::Gemm affine_t(const float* in, const float* W, float* out, int M, int C, int acc) {
+  pa::Gemm g{};
+  g.A = in; g.sai = C; g.sak = 1;
+  g.B = W; g.sbk = 1; g.sbj = C;
+  g.out = out; g.ldo = C;
+  g.rows = M; g.cols = C; g.K = C;
+  g.accumulate = acc;
+  return g;
+}
+// out [C,C] = a^T [C,M] b [M,C]
+pa::Gemm outer(const float* a, const float* b, float* out, int M, int C) {
+  pa::Gemm g{};
+  g.A = a; g.sai = 1; g.sak = C;
+  g.B = b; g.sbk = C; g.sbj = 1;
+  g.out = out; g.ldo = C;
+  g.rows = C; g.cols = C; g.K = M;
+  return g;
+}
+
+pa_status attn_forward(const pa_dims& d, const float* S, const pa_attn_params* ap, float* Sp,
+                       const AttnWs& w, hipStream_t st) {
+  const int M = d.M, C = d.C;
+  PA_HIP(pa::launch_gemm(affine(S, ap->Wq, ap->bq, w.Q, M, C), st), "Q projection");
+  PA_HIP(pa::launch_gemm(affine(S, ap->Wk, ap->bk, w.K, M, C), st), "K projection");
+  PA_HIP(pa::launch_gemm(affine(S, ap->Wv, ap->bv, w.V, M, C), st), "V projection");
+  // the heads' output goes straight to Sp only when Sp is wanted and there is
+  // no output projection; otherwise (and for the backward's recompute, which
+  // passes Sp = NULL) it goes to the workspace.
+  float* O = (ap->Wo || !Sp) ? w.O : Sp;
+  PA_HIP(pa::launch_attn_core(w.Q, w.K, w.V, w.P, O, M, C, d.H, st), "attention core");
+  if (ap->Wo) {
+    if (Sp) PA_HIP(pa::launch_gemm(affine(w.O, ap->Wo, ap->bo, Sp, M, C), st), "O projection");
+  }
+  return PA_OK;
+}
+}  // namespace
+
+pa_status pa_token_attention(const pa_dims* dims, const float* S, const pa_attn_params* ap,
+                             float* Sp, void* ws, size_t ws_bytes, void* stream) {
+  PA_TRY(check_attn(dims, S, ap));
+  PA_TRY(check_ptr(Sp, "Sp", true));
+  PA_TRY(check_ws(*dims, ws, ws_bytes));
+  return attn_forward(*dims, S, ap, Sp, attn_ws(*dims, ws), as_stream(stream));
+}
+
+pa_status pa_token_attention_backward(const pa_dims* dims, const float* S,
+                                      const pa_attn_params* ap, const float* dSp, float* dS,
+                                      const pa_attn_grads* ag, void* ws, size_t ws_bytes,
+                                      void* stream) {
+  PA_TRY(check_attn(dims, S, ap));
+  PA_TRY(check_ptr(dSp, "dSp", true));
+  PA_TRY(check_ptr(dS, "dS", true));
+  if (ag) {
+    const float* gs[] = {ag->dWq, ag->dbq, ag->dWk, ag->dbk, ag->dWv, ag->dbv, ag->dWo, ag->dbo};
+    for (const float* p : gs) PA_TRY(check_ptr(p, "attention gradient", false));
+  }
+  PA_TRY(check_ws(*dims, ws, ws_bytes));
+  hipStream_t st = as_stream(stream);
+  const int M = dims->M, C = dims->C;
+  const AttnWs w = attn_ws(*dims, ws);
+  PA_TRY(attn_forward(*dims, S, ap, nullptr, w, st));  // Q, K, V, P, O
+  const float* dO = dSp;
+  if (ap->Wo) {
+    PA_HIP(pa::launch_gemm(affine_t(dSp, ap->Wo, w.dO, M, C, 0), st), "dO");
+    dO = w.dO;
+    if (ag && ag->dWo) PA_HIP(pa::launch_gemm(outer(w.O, dSp, ag->dWo, M, C), st), "dWo");
+    if (ag && ag->dbo) PA_HIP(pa::launch_colsum(dSp, M, C, C, ag->dbo, st), "dbo");
+  }
+  PA_HIP(pa::launch_attn_core_bwd(w.Q, w.K, w.V, w.P, dO, w.dQ, w.dK, w.dV, M, C, dims->H, st),
+         "attention core backward");
+  PA_HIP(pa::launch_gemm(affine_t(w.dQ, ap->Wq, dS, M, C, 0), st), "dS");
+  PA_HIP(pa::launch_gemm(affine_t(w.dK, ap->Wk, dS, M, C, 1), st), "dS");
+  PA_HIP(pa::launch_gemm(affine_t(w.dV, ap->Wv, dS, M, C, 1), st), "dS");
+  if (ag) {
+    const float* d3[3] = {w.dQ, w.dK, w.dV};
+    float* dW3[3] = {ag->dWq, ag->dWk, ag->dWv};
+    float* db3[3] = {ag->dbq, ag->dbk, ag->dbv};
+    for (int t = 0; t < 3; ++t) {
+      if (dW3[t]) PA_HIP(pa::launch_gemm(outer(S, d3[t], dW3[t], M, C), st), "dW");
+      if (db3[t]) PA_HIP(pa::launch_colsum(d3[t], M, C, C, db3[t], st), "db");
+    }
+  }
+  return PA_OK;
+}
+
+pa_status pa_deslice(const pa_dims* dims, const void* x, const void* G,
+                     const pa_slice_params* sp, const float* Sp, void* y, void* ws,
+                     size_t ws_bytes, void* stream) {
+  PA_TRY(check_slice(dims, x, G, sp));
+  PA_TRY(check_ptr(Sp, "Sp", true));
+  PA_TRY(check_ptr(y, "y", true));
+  PA_TRY(check_pass(*dims, pa::kDeslice));
+  PA_TRY(check_ws(*dims, ws, ws_bytes));
+  hipStream_t st = as_stream(stream);
+  pa::PrepArgs p = prep_of(*dims, pa::kDeslice, sp, ws);
+  p.Sp = Sp;
+  PA_HIP(pa::launch_prep(p, st), "prep");
+  pa::StreamLaunch L = stream_of(*dims, pa::kDeslice, x, G, sp, ws);
+  L.out = y;
+  PA_HIP(pa::launch_stream(pa::kDeslice, dims->dtype, dims->C, mblocks(dims->M), L, st),
+         "deslice");
+  return PA_OK;
+}
+
+pa_status pa_deslice_backward(const pa_dims* dims, const void* x, const void* G,
+                              const pa_slice_params* sp, const void* dY, float* dSp, void* ws,
+                              size_t ws_bytes, void* stream) {
+  PA_TRY(check_slice(dims, x, G, sp));
+  PA_TRY(check_ptr(dY, "dY", true));
+  PA_TRY(check_ptr(dSp, "dSp", true));
+  PA_TRY(check_pass(*dims, pa::kDesliceBwd));
+  PA_TRY(check_ws(*dims, ws, ws_bytes));
+  hipStream_t st = as_stream(stream);
+  PA_HIP(pa::launch_prep(prep_of(*dims, pa::kDesliceBwd, sp, ws), st), "prep");
+  pa::StreamLaunch L = stream_of(*dims, pa::kDesliceBwd, x, G, sp, ws);
+  L.dY = dY;
+  PA_HIP(pa::launch_stream(pa::kDesliceBwd, dims->dtype, dims->C, mblocks(dims->M), L, st),
+         "deslice backward");
+  pa::Segments seg{};
+  seg.dst[0] = dSp; seg.len[0] = (int64_t)dims->M * dims->C;
+  seg.n = 1;
+  PA_HIP(pa::launch_reduce(L.partials, L.P, L.rec, seg, st), "reduce");
+  return PA_OK;
+}
+
+namespace {
+pa_status reduce_slice_grads(const pa_dims& d, const pa::StreamLaunch& L,
+                             const pa_slice_grads* gr, hipStream_t st) {
+  if (!gr) return PA_OK;
+  pa::Segments seg{};
+  seg.dst[0] = gr->dA; seg.len[0] = (int64_t)d.C * d.M;
+  seg.dst[1] = gr->db; seg.len[1] = d.M;
+  seg.dst[2] = gr->da; seg.len[2] = d.C;
+  seg.dst[3] = gr->db_t ? gr->db_t : gr->dtau0; seg.len[3] = 1;
+  seg.n = 4;
+  PA_HIP(pa::launch_reduce(L.partials, L.P, L.rec, seg, st), "reduce");
+  if (gr->db_t && gr->dtau0)
+    PA_HIP(hipMemcpyAsync(gr->dtau0, gr->db_t, sizeof(float), hipMemcpyDeviceToDevice, st),
+           "dtau0 copy");
+  return PA_OK;
+}
+
+pa_status check_grads(const pa_slice_grads* gr) {
+  if (!gr) return PA_OK;
+  PA_TRY(check_ptr(gr->dA, "dA", false));
+  PA_TRY(check_ptr(gr->db, "db", false));
+  PA_TRY(check_ptr(gr->da, "da", false));
+  if (gr->db_t && ((uintptr_t)gr->db_t & 3u)) return fail(PA_ERR_INVALID, "db_t misaligned");
+  if (gr->dtau0 && ((uintptr_t)gr->dtau0 & 3u)) return fail(PA_ERR_INVALID, "dtau0 misaligned");
+  return PA_OK;
+}
+}  // namespace
+
+pa_status pa_slice_aggregate_backward(const pa_dims* dims, const void* x, const void* G,
+                                      const pa_slice_params* sp, const float* num,
+                                      const float* den, const float* dS, const float* Sp,
+                                      const void* dY, void* dx, const pa_slice_grads* gr,
+                                      void* ws, size_t ws_bytes, void* stream) {
+  PA_TRY(check_slice(dims, x, G, sp));
+  PA_TRY(check_ptr(dS, "dS", false));
+  PA_TRY(check_ptr(Sp, "Sp", false));
+  PA_TRY(check_ptr(dY, "dY", false));
+  PA_TRY(check_ptr(dx, "dx", true));
+  if ((Sp == nullptr) != (dY == nullptr))
+    return fail(PA_ERR_INVALID, "Sp and dY must both be given or both be NULL");
+  if (dS) {
+    PA_TRY(check_ptr(num, "num", true));
+    PA_TRY(check_ptr(den, "den", true));
+  }
+  PA_TRY(check_grads(gr));
+  PA_TRY(check_pass(*dims, pa::kSliceBwd));
+  PA_TRY(check_ws(*dims, ws, ws_bytes));
+  hipStream_t st = as_stream(stream);
+  pa::PrepArgs p = prep_of(*dims, pa::kSliceBwd, sp, ws);
+  p.num = num;
+  p.den = den;
+  p.dS = dS;
+  p.Sp = Sp;
+  PA_HIP(pa::launch_prep(p, st), "prep");
+  pa::StreamLaunch L = stream_of(*dims, pa::kSliceBwd, x, G, sp, ws);
+  L.dY = dY;
+  L.out = dx;
+  L.states = dS != nullptr;
+  L.deslice = Sp != nullptr;
+  PA_HIP(pa::launch_stream(pa::kSliceBwd, dims->dtype, dims->C, mblocks(dims->M), L, st),
+         "slice backward");
+  return reduce_slice_grads(*dims, L, gr, st);
+}
+
+pa_status pa_slice_weights_backward(const pa_dims* dims, const void* x, const void* G,
+                                    const pa_slice_params* sp, const float* dW,
+                                    const float* dtau, void* dx, const pa_slice_grads* gr,
+                                    void* ws, size_t ws_bytes, void* stream) {
+  PA_TRY(check_slice(dims, x, G, sp));
+  PA_TRY(check_ptr(dW, "dW", true));
+  PA_TRY(check_ptr(dtau, "dtau", false));
+  PA_TRY(check_ptr(dx, "dx", true));
+  PA_TRY(check_grads(gr));
+  PA_TRY(check_pass(*dims, pa::kWeightsBwd));
+  PA_TRY(check_ws(*dims, ws, ws_bytes));
+  hipStream_t st = as_stream(stream);
+  PA_HIP(pa::launch_prep(prep_of(*dims, pa::kWeightsBwd, sp, ws), st), "prep");
+  pa::StreamLaunch L = stream_of(*dims, pa::kWeightsBwd, x, G, sp, ws);
+  L.dW = dW;
+  L.dtau = dtau;
+  L.out = dx;
+  PA_HIP(pa::launch_stream(pa::kWeightsBwd, dims->dtype, dims->C, mblocks(dims->M), L, st),
+         "slice weights backward");
+  return reduce_slice_grads(*dims, L, gr, st);
+}
+
+}  // extern "C"

@@ -1,0 +1,93 @@
+// Compile-time geometry shared by the host launchers and the gfx950 kernels:
+// the byte layout of the per-block LDS "table image" (built once per call by
+// the prep kernel into the workspace, then copied by every block into LDS),
+// the per-wave LDS regions, and the partial-sum record sizes.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+namespace pa {
+
+enum Pass { kAggregate = 0, kDeslice = 1, kDesliceBwd = 2, kWeights = 3, kSliceBwd = 4,
+            kWeightsBwd = 5 };
+
+constexpr int kLdsBytes = 160 * 1024;  // LDS per CU on gfx950
+constexpr int kPartialsMax = 256;      // blocks (point chunks) per streaming pass
+
+template <int SZ, int C, int MB>
+struct Geo {
+  static constexpr int M16 = 16 * MB;            // slices padded to 16
+  static constexpr int NB = MB + 1;              // + one temperature block
+  static constexpr int XF = C / 32;              // K32 fragments per point row
+  static constexpr int CB = C / 16;              // 16-channel blocks
+  // table image (bytes); every region starts on a 16-byte boundary
+  static constexpr int TROW = C * SZ + 16;       // logits table row: A[:,j] or a
+  static constexpr int SROW = M16 * SZ + 16;     // deslice table row: s'[:,c]
+  static constexpr int WROW = 2 * C * SZ + 16;   // dw table row: (dnum_j | s'_j)
+  // header (fp32): bias[M16], dden[M16] (centred), cN[C], cS[C]: the means over
+  // slices of dnum_j and s'_j that the backward table rows are centred by
+  static constexpr int HDR = (2 * M16 + 2 * C) * 4;
+  static constexpr int OFF_L = HDR;
+  static constexpr int SZ_L = NB * 16 * TROW;
+  static constexpr int OFF_2 = OFF_L + SZ_L;     // second table (S or W)
+  static constexpr int SZ_S = C * SROW;
+  static constexpr int SZ_W = M16 * WROW;
+  // per-wave regions
+  static constexpr int XT_ROW = C * SZ + 16;     // point tile row (x or dY)
+  static constexpr int XT = 16 * XT_ROW;
+  static constexpr int GT = 16 * M16 * SZ;       // Gumbel tile (raw rows of M)
+  static constexpr int SCR = 16 * (M16 + 1) * 4 + 64;  // dl transpose + dt
+
+  static constexpr int img_bytes(int pass) {
+    return pass == kDeslice ? OFF_2 + SZ_S
+         : (pass == kSliceBwd || pass == kWeightsBwd) ? OFF_2 + SZ_W
+         : OFF_2;
+  }
+  static constexpr int wave_bytes(int pass) {
+    return pass == kDeslice || pass == kWeights ? GT
+         : pass == kSliceBwd || pass == kWeightsBwd ? XT + GT + SCR
+         : XT + GT;
+  }
+  // floats of one block's partial-sum record
+  static constexpr int red_floats(int pass, int M) {
+    return pass == kAggregate ? M16 * C + M16
+         : pass == kDesliceBwd ? M16 * C
+         : (pass == kSliceBwd || pass == kWeightsBwd) ? C * M16 + M16 + C + 1
+         : 0;
+    (void)M;
+  }
+  static constexpr int waves(int pass) {
+    return (img_bytes(pass) + 4 * wave_bytes(pass) <= kLdsBytes) ? 4
+         : (img_bytes(pass) + 2 * wave_bytes(pass) <= kLdsBytes) ? 2 : 1;
+  }
+  static constexpr int lds_bytes(int pass) {
+    return (img_bytes(pass) + waves(pass) * wave_bytes(pass)) > red_floats(pass, 0) * 4
+               ? img_bytes(pass) + waves(pass) * wave_bytes(pass)
+               : red_floats(pass, 0) * 4;
+  }
+  static constexpr bool fits(int pass) {
+    return img_bytes(pass) + wave_bytes(pass) <= kLdsBytes && red_floats(pass, 0) * 4 <= kLdsBytes;
+  }
+};
+
+// Number of point chunks (blocks) of a streaming pass: a function of N only,
+// so every reduction sums the same partials in the same order everywhere.
+inline int num_chunks(int64_t N, int waves) {
+  int64_t tiles = (N + 15) / 16;
+  int64_t p = (tiles + waves - 1) / waves;
+  return (int)(p < kPartialsMax ? (p > 0 ? p : 1) : kPartialsMax);
+}
+
+// Floats in the record a pass writes per block (valid slices only).
+inline int64_t record_floats(int pass, int C, int M) {
+  switch (pass) {
+    case kAggregate: return (int64_t)M * C + M;
+    case kDesliceBwd: return (int64_t)M * C;
+    case kSliceBwd:
+    case kWeightsBwd: return (int64_t)C * M + M + C + 1;
+    default: return 0;
+  }
+}
+
+}  // namespace pa

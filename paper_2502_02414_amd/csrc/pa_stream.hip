@@ -1,0 +1,52 @@
+// Dispatch of the streaming passes (kernels in pa_stream.hpp, instantiated
+// per pass in pa_stream_<pass>.hip).
+#include "pa_stream.hpp"
+
+namespace pa {
+
+template <int SZ>
+static int waves_of(int pass, int C, int MB) {
+#define PA_W(CC, BB) \
+  if (C == CC && MB == BB) return Geo<SZ, CC, BB>::fits(pass) ? Geo<SZ, CC, BB>::waves(pass) : 0;
+  PA_W(32, 1) PA_W(32, 2) PA_W(32, 3) PA_W(32, 4)
+  PA_W(64, 1) PA_W(64, 2) PA_W(64, 3) PA_W(64, 4)
+  PA_W(128, 1) PA_W(128, 2) PA_W(128, 3) PA_W(128, 4)
+  PA_W(256, 1) PA_W(256, 2) PA_W(256, 3) PA_W(256, 4)
+#undef PA_W
+  return 0;
+}
+
+int stream_waves(int pass, int dtype, int C, int MB) {
+  return dtype == 1 ? waves_of<2>(pass, C, MB) : waves_of<4>(pass, C, MB);
+}
+
+hipError_t launch_stream(int pass, int dtype, int C, int MB, const StreamLaunch& L,
+                         hipStream_t st) {
+  // every pointer a pass dereferences must be there (a NULL is an error here,
+  // never a device fault)
+  if (!L.x || !L.img || L.N < 1 || L.M < 1 || L.M > 16 * MB || L.P < 1) return hipErrorInvalidValue;
+  const bool reduces = pass == kAggregate || pass == kDesliceBwd || pass == kSliceBwd ||
+                       pass == kWeightsBwd;
+  if (reduces && !L.partials) return hipErrorInvalidValue;
+  if ((pass == kDeslice || pass == kWeights || pass == kSliceBwd || pass == kWeightsBwd) && !L.out)
+    return hipErrorInvalidValue;
+  if (pass == kDesliceBwd && !L.dY) return hipErrorInvalidValue;
+  if (pass == kSliceBwd && L.deslice && !L.dY) return hipErrorInvalidValue;
+  if (pass == kWeightsBwd && !L.dW) return hipErrorInvalidValue;
+  StreamArgs a;
+  a.x = L.x; a.G = L.G; a.dY = L.dY; a.img = L.img; a.out = L.out; a.tau_out = L.tau_out;
+  a.dW = L.dW; a.dtau = L.dtau; a.partials = L.partials; a.N = L.N; a.M = L.M; a.rec = L.rec;
+  a.tb = L.tb; a.tau_min = L.tau_min;
+  a.flags = (L.G ? kHasG : 0) | (L.states ? kStatesTerm : 0) | (L.deslice ? kDesliceTerm : 0);
+  switch (pass) {
+    case kAggregate: return launch_aggregate_pass(dtype, C, MB, a, L.P, st);
+    case kDeslice: return launch_deslice_pass(dtype, C, MB, a, L.P, st);
+    case kDesliceBwd: return launch_deslice_bwd_pass(dtype, C, MB, a, L.P, st);
+    case kWeights: return launch_weights_pass(dtype, C, MB, a, L.P, st);
+    case kSliceBwd: return launch_slice_bwd_pass(dtype, C, MB, a, L.P, st);
+    case kWeightsBwd: return launch_weights_bwd_pass(dtype, C, MB, a, L.P, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace pa

@@ -1,0 +1,205 @@
+"""Shared helpers of the GPU parity tests (not collected by pytest).
+
+Inputs come from the seeded generators in ``paper_2502_02414_amd.inputs``;
+the HIP path is called through the C ABI (``binding``) and the expected
+values come from ``oracle`` on the same stored values (bf16 inputs are
+upcast exactly).  Comparison is by relative L2 error,
+||gpu - oracle|| / ||oracle|| (the paper's relative L2, Appendix B.2), per
+tensor.
+"""
+from __future__ import annotations
+
+import dataclasses
+import sys
+from typing import Optional
+
+import numpy as np
+
+import oracle
+from paper_2502_02414_amd import binding as B
+from paper_2502_02414_amd import inputs as I
+
+# Parity bars: relative L2 per output tensor.
+TOL = {"f32": 1e-5, "bf16": 2e-2}
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def rel_l2(gpu, ref) -> float:
+    gpu = np.asarray(gpu, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    den = np.linalg.norm(ref)
+    num = np.linalg.norm(gpu - ref)
+    if den == 0.0:
+        return float(num)
+    return float(num / den)
+
+
+def torch_dtype(dt):
+    import torch
+    return torch.bfloat16 if dt == "bf16" else torch.float32
+
+
+def dev(a, dt="f32"):
+    """numpy (float32, values representable in dt) -> contiguous device tensor."""
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to("cuda")
+    return t.to(torch_dtype(dt)).contiguous()
+
+
+def host(t) -> np.ndarray:
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+@dataclasses.dataclass
+class Case:
+    """One layer's inputs as numpy (float32 holding dtype values) arrays."""
+    N: int
+    C: int
+    H: int
+    M: int
+    dt: str
+    x: np.ndarray
+    G: Optional[np.ndarray]
+    p: dict
+    dY: np.ndarray
+    tau0: float = 0.5
+    tau_min: float = 0.01
+    eps: float = 1e-5
+    out_proj: bool = False
+
+    @property
+    def pa_dtype(self):
+        return B.PA_BF16 if self.dt == "bf16" else B.PA_F32
+
+    def dims(self):
+        return B.make_dims(self.N, self.C, self.H, self.M, self.tau0, self.tau_min, self.eps,
+                           self.pa_dtype)
+
+
+def make_case(N, C, H, M, dt="f32", seed=11, geometry="normal", noise=True, biases=True,
+              ada=True, out_proj=False, tau0=0.5, tau_min=0.01, eps=1e-5, workload=None):
+    w = workload or I.small("case", N, C, H, M, dt, geometry=geometry, seed=seed, tau0=tau0,
+                            tau_min=tau_min, eps=eps)
+    x = I.make_x(w, N)
+    G = I.make_gumbel(w, N) if noise else None
+    p = I.make_params(w, biases=biases, out_proj=out_proj)
+    if not ada:
+        p["a"] = None
+    dY = I.make_grad(w, N)
+    return Case(N, C, H, M, dt, x, G, p, dY, w.tau0, w.tau_min, w.eps, out_proj)
+
+
+class Gpu:
+    """Device copies of a case's inputs plus the C-ABI calls of one layer."""
+
+    def __init__(self, case: Case):
+        import torch
+        self.c = case
+        dt = case.dt
+        self.x = dev(case.x, dt)
+        self.G = dev(case.G, dt) if case.G is not None else None
+        self.A = dev(case.p["A"], dt)
+        self.b = dev(case.p["b"]) if case.p.get("b") is not None else None
+        self.a = dev(case.p["a"], dt) if case.p.get("a") is not None else None
+        self.dY = dev(case.dY, dt)
+        self.att = {k: dev(case.p[k]) for k in ("Wq", "bq", "Wk", "bk", "Wv", "bv", "Wo", "bo")
+                    if case.p.get(k) is not None}
+        self.dims = case.dims()
+        self.sp = B.make_slice_params(self.A, self.b, self.a, case.p.get("b_t", 0.0))
+        self.ap = B.make_attn_params(**self.att)
+        self.ws = B.workspace(self.dims)
+        self.torch = torch
+
+    def empty(self, *shape, dt="f32"):
+        return self.torch.empty(*shape, dtype=torch_dtype(dt), device="cuda")
+
+    def slice_weights(self):
+        c = self.c
+        W = self.empty(c.N, c.M)
+        tau = self.empty(c.N)
+        B.pa_slice_weights(self.dims, self.x, self.G, self.sp, W, tau, self.ws)
+        return W, tau
+
+    def aggregate(self):
+        c = self.c
+        num, den, S = self.empty(c.M, c.C), self.empty(c.M), self.empty(c.M, c.C)
+        B.pa_slice_aggregate(self.dims, self.x, self.G, self.sp, num, den, S, self.ws)
+        return num, den, S
+
+    def attention(self, S):
+        Sp = self.empty(self.c.M, self.c.C)
+        B.pa_token_attention(self.dims, S, self.ap, Sp, self.ws)
+        return Sp
+
+    def deslice(self, Sp):
+        y = self.empty(self.c.N, self.c.C, dt=self.c.dt)
+        B.pa_deslice(self.dims, self.x, self.G, self.sp, Sp, y, self.ws)
+        return y
+
+    def deslice_backward(self):
+        dSp = self.empty(self.c.M, self.c.C)
+        B.pa_deslice_backward(self.dims, self.x, self.G, self.sp, self.dY, dSp, self.ws)
+        return dSp
+
+    def attention_backward(self, S, dSp):
+        c = self.c
+        g = {k: self.empty(c.C, c.C) for k in ("dWq", "dWk", "dWv")}
+        g.update({k: self.empty(c.C) for k in ("dbq", "dbk", "dbv")})
+        if "Wo" in self.att:
+            g["dWo"] = self.empty(c.C, c.C)
+            g["dbo"] = self.empty(c.C)
+        dS = self.empty(c.M, c.C)
+        B.pa_token_attention_backward(self.dims, S, self.ap, dSp, dS, B.make_attn_grads(**g),
+                                      self.ws)
+        g["dS"] = dS
+        return g
+
+    def _slice_grads(self):
+        c = self.c
+        return {"dA": self.empty(c.C, c.M), "db": self.empty(c.M), "da": self.empty(c.C),
+                "db_t": self.empty(1), "dtau0": self.empty(1)}
+
+    def slice_backward(self, num, den, dS, Sp, use_dY=True):
+        g = self._slice_grads()
+        dx = self.empty(self.c.N, self.c.C, dt=self.c.dt)
+        B.pa_slice_aggregate_backward(self.dims, self.x, self.G, self.sp, num, den, dS, Sp,
+                                      self.dY if use_dY else None, dx, B.make_slice_grads(**g),
+                                      self.ws)
+        g["dx"] = dx
+        return g
+
+    def weights_backward(self, dW, dtau=None):
+        g = self._slice_grads()
+        dx = self.empty(self.c.N, self.c.C, dt=self.c.dt)
+        B.pa_slice_weights_backward(self.dims, self.x, self.G, self.sp, dW, dtau, dx,
+                                    B.make_slice_grads(**g), self.ws)
+        g["dx"] = dx
+        return g
+
+    def layer(self):
+        """Forward then backward of the whole layer through the C ABI."""
+        num, den, S = self.aggregate()
+        Sp = self.attention(S)
+        y = self.deslice(Sp)
+        dSp = self.deslice_backward()
+        ga = self.attention_backward(S, dSp)
+        gs = self.slice_backward(num, den, ga["dS"], Sp)
+        out = {"num": num, "den": den, "S": S, "Sp": Sp, "y": y, "dSp": dSp}
+        out.update(ga)
+        out.update(gs)
+        return out
+
+
+def oracle_params(c: Case) -> dict:
+    return {k: v for k, v in c.p.items() if v is not None}
+
+
+def oracle_layer(c: Case):
+    p = oracle_params(c)
+    f = oracle.layer_forward(c.x, c.G, p, c.tau0, c.tau_min, c.eps, c.H)
+    g = oracle.layer_backward(c.x, c.G, p, c.tau0, c.tau_min, c.eps, c.H, f, c.dY)
+    return f, g

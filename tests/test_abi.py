@@ -1,0 +1,139 @@
+"""The C-ABI library loads, exports every symbol include/pa.h declares, and
+rejects bad arguments on the host before launching anything.
+
+These tests make no compute calls: every call below fails validation (or only
+asks for the workspace size), so they run without a GPU.  The fake device
+addresses are never dereferenced.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2502_02414_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(B.LIB_PATH):
+        from paper_2502_02414_amd import build
+        build.build()
+    return B.load()
+
+
+def _declared_symbols():
+    with open(os.path.join(ROOT, "include", "pa.h")) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"\b(pa_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported(lib):
+    declared = _declared_symbols()
+    assert len(declared) == 11
+    assert sorted(B.SYMBOLS) == declared
+    for name in declared:
+        assert hasattr(lib, name), name
+
+
+def test_version(lib):
+    assert lib.pa_version() == 1
+
+
+def _dims(**kw):
+    d = dict(N=1000, C=64, H=4, M=16, tau0=0.5, tau_min=0.01, eps=1e-5, dtype=B.PA_F32)
+    d.update(kw)
+    return B.make_dims(**d)
+
+
+def _ws_size(lib, dims):
+    n = ctypes.c_size_t(0)
+    st = lib.pa_workspace_size(ctypes.byref(dims), ctypes.byref(n))
+    return st, n.value
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(N=0), B.PA_ERR_INVALID),
+    (dict(M=0), B.PA_ERR_INVALID),
+    (dict(M=65), B.PA_ERR_INVALID),
+    (dict(H=3), B.PA_ERR_INVALID),
+    (dict(tau_min=0.0), B.PA_ERR_INVALID),
+    (dict(eps=-1.0), B.PA_ERR_INVALID),
+    (dict(tau0=float("nan")), B.PA_ERR_INVALID),
+    (dict(dtype=7), B.PA_ERR_INVALID),
+    (dict(C=48, H=4), B.PA_ERR_UNSUPPORTED),
+    (dict(C=512, H=8), B.PA_ERR_UNSUPPORTED),
+])
+def test_dims_validation(lib, kw, status):
+    st, _ = _ws_size(lib, _dims(**kw))
+    assert st == status
+    assert lib.pa_last_error().decode() != ""
+
+
+def test_workspace_size_grows_with_shape(lib):
+    st1, n1 = _ws_size(lib, _dims())
+    st2, n2 = _ws_size(lib, _dims(C=256, H=8, M=32, dtype=B.PA_BF16, N=1_000_000))
+    assert st1 == st2 == B.PA_OK
+    assert 0 < n1 < n2
+    assert n2 < 64 << 20  # partial records and tables only: no O(N) scratch
+
+
+FAKE = 0x7f0000000000  # aligned, never dereferenced
+
+
+def test_null_and_misaligned_pointers_rejected(lib):
+    d = _dims()
+    sp = B.pa_slice_params(FAKE, None, None, 0.0)
+    _, n = _ws_size(lib, d)
+    # x missing
+    st = lib.pa_slice_aggregate(ctypes.byref(d), None, None, ctypes.byref(sp), FAKE, FAKE, FAKE,
+                                FAKE, n, None)
+    assert st == B.PA_ERR_INVALID and "x" in lib.pa_last_error().decode()
+    # misaligned x
+    st = lib.pa_slice_aggregate(ctypes.byref(d), FAKE + 2, None, ctypes.byref(sp), FAKE, FAKE,
+                                FAKE, FAKE, n, None)
+    assert st == B.PA_ERR_INVALID and "aligned" in lib.pa_last_error().decode()
+    # A missing
+    sp0 = B.pa_slice_params(None, None, None, 0.0)
+    st = lib.pa_deslice(ctypes.byref(d), FAKE, None, ctypes.byref(sp0), FAKE, FAKE, FAKE, n,
+                        None)
+    assert st == B.PA_ERR_INVALID
+    # only one of Sp / dY
+    st = lib.pa_slice_aggregate_backward(ctypes.byref(d), FAKE, None, ctypes.byref(sp), FAKE,
+                                         FAKE, FAKE, FAKE, None, FAKE, None, FAKE, n, None)
+    assert st == B.PA_ERR_INVALID and "both" in lib.pa_last_error().decode()
+
+
+def test_small_workspace_rejected(lib):
+    d = _dims()
+    sp = B.pa_slice_params(FAKE, None, None, 0.0)
+    _, n = _ws_size(lib, d)
+    st = lib.pa_slice_aggregate(ctypes.byref(d), FAKE, None, ctypes.byref(sp), FAKE, FAKE, FAKE,
+                                FAKE, n - 256, None)
+    assert st == B.PA_ERR_WORKSPACE
+    st = lib.pa_slice_aggregate(ctypes.byref(d), FAKE, None, ctypes.byref(sp), FAKE, FAKE, FAKE,
+                                None, n, None)
+    assert st == B.PA_ERR_WORKSPACE
+
+
+def test_attention_argument_checks(lib):
+    d = _dims()
+    _, n = _ws_size(lib, d)
+    ap = B.pa_attn_params(FAKE, None, None, None, FAKE, None, None, None)  # Wk missing
+    st = lib.pa_token_attention(ctypes.byref(d), FAKE, ctypes.byref(ap), FAKE, FAKE, n, None)
+    assert st == B.PA_ERR_INVALID and "Wk" in lib.pa_last_error().decode()
+    ap = B.pa_attn_params(FAKE, None, FAKE, None, FAKE, None, None, FAKE)  # bo without Wo
+    st = lib.pa_token_attention(ctypes.byref(d), FAKE, ctypes.byref(ap), FAKE, FAKE, n, None)
+    assert st == B.PA_ERR_INVALID
+
+
+def test_unserved_table_shape_is_unsupported(lib):
+    # the backward tables of C=256, M=64 in fp32 exceed the 160 KB of LDS
+    d = _dims(C=256, H=8, M=64, dtype=B.PA_F32)
+    sp = B.pa_slice_params(FAKE, None, None, 0.0)
+    _, n = _ws_size(lib, d)
+    st = lib.pa_slice_aggregate_backward(ctypes.byref(d), FAKE, None, ctypes.byref(sp), FAKE,
+                                         FAKE, FAKE, None, None, FAKE, None, FAKE, n, None)
+    assert st == B.PA_ERR_UNSUPPORTED

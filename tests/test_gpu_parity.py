@@ -1,0 +1,258 @@
+"""HIP path vs the CPU oracle, element by element, through the C ABI.
+
+Each entry point of include/pa.h is fed the same seeded inputs as the oracle
+and compared by relative L2 per output tensor: <= 1e-5 for fp32 storage and
+<= 2e-2 for bf16 storage with fp32 accumulation.  Shapes span several
+16-point tiles with a ragged tail, ragged slice blocks (M not a multiple of
+16), M = 1, missing noise / Ada-Temp, the denominator floor, and the layer
+configurations of the benchmark suite.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from pa_cases import TOL, Gpu, host, make_case, oracle_layer, oracle_params, rel_l2, say
+
+pytestmark = pytest.mark.gpu
+
+SHAPES = [
+    # N, C, H, M, dtype
+    (1000, 32, 2, 5, "f32"),
+    (4096, 64, 4, 16, "f32"),
+    (2049, 128, 8, 64, "f32"),
+    (3001, 256, 8, 32, "bf16"),
+    (777, 64, 4, 33, "bf16"),
+    (257, 128, 8, 1, "f32"),
+    (517, 256, 8, 64, "bf16"),
+]
+IDS = [f"N{n}-C{c}-H{h}-M{m}-{d}" for n, c, h, m, d in SHAPES]
+
+
+def check(name, gpu, ref, dt, tol=None):
+    e = rel_l2(host(gpu) if not isinstance(gpu, np.ndarray) else gpu, ref)
+    bar = TOL[dt] if tol is None else tol
+    say(f"  {name:8s} rel_l2 = {e:.3e}  (bar {bar:.0e})")
+    assert np.isfinite(e) and e <= bar, (name, e, bar)
+
+
+def check_ada_temp(out, ref, dt):
+    """The Ada-Temp Linear (Eq. 3) has parameters (a, b_t); its gradient is
+    checked as one tensor [da, db_t].  db_t alone is a sum over points of dt_i
+    of both signs whose value is a fraction of a percent of sum |dt_i|, so on
+    its own its relative error is the per-point error times that condition
+    number."""
+    g = np.concatenate([host(out["da"]).ravel(), host(out["db_t"]).ravel()])
+    r = np.concatenate([np.asarray(ref["da"]).ravel(), [ref["db_t"]]])
+    check("d(a,b_t)", g, r, dt)
+
+
+def check_key_bias(gpu_dbk, gpu_dbq, dt="f32"):
+    """The key bias shifts every score of a row by the same q.b_k, which the
+    row softmax cancels (Eq. 2): dbk is exactly 0.  Relative error against a
+    zero reference is meaningless, so bound |dbk| by the scale of dbq."""
+    a, scale = np.linalg.norm(host(gpu_dbk)), np.linalg.norm(host(gpu_dbq))
+    say(f"  dbk      |dbk|/|dbq| = {a / max(scale, 1e-30):.3e}")
+    assert a <= TOL[dt] * max(scale, 1e-30)
+
+
+@pytest.fixture(scope="module")
+def cases():
+    return {}
+
+
+def get_case(cases, shape, **kw):
+    key = (shape, tuple(sorted(kw.items())))
+    if key not in cases:
+        N, C, H, M, dt = shape
+        c = make_case(N, C, H, M, dt, **kw)
+        cases[key] = (c, Gpu(c), oracle_layer(c))
+    return cases[key]
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=IDS)
+def test_slice_weights(cases, shape):
+    say(f"slice_weights {shape}")
+    c, g, (f, _) = get_case(cases, shape)
+    W, tau = g.slice_weights()
+    check("W", W, f["W"], c.dt)
+    check("tau", tau, f["tau"], c.dt)
+    Wh = host(W)
+    assert np.abs(Wh.sum(1) - 1).max() < 1e-5
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=IDS)
+def test_slice_aggregate(cases, shape):
+    say(f"slice_aggregate {shape}")
+    c, g, (f, _) = get_case(cases, shape)
+    num, den, S = g.aggregate()
+    check("num", num, f["num"], c.dt)
+    check("den", den, f["den"], c.dt)
+    check("S", S, f["S"], c.dt)
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=IDS)
+def test_token_attention(cases, shape):
+    say(f"token_attention {shape}")
+    c, g, (f, _) = get_case(cases, shape)
+    S = g.torch.from_numpy(f["S"].astype(np.float32)).cuda()
+    Sp = g.attention(S)
+    p = oracle_params(c)
+    ref = oracle.token_attention(S.cpu().numpy(), c.H, p["Wq"], p.get("bq"), p["Wk"],
+                                 p.get("bk"), p["Wv"], p.get("bv"), p.get("Wo"), p.get("bo"))
+    check("Sp", Sp, ref, "f32")
+
+
+def test_token_attention_output_projection(cases):
+    shape = (600, 64, 4, 16, "f32")
+    c, g, (f, _) = get_case(cases, shape, out_proj=True)
+    S = g.torch.from_numpy(f["S"].astype(np.float32)).cuda()
+    Sp = g.attention(S)
+    check("Sp", Sp, f["Sp"], "f32")
+    dSp = g.torch.from_numpy(np.asarray(f["S"][::-1], dtype=np.float32).copy()).cuda()
+    ga = g.attention_backward(S, dSp)
+    p = oracle_params(c)
+    ref = oracle.token_attention_backward(S.cpu().numpy(), c.H, p["Wq"], p["bq"], p["Wk"],
+                                          p["bk"], p["Wv"], p["bv"], p["Wo"], p["bo"],
+                                          dSp.cpu().numpy())
+    for k in ("dS", "dWq", "dbq", "dWk", "dWv", "dbv", "dWo", "dbo"):
+        check(k, ga[k], ref[k], "f32")
+    check_key_bias(ga["dbk"], ga["dbq"])
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=IDS)
+def test_deslice(cases, shape):
+    say(f"deslice {shape}")
+    c, g, (f, _) = get_case(cases, shape)
+    Sp = g.torch.from_numpy(f["Sp"].astype(np.float32)).cuda()
+    y = g.deslice(Sp)
+    check("y", y, oracle.deslice(f["W"], Sp.cpu().numpy()), c.dt)
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=IDS)
+def test_deslice_backward(cases, shape):
+    say(f"deslice_backward {shape}")
+    c, g, (f, gr) = get_case(cases, shape)
+    dSp = g.deslice_backward()
+    check("dSp", dSp, gr["dSp"], c.dt)
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=IDS)
+def test_token_attention_backward(cases, shape):
+    say(f"token_attention_backward {shape}")
+    c, g, (f, _) = get_case(cases, shape)
+    S = g.torch.from_numpy(f["S"].astype(np.float32)).cuda()
+    rng = np.random.default_rng(5)
+    dSp = g.torch.from_numpy(rng.standard_normal((c.M, c.C)).astype(np.float32)).cuda()
+    ga = g.attention_backward(S, dSp)
+    p = oracle_params(c)
+    ref = oracle.token_attention_backward(S.cpu().numpy(), c.H, p["Wq"], p.get("bq"), p["Wk"],
+                                          p.get("bk"), p["Wv"], p.get("bv"), None, None,
+                                          dSp.cpu().numpy())
+    for k in ("dS", "dWq", "dbq", "dWk", "dWv", "dbv"):
+        check(k, ga[k], ref[k], "f32")
+    check_key_bias(ga["dbk"], ga["dbq"])
+
+
+def _slice_backward_ref(c, f, dS, Sp, use_dY):
+    """Oracle of pa_slice_aggregate_backward for the given dS / Sp / dY."""
+    p = oracle_params(c)
+    dW = np.zeros((c.N, c.M))
+    dx = np.zeros((c.N, c.C))
+    if dS is not None:
+        dx_a, dW_a = oracle.aggregate_backward(c.x, f["W"], f["num"], f["den"], dS, c.eps)
+        dx += dx_a
+        dW += dW_a
+    if use_dY:
+        _, dW_d = oracle.deslice_backward(f["W"], Sp, c.dY)
+        dW += dW_d
+    sw = oracle.slice_weights_backward(c.x, c.G, p["A"], p.get("b"), p.get("a"),
+                                       p.get("b_t", 0.0), c.tau0, c.tau_min, dW)
+    sw["dx"] = sw["dx"] + dx
+    return sw
+
+
+@pytest.mark.parametrize("terms", ["both", "states", "deslice"])
+@pytest.mark.parametrize("shape", SHAPES, ids=IDS)
+def test_slice_aggregate_backward(cases, shape, terms):
+    say(f"slice_aggregate_backward {shape} {terms}")
+    c, g, (f, gr) = get_case(cases, shape)
+    use_dS = terms in ("both", "states")
+    use_dY = terms in ("both", "deslice")
+    # the forward quantities, as fp32, are the inputs of both sides
+    f32 = lambda a: g.torch.from_numpy(np.asarray(a, dtype=np.float32)).cuda()
+    num, den, Sp = f32(f["num"]), f32(f["den"]), f32(f["Sp"])
+    dS = f32(gr["dS"]) if use_dS else None
+    out = g.slice_backward(num, den, dS, Sp if use_dY else None, use_dY=use_dY)
+    f64 = dict(f)
+    f64["num"], f64["den"] = host(num), host(den)
+    ref = _slice_backward_ref(c, f64, host(dS) if use_dS else None, host(Sp), use_dY)
+    for k in ("dx", "dA", "db", "da"):
+        check(k, out[k], ref[k], c.dt)
+    check_ada_temp(out, ref, c.dt)
+    assert host(out["dtau0"])[0] == host(out["db_t"])[0]
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=IDS)
+def test_slice_weights_backward(cases, shape):
+    say(f"slice_weights_backward {shape}")
+    c, g, (f, _) = get_case(cases, shape)
+    rng = np.random.default_rng(9)
+    dW = rng.standard_normal((c.N, c.M)).astype(np.float32)
+    dtau = rng.standard_normal(c.N).astype(np.float32)
+    t = lambda a: g.torch.from_numpy(a).cuda()
+    out = g.weights_backward(t(dW), t(dtau))
+    p = oracle_params(c)
+    ref = oracle.slice_weights_backward(c.x, c.G, p["A"], p.get("b"), p.get("a"),
+                                        p.get("b_t", 0.0), c.tau0, c.tau_min, dW, dtau)
+    for k in ("dx", "dA", "db", "da"):
+        check(k, out[k], ref[k], c.dt)
+    check_ada_temp(out, ref, c.dt)
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=IDS)
+def test_layer_chain(cases, shape):
+    """Forward then backward of the whole layer, GPU outputs feeding GPU calls."""
+    say(f"layer {shape}")
+    c, g, (f, gr) = get_case(cases, shape)
+    out = g.layer()
+    for k in ("num", "den", "S", "Sp", "y"):
+        check(k, out[k], f[k], c.dt)
+    for k in ("dSp", "dS", "dWq", "dbq", "dWk", "dWv", "dbv", "dx", "dA", "db", "da"):
+        check(k, out[k], gr[k], c.dt)
+    check_ada_temp(out, gr, c.dt)
+    check_key_bias(out["dbk"], out["dbq"], c.dt)
+
+
+def test_deterministic(cases):
+    shape = (3001, 256, 8, 32, "bf16")
+    c, g, _ = get_case(cases, shape)
+    a = g.layer()
+    b = g.layer()
+    for k in a:
+        assert g.torch.equal(a[k], b[k]), k
+
+
+@pytest.mark.parametrize("variant", ["no_noise", "no_adatemp", "single_point", "empty_slice"])
+def test_edge_cases(variant):
+    say(f"edge {variant}")
+    if variant == "no_noise":
+        c = make_case(300, 64, 4, 16, "f32", noise=False)
+    elif variant == "no_adatemp":
+        c = make_case(300, 64, 4, 16, "bf16", ada=False)
+    elif variant == "single_point":
+        c = make_case(1, 32, 1, 3, "f32")
+    else:
+        c = make_case(500, 64, 4, 8, "f32")
+        c.p["b"] = c.p["b"].copy()
+        c.p["b"][2] = -60.0            # slice 2 is (numerically) empty: den < eps
+        c.p["A"] = c.p["A"].copy()
+        c.p["A"][:, 2] = 0.0
+    g = Gpu(c)
+    f, gr = oracle_layer(c)
+    if variant == "empty_slice":
+        assert f["den"][2] < c.eps
+    out = g.layer()
+    for k in ("num", "den", "S", "Sp", "y"):
+        check(k, out[k], f[k], c.dt)
+    for k in ("dSp", "dS", "dx", "dA", "db", "da"):
+        check(k, out[k], gr[k], c.dt)

@@ -293,6 +293,19 @@ def test_attention_matches_library_sdpa(M, C, H, out_proj):
     np.testing.assert_allclose(Sp, o.numpy(), rtol=1e-12, atol=1e-13)
 
 
+def test_attention_key_bias_has_zero_gradient():
+    # A key bias adds q_r . b_k to every score of row r; the row softmax of
+    # Eq. 2 cancels it, so the gradient of the loss in b_k is exactly 0.
+    M, C, H = 12, 16, 4
+    rng = np.random.default_rng(4)
+    S = _rand(M, C, rng=rng)
+    p = _params(C, 2, rng, out_proj=True)
+    g = oracle.token_attention_backward(S, H, p["Wq"], p["bq"], p["Wk"], p["bk"], p["Wv"],
+                                        p["bv"], p["Wo"], p["bo"], _rand(M, C, rng=rng))
+    assert np.abs(g["dbk"]).max() < 1e-12 * max(1.0, np.abs(g["dbq"]).max())
+    assert np.abs(g["dbq"]).max() > 1e-3
+
+
 def test_attention_single_token_is_value_projection():
     C = 10
     S = _rand(1, C)
