@@ -1,0 +1,240 @@
+"""Benchmark: one Physics-Attention layer, forward + backward, on one MI355X.
+
+A step is one pass of the whole hot path over one batch of synthetic input:
+    pa_slice_aggregate -> pa_token_attention -> pa_deslice        (forward)
+    pa_deslice_backward -> pa_token_attention_backward
+                        -> pa_slice_aggregate_backward           (backward)
+on the million-point car-surface workload (N = 1,000,000, C = 256, H = 8,
+M = 32, bf16 storage, fp32 accumulation).  Inputs are resident in HBM before
+the timed region.  Prints one JSON line (rank 0).
+
+    python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--no-cpu-baseline]
+
+Roofline: the dominant call is timed with HIP events (torch.cuda.Event on
+the stream the library launches on) over every timed step; its achieved
+bandwidth is its algorithmic bytes per call over that time.  Traffic (HBM
+bytes per call from the rocprofv3 FETCH_SIZE / WRITE_SIZE counters) is read
+from profiles/traffic_*.txt when that file was measured on the current
+kernel sources, else null.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = ("mesh points/sec per Physics-Attention layer fwd+bwd at N=1M, C=256, M=32; "
+          "% roofline")
+WORKLOAD = "car_1m_bf16"
+HBM_PEAK_GBS = 8000.0
+# Algorithmic HBM bytes per point of each streaming call (b = 2, g = 2 for
+# bf16): the inputs each call must read and the outputs it must write.
+def algo_bytes_per_point(C, M, b, g):
+    return {
+        "pa_slice_aggregate": C * b + M * g,           # x, G
+        "pa_deslice": 2 * C * b + M * g,               # x, G, y
+        "pa_deslice_backward": 2 * C * b + M * g,      # x, G, dY
+        "pa_slice_aggregate_backward": 3 * C * b + M * g,  # x, G, dY, dx
+        "pa_token_attention": 0,
+        "pa_token_attention_backward": 0,
+    }
+
+
+def kernel_sources_sha() -> str:
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2502_02414_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(name.encode())
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(kernel: str):
+    """Per-call HBM bytes (fetch + write) measured by rocprofv3 counters, if the
+    summary in profiles/ was taken on the current kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{WORKLOAD}.txt")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                vals[k.strip()] = v.strip()
+    if vals.get("kernel_sources_sha") != kernel_sources_sha():
+        return None
+    try:
+        return float(vals["hbm_bytes_per_call"])
+    except (KeyError, ValueError):
+        return None
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain 1 GiB device copy (counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); this build runs the "
+              "hot path on a single MI355X and has no multi-GPU path.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2502_02414_amd import binding as B
+    from paper_2502_02414_amd import inputs as I
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = I.WORKLOADS[WORKLOAD]
+    N, C, H, M = w.N, w.C, w.H, w.M
+
+    t0 = time.time()
+    x_np = I.make_x(w)
+    G_np = I.make_gumbel(w)
+    dY_np = I.make_grad(w)
+    p = I.make_params(w)
+    print(f"[bench] inputs generated in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
+
+    bf = torch.bfloat16
+    to = lambda a, dt=torch.float32: torch.from_numpy(np.ascontiguousarray(a)).to(dev).to(dt)
+    x, G, dY = to(x_np, bf), to(G_np, bf), to(dY_np, bf)
+    A, a = to(p["A"], bf), to(p["a"], bf)
+    b = to(p["b"])
+    att = {k: to(p[k]) for k in ("Wq", "bq", "Wk", "bk", "Wv", "bv")}
+    dims = B.make_dims(N, C, H, M, w.tau0, w.tau_min, w.eps, B.PA_BF16)
+    sp = B.make_slice_params(A, b, a, p["b_t"])
+    apr = B.make_attn_params(**att)
+    ws = B.workspace(dims, dev)
+    f32 = lambda *s: torch.empty(*s, dtype=torch.float32, device=dev)
+    num, den, S, Sp, dSp, dS = f32(M, C), f32(M), f32(M, C), f32(M, C), f32(M, C), f32(M, C)
+    y = torch.empty(N, C, dtype=bf, device=dev)
+    dx = torch.empty(N, C, dtype=bf, device=dev)
+    ag = {k: f32(C, C) for k in ("dWq", "dWk", "dWv")}
+    ag.update({k: f32(C) for k in ("dbq", "dbk", "dbv")})
+    agr = B.make_attn_grads(**ag)
+    sg = {"dA": f32(C, M), "db": f32(M), "da": f32(C), "db_t": f32(1), "dtau0": f32(1)}
+    sgr = B.make_slice_grads(**sg)
+
+    calls = [
+        ("pa_slice_aggregate", lambda: B.pa_slice_aggregate(dims, x, G, sp, num, den, S, ws)),
+        ("pa_token_attention", lambda: B.pa_token_attention(dims, S, apr, Sp, ws)),
+        ("pa_deslice", lambda: B.pa_deslice(dims, x, G, sp, Sp, y, ws)),
+        ("pa_deslice_backward", lambda: B.pa_deslice_backward(dims, x, G, sp, dY, dSp, ws)),
+        ("pa_token_attention_backward",
+         lambda: B.pa_token_attention_backward(dims, S, apr, dSp, dS, agr, ws)),
+        ("pa_slice_aggregate_backward",
+         lambda: B.pa_slice_aggregate_backward(dims, x, G, sp, num, den, dS, Sp, dY, dx, sgr, ws)),
+    ]
+
+    def step(events=None):
+        for k, (name, fn) in enumerate(calls):
+            if events is not None:
+                events[k][0].record()
+            fn()
+            if events is not None:
+                events[k][1].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    per_call = {name: 0.0 for name, _ in calls}
+    evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            for _ in calls] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t_wall = time.perf_counter()
+    start.record()
+    for s in range(args.steps):
+        step(evs[s])
+    end.record()
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    total_ms = start.elapsed_time(end)
+    for s in range(args.steps):
+        for k, (name, _) in enumerate(calls):
+            per_call[name] += evs[s][k][0].elapsed_time(evs[s][k][1]) / args.steps
+    ms_per_step = total_ms / args.steps
+    value = N / (ms_per_step * 1e-3)
+
+    if args.copy_calibration:
+        src = torch.empty(1 << 28, dtype=torch.float32, device=dev)  # 1 GiB
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    bpp = algo_bytes_per_point(C, M, 2, 2)
+    dom = max((n for n in per_call if bpp[n] > 0), key=lambda n: per_call[n])
+    dom_bytes = bpp[dom] * N
+    achieved = dom_bytes / (per_call[dom] * 1e-3) / 1e9
+    step_bytes = sum(bpp.values()) * N
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": read_traffic("slice_bwd"), "kernel": dom,
+                "algo_bytes_per_call": dom_bytes}
+
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "points/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": WORKLOAD, "N": N, "C": C, "H": H, "M": M, "tau0": w.tau0,
+                   "tau_min": w.tau_min, "storage": "bf16", "accumulate": "fp32",
+                   "pass": "forward+backward"},
+        "roofline": roofline,
+        "step_hbm": {"algo_bytes": step_bytes,
+                     "achieved_GBs": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
+                     "frac": round(step_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
+        "per_call_ms": {k: round(v, 4) for k, v in per_call.items()},
+        "wall_s_timed": round(t_wall, 4),
+    }
+
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(x_np, G_np, dY_np, p, w)
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(x_np, G_np, dY_np, p, w, target_s: float = 10.0):
+    """The oracle, as it stands, on the first n points of the same workload:
+    forward + backward of the layer in float64 on the host cores.  n is sized
+    from a short calibration run so that the timed run takes about
+    ``target_s`` seconds."""
+    import numpy as np
+    import oracle
+    pp = {k: v for k, v in p.items() if v is not None}
+
+    def run(n):
+        xs, Gs, dYs = x_np[:n], G_np[:n], dY_np[:n]
+        t = time.perf_counter()
+        f = oracle.layer_forward(xs, Gs, pp, w.tau0, w.tau_min, w.eps, w.H)
+        oracle.layer_backward(xs, Gs, pp, w.tau0, w.tau_min, w.eps, w.H, f, dYs)
+        return time.perf_counter() - t
+
+    n0 = 16384
+    rate0 = n0 / run(n0)
+    n = int(min(len(x_np), max(n0, rate0 * target_s)))
+    n = (n // 1024) * 1024 or n0
+    dt = run(n)
+    return {"value": round(n / dt, 1), "unit": "points/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"first {n} of the {len(x_np)} points of {WORKLOAD}, fwd+bwd in float64 "
+                      f"({dt:.1f} s)"}
+
+
+if __name__ == "__main__":
+    main()

@@ -261,48 +261,26 @@ AttnWs attn_ws(const pa_dims& d, void* ws) {
   return a;
 }
 
-// out [M,C] = in [M,C] W [C,C] + b
-pa::Gemm affine(const float* in, const float* W, const float* b, float* out, int M, int C) {
-  pa::Gemm g{};
-  g.A = in; g.sai = C; g.sak = 1;
-  g.B = W; g.sbk = C; g.sbj = 1;
-  g.bias = b; g.out = out; g.ldo = C;
-  g.rows = M; g.cols = C; g.K = C;
-  return g;
-}
-// out [M,C] (+)= in [M,C] W^T
-pa::Gemm affine_t(const float* in, const float* W, float* out, int M, int C, int acc) {
-  pa::Gemm g{};
-  g.A = in; g.sai = C; g.sak = 1;
-  g.B = W; g.sbk = 1; g.sbj = C;
-  g.out = out; g.ldo = C;
-  g.rows = M; g.cols = C; g.K = C;
-  g.accumulate = acc;
-  return g;
-}
-// out [C,C] = a^T [C,M] b [M,C]
-pa::Gemm outer(const float* a, const float* b, float* out, int M, int C) {
-  pa::Gemm g{};
-  g.A = a; g.sai = 1; g.sak = C;
-  g.B = b; g.sbk = C; g.sbj = 1;
-  g.out = out; g.ldo = C;
-  g.rows = C; g.cols = C; g.K = M;
-  return g;
-}
-
 pa_status attn_forward(const pa_dims& d, const float* S, const pa_attn_params* ap, float* Sp,
                        const AttnWs& w, hipStream_t st) {
   const int M = d.M, C = d.C;
-  PA_HIP(pa::launch_gemm(affine(S, ap->Wq, ap->bq, w.Q, M, C), st), "Q projection");
-  PA_HIP(pa::launch_gemm(affine(S, ap->Wk, ap->bk, w.K, M, C), st), "K projection");
-  PA_HIP(pa::launch_gemm(affine(S, ap->Wv, ap->bv, w.V, M, C), st), "V projection");
+  pa::Proj q{};
+  q.n = 3; q.M = M; q.Cin = C; q.Cout = C;
+  q.in[0] = q.in[1] = q.in[2] = S;
+  q.W[0] = ap->Wq; q.W[1] = ap->Wk; q.W[2] = ap->Wv;
+  q.b[0] = ap->bq; q.b[1] = ap->bk; q.b[2] = ap->bv;
+  q.out[0] = w.Q; q.out[1] = w.K; q.out[2] = w.V;
+  PA_HIP(pa::launch_proj(q, st), "QKV projection");
   // the heads' output goes straight to Sp only when Sp is wanted and there is
   // no output projection; otherwise (and for the backward's recompute, which
   // passes Sp = NULL) it goes to the workspace.
   float* O = (ap->Wo || !Sp) ? w.O : Sp;
   PA_HIP(pa::launch_attn_core(w.Q, w.K, w.V, w.P, O, M, C, d.H, st), "attention core");
-  if (ap->Wo) {
-    if (Sp) PA_HIP(pa::launch_gemm(affine(w.O, ap->Wo, ap->bo, Sp, M, C), st), "O projection");
+  if (ap->Wo && Sp) {
+    pa::Proj o{};
+    o.n = 1; o.M = M; o.Cin = C; o.Cout = C;
+    o.in[0] = w.O; o.W[0] = ap->Wo; o.b[0] = ap->bo; o.out[0] = Sp;
+    PA_HIP(pa::launch_proj(o, st), "output projection");
   }
   return PA_OK;
 }
@@ -334,24 +312,45 @@ pa_status pa_token_attention_backward(const pa_dims* dims, const float* S,
   PA_TRY(attn_forward(*dims, S, ap, nullptr, w, st));  // Q, K, V, P, O
   const float* dO = dSp;
   if (ap->Wo) {
-    PA_HIP(pa::launch_gemm(affine_t(dSp, ap->Wo, w.dO, M, C, 0), st), "dO");
+    pa::Proj q{};  // dO = dSp Wo^T
+    q.n = 1; q.M = M; q.Cin = C; q.Cout = C; q.transW = 1;
+    q.in[0] = dSp; q.W[0] = ap->Wo; q.out[0] = w.dO;
+    PA_HIP(pa::launch_proj(q, st), "dO");
     dO = w.dO;
-    if (ag && ag->dWo) PA_HIP(pa::launch_gemm(outer(w.O, dSp, ag->dWo, M, C), st), "dWo");
-    if (ag && ag->dbo) PA_HIP(pa::launch_colsum(dSp, M, C, C, ag->dbo, st), "dbo");
+    if (ag && ag->dWo) {
+      pa::Outer o{};
+      o.n = 1; o.M = M; o.C = C; o.S = w.O; o.dX[0] = dSp; o.out[0] = ag->dWo;
+      PA_HIP(pa::launch_outer(o, st), "dWo");
+    }
+    if (ag && ag->dbo) {
+      pa::ColSum cs{};
+      cs.n = 1; cs.M = M; cs.C = C; cs.in[0] = dSp; cs.out[0] = ag->dbo;
+      PA_HIP(pa::launch_colsum(cs, st), "dbo");
+    }
   }
   PA_HIP(pa::launch_attn_core_bwd(w.Q, w.K, w.V, w.P, dO, w.dQ, w.dK, w.dV, M, C, dims->H, st),
          "attention core backward");
-  PA_HIP(pa::launch_gemm(affine_t(w.dQ, ap->Wq, dS, M, C, 0), st), "dS");
-  PA_HIP(pa::launch_gemm(affine_t(w.dK, ap->Wk, dS, M, C, 1), st), "dS");
-  PA_HIP(pa::launch_gemm(affine_t(w.dV, ap->Wv, dS, M, C, 1), st), "dS");
+  {
+    pa::Proj q{};  // dS = dQ Wq^T + dK Wk^T + dV Wv^T
+    q.n = 3; q.M = M; q.Cin = C; q.Cout = C; q.transW = 1; q.sum = 1;
+    q.in[0] = w.dQ; q.in[1] = w.dK; q.in[2] = w.dV;
+    q.W[0] = ap->Wq; q.W[1] = ap->Wk; q.W[2] = ap->Wv;
+    q.out[0] = dS;
+    PA_HIP(pa::launch_proj(q, st), "dS");
+  }
   if (ag) {
-    const float* d3[3] = {w.dQ, w.dK, w.dV};
     float* dW3[3] = {ag->dWq, ag->dWk, ag->dWv};
     float* db3[3] = {ag->dbq, ag->dbk, ag->dbv};
-    for (int t = 0; t < 3; ++t) {
-      if (dW3[t]) PA_HIP(pa::launch_gemm(outer(S, d3[t], dW3[t], M, C), st), "dW");
-      if (db3[t]) PA_HIP(pa::launch_colsum(d3[t], M, C, C, db3[t], st), "db");
-    }
+    const float* d3[3] = {w.dQ, w.dK, w.dV};
+    pa::Outer o{};
+    o.M = M; o.C = C; o.S = S;
+    for (int t = 0; t < 3; ++t)
+      if (dW3[t]) { o.dX[o.n] = d3[t]; o.out[o.n] = dW3[t]; ++o.n; }
+    if (o.n) PA_HIP(pa::launch_outer(o, st), "dW");
+    pa::ColSum cs{};
+    cs.n = 3; cs.M = M; cs.C = C;
+    for (int t = 0; t < 3; ++t) { cs.in[t] = d3[t]; cs.out[t] = db3[t]; }
+    if (db3[0] || db3[1] || db3[2]) PA_HIP(pa::launch_colsum(cs, st), "db");
   }
   return PA_OK;
 }

@@ -67,21 +67,33 @@ hipError_t launch_reduce(const float* partials, int P, int64_t rec, const Segmen
 hipError_t launch_states(const float* num, const float* den, float* S, int M, int C, float eps,
                          hipStream_t st);
 
-// Small dense products for the token attention (fp32):
-//   out[i][j] = beta*out[i][j] + sum_k A(i,k) B(k,j) (+ bias[j]),
-//   A(i,k) = A[i*sai + k*sak], B(k,j) = B[k*sbk + j*sbj].
-struct Gemm {
-  const float* A; int64_t sai, sak;
-  const float* B; int64_t sbk, sbj;
-  const float* bias;
-  float* out; int64_t ldo;
-  int rows, cols, K;
-  int accumulate;
+// Token-side products (fp32, M <= 64 rows):
+//   sum = 0: out_p [M,Cout] = in_p [M,Cin] op(W_p) + b_p   for p < n
+//   sum = 1: out_0 [M,Cout] = sum_p in_p op(W_p) + b_0
+//   op(W) = W ([Cin,Cout]) or, with transW, W^T (W given as [Cout,Cin]).
+struct Proj {
+  const float* in[3];
+  const float* W[3];
+  const float* b[3];
+  float* out[3];
+  int n, M, Cin, Cout, transW, sum;
 };
-hipError_t launch_gemm(const Gemm& g, hipStream_t st);
-// Column sums: out[j] = sum_i in[i*ld + j], i < rows.
-hipError_t launch_colsum(const float* in, int rows, int cols, int64_t ld, float* out,
-                         hipStream_t st);
+hipError_t launch_proj(const Proj& q, hipStream_t st);
+// out_p [C,C] = S^T [C,M] dX_p [M,C]   (weight gradients)
+struct Outer {
+  const float* S;
+  const float* dX[3];
+  float* out[3];
+  int n, M, C;
+};
+hipError_t launch_outer(const Outer& q, hipStream_t st);
+// out_p [C] = column sums of in_p [M,C]   (bias gradients; NULL out skipped)
+struct ColSum {
+  const float* in[3];
+  float* out[3];
+  int n, M, C;
+};
+hipError_t launch_colsum(const ColSum& q, hipStream_t st);
 // Per-head attention core: P_h = softmax(Q_h K_h^T * scale), O_h = P_h V_h.
 hipError_t launch_attn_core(const float* Q, const float* K, const float* V, float* P, float* O,
                             int M, int C, int H, hipStream_t st);

@@ -25,9 +25,10 @@ struct Geo {
   static constexpr int TROW = C * SZ + 16;       // logits table row: A[:,j] or a
   static constexpr int SROW = M16 * SZ + 16;     // deslice table row: s'[:,c]
   static constexpr int WROW = 2 * C * SZ + 16;   // dw table row: (dnum_j | s'_j)
-  // header (fp32): bias[M16], dden[M16] (centred), cN[C], cS[C]: the means over
-  // slices of dnum_j and s'_j that the backward table rows are centred by
-  static constexpr int HDR = (2 * M16 + 2 * C) * 4;
+  // header (fp32): bias[M16], dden[M16], cN[C], cS[C], sw[M16]: cN and cS are
+  // the den-weighted means over slices of dnum_j and s'_j that the backward
+  // table rows are centred by; sw_j = den_j / sum den are those weights
+  static constexpr int HDR = (3 * M16 + 2 * C) * 4;
   static constexpr int OFF_L = HDR;
   static constexpr int SZ_L = NB * 16 * TROW;
   static constexpr int OFF_2 = OFF_L + SZ_L;     // second table (S or W)

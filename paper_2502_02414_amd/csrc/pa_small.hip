@@ -5,9 +5,7 @@
 //   - the ordered reduction of per-block partial-sum records (the partial
 //     sums of Section 4.2, here over point chunks of one GPU);
 //   - the states s_j = num_j / max(den_j, eps) (Eq. 1);
-//   - token attention among the M states and its backward (Eq. 2), built
-//     from a small fp32 product kernel and a per-head core kernel.  These
-//     work on M <= 64 tokens and are latency-bound, not throughput-bound.
+// (token attention lives in pa_tokens.hip).
 #include "pa_device.hpp"
 #include "pa_internal.h"
 #include "pa_layout.h"
@@ -28,7 +26,7 @@ static PrepGeo prep_geo(int dtype, int C, int M, int MB) {
   g.TROW = C * g.SZ + 16;
   g.SROW = g.M16 * g.SZ + 16;
   g.WROW = 2 * C * g.SZ + 16;
-  g.OFF_L = (2 * g.M16 + 2 * C) * 4;  // header: bias, dden, cN, cS
+  g.OFF_L = (3 * g.M16 + 2 * C) * 4;  // header: bias, dden, cN, cS, sw
   g.OFF_2 = g.OFF_L + (MB + 1) * 16 * g.TROW;
   return g;
 }
@@ -56,9 +54,10 @@ __global__ void k_prep(PrepGeo g, PrepArgs p) {
   float* hdr = reinterpret_cast<float*>(img);
   for (int64_t j = tid; j < M16; j += nth) hdr[j] = (j < M && p.b) ? p.b[j] : 0.f;
   if (p.pass != kSliceBwd)
-    for (int64_t k = tid; k < M16 + 2 * C; k += nth) hdr[M16 + k] = 0.f;
+    for (int64_t k = tid; k < 2 * M16 + 2 * C; k += nth) hdr[M16 + k] = 0.f;
   // logits table: rows j < M16: A[:, j] (0 beyond M); rows M16..M16+15: a
   const int64_t nL = (int64_t)(M16 + 16) * C;
+#pragma unroll 4
   for (int64_t k = tid; k < nL; k += nth) {
     const int j = (int)(k / C), c = (int)(k - (int64_t)j * C);
     T v;
@@ -71,6 +70,7 @@ __global__ void k_prep(PrepGeo g, PrepArgs p) {
   if (p.pass == kDeslice) {
     // S'^T: row c, column j
     const int64_t nS = (int64_t)C * M16;
+#pragma unroll 4
     for (int64_t k = tid; k < nS; k += nth) {
       const int c = (int)(k / M16), j = (int)(k - (int64_t)c * M16);
       const float v = (j < M) ? p.Sp[j * C + c] : 0.f;
@@ -80,6 +80,7 @@ __global__ void k_prep(PrepGeo g, PrepArgs p) {
   if (p.pass == kSliceBwd || p.pass == kWeightsBwd) {
     // row j: (dnum_j | s'_j)
     const int64_t nW = (int64_t)M16 * 2 * C;
+#pragma unroll 4
     for (int64_t k = tid; k < nW; k += nth) {
       const int j = (int)(k / (2 * C)), cc = (int)(k - (int64_t)j * 2 * C);
       // rows centred by cN / cS: a shift common to all slices leaves the
@@ -101,51 +102,75 @@ __global__ void k_prep(PrepGeo g, PrepArgs p) {
   }
 }
 
-// Backward header: dden_j (chain rule of Eq. 1; 0 when den_j < eps) and
-// the centres cN, cS, cD of dnum_j, s'_j, dden_j over slices.  Any centre
-// common to all slices leaves the softmax backward unchanged; the mean
-// weighted by den_j (the slices' share of the points) keeps a slice with a
-// tiny or floored denominator -- whose dnum_j = dS_j / max(den_j, eps) can
-// be huge -- from dragging the centre away from the rows that carry weight.
-// Without the states term den is not given and cS is the plain mean.  The
-// header stores dden_j - cD.  One block.
+// Backward header: dden_j (chain rule of Eq. 1; 0 when den_j < eps), the
+// normalised slice weights sw_j = den_j / sum den, and the centres cN, cS of
+// dnum_j, s'_j over slices.  Any centre common to all slices leaves the
+// softmax backward unchanged; the mean weighted by den_j (the slices' share
+// of the points) keeps a slice with a tiny or floored denominator -- whose
+// dnum_j = dS_j / max(den_j, eps) can be huge -- from dragging the centre
+// away from the rows that carry weight.  Without the states term den is not
+// given and the weights are uniform.  Blocks [0, M) reduce dden_j over C;
+// the others compute the centres of 256 channels each.
 __global__ void k_prep_center(PrepGeo g, PrepArgs p) {
-  __shared__ float sdd[64], sw[64];
+  __shared__ float red[256];
   float* hdr = reinterpret_cast<float*>(p.img);
   const int C = g.C, M = g.M, M16 = g.M16;
   const bool states = p.dS != nullptr;
   const bool desl = p.Sp != nullptr;
-  for (int j = threadIdx.x; j < 64; j += blockDim.x) {
-    float dd = 0.f;
-    if (states && j < M && p.den[j] >= p.eps) {
+  if ((int)blockIdx.x < M) {
+    const int j = blockIdx.x;
+    float s = 0.f;
+    if (states && p.den[j] >= p.eps) {
       const float d = p.den[j];
-      float s = 0.f;
-      for (int c = 0; c < C; ++c) s += p.dS[j * C + c] * (p.num[j * C + c] / d);
-      dd = -s / d;
+      for (int c = threadIdx.x; c < C; c += 256) s += p.dS[j * C + c] * (p.num[j * C + c] / d);
     }
-    sdd[j] = dd;
-    sw[j] = j < M ? (states ? fmaxf(p.den[j], 0.f) : 1.f) : 0.f;
-  }
-  __syncthreads();
-  float wsum = 0.f;
-  for (int j = 0; j < M; ++j) wsum += sw[j];
-  const float inv = wsum > 0.f ? 1.0f / wsum : 0.f;
-  for (int c = threadIdx.x; c < C; c += blockDim.x) {
-    float sn = 0.f, ss = 0.f;
-    for (int j = 0; j < M; ++j) {
-      if (states) {
-        const float d = p.den[j] >= p.eps ? p.den[j] : p.eps;
-        sn += sw[j] * (p.dS[j * C + c] / d);
+    red[threadIdx.x] = s;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+      if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+      __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+      const float dd = (states && p.den[j] >= p.eps) ? -red[0] / p.den[j] : 0.f;
+      hdr[M16 + j] = dd;
+      float wsum = 0.f;
+#pragma unroll 8
+      for (int k = 0; k < M; ++k) wsum += states ? fmaxf(p.den[k], 0.f) : 1.f;
+      hdr[2 * M16 + 2 * C + j] = (states ? fmaxf(p.den[j], 0.f) : 1.f) / wsum;
+    }
+    if (j == 0)
+      for (int k = M + threadIdx.x; k < M16; k += blockDim.x) {
+        hdr[M16 + k] = 0.f;
+        hdr[2 * M16 + 2 * C + k] = 0.f;
       }
-      if (desl) ss += sw[j] * p.Sp[j * C + c];
-    }
-    hdr[2 * M16 + c] = sn * inv;
-    hdr[2 * M16 + C + c] = ss * inv;
+    return;
   }
-  float cD = 0.f;
-  for (int j = 0; j < M; ++j) cD += sw[j] * sdd[j];
-  cD *= inv;
-  for (int j = threadIdx.x; j < M16; j += blockDim.x) hdr[M16 + j] = j < M ? sdd[j] - cD : 0.f;
+  const int c = (blockIdx.x - M) * blockDim.x + threadIdx.x;
+  if (c >= C) return;
+  float wsum = 0.f, sn = 0.f, ss = 0.f;
+  // weights and values for 8 slices at a time, loads first
+  for (int j0 = 0; j0 < M; j0 += 8) {
+    float wj[8], dv[8], sv[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int j = j0 + u < M ? j0 + u : M - 1;
+      wj[u] = states ? p.den[j] : 1.f;
+      dv[u] = states ? p.dS[j * C + c] : 0.f;
+      sv[u] = desl ? p.Sp[j * C + c] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      if (j0 + u >= M) break;
+      const float w = states ? fmaxf(wj[u], 0.f) : 1.f;
+      const float d = wj[u] >= p.eps ? wj[u] : p.eps;
+      wsum += w;
+      sn += w * (dv[u] / d);
+      ss += w * sv[u];
+    }
+  }
+  const float inv = wsum > 0.f ? 1.0f / wsum : 0.f;
+  hdr[2 * M16 + c] = sn * inv;
+  hdr[2 * M16 + C + c] = ss * inv;
 }
 
 hipError_t launch_prep(const PrepArgs& p, hipStream_t st) {
@@ -154,7 +179,7 @@ hipError_t launch_prep(const PrepArgs& p, hipStream_t st) {
   if (p.pass == kSliceBwd && p.dS && (!p.num || !p.den)) return hipErrorInvalidValue;
   PrepGeo g = prep_geo(p.dtype, p.C, p.M, p.MB);
   if (p.pass == kSliceBwd) {
-    hipLaunchKernelGGL(k_prep_center, dim3(1), dim3(256), 0, st, g, p);
+    hipLaunchKernelGGL(k_prep_center, dim3(p.M + (p.C + 255) / 256), dim3(256), 0, st, g, p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -170,16 +195,24 @@ hipError_t launch_prep(const PrepArgs& p, hipStream_t st) {
 // Ordered reduction of partial records
 // ---------------------------------------------------------------------------
 __global__ void k_reduce(const float* __restrict__ parts, int P, int64_t rec, Segments seg) {
-  __shared__ float sh[4][64];
-  const int kk = threadIdx.x & 63, pg = threadIdx.x >> 6;
-  const int64_t k = (int64_t)blockIdx.x * 64 + kk;
-  float s = 0.f;
-  if (k < rec)
-    for (int p = pg; p < P; p += 4) s += parts[(int64_t)p * rec + k];
-  sh[pg][kk] = s;
+  // 16 record columns x 16 partial groups per block: each thread adds every
+  // 16th partial (few dependent loads per thread), then the 16 group sums
+  // are added in a fixed tree order.
+  __shared__ float sh[16][17];
+  const int kk = threadIdx.x & 15, pg = threadIdx.x >> 4;
+  const int64_t k = (int64_t)blockIdx.x * 16 + kk;
+  float acc = 0.f;
+  if (k < rec) {
+#pragma unroll 8
+    for (int p = pg; p < P; p += 16) acc += parts[(int64_t)p * rec + k];
+  }
+  sh[pg][kk] = acc;
   __syncthreads();
   if (pg == 0 && k < rec) {
-    const float tot = (sh[0][kk] + sh[1][kk]) + (sh[2][kk] + sh[3][kk]);
+    float t[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) t[q] = sh[2 * q][kk] + sh[2 * q + 1][kk];
+    const float tot = ((t[0] + t[1]) + (t[2] + t[3])) + ((t[4] + t[5]) + (t[6] + t[7]));
     int64_t off = k;
     for (int i = 0; i < seg.n; ++i) {
       if (off < seg.len[i]) {
@@ -194,7 +227,7 @@ __global__ void k_reduce(const float* __restrict__ parts, int P, int64_t rec, Se
 hipError_t launch_reduce(const float* partials, int P, int64_t rec, const Segments& seg,
                          hipStream_t st) {
   if (!partials || P < 1 || rec < 1) return hipErrorInvalidValue;
-  const int blocks = (int)((rec + 63) / 64);
+  const int blocks = (int)((rec + 15) / 16);
   hipLaunchKernelGGL(k_reduce, dim3(blocks), dim3(256), 0, st, partials, P, rec, seg);
   return hipGetLastError();
 }
@@ -216,148 +249,6 @@ hipError_t launch_states(const float* num, const float* den, float* S, int M, in
   const int64_t n = (int64_t)M * C;
   hipLaunchKernelGGL(k_states, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, num, den, S,
                      M, C, eps);
-  return hipGetLastError();
-}
-
-// ---------------------------------------------------------------------------
-// Small fp32 products (token side)
-// ---------------------------------------------------------------------------
-__global__ void k_gemm(Gemm g) {
-  // one 16x16 output tile per block, one output per thread, K in chunks of 16
-  __shared__ float sa[16][17], sb[16][17];
-  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
-  const int i = blockIdx.y * 16 + ty, j = blockIdx.x * 16 + tx;
-  float acc = 0.f;
-  for (int k0 = 0; k0 < g.K; k0 += 16) {
-    const int ka = k0 + tx, kb = k0 + ty;
-    const int ia = blockIdx.y * 16 + ty, jb = blockIdx.x * 16 + tx;
-    sa[ty][tx] = (ia < g.rows && ka < g.K) ? g.A[ia * g.sai + ka * g.sak] : 0.f;
-    sb[ty][tx] = (kb < g.K && jb < g.cols) ? g.B[kb * g.sbk + jb * g.sbj] : 0.f;
-    __syncthreads();
-#pragma unroll
-    for (int kk = 0; kk < 16; ++kk) acc += sa[ty][kk] * sb[kk][tx];
-    __syncthreads();
-  }
-  if (i < g.rows && j < g.cols) {
-    if (g.bias) acc += g.bias[j];
-    float* o = g.out + (int64_t)i * g.ldo + j;
-    *o = g.accumulate ? *o + acc : acc;
-  }
-}
-
-hipError_t launch_gemm(const Gemm& g, hipStream_t st) {
-  if (!g.A || !g.B || !g.out || g.rows < 1 || g.cols < 1 || g.K < 1) return hipErrorInvalidValue;
-  dim3 grid((g.cols + 15) / 16, (g.rows + 15) / 16);
-  hipLaunchKernelGGL(k_gemm, grid, dim3(256), 0, st, g);
-  return hipGetLastError();
-}
-
-__global__ void k_colsum(const float* in, int rows, int cols, int64_t ld, float* out) {
-  const int j = blockIdx.x * blockDim.x + threadIdx.x;
-  if (j >= cols) return;
-  float s = 0.f;
-  for (int i = 0; i < rows; ++i) s += in[(int64_t)i * ld + j];
-  out[j] = s;
-}
-
-hipError_t launch_colsum(const float* in, int rows, int cols, int64_t ld, float* out,
-                         hipStream_t st) {
-  if (!in || !out) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_colsum, dim3((cols + 255) / 256), dim3(256), 0, st, in, rows, cols, ld,
-                     out);
-  return hipGetLastError();
-}
-
-// ---------------------------------------------------------------------------
-// Attention core, one block per head (M <= 64).
-// ---------------------------------------------------------------------------
-__global__ void k_attn_core(const float* Q, const float* K, const float* V, float* P, float* O,
-                            int M, int C, int H) {
-  __shared__ float sp[64][65];
-  const int h = blockIdx.x, D = C / H, off = h * D;
-  const float scale = 1.0f / sqrtf((float)D);
-  for (int e = threadIdx.x; e < M * M; e += blockDim.x) {
-    const int r = e / M, c = e - r * M;
-    float s = 0.f;
-    for (int d = 0; d < D; ++d) s += Q[r * C + off + d] * K[c * C + off + d];
-    sp[r][c] = s * scale;
-  }
-  __syncthreads();
-  for (int r = threadIdx.x; r < M; r += blockDim.x) {
-    float mx = -INFINITY;
-    for (int c = 0; c < M; ++c) mx = fmaxf(mx, sp[r][c]);
-    float sum = 0.f;
-    for (int c = 0; c < M; ++c) {
-      const float e = expf(sp[r][c] - mx);
-      sp[r][c] = e;
-      sum += e;
-    }
-    const float inv = 1.0f / sum;
-    for (int c = 0; c < M; ++c) sp[r][c] *= inv;
-  }
-  __syncthreads();
-  for (int e = threadIdx.x; e < M * M; e += blockDim.x) {
-    const int r = e / M, c = e - r * M;
-    P[(int64_t)h * M * M + e] = sp[r][c];
-  }
-  for (int e = threadIdx.x; e < M * D; e += blockDim.x) {
-    const int r = e / D, d = e - r * D;
-    float s = 0.f;
-    for (int c = 0; c < M; ++c) s += sp[r][c] * V[c * C + off + d];
-    O[r * C + off + d] = s;
-  }
-}
-
-hipError_t launch_attn_core(const float* Q, const float* K, const float* V, float* P, float* O,
-                            int M, int C, int H, hipStream_t st) {
-  if (!Q || !K || !V || !P || !O || M < 1 || M > 64 || H < 1 || C % H) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_attn_core, dim3(H), dim3(256), 0, st, Q, K, V, P, O, M, C, H);
-  return hipGetLastError();
-}
-
-__global__ void k_attn_core_bwd(const float* Q, const float* K, const float* V, const float* P,
-                                const float* dO, float* dQ, float* dK, float* dV, int M, int C,
-                                int H) {
-  __shared__ float sp[64][65];
-  __shared__ float se[64][65];
-  const int h = blockIdx.x, D = C / H, off = h * D;
-  const float scale = 1.0f / sqrtf((float)D);
-  const float* Ph = P + (int64_t)h * M * M;
-  for (int e = threadIdx.x; e < M * M; e += blockDim.x) {
-    const int r = e / M, c = e - r * M;
-    sp[r][c] = Ph[e];
-    float s = 0.f;  // dP = dO_h V_h^T
-    for (int d = 0; d < D; ++d) s += dO[r * C + off + d] * V[c * C + off + d];
-    se[r][c] = s;
-  }
-  __syncthreads();
-  for (int r = threadIdx.x; r < M; r += blockDim.x) {
-    float rs = 0.f;
-    for (int c = 0; c < M; ++c) rs += se[r][c] * sp[r][c];
-    for (int c = 0; c < M; ++c) se[r][c] = sp[r][c] * (se[r][c] - rs);
-  }
-  __syncthreads();
-  for (int e = threadIdx.x; e < M * D; e += blockDim.x) {
-    const int r = e / D, d = e - r * D;
-    float sv = 0.f, sq = 0.f, sk = 0.f;
-    for (int c = 0; c < M; ++c) {
-      sv += sp[c][r] * dO[c * C + off + d];
-      sq += se[r][c] * K[c * C + off + d];
-      sk += se[c][r] * Q[c * C + off + d];
-    }
-    dV[r * C + off + d] = sv;
-    dQ[r * C + off + d] = scale * sq;
-    dK[r * C + off + d] = scale * sk;
-  }
-}
-
-hipError_t launch_attn_core_bwd(const float* Q, const float* K, const float* V,
-                                const float* P, const float* dO, float* dQ, float* dK,
-                                float* dV, int M, int C, int H, hipStream_t st) {
-  if (!Q || !K || !V || !P || !dO || !dQ || !dK || !dV || M < 1 || M > 64 || H < 1 || C % H)
-    return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_attn_core_bwd, dim3(H), dim3(256), 0, st, Q, K, V, P, dO, dQ, dK, dV, M,
-                     C, H);
   return hipGetLastError();
 }
 

@@ -340,23 +340,47 @@ __device__ __forceinline__ void softmax_sp(const V (&acc)[MB + 1],
     for (int i = 0; i < 4; ++i) w[nb][i] = pv ? e[nb][i] * inv : 0.f;
 }
 
-// Transposed operand of a point contraction: lane (r,g) element i =
-// tile[4g+i][16cb + r] (points along K, channels along the 16 columns).
-template <typename T, int C>
-__device__ __forceinline__ void ld_transposed(K16<T>& f, const char* tile, int cb) {
+// Transposed K16 fragment of a row-major LDS array with row stride ROW
+// bytes: lane (r,g) element i = arr[row0 + 4g + i][col0 + r].  bf16 uses
+// ds_read_b64_tr_b16: within each 16-lane group, lane 4a+e receives element
+// e of the 8-byte chunks addressed by lanes a, a+4, a+8, a+12, so lane k
+// addresses row row0 + 4g + k/4, columns col0 + 4 (k%4) .. +3.  fp32 reads
+// the four elements one by one.
+template <typename T>
+__device__ __forceinline__ void ld_k16_t(K16<T>& f, const char* base, int ROW, int row0,
+                                         int col0) {
   const int r = lane_id() & 15, g = lane_id() >> 4;
-  constexpr int ROW = C * (int)sizeof(T) + 16;
-  const char* p = tile + (4 * g) * ROW + (16 * cb + r) * (int)sizeof(T);
   if constexpr (sizeof(T) == 2) {
-    f.v[0] = *reinterpret_cast<const bf16*>(p);
-    f.v[1] = *reinterpret_cast<const bf16*>(p + ROW);
-    f.v[2] = *reinterpret_cast<const bf16*>(p + 2 * ROW);
-    f.v[3] = *reinterpret_cast<const bf16*>(p + 3 * ROW);
+    typedef __bf16 bf16x4v __attribute__((__vector_size__(4 * sizeof(__bf16))));
+    const char* p = base + (row0 + 4 * g + (r >> 2)) * ROW + (col0 + 4 * (r & 3)) * 2;
+    bf16x4v v = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+        (__attribute__((address_space(3))) bf16x4v*)(p));
+    f.v = __builtin_bit_cast(bf16x4, v);
   } else {
+    const char* p = base + (row0 + 4 * g) * ROW + (col0 + r) * 4;
     f.v[0] = *reinterpret_cast<const float*>(p);
     f.v[1] = *reinterpret_cast<const float*>(p + ROW);
     f.v[2] = *reinterpret_cast<const float*>(p + 2 * ROW);
     f.v[3] = *reinterpret_cast<const float*>(p + 3 * ROW);
+  }
+}
+
+// Tile loop with a register ping-pong: the loads of tile t+1 are issued into
+// one register set while tile t is processed from the other, so a tile's
+// loads have a whole tile of work to land (no register copies, which the
+// compiler would wait on early).
+template <typename Regs, typename Load, typename Proc>
+__device__ __forceinline__ void stream_tiles(int64_t t0, int64_t t1, Load&& load, Proc&& proc) {
+  if (t0 >= t1) return;
+  Regs A, B;
+  load(A, t0);
+  for (int64_t t = t0;;) {
+    if (t + 1 < t1) load(B, t + 1);
+    proc(A, t);
+    if (++t >= t1) break;
+    if (t + 1 < t1) load(A, t + 1);
+    proc(B, t);
+    if (++t >= t1) break;
   }
 }
 
@@ -424,37 +448,37 @@ __global__ void __launch_bounds__(256) k_aggregate(StreamArgs a) {
   int64_t t0, t1;
   tile_range(a.N, WAVES, t0, t1);
 
-  K32<T> xn[G_::XF], yn[G_::XF];
-  GRegs<T, MB> gn;
+  // One register set per stream; the next tile's loads are issued into it
+  // right after its last use in this tile, so they land while the rest of
+  // the tile is computed.
+  K32<T> xr[G_::XF], yr[G_::XF];
+  GRegs<T, MB> gr;
   if (t0 < t1) {
-    load_rows<T, C>(xn, X, t0 * 16, a.N);
-    if (BWD) load_rows<T, C>(yn, Y, t0 * 16, a.N);
-    load_g<T, MB>(gn, Gp, t0 * 16, a.N, a.M, hasG);
+    load_rows<T, C>(xr, X, t0 * 16, a.N);
+    if constexpr (BWD) load_rows<T, C>(yr, Y, t0 * 16, a.N);
+    load_g<T, MB>(gr, Gp, t0 * 16, a.N, a.M, hasG);
   }
   for (int64_t t = t0; t < t1; ++t) {
-    K32<T> xc[G_::XF], yc[G_::XF];
-    GRegs<T, MB> gc = gn;
-#pragma unroll
-    for (int s = 0; s < G_::XF; ++s) {
-      xc[s] = xn[s];
-      if (BWD) yc[s] = yn[s];
-    }
     const int64_t p0 = t * 16;
-    if (t + 1 < t1) {
-      load_rows<T, C>(xn, X, p0 + 16, a.N);
-      if (BWD) load_rows<T, C>(yn, Y, p0 + 16, a.N);
-      load_g<T, MB>(gn, Gp, p0 + 16, a.N, a.M, hasG);
-    }
+    const bool more = t + 1 < t1;
     const int nvalid = (int)(a.N - p0 < 16 ? a.N - p0 : 16);
     wave_sync();
-    store_rows_lds<T, C>(xt, BWD ? yc : xc);
-    store_g_lds<T, MB>(gt, gc, a.M);
+    if constexpr (BWD)
+      store_rows_lds<T, C>(xt, yr);
+    else
+      store_rows_lds<T, C>(xt, xr);
+    store_g_lds<T, MB>(gt, gr, a.M);
     wave_sync();
+    if (more) {
+      load_g<T, MB>(gr, Gp, p0 + 16, a.N, a.M, hasG);
+      if constexpr (BWD) load_rows<T, C>(yr, Y, p0 + 16, a.N);
+    }
 
     typename LAcc<T, false>::v lg[MB + 1];
-    logits<T, C, MB, false>(lg, xc, tabL);
+    logits<T, C, MB, false>(lg, xr, tabL);
     float w[MB][4], tau[4], tt[4];
-    temperature_ps<T, C, MB>(lg, xc, tabL, a.tb, tt);
+    temperature_ps<T, C, MB>(lg, xr, tabL, a.tb, tt);
+    if (more) load_rows<T, C>(xr, X, p0 + 16, a.N);
     softmax_ps<T, MB>(lg, gt, bias, a.M, hasG, tt, a.tau_min, nvalid, w, tau);
 
     K16<T> wt[MB];
@@ -468,7 +492,7 @@ __global__ void __launch_bounds__(256) k_aggregate(StreamArgs a) {
 #pragma unroll
     for (int cb = 0; cb < G_::CB; ++cb) {
       K16<T> xb;
-      ld_transposed<T, C>(xb, xt, cb);
+      ld_k16_t<T>(xb, xt, G_::XT_ROW, 0, 16 * cb);
 #pragma unroll
       for (int nb = 0; nb < MB; ++nb) acc[nb][cb] = mma16(wt[nb], xb, acc[nb][cb]);
     }
@@ -534,31 +558,26 @@ __global__ void __launch_bounds__(256) k_deslice(StreamArgs a) {
   int64_t t0, t1;
   tile_range(a.N, WAVES, t0, t1);
 
-  K32<T> xn[G_::XF];
-  GRegs<T, MB> gn;
+  K32<T> xr[G_::XF];
+  GRegs<T, MB> gr;
   if (t0 < t1) {
-    load_rows<T, C>(xn, X, t0 * 16, a.N);
-    load_g<T, MB>(gn, Gp, t0 * 16, a.N, a.M, hasG);
+    load_rows<T, C>(xr, X, t0 * 16, a.N);
+    load_g<T, MB>(gr, Gp, t0 * 16, a.N, a.M, hasG);
   }
   for (int64_t t = t0; t < t1; ++t) {
-    K32<T> xc[G_::XF];
-    GRegs<T, MB> gc = gn;
-#pragma unroll
-    for (int s = 0; s < G_::XF; ++s) xc[s] = xn[s];
     const int64_t p0 = t * 16;
-    if (t + 1 < t1) {
-      load_rows<T, C>(xn, X, p0 + 16, a.N);
-      load_g<T, MB>(gn, Gp, p0 + 16, a.N, a.M, hasG);
-    }
+    const bool more = t + 1 < t1;
     const int nvalid = (int)(a.N - p0 < 16 ? a.N - p0 : 16);
     wave_sync();
-    store_g_lds<T, MB>(gt, gc, a.M);
+    store_g_lds<T, MB>(gt, gr, a.M);
     wave_sync();
+    if (more) load_g<T, MB>(gr, Gp, p0 + 16, a.N, a.M, hasG);
 
     typename LAcc<T, true>::v lg[MB + 1];
-    logits<T, C, MB, true>(lg, xc, tabL);
+    logits<T, C, MB, true>(lg, xr, tabL);
     float w[MB][4], zs[MB][4], tau;
-    const float tt = temperature_own<T, C, MB>(lg, xc, tabL, a.tb);
+    const float tt = temperature_own<T, C, MB>(lg, xr, tabL, a.tb);
+    if (more) load_rows<T, C>(xr, X, p0 + 16, a.N);
     softmax_sp<T, MB>(lg, gt, bias, a.M, hasG, tt, a.tau_min, nvalid, w, zs, tau);
 
     K16<T> wb[MB];
@@ -612,20 +631,24 @@ __global__ void __launch_bounds__(256) k_weights(StreamArgs a) {
   float* W = reinterpret_cast<float*>(a.out);
   int64_t t0, t1;
   tile_range(a.N, WAVES, t0, t1);
-  for (int64_t t = t0; t < t1; ++t) {
+  struct Regs {
+    K32<T> x[G_::XF];
+    GRegs<T, MB> g;
+  };
+  auto load = [&](Regs& R, int64_t t) {
+    load_rows<T, C>(R.x, X, t * 16, a.N);
+    load_g<T, MB>(R.g, Gp, t * 16, a.N, a.M, hasG);
+  };
+  auto proc = [&](Regs& R, int64_t t) {
     const int64_t p0 = t * 16;
-    K32<T> xc[G_::XF];
-    GRegs<T, MB> gc;
-    load_rows<T, C>(xc, X, p0, a.N);
-    load_g<T, MB>(gc, Gp, p0, a.N, a.M, hasG);
     const int nvalid = (int)(a.N - p0 < 16 ? a.N - p0 : 16);
     wave_sync();
-    store_g_lds<T, MB>(gt, gc, a.M);
+    store_g_lds<T, MB>(gt, R.g, a.M);
     wave_sync();
     typename LAcc<T, false>::v lg[MB + 1];
-    logits<T, C, MB, false>(lg, xc, tabL);
+    logits<T, C, MB, false>(lg, R.x, tabL);
     float w[MB][4], tau[4], tt[4];
-    temperature_ps<T, C, MB>(lg, xc, tabL, a.tb, tt);
+    temperature_ps<T, C, MB>(lg, R.x, tabL, a.tb, tt);
     softmax_ps<T, MB>(lg, gt, bias, a.M, hasG, tt, a.tau_min, nvalid, w, tau);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -639,7 +662,8 @@ __global__ void __launch_bounds__(256) k_weights(StreamArgs a) {
         if (r == 0 && a.tau_out) a.tau_out[p0 + p] = tau[i];
       }
     }
-  }
+  };
+  stream_tiles<Regs>(t0, t1, load, proc);
 }
 
 // ---------------------------------------------------------------------------
@@ -674,13 +698,20 @@ __global__ void __launch_bounds__(256) k_slice_bwd(StreamArgs a) {
   float* scr = reinterpret_cast<float*>(wreg + G_::XT + G_::GT);  // [16][M16+1]
   float* scr_dt = scr + 16 * SROWF;                                // [16]
 
+  // dden_j centred by its den-weighted mean (a shift common to all slices)
+  float cD = 0.f;
+  {
+    const float* sw = reinterpret_cast<const float*>(smem) + 2 * M16 + 2 * C;
+    for (int j = 0; j < a.M; ++j) cD += sw[j] * dden_tab[j];
+  }
   float bias[MB][4], dden[MB][4];
 #pragma unroll
   for (int nb = 0; nb < MB; ++nb)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      bias[nb][i] = reinterpret_cast<const float*>(smem)[16 * nb + 4 * g + i];
-      dden[nb][i] = dden_tab[16 * nb + 4 * g + i];
+      const int j = 16 * nb + 4 * g + i;
+      bias[nb][i] = reinterpret_cast<const float*>(smem)[j];
+      dden[nb][i] = j < a.M ? dden_tab[j] - cD : 0.f;
     }
 
   f32x4 dA[G_::CB][MB];
@@ -703,33 +734,23 @@ __global__ void __launch_bounds__(256) k_slice_bwd(StreamArgs a) {
   int64_t t0, t1;
   tile_range(a.N, WAVES, t0, t1);
 
-  K32<T> xn[G_::XF], yn[G_::XF];
-  GRegs<T, MB> gn;
+  K32<T> xc[G_::XF], yc[G_::XF];
+  GRegs<T, MB> gr;
   if (t0 < t1) {
-    load_rows<T, C>(xn, X, t0 * 16, a.N);
-    if (deslice) load_rows<T, C>(yn, Y, t0 * 16, a.N);
-    load_g<T, MB>(gn, Gp, t0 * 16, a.N, a.M, hasG);
+    load_rows<T, C>(xc, X, t0 * 16, a.N);
+    if (deslice) load_rows<T, C>(yc, Y, t0 * 16, a.N);
+    load_g<T, MB>(gr, Gp, t0 * 16, a.N, a.M, hasG);
   }
   for (int64_t t = t0; t < t1; ++t) {
-    K32<T> xc[G_::XF], yc[G_::XF];
-    GRegs<T, MB> gc = gn;
-#pragma unroll
-    for (int s = 0; s < G_::XF; ++s) {
-      xc[s] = xn[s];
-      yc[s] = yn[s];
-    }
     const int64_t p0 = t * 16;
-    if (t + 1 < t1) {
-      load_rows<T, C>(xn, X, p0 + 16, a.N);
-      if (deslice) load_rows<T, C>(yn, Y, p0 + 16, a.N);
-      load_g<T, MB>(gn, Gp, p0 + 16, a.N, a.M, hasG);
-    }
+    const bool more = t + 1 < t1;
     const int nvalid = (int)(a.N - p0 < 16 ? a.N - p0 : 16);
     const bool pv = r < nvalid;
     wave_sync();
     store_rows_lds<T, C>(xt, xc);
-    store_g_lds<T, MB>(gt, gc, a.M);
+    store_g_lds<T, MB>(gt, gr, a.M);
     wave_sync();
+    if (more) load_g<T, MB>(gr, Gp, p0 + 16, a.N, a.M, hasG);
 
     typename LAcc<T, true>::v lg[MB + 1];
     logits<T, C, MB, true>(lg, xc, tabL);
@@ -779,6 +800,11 @@ __global__ void __launch_bounds__(256) k_slice_bwd(StreamArgs a) {
         }
     }
 
+    if (more) {  // x and dY registers are free from here on
+      load_rows<T, C>(xc, X, p0 + 16, a.N);
+      if (deslice) load_rows<T, C>(yc, Y, p0 + 16, a.N);
+    }
+
     // softmax backward, dz = w (dw - <w, dw>), with <w, dw> compensated by a
     // second pass over the residuals (rows can be nearly one-hot, where the
     // difference is tiny next to dw), then the temperature chain.  The
@@ -825,37 +851,13 @@ __global__ void __launch_bounds__(256) k_slice_bwd(StreamArgs a) {
       f32x4 d = zero4();
 #pragma unroll
       for (int nb = 0; nb < MB; ++nb) {
-        // A^T rows of the logits table, read transposed: [channel][slice]
+        // A^T rows of the logits table read transposed: [channel][slice]
         K16<T> ta;
-        {
-          const char* p = tabL + (16 * nb + 4 * g) * G_::TROW + (16 * cb + r) * (int)sizeof(T);
-          if constexpr (sizeof(T) == 2) {
-            ta.v[0] = *reinterpret_cast<const bf16*>(p);
-            ta.v[1] = *reinterpret_cast<const bf16*>(p + G_::TROW);
-            ta.v[2] = *reinterpret_cast<const bf16*>(p + 2 * G_::TROW);
-            ta.v[3] = *reinterpret_cast<const bf16*>(p + 3 * G_::TROW);
-          } else {
-            ta.v[0] = *reinterpret_cast<const float*>(p);
-            ta.v[1] = *reinterpret_cast<const float*>(p + G_::TROW);
-            ta.v[2] = *reinterpret_cast<const float*>(p + 2 * G_::TROW);
-            ta.v[3] = *reinterpret_cast<const float*>(p + 3 * G_::TROW);
-          }
-        }
+        ld_k16_t<T>(ta, tabL, G_::TROW, 16 * nb, 16 * cb);
         d = mma16(ta, lb[nb], d);
         if (states) {
-          K16<T> tn;
-          const char* p = tabW + (16 * nb + 4 * g) * G_::WROW + (16 * cb + r) * (int)sizeof(T);
-          if constexpr (sizeof(T) == 2) {
-            tn.v[0] = *reinterpret_cast<const bf16*>(p);
-            tn.v[1] = *reinterpret_cast<const bf16*>(p + G_::WROW);
-            tn.v[2] = *reinterpret_cast<const bf16*>(p + 2 * G_::WROW);
-            tn.v[3] = *reinterpret_cast<const bf16*>(p + 3 * G_::WROW);
-          } else {
-            tn.v[0] = *reinterpret_cast<const float*>(p);
-            tn.v[1] = *reinterpret_cast<const float*>(p + G_::WROW);
-            tn.v[2] = *reinterpret_cast<const float*>(p + 2 * G_::WROW);
-            tn.v[3] = *reinterpret_cast<const float*>(p + 3 * G_::WROW);
-          }
+          K16<T> tn;  // (dnum_j - cN) rows of the backward table, transposed
+          ld_k16_t<T>(tn, tabW, G_::WROW, 16 * nb, 16 * cb);
           d = mma16(tn, wb[nb], d);
         }
       }
@@ -902,7 +904,7 @@ __global__ void __launch_bounds__(256) k_slice_bwd(StreamArgs a) {
 #pragma unroll
     for (int cb = 0; cb < G_::CB; ++cb) {
       K16<T> xa;
-      ld_transposed<T, C>(xa, xt, cb);
+      ld_k16_t<T>(xa, xt, G_::XT_ROW, 0, 16 * cb);
       da[cb] += (k16_elem(xa, 0) * dtp[0] + k16_elem(xa, 1) * dtp[1]) +
                 (k16_elem(xa, 2) * dtp[2] + k16_elem(xa, 3) * dtp[3]);
 #pragma unroll
