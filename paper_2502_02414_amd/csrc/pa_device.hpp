@@ -29,6 +29,12 @@ constexpr float kLn2 = 0.6931471805599453f;
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
 
+// Byte offset of (row, byte column) in a swizzled LDS array with row stride
+// RB bytes: the 16-byte chunk index is XORed with bit 3 of the row.
+__device__ __forceinline__ int swz(int row, int bcol, int RB) {
+  return row * RB + ((bcol >> 4) ^ ((row >> 3) & 1)) * 16 + (bcol & 15);
+}
+
 // ---------------------------------------------------------------------------
 // Scalar conversions
 // ---------------------------------------------------------------------------

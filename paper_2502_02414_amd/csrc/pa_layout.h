@@ -15,6 +15,11 @@ enum Pass { kAggregate = 0, kDeslice = 1, kDesliceBwd = 2, kWeights = 3, kSliceB
 constexpr int kLdsBytes = 160 * 1024;  // LDS per CU on gfx950
 constexpr int kPartialsMax = 256;      // blocks (point chunks) per streaming pass
 
+// LDS rows of the tables and point tiles are padded by 32 bytes and their
+// 16-byte chunks are swizzled (chunk ^ bit 3 of the row; see swz() in
+// pa_device.hpp): row reads of 16 bytes per lane (MFMA operands) and the
+// transposed reads of 8 bytes per lane (ds_read_b64_tr_b16) then hit
+// distinct banks.
 template <int SZ, int C, int MB>
 struct Geo {
   static constexpr int M16 = 16 * MB;            // slices padded to 16
@@ -22,9 +27,9 @@ struct Geo {
   static constexpr int XF = C / 32;              // K32 fragments per point row
   static constexpr int CB = C / 16;              // 16-channel blocks
   // table image (bytes); every region starts on a 16-byte boundary
-  static constexpr int TROW = C * SZ + 16;       // logits table row: A[:,j] or a
+  static constexpr int TROW = C * SZ + 32;       // logits table row: A[:,j] or a
   static constexpr int SROW = M16 * SZ + 16;     // deslice table row: s'[:,c]
-  static constexpr int WROW = 2 * C * SZ + 16;   // dw table row: (dnum_j | s'_j)
+  static constexpr int WROW = 2 * C * SZ + 32;   // dw table row: (dnum_j | s'_j)
   // header (fp32): bias[M16], dden[M16], cN[C], cS[C], sw[M16]: cN and cS are
   // the den-weighted means over slices of dnum_j and s'_j that the backward
   // table rows are centred by; sw_j = den_j / sum den are those weights
@@ -34,10 +39,11 @@ struct Geo {
   static constexpr int OFF_2 = OFF_L + SZ_L;     // second table (S or W)
   static constexpr int SZ_S = C * SROW;
   static constexpr int SZ_W = M16 * WROW;
-  // per-wave regions
-  static constexpr int XT_ROW = C * SZ + 16;     // point tile row (x or dY)
+  // per-wave regions: point tiles (x, dY), the Gumbel rows, backward scratch
+  static constexpr int XT_ROW = C * SZ + 32;
   static constexpr int XT = 16 * XT_ROW;
-  static constexpr int GT = 16 * M16 * SZ;       // Gumbel tile (raw rows of M)
+  static constexpr int GROW = M16 * SZ + 16;     // Gumbel tile row (M used)
+  static constexpr int GT = 16 * GROW;
   static constexpr int SCR = 16 * (M16 + 1) * 4 + 64;  // dl transpose + dt
 
   static constexpr int img_bytes(int pass) {
@@ -46,29 +52,36 @@ struct Geo {
          : OFF_2;
   }
   static constexpr int wave_bytes(int pass) {
-    return pass == kDeslice || pass == kWeights ? GT
-         : pass == kSliceBwd || pass == kWeightsBwd ? XT + GT + SCR
+    return pass == kSliceBwd ? 2 * XT + GT + SCR
+         : pass == kWeightsBwd ? XT + GT + SCR
+         : pass == kDesliceBwd ? 2 * XT + GT
          : XT + GT;
   }
   // floats of one block's partial-sum record
-  static constexpr int red_floats(int pass, int M) {
+  static constexpr int red_floats(int pass) {
     return pass == kAggregate ? M16 * C + M16
          : pass == kDesliceBwd ? M16 * C
          : (pass == kSliceBwd || pass == kWeightsBwd) ? C * M16 + M16 + C + 1
          : 0;
-    (void)M;
+  }
+  // the light passes run 8 waves per block with bf16 storage (two waves per
+  // SIMD hide each other's latency); the accumulating passes, and fp32
+  // storage (whose tiles take twice the registers), run 4
+  static constexpr int max_waves(int pass) {
+    return (pass == kDeslice || pass == kWeights) && SZ == 2 ? 8 : 4;
   }
   static constexpr int waves(int pass) {
-    return (img_bytes(pass) + 4 * wave_bytes(pass) <= kLdsBytes) ? 4
+    return (max_waves(pass) >= 8 && img_bytes(pass) + 8 * wave_bytes(pass) <= kLdsBytes) ? 8
+         : (img_bytes(pass) + 4 * wave_bytes(pass) <= kLdsBytes) ? 4
          : (img_bytes(pass) + 2 * wave_bytes(pass) <= kLdsBytes) ? 2 : 1;
   }
   static constexpr int lds_bytes(int pass) {
-    return (img_bytes(pass) + waves(pass) * wave_bytes(pass)) > red_floats(pass, 0) * 4
+    return (img_bytes(pass) + waves(pass) * wave_bytes(pass)) > red_floats(pass) * 4
                ? img_bytes(pass) + waves(pass) * wave_bytes(pass)
-               : red_floats(pass, 0) * 4;
+               : red_floats(pass) * 4;
   }
   static constexpr bool fits(int pass) {
-    return img_bytes(pass) + wave_bytes(pass) <= kLdsBytes && red_floats(pass, 0) * 4 <= kLdsBytes;
+    return img_bytes(pass) + wave_bytes(pass) <= kLdsBytes && red_floats(pass) * 4 <= kLdsBytes;
   }
 };
 

@@ -1,7 +1,8 @@
 // Small kernels around the streaming passes (gfx950):
 //   - the per-call table image (logits table [A^T ; a], deslice table S'^T,
 //     backward table [dnum | S'], biases, dden) in the exact byte layout the
-//     streaming kernels copy into LDS;
+//     streaming kernels copy into LDS (rows of the logits and backward tables
+//     padded and chunk-swizzled as in pa_layout.h);
 //   - the ordered reduction of per-block partial-sum records (the partial
 //     sums of Section 4.2, here over point chunks of one GPU);
 //   - the states s_j = num_j / max(den_j, eps) (Eq. 1);
@@ -23,9 +24,9 @@ struct PrepGeo {
 static PrepGeo prep_geo(int dtype, int C, int M, int MB) {
   PrepGeo g;
   g.C = C; g.M = M; g.MB = MB; g.M16 = 16 * MB; g.SZ = dtype == 1 ? 2 : 4;
-  g.TROW = C * g.SZ + 16;
+  g.TROW = C * g.SZ + 32;
   g.SROW = g.M16 * g.SZ + 16;
-  g.WROW = 2 * C * g.SZ + 16;
+  g.WROW = 2 * C * g.SZ + 32;
   g.OFF_L = (3 * g.M16 + 2 * C) * 4;  // header: bias, dden, cN, cS, sw
   g.OFF_2 = g.OFF_L + (MB + 1) * 16 * g.TROW;
   return g;
@@ -65,7 +66,7 @@ __global__ void k_prep(PrepGeo g, PrepArgs p) {
       v = j < M ? A[(int64_t)c * M + j] : from_f<T>(0.f);
     else
       v = av ? av[c] : from_f<T>(0.f);
-    *reinterpret_cast<T*>(img + g.OFF_L + j * g.TROW + c * g.SZ) = v;
+    *reinterpret_cast<T*>(img + g.OFF_L + swz(j, c * g.SZ, g.TROW)) = v;
   }
   if (p.pass == kDeslice) {
     // S'^T: row c, column j
@@ -97,7 +98,7 @@ __global__ void k_prep(PrepGeo g, PrepArgs p) {
           v = p.Sp[j * C + (cc - C)] - hdr[2 * M16 + C + (cc - C)];
         }
       }
-      *reinterpret_cast<T*>(img + g.OFF_2 + j * g.WROW + cc * g.SZ) = from_f<T>(v);
+      *reinterpret_cast<T*>(img + g.OFF_2 + swz(j, cc * g.SZ, g.WROW)) = from_f<T>(v);
     }
   }
 }

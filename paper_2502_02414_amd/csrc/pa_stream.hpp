@@ -15,13 +15,16 @@
 // Work split: a block has WAVES wavefronts; the grid has P = num_chunks(N)
 // blocks; global wave w owns the contiguous tile range
 // [T*w/(P*WAVES), T*(w+1)/(P*WAVES)) of the T = ceil(N/16) tiles.  Each wave
-// streams its tiles independently (no block barrier inside the loop): the
-// point rows are loaded from HBM straight into MFMA operand registers, one
-// tile ahead (register double buffer); only the operand that must be read
-// transposed (x or dY with points along K) is staged in a wave-private LDS
-// tile.  Sums over points are accumulated in registers, reduced across the
-// block's waves in LDS in wave order, and written as one fp32 record per
-// block; a separate kernel adds the P records in block order.
+// streams its tiles independently (no block barrier inside the loop).  A
+// tile's rows are loaded from HBM in 16-byte chunks (1 KB contiguous per wave
+// instruction) into registers, written to a wave-private LDS tile at the top
+// of the iteration, and the next tile's loads are issued into the same
+// registers right away, so they have a whole tile of work to land.  All MFMA
+// operands are then read from LDS (16-byte row reads, or ds_read_b64_tr_b16
+// for the transposed operand of the contractions over points).  Sums over
+// points are accumulated in registers, reduced across the block's waves in
+// LDS in wave order and written as one fp32 record per block; a separate
+// kernel adds the P records in block order.
 #pragma once
 
 #include "pa_device.hpp"
@@ -50,67 +53,57 @@ struct StreamArgs {
 
 enum Flags { kHasG = 1, kStatesTerm = 2, kDesliceTerm = 4 };
 
-// ---------------------------------------------------------------------------
-// Per-wave tile I/O
-// ---------------------------------------------------------------------------
 __device__ __forceinline__ uint4 ld_global16(const void* p) {
   return *reinterpret_cast<const uint4*>(p);
 }
 
-// Rows [p0, p0+16) of a [N,C] tensor into K32 operand fragments: lane (r,g)
-// holds row p0+r, elements 32 s + 8 g .. +7 for s = 0..C/32-1.  Rows >= N
-// are zero.
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// ---------------------------------------------------------------------------
+// Point tiles: HBM -> registers -> swizzled LDS
+// ---------------------------------------------------------------------------
+// Rows [p0, p0+16) of a [N,C] tensor are 16*C*SZ contiguous bytes; lane l
+// holds 16-byte chunks q = l + 64k.  Rows >= N are zero.
 template <typename T, int C>
-__device__ __forceinline__ void load_rows(K32<T> (&f)[C / 32], const T* base, int64_t p0,
+struct TileRegs {
+  static constexpr int RCH = C * (int)sizeof(T) / 16;  // chunks per row
+  static constexpr int NCH = 16 * RCH / 64;            // chunks per lane
+  uint4 c[NCH];
+};
+
+template <typename T, int C>
+__device__ __forceinline__ void load_tile(TileRegs<T, C>& R, const T* base, int64_t p0,
                                           int64_t N) {
-  const int r = lane_id() & 15, g = lane_id() >> 4;
-  const int64_t p = p0 + r;
-  if (p < N) {
-    const T* row = base + p * C + 8 * g;
+  constexpr int RCH = TileRegs<T, C>::RCH;
+  const int lane = lane_id();
+  const char* src = reinterpret_cast<const char*>(base + p0 * C);
 #pragma unroll
-    for (int s = 0; s < C / 32; ++s) {
-      if constexpr (sizeof(T) == 2) {
-        uint4 u = ld_global16(row + 32 * s);
-        f[s].v = __builtin_bit_cast(bf16x8, u);
-      } else {
-        uint4 u0 = ld_global16(row + 32 * s);
-        uint4 u1 = ld_global16(row + 32 * s + 4);
-        f[s].lo = __builtin_bit_cast(f32x4, u0);
-        f[s].hi = __builtin_bit_cast(f32x4, u1);
-      }
-    }
-  } else {
-#pragma unroll
-    for (int s = 0; s < C / 32; ++s) {
-      if constexpr (sizeof(T) == 2) {
-        f[s].v = __builtin_bit_cast(bf16x8, uint4{0, 0, 0, 0});
-      } else {
-        f[s].lo = zero4();
-        f[s].hi = zero4();
-      }
-    }
+  for (int k = 0; k < TileRegs<T, C>::NCH; ++k) {
+    const int q = lane + 64 * k;
+    R.c[k] = (p0 + q / RCH < N) ? ld_global16(src + 16 * q) : uint4{0, 0, 0, 0};
   }
 }
 
-// Store the fragments of a tile into a wave-private LDS tile [16][XT_ROW].
 template <typename T, int C>
-__device__ __forceinline__ void store_rows_lds(char* tile, const K32<T> (&f)[C / 32]) {
-  const int r = lane_id() & 15, g = lane_id() >> 4;
-  constexpr int ROW = C * (int)sizeof(T) + 16;
-  char* row = tile + r * ROW + 8 * g * (int)sizeof(T);
+__device__ __forceinline__ void store_tile(char* tile, const TileRegs<T, C>& R) {
+  constexpr int RCH = TileRegs<T, C>::RCH;
+  constexpr int ROW = C * (int)sizeof(T) + 32;
+  const int lane = lane_id();
 #pragma unroll
-  for (int s = 0; s < C / 32; ++s) {
-    if constexpr (sizeof(T) == 2) {
-      *reinterpret_cast<bf16x8*>(row + 64 * s) = f[s].v;
-    } else {
-      *reinterpret_cast<f32x4*>(row + 128 * s) = f[s].lo;
-      *reinterpret_cast<f32x4*>(row + 128 * s + 16) = f[s].hi;
-    }
+  for (int k = 0; k < TileRegs<T, C>::NCH; ++k) {
+    const int q = lane + 64 * k;
+    const int row = q / RCH, cc = q - row * RCH;
+    *reinterpret_cast<uint4*>(tile + swz(row, 16 * cc, ROW)) = R.c[k];
   }
 }
 
 // The Gumbel rows of a tile: 16*M elements, contiguous in G.  GCH 16-byte
-// chunks per lane cover the largest tile (M = 16*MB).
+// chunks per lane cover the largest tile (M = 16*MB).  In LDS each row has
+// stride GROW = 16*MB*sz + 16 bytes (only the first M elements are used).
 template <typename T, int MB>
 struct GRegs {
   static constexpr int BYTES = 16 * 16 * MB * (int)sizeof(T);
@@ -149,20 +142,87 @@ __device__ __forceinline__ void load_g(GRegs<T, MB>& gr, const T* G, int64_t p0,
 }
 
 template <typename T, int MB>
-__device__ __forceinline__ void store_g_lds(char* gt, const GRegs<T, MB>& gr, int M) {
+__device__ __forceinline__ void store_g(char* gt, const GRegs<T, MB>& gr, int M) {
+  constexpr int SZ = (int)sizeof(T);
+  constexpr int GROW = 16 * MB * SZ + 16;
   const int lane = lane_id();
-  const int nchunk = M * (int)sizeof(T);
+  const int nchunk = M * SZ;
+  const int rch = (M * SZ) / 16;  // chunks per row when rows are 16-byte multiples
 #pragma unroll
   for (int k = 0; k < GRegs<T, MB>::GCH; ++k) {
     const int q = lane + 64 * k;
-    if (q < nchunk) *reinterpret_cast<uint4*>(gt + 16 * q) = gr.c[k];
+    if (q >= nchunk) continue;
+    if ((M * SZ) % 16 == 0) {
+      const int row = q / rch, cc = q - row * rch;
+      *reinterpret_cast<uint4*>(gt + row * GROW + 16 * cc) = gr.c[k];
+    } else {
+      const T* e = reinterpret_cast<const T*>(&gr.c[k]);
+#pragma unroll
+      for (int u = 0; u < 16 / SZ; ++u) {
+        const int el = q * (16 / SZ) + u, row = el / M, col = el - row * M;
+        *reinterpret_cast<T*>(gt + row * GROW + col * SZ) = e[u];
+      }
+    }
   }
 }
 
-__device__ __forceinline__ void wave_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+// ---------------------------------------------------------------------------
+// LDS operand reads
+// ---------------------------------------------------------------------------
+// K32 fragment of row `row`, elements [col, col+8) of a swizzled array.
+template <typename T>
+__device__ __forceinline__ void ld_k32s(K32<T>& f, const char* base, int row, int col, int RB) {
+  if constexpr (sizeof(T) == 2) {
+    f.v = *reinterpret_cast<const bf16x8*>(base + swz(row, 2 * col, RB));
+  } else {
+    f.lo = *reinterpret_cast<const f32x4*>(base + swz(row, 4 * col, RB));
+    f.hi = *reinterpret_cast<const f32x4*>(base + swz(row, 4 * col + 16, RB));
+  }
+}
+
+// Transposed K16 fragment: lane (r,g) element i = arr[row0 + 4g + i][col0 + r]
+// (row stride RB bytes; swizzled or plain).  bf16 uses ds_read_b64_tr_b16:
+// within each 16-lane group, lane 4a+e receives element e of the 8-byte
+// chunks addressed by lanes a, a+4, a+8, a+12, so lane k addresses row
+// row0 + 4g + k/4, columns col0 + 4 (k%4) .. +3.  fp32 reads the four
+// elements one by one.
+template <typename T, bool SWZ>
+__device__ __forceinline__ void ld_k16_t(K16<T>& f, const char* base, int RB, int row0,
+                                         int col0) {
+  const int r = lane_id() & 15, g = lane_id() >> 4;
+  if constexpr (sizeof(T) == 2) {
+    typedef __bf16 bf16x4v __attribute__((__vector_size__(4 * sizeof(__bf16))));
+    const int row = row0 + 4 * g + (r >> 2), bcol = (col0 + 4 * (r & 3)) * 2;
+    const char* p = base + (SWZ ? swz(row, bcol, RB) : row * RB + bcol);
+    bf16x4v v = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+        (__attribute__((address_space(3))) bf16x4v*)(p));
+    f.v = __builtin_bit_cast(bf16x4, v);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = row0 + 4 * g + i, bcol = (col0 + r) * 4;
+      f.v[i] = *reinterpret_cast<const float*>(base + (SWZ ? swz(row, bcol, RB) : row * RB + bcol));
+    }
+  }
+}
+
+// Four consecutive elements [col, col+4) of a swizzled row, as floats.
+template <typename T>
+__device__ __forceinline__ void ld4s(float (&v)[4], const char* base, int row, int col, int RB) {
+  if constexpr (sizeof(T) == 2) {
+    const bf16x4 q = *reinterpret_cast<const bf16x4*>(base + swz(row, 2 * col, RB));
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = (float)q[i];
+  } else {
+    const f32x4 q = *reinterpret_cast<const f32x4*>(base + swz(row, 4 * col, RB));
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = q[i];
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ float lds_elem(const char* base, int idx) {
+  return to_f<T>(reinterpret_cast<const T*>(base)[idx]);
 }
 
 // ---------------------------------------------------------------------------
@@ -171,15 +231,14 @@ __device__ __forceinline__ void wave_sync() {
 //                           slice 16nb+r.
 //   SP layout (SP = true):  D[slice][point]; lane (r,g) holds slice
 //                           16nb+4g+i, point r.
-// Block nb = MB is the temperature block (every row of the table is a), so
-// every lane receives x.a for its point(s).
+// bf16: block nb = MB is the temperature block (every row of the table is
+// a), so every lane receives x.a for its point(s).
 // ---------------------------------------------------------------------------
 template <typename T, int C, int MB, bool SP>
-__device__ __forceinline__ void logits(typename LAcc<T, SP>::v (&acc)[MB + 1],
-                                       const K32<T> (&xf)[C / 32], const char* tabL) {
+__device__ __forceinline__ void logits(typename LAcc<T, SP>::v (&acc)[MB + 1], const char* xt,
+                                       const char* tabL) {
   using G_ = Geo<sizeof(T), C, MB>;
   using V = typename LAcc<T, SP>::v;
-  // bf16: the temperature rides along as block MB; fp32: see temperature_own()
   constexpr int NT = sizeof(T) == 2 ? MB + 1 : MB;
   const int r = lane_id() & 15, g = lane_id() >> 4;
   const int ra = SP ? a_row<V>(r) : r;  // table row supplied by this lane
@@ -187,18 +246,15 @@ __device__ __forceinline__ void logits(typename LAcc<T, SP>::v (&acc)[MB + 1],
   for (int nb = 0; nb <= MB; ++nb) acc[nb] = zero_acc<V>();
 #pragma unroll
   for (int s = 0; s < C / 32; ++s) {
+    K32<T> xa;
+    ld_k32s<T>(xa, xt, r, 32 * s + 8 * g, G_::XT_ROW);
 #pragma unroll
     for (int nb = 0; nb < NT; ++nb) {
       K32<T> t;
-      ld_k32(t, tabL + (nb * 16 + ra) * G_::TROW + (32 * s + 8 * g) * (int)sizeof(T));
-      acc[nb] = SP ? mma_acc(t, xf[s], acc[nb]) : mma_acc(xf[s], t, acc[nb]);
+      ld_k32s<T>(t, tabL, nb * 16 + ra, 32 * s + 8 * g, G_::TROW);
+      acc[nb] = SP ? mma_acc(t, xa, acc[nb]) : mma_acc(xa, t, acc[nb]);
     }
   }
-}
-
-template <typename T>
-__device__ __forceinline__ float lds_elem(const char* base, int idx) {
-  return to_f<T>(reinterpret_cast<const T*>(base)[idx]);
 }
 
 // Unclamped temperature t = tau0 + b_t + x.a of the lane's own point (row r
@@ -208,24 +264,23 @@ __device__ __forceinline__ float lds_elem(const char* base, int idx) {
 // x.a) and the backward scales with 1/tau^2; an fp32 sum would lose about
 // 1e-5 of tau there.
 template <typename T, int C, int MB, typename V>
-__device__ __forceinline__ float temperature_own(const V (&acc)[MB + 1],
-                                                 const K32<T> (&xf)[C / 32], const char* tabL,
-                                                 double tb) {
+__device__ __forceinline__ float temperature_own(const V (&acc)[MB + 1], const char* xt,
+                                                 const char* tabL, double tb) {
   using G_ = Geo<sizeof(T), C, MB>;
   if constexpr (sizeof(T) == 2) {
-    // SP layout: every element of block MB holds x_r . a
     return (float)((double)acc[MB][0] + tb);
   } else {
-    const int g = lane_id() >> 4;
-    const float* arow = reinterpret_cast<const float*>(tabL + (16 * MB) * G_::TROW);
+    const int r = lane_id() & 15, g = lane_id() >> 4;
     double s = 0.0;
 #pragma unroll
     for (int q = 0; q < C / 32; ++q) {
-      const float* av = arow + 32 * q + 8 * g;
+      K32<float> xa, av;
+      ld_k32s<float>(xa, xt, r, 32 * q + 8 * g, G_::XT_ROW);
+      ld_k32s<float>(av, tabL, 16 * MB, 32 * q + 8 * g, G_::TROW);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        s = fma((double)xf[q].lo[e], (double)av[e], s);
-        s = fma((double)xf[q].hi[e], (double)av[4 + e], s);
+        s = fma((double)xa.lo[e], (double)av.lo[e], s);
+        s = fma((double)xa.hi[e], (double)av.hi[e], s);
       }
     }
     s = s + __shfl_xor(s, 16);
@@ -236,14 +291,13 @@ __device__ __forceinline__ float temperature_own(const V (&acc)[MB + 1],
 
 // PS layout: temperatures of points 4g+i (i = 0..3).
 template <typename T, int C, int MB, typename V>
-__device__ __forceinline__ void temperature_ps(const V (&acc)[MB + 1],
-                                               const K32<T> (&xf)[C / 32], const char* tabL,
-                                               double tb, float (&t)[4]) {
+__device__ __forceinline__ void temperature_ps(const V (&acc)[MB + 1], const char* xt,
+                                               const char* tabL, double tb, float (&t)[4]) {
   if constexpr (sizeof(T) == 2) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) t[i] = (float)((double)acc[MB][i] + tb);
   } else {
-    const float own = temperature_own<T, C, MB, V>(acc, xf, tabL, tb);
+    const float own = temperature_own<T, C, MB, V>(acc, xt, tabL, tb);
     const int g = lane_id() >> 4;
 #pragma unroll
     for (int i = 0; i < 4; ++i) t[i] = __shfl(own, 4 * g + i);
@@ -254,23 +308,28 @@ __device__ __forceinline__ void temperature_ps(const V (&acc)[MB + 1],
 // row maximum; the base-2 exponent zs = (u - m) log2(e) / tau is formed
 // after the shift, so its error is relative to u - m (not to u / tau, which
 // is large when tau is clamped); w = 2^zs / sum.  Invalid slices (j >= M)
-// and points beyond N get w = 0.
+// and points beyond N get w = 0.  The Gumbel values are read transposed
+// from the padded G tile (rows 4g+i, column 16nb+r).
 template <typename T, int MB, typename V>
-__device__ __forceinline__ void softmax_ps(const V (&acc)[MB + 1],
-                                           const char* gt, const float (&bias)[MB], int M,
-                                           bool hasG, const float (&t)[4], float tau_min,
-                                           int nvalid, float (&w)[MB][4], float (&tau)[4]) {
+__device__ __forceinline__ void softmax_ps(const V (&acc)[MB + 1], const char* gt,
+                                           const float (&bias)[MB], int M, bool hasG,
+                                           const float (&t)[4], float tau_min, int nvalid,
+                                           float (&w)[MB][4], float (&tau)[4]) {
   using R = decltype(acc[0][0] + 0.f);
+  constexpr int GROW = 16 * MB * (int)sizeof(T) + 16;
   const int r = lane_id() & 15, g = lane_id() >> 4;
   R u[MB][4];
 #pragma unroll
   for (int nb = 0; nb < MB; ++nb) {
     const int j = 16 * nb + r;
     const bool valid = j < M;
+    K16<T> gv;
+    if (hasG)
+      ld_k16_t<T, false>(gv, gt, GROW, 0, 16 * nb);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const float gv = (hasG && valid) ? lds_elem<T>(gt, (4 * g + i) * M + j) : 0.f;
-      u[nb][i] = valid ? (R)acc[nb][i] + (R)bias[nb] + (R)gv : (R)-INFINITY;
+      const float gg = (hasG && valid) ? k16_elem(gv, i) : 0.f;
+      u[nb][i] = valid ? (R)acc[nb][i] + (R)bias[nb] + (R)gg : (R)-INFINITY;
     }
   }
 #pragma unroll
@@ -297,13 +356,16 @@ __device__ __forceinline__ void softmax_ps(const V (&acc)[MB + 1],
 
 // Softmax over slices, SP layout (the lane's point is r).  Also returns the
 // shifted base-2 exponents zs (the natural logit is zs ln 2 + const) for
-// the temperature gradient.
+// the temperature gradient.  The Gumbel values are four consecutive
+// elements of row r of the G tile.
 template <typename T, int MB, typename V>
-__device__ __forceinline__ void softmax_sp(const V (&acc)[MB + 1],
-                                           const char* gt, const float (&bias)[MB][4], int M,
-                                           bool hasG, float t, float tau_min, int nvalid,
-                                           float (&w)[MB][4], float (&zs)[MB][4], float& tau) {
+__device__ __forceinline__ void softmax_sp(const V (&acc)[MB + 1], const char* gt,
+                                           const float (&bias)[MB][4], int M, bool hasG, float t,
+                                           float tau_min, int nvalid, float (&w)[MB][4],
+                                           float (&zs)[MB][4], float& tau) {
   using R = decltype(acc[0][0] + 0.f);
+  constexpr int SZ = (int)sizeof(T);
+  constexpr int GROW = 16 * MB * SZ + 16;
   const int r = lane_id() & 15, g = lane_id() >> 4;
   tau = fmaxf(t, tau_min);
   const R k = (R)(kLog2e / tau);
@@ -311,12 +373,24 @@ __device__ __forceinline__ void softmax_sp(const V (&acc)[MB + 1],
   float m = -INFINITY;
 #pragma unroll
   for (int nb = 0; nb < MB; ++nb) {
+    float gv[4] = {0.f, 0.f, 0.f, 0.f};
+    if (hasG) {
+      const char* p = gt + r * GROW + (16 * nb + 4 * g) * SZ;
+      if constexpr (SZ == 2) {
+        const bf16x4 q = *reinterpret_cast<const bf16x4*>(p);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) gv[i] = (float)q[i];
+      } else {
+        const f32x4 q = *reinterpret_cast<const f32x4*>(p);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) gv[i] = q[i];
+      }
+    }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int j = 16 * nb + 4 * g + i;
       const bool valid = j < M;
-      const float gv = (hasG && valid) ? lds_elem<T>(gt, r * M + j) : 0.f;
-      u[nb][i] = valid ? (R)acc[nb][i] + (R)bias[nb][i] + (R)gv : (R)-INFINITY;
+      u[nb][i] = valid ? (R)acc[nb][i] + (R)bias[nb][i] + (R)gv[i] : (R)-INFINITY;
       m = fmaxf(m, (float)u[nb][i]);
     }
   }
@@ -340,50 +414,6 @@ __device__ __forceinline__ void softmax_sp(const V (&acc)[MB + 1],
     for (int i = 0; i < 4; ++i) w[nb][i] = pv ? e[nb][i] * inv : 0.f;
 }
 
-// Transposed K16 fragment of a row-major LDS array with row stride ROW
-// bytes: lane (r,g) element i = arr[row0 + 4g + i][col0 + r].  bf16 uses
-// ds_read_b64_tr_b16: within each 16-lane group, lane 4a+e receives element
-// e of the 8-byte chunks addressed by lanes a, a+4, a+8, a+12, so lane k
-// addresses row row0 + 4g + k/4, columns col0 + 4 (k%4) .. +3.  fp32 reads
-// the four elements one by one.
-template <typename T>
-__device__ __forceinline__ void ld_k16_t(K16<T>& f, const char* base, int ROW, int row0,
-                                         int col0) {
-  const int r = lane_id() & 15, g = lane_id() >> 4;
-  if constexpr (sizeof(T) == 2) {
-    typedef __bf16 bf16x4v __attribute__((__vector_size__(4 * sizeof(__bf16))));
-    const char* p = base + (row0 + 4 * g + (r >> 2)) * ROW + (col0 + 4 * (r & 3)) * 2;
-    bf16x4v v = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-        (__attribute__((address_space(3))) bf16x4v*)(p));
-    f.v = __builtin_bit_cast(bf16x4, v);
-  } else {
-    const char* p = base + (row0 + 4 * g) * ROW + (col0 + r) * 4;
-    f.v[0] = *reinterpret_cast<const float*>(p);
-    f.v[1] = *reinterpret_cast<const float*>(p + ROW);
-    f.v[2] = *reinterpret_cast<const float*>(p + 2 * ROW);
-    f.v[3] = *reinterpret_cast<const float*>(p + 3 * ROW);
-  }
-}
-
-// Tile loop with a register ping-pong: the loads of tile t+1 are issued into
-// one register set while tile t is processed from the other, so a tile's
-// loads have a whole tile of work to land (no register copies, which the
-// compiler would wait on early).
-template <typename Regs, typename Load, typename Proc>
-__device__ __forceinline__ void stream_tiles(int64_t t0, int64_t t1, Load&& load, Proc&& proc) {
-  if (t0 >= t1) return;
-  Regs A, B;
-  load(A, t0);
-  for (int64_t t = t0;;) {
-    if (t + 1 < t1) load(B, t + 1);
-    proc(A, t);
-    if (++t >= t1) break;
-    if (t + 1 < t1) load(A, t + 1);
-    proc(B, t);
-    if (++t >= t1) break;
-  }
-}
-
 // Copy the table image from global memory into LDS (all threads).
 __device__ __forceinline__ void copy_image(char* lds, const void* img, int bytes) {
   const uint4* src = reinterpret_cast<const uint4*>(img);
@@ -400,7 +430,7 @@ __device__ __forceinline__ void tile_range(int64_t N, int waves, int64_t& t0, in
 }
 
 // Ordered (wave 0, 1, ...) sum of per-wave register partials into an LDS
-// region; `put(region, first)` writes (first) or adds this wave's values.
+// region; `put(first)` writes (first) or adds this wave's values.
 template <typename Put>
 __device__ __forceinline__ void block_ordered_reduce(int waves, Put put) {
   const int wave = threadIdx.x >> 6;
@@ -411,10 +441,11 @@ __device__ __forceinline__ void block_ordered_reduce(int waves, Put put) {
 }
 
 // ---------------------------------------------------------------------------
-// kAggregate and kDesliceBwd (PS layout): W^T [x | dY] per block.
+// kAggregate and kDesliceBwd (PS layout): W^T x (with den) or W^T dY.
 // ---------------------------------------------------------------------------
 template <typename T, int C, int MB, bool BWD>
-__global__ void __launch_bounds__(256) k_aggregate(StreamArgs a) {
+__global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(BWD ? kDesliceBwd : kAggregate)))
+k_aggregate(StreamArgs a) {
   using G_ = Geo<sizeof(T), C, MB>;
   constexpr int PASS = BWD ? kDesliceBwd : kAggregate;
   constexpr int WAVES = G_::waves(PASS);
@@ -426,8 +457,9 @@ __global__ void __launch_bounds__(256) k_aggregate(StreamArgs a) {
   __syncthreads();
   const char* tabL = smem + G_::OFF_L;
   char* wreg = smem + G_::img_bytes(PASS) + wave * G_::wave_bytes(PASS);
-  char* xt = wreg;                 // transposed-operand tile (x or dY)
-  char* gt = wreg + G_::XT;        // Gumbel rows
+  char* xt = wreg;                          // x tile (logits)
+  char* yt = BWD ? wreg + G_::XT : wreg;    // tile contracted over points
+  char* gt = wreg + (BWD ? 2 : 1) * G_::XT; // Gumbel rows
 
   float bias[MB];
 #pragma unroll
@@ -448,37 +480,31 @@ __global__ void __launch_bounds__(256) k_aggregate(StreamArgs a) {
   int64_t t0, t1;
   tile_range(a.N, WAVES, t0, t1);
 
-  // One register set per stream; the next tile's loads are issued into it
-  // right after its last use in this tile, so they land while the rest of
-  // the tile is computed.
-  K32<T> xr[G_::XF], yr[G_::XF];
+  TileRegs<T, C> xr, yr;
   GRegs<T, MB> gr;
   if (t0 < t1) {
-    load_rows<T, C>(xr, X, t0 * 16, a.N);
-    if constexpr (BWD) load_rows<T, C>(yr, Y, t0 * 16, a.N);
+    load_tile<T, C>(xr, X, t0 * 16, a.N);
+    if constexpr (BWD) load_tile<T, C>(yr, Y, t0 * 16, a.N);
     load_g<T, MB>(gr, Gp, t0 * 16, a.N, a.M, hasG);
   }
   for (int64_t t = t0; t < t1; ++t) {
     const int64_t p0 = t * 16;
-    const bool more = t + 1 < t1;
     const int nvalid = (int)(a.N - p0 < 16 ? a.N - p0 : 16);
     wave_sync();
-    if constexpr (BWD)
-      store_rows_lds<T, C>(xt, yr);
-    else
-      store_rows_lds<T, C>(xt, xr);
-    store_g_lds<T, MB>(gt, gr, a.M);
+    store_tile<T, C>(xt, xr);
+    if constexpr (BWD) store_tile<T, C>(yt, yr);
+    store_g<T, MB>(gt, gr, a.M);
     wave_sync();
-    if (more) {
+    if (t + 1 < t1) {
+      load_tile<T, C>(xr, X, p0 + 16, a.N);
+      if constexpr (BWD) load_tile<T, C>(yr, Y, p0 + 16, a.N);
       load_g<T, MB>(gr, Gp, p0 + 16, a.N, a.M, hasG);
-      if constexpr (BWD) load_rows<T, C>(yr, Y, p0 + 16, a.N);
     }
 
     typename LAcc<T, false>::v lg[MB + 1];
-    logits<T, C, MB, false>(lg, xr, tabL);
+    logits<T, C, MB, false>(lg, xt, tabL);
     float w[MB][4], tau[4], tt[4];
-    temperature_ps<T, C, MB>(lg, xr, tabL, a.tb, tt);
-    if (more) load_rows<T, C>(xr, X, p0 + 16, a.N);
+    temperature_ps<T, C, MB>(lg, xt, tabL, a.tb, tt);
     softmax_ps<T, MB>(lg, gt, bias, a.M, hasG, tt, a.tau_min, nvalid, w, tau);
 
     K16<T> wt[MB];
@@ -492,7 +518,7 @@ __global__ void __launch_bounds__(256) k_aggregate(StreamArgs a) {
 #pragma unroll
     for (int cb = 0; cb < G_::CB; ++cb) {
       K16<T> xb;
-      ld_k16_t<T>(xb, xt, G_::XT_ROW, 0, 16 * cb);
+      ld_k16_t<T, true>(xb, yt, G_::XT_ROW, 0, 16 * cb);
 #pragma unroll
       for (int nb = 0; nb < MB; ++nb) acc[nb][cb] = mma16(wt[nb], xb, acc[nb][cb]);
     }
@@ -532,7 +558,7 @@ __global__ void __launch_bounds__(256) k_aggregate(StreamArgs a) {
 // kDeslice (SP layout): y = W S'.
 // ---------------------------------------------------------------------------
 template <typename T, int C, int MB>
-__global__ void __launch_bounds__(256) k_deslice(StreamArgs a) {
+__global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kDeslice))) k_deslice(StreamArgs a) {
   using G_ = Geo<sizeof(T), C, MB>;
   constexpr int WAVES = G_::waves(kDeslice);
   extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -543,7 +569,8 @@ __global__ void __launch_bounds__(256) k_deslice(StreamArgs a) {
   __syncthreads();
   const char* tabL = smem + G_::OFF_L;
   const char* tabS = smem + G_::OFF_2;
-  char* gt = smem + G_::img_bytes(kDeslice) + wave * G_::wave_bytes(kDeslice);
+  char* xt = smem + G_::img_bytes(kDeslice) + wave * G_::wave_bytes(kDeslice);
+  char* gt = xt + G_::XT;
 
   float bias[MB][4];
 #pragma unroll
@@ -558,26 +585,28 @@ __global__ void __launch_bounds__(256) k_deslice(StreamArgs a) {
   int64_t t0, t1;
   tile_range(a.N, WAVES, t0, t1);
 
-  K32<T> xr[G_::XF];
+  TileRegs<T, C> xr;
   GRegs<T, MB> gr;
   if (t0 < t1) {
-    load_rows<T, C>(xr, X, t0 * 16, a.N);
+    load_tile<T, C>(xr, X, t0 * 16, a.N);
     load_g<T, MB>(gr, Gp, t0 * 16, a.N, a.M, hasG);
   }
   for (int64_t t = t0; t < t1; ++t) {
     const int64_t p0 = t * 16;
-    const bool more = t + 1 < t1;
     const int nvalid = (int)(a.N - p0 < 16 ? a.N - p0 : 16);
     wave_sync();
-    store_g_lds<T, MB>(gt, gr, a.M);
+    store_tile<T, C>(xt, xr);
+    store_g<T, MB>(gt, gr, a.M);
     wave_sync();
-    if (more) load_g<T, MB>(gr, Gp, p0 + 16, a.N, a.M, hasG);
+    if (t + 1 < t1) {
+      load_tile<T, C>(xr, X, p0 + 16, a.N);
+      load_g<T, MB>(gr, Gp, p0 + 16, a.N, a.M, hasG);
+    }
 
     typename LAcc<T, true>::v lg[MB + 1];
-    logits<T, C, MB, true>(lg, xr, tabL);
+    logits<T, C, MB, true>(lg, xt, tabL);
     float w[MB][4], zs[MB][4], tau;
-    const float tt = temperature_own<T, C, MB>(lg, xr, tabL, a.tb);
-    if (more) load_rows<T, C>(xr, X, p0 + 16, a.N);
+    const float tt = temperature_own<T, C, MB>(lg, xt, tabL, a.tb);
     softmax_sp<T, MB>(lg, gt, bias, a.M, hasG, tt, a.tau_min, nvalid, w, zs, tau);
 
     K16<T> wb[MB];
@@ -611,7 +640,7 @@ __global__ void __launch_bounds__(256) k_deslice(StreamArgs a) {
 // kWeights (PS layout): W [N,M] fp32 and tau [N] written out.
 // ---------------------------------------------------------------------------
 template <typename T, int C, int MB>
-__global__ void __launch_bounds__(256) k_weights(StreamArgs a) {
+__global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kWeights))) k_weights(StreamArgs a) {
   using G_ = Geo<sizeof(T), C, MB>;
   constexpr int WAVES = G_::waves(kWeights);
   extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -621,7 +650,8 @@ __global__ void __launch_bounds__(256) k_weights(StreamArgs a) {
   copy_image(smem, a.img, G_::img_bytes(kWeights));
   __syncthreads();
   const char* tabL = smem + G_::OFF_L;
-  char* gt = smem + G_::img_bytes(kWeights) + wave * G_::wave_bytes(kWeights);
+  char* xt = smem + G_::img_bytes(kWeights) + wave * G_::wave_bytes(kWeights);
+  char* gt = xt + G_::XT;
   float bias[MB];
 #pragma unroll
   for (int nb = 0; nb < MB; ++nb) bias[nb] = reinterpret_cast<const float*>(smem)[16 * nb + r];
@@ -631,24 +661,21 @@ __global__ void __launch_bounds__(256) k_weights(StreamArgs a) {
   float* W = reinterpret_cast<float*>(a.out);
   int64_t t0, t1;
   tile_range(a.N, WAVES, t0, t1);
-  struct Regs {
-    K32<T> x[G_::XF];
-    GRegs<T, MB> g;
-  };
-  auto load = [&](Regs& R, int64_t t) {
-    load_rows<T, C>(R.x, X, t * 16, a.N);
-    load_g<T, MB>(R.g, Gp, t * 16, a.N, a.M, hasG);
-  };
-  auto proc = [&](Regs& R, int64_t t) {
+  TileRegs<T, C> xr;
+  GRegs<T, MB> gr;
+  for (int64_t t = t0; t < t1; ++t) {
     const int64_t p0 = t * 16;
+    load_tile<T, C>(xr, X, p0, a.N);
+    load_g<T, MB>(gr, Gp, p0, a.N, a.M, hasG);
     const int nvalid = (int)(a.N - p0 < 16 ? a.N - p0 : 16);
     wave_sync();
-    store_g_lds<T, MB>(gt, R.g, a.M);
+    store_tile<T, C>(xt, xr);
+    store_g<T, MB>(gt, gr, a.M);
     wave_sync();
     typename LAcc<T, false>::v lg[MB + 1];
-    logits<T, C, MB, false>(lg, R.x, tabL);
+    logits<T, C, MB, false>(lg, xt, tabL);
     float w[MB][4], tau[4], tt[4];
-    temperature_ps<T, C, MB>(lg, R.x, tabL, a.tb, tt);
+    temperature_ps<T, C, MB>(lg, xt, tabL, a.tb, tt);
     softmax_ps<T, MB>(lg, gt, bias, a.M, hasG, tt, a.tau_min, nvalid, w, tau);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -662,8 +689,7 @@ __global__ void __launch_bounds__(256) k_weights(StreamArgs a) {
         if (r == 0 && a.tau_out) a.tau_out[p0 + p] = tau[i];
       }
     }
-  };
-  stream_tiles<Regs>(t0, t1, load, proc);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -673,9 +699,12 @@ __global__ void __launch_bounds__(256) k_weights(StreamArgs a) {
 //   dl   = dz / tau;  dtau = dtau_in - <dz, z> / tau;  dt = dtau if t > tau_min
 //   dx   = W dnum + A dl + a dt   (W dnum only with the states term)
 //   dA  += x^T dl,  db += 1^T dl,  da += x^T dt,  db_t += 1^T dt
+// The backward table rows hold dnum_j - cN and s'_j - cS (a shift common to
+// all slices, which the softmax backward does not see); the header's dden is
+// centred here by its den-weighted mean cD.
 // ---------------------------------------------------------------------------
 template <typename T, int C, int MB, int PASS>
-__global__ void __launch_bounds__(256) k_slice_bwd(StreamArgs a) {
+__global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_slice_bwd(StreamArgs a) {
   using G_ = Geo<sizeof(T), C, MB>;
   constexpr int WAVES = G_::waves(PASS);
   constexpr int M16 = G_::M16;
@@ -688,20 +717,22 @@ __global__ void __launch_bounds__(256) k_slice_bwd(StreamArgs a) {
 
   copy_image(smem, a.img, G_::img_bytes(PASS));
   __syncthreads();
-  const float* dden_tab = reinterpret_cast<const float*>(smem) + M16;
-  const float* cN = reinterpret_cast<const float*>(smem) + 2 * M16;
+  const float* hdr = reinterpret_cast<const float*>(smem);
+  const float* dden_tab = hdr + M16;
+  const float* cN = hdr + 2 * M16;
   const char* tabL = smem + G_::OFF_L;
   const char* tabW = smem + G_::OFF_2;
   char* wreg = smem + G_::img_bytes(PASS) + wave * G_::wave_bytes(PASS);
   char* xt = wreg;
-  char* gt = wreg + G_::XT;
-  float* scr = reinterpret_cast<float*>(wreg + G_::XT + G_::GT);  // [16][M16+1]
-  float* scr_dt = scr + 16 * SROWF;                                // [16]
+  char* yt = wreg + G_::XT;  // dY tile (kSliceBwd only)
+  char* gt = wreg + (PASS == kSliceBwd ? 2 : 1) * G_::XT;
+  float* scr = reinterpret_cast<float*>(gt + G_::GT);  // [16][M16+1]
+  float* scr_dt = scr + 16 * SROWF;                     // [16]
 
   // dden_j centred by its den-weighted mean (a shift common to all slices)
   float cD = 0.f;
   {
-    const float* sw = reinterpret_cast<const float*>(smem) + 2 * M16 + 2 * C;
+    const float* sw = hdr + 2 * M16 + 2 * C;
     for (int j = 0; j < a.M; ++j) cD += sw[j] * dden_tab[j];
   }
   float bias[MB][4], dden[MB][4];
@@ -710,7 +741,7 @@ __global__ void __launch_bounds__(256) k_slice_bwd(StreamArgs a) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int j = 16 * nb + 4 * g + i;
-      bias[nb][i] = reinterpret_cast<const float*>(smem)[j];
+      bias[nb][i] = hdr[j];
       dden[nb][i] = j < a.M ? dden_tab[j] - cD : 0.f;
     }
 
@@ -734,28 +765,32 @@ __global__ void __launch_bounds__(256) k_slice_bwd(StreamArgs a) {
   int64_t t0, t1;
   tile_range(a.N, WAVES, t0, t1);
 
-  K32<T> xc[G_::XF], yc[G_::XF];
+  TileRegs<T, C> xr, yr;
   GRegs<T, MB> gr;
   if (t0 < t1) {
-    load_rows<T, C>(xc, X, t0 * 16, a.N);
-    if (deslice) load_rows<T, C>(yc, Y, t0 * 16, a.N);
+    load_tile<T, C>(xr, X, t0 * 16, a.N);
+    if (deslice) load_tile<T, C>(yr, Y, t0 * 16, a.N);
     load_g<T, MB>(gr, Gp, t0 * 16, a.N, a.M, hasG);
   }
   for (int64_t t = t0; t < t1; ++t) {
     const int64_t p0 = t * 16;
-    const bool more = t + 1 < t1;
     const int nvalid = (int)(a.N - p0 < 16 ? a.N - p0 : 16);
     const bool pv = r < nvalid;
     wave_sync();
-    store_rows_lds<T, C>(xt, xc);
-    store_g_lds<T, MB>(gt, gr, a.M);
+    store_tile<T, C>(xt, xr);
+    if (deslice) store_tile<T, C>(yt, yr);
+    store_g<T, MB>(gt, gr, a.M);
     wave_sync();
-    if (more) load_g<T, MB>(gr, Gp, p0 + 16, a.N, a.M, hasG);
+    if (t + 1 < t1) {
+      load_tile<T, C>(xr, X, p0 + 16, a.N);
+      if (deslice) load_tile<T, C>(yr, Y, p0 + 16, a.N);
+      load_g<T, MB>(gr, Gp, p0 + 16, a.N, a.M, hasG);
+    }
 
     typename LAcc<T, true>::v lg[MB + 1];
-    logits<T, C, MB, true>(lg, xc, tabL);
+    logits<T, C, MB, true>(lg, xt, tabL);
     float w[MB][4], zs[MB][4], tau;
-    const float tt = temperature_own<T, C, MB>(lg, xc, tabL, a.tb);
+    const float tt = temperature_own<T, C, MB>(lg, xt, tabL, a.tb);
     softmax_sp<T, MB>(lg, gt, bias, a.M, hasG, tt, a.tau_min, nvalid, w, zs, tau);
 
     // dw in the SP layout
@@ -768,23 +803,29 @@ __global__ void __launch_bounds__(256) k_slice_bwd(StreamArgs a) {
       for (int nb = 0; nb < MB; ++nb) acc[nb] = zero_acc<V>();
       if (states) {
 #pragma unroll
-        for (int s = 0; s < G_::XF; ++s)
+        for (int s = 0; s < G_::XF; ++s) {
+          K32<T> xa;
+          ld_k32s<T>(xa, xt, r, 32 * s + 8 * g, G_::XT_ROW);
 #pragma unroll
           for (int nb = 0; nb < MB; ++nb) {
             K32<T> tw;
-            ld_k32(tw, tabW + (16 * nb + ra) * G_::WROW + (32 * s + 8 * g) * (int)sizeof(T));
-            acc[nb] = mma_acc(tw, xc[s], acc[nb]);
+            ld_k32s<T>(tw, tabW, 16 * nb + ra, 32 * s + 8 * g, G_::WROW);
+            acc[nb] = mma_acc(tw, xa, acc[nb]);
           }
+        }
       }
       if (deslice) {
 #pragma unroll
-        for (int s = 0; s < G_::XF; ++s)
+        for (int s = 0; s < G_::XF; ++s) {
+          K32<T> ya;
+          ld_k32s<T>(ya, yt, r, 32 * s + 8 * g, G_::XT_ROW);
 #pragma unroll
           for (int nb = 0; nb < MB; ++nb) {
             K32<T> tw;
-            ld_k32(tw, tabW + (16 * nb + ra) * G_::WROW + (C + 32 * s + 8 * g) * (int)sizeof(T));
-            acc[nb] = mma_acc(tw, yc[s], acc[nb]);
+            ld_k32s<T>(tw, tabW, 16 * nb + ra, C + 32 * s + 8 * g, G_::WROW);
+            acc[nb] = mma_acc(tw, ya, acc[nb]);
           }
+        }
       }
 #pragma unroll
       for (int nb = 0; nb < MB; ++nb)
@@ -798,11 +839,6 @@ __global__ void __launch_bounds__(256) k_slice_bwd(StreamArgs a) {
           const int j = 16 * nb + 4 * g + i;
           dw[nb][i] = (pv && j < a.M) ? a.dW[(p0 + r) * a.M + j] : 0.f;
         }
-    }
-
-    if (more) {  // x and dY registers are free from here on
-      load_rows<T, C>(xc, X, p0 + 16, a.N);
-      if (deslice) load_rows<T, C>(yc, Y, p0 + 16, a.N);
     }
 
     // softmax backward, dz = w (dw - <w, dw>), with <w, dw> compensated by a
@@ -838,7 +874,7 @@ __global__ void __launch_bounds__(256) k_slice_bwd(StreamArgs a) {
     if (PASS == kWeightsBwd && a.dtau != nullptr && pv) dtau += a.dtau[p0 + r];
     const float dt = (pv && tt > a.tau_min) ? dtau : 0.f;
 
-    // dx = [W | dl] [dnum ; A^T] + a dt   (SP: D[channel][point])
+    // dx = [W | dl] [dnum - cN ; A^T] + a dt + cN   (SP: D[channel][point])
     K16<T> wb[MB], lb[MB];
 #pragma unroll
     for (int nb = 0; nb < MB; ++nb) {
@@ -851,23 +887,25 @@ __global__ void __launch_bounds__(256) k_slice_bwd(StreamArgs a) {
       f32x4 d = zero4();
 #pragma unroll
       for (int nb = 0; nb < MB; ++nb) {
-        // A^T rows of the logits table read transposed: [channel][slice]
-        K16<T> ta;
-        ld_k16_t<T>(ta, tabL, G_::TROW, 16 * nb, 16 * cb);
+        K16<T> ta;  // A^T rows of the logits table, read transposed
+        ld_k16_t<T, true>(ta, tabL, G_::TROW, 16 * nb, 16 * cb);
         d = mma16(ta, lb[nb], d);
         if (states) {
           K16<T> tn;  // (dnum_j - cN) rows of the backward table, transposed
-          ld_k16_t<T>(tn, tabW, G_::WROW, 16 * nb, 16 * cb);
+          ld_k16_t<T, true>(tn, tabW, G_::WROW, 16 * nb, 16 * cb);
           d = mma16(tn, wb[nb], d);
         }
       }
       // + a dt (a is any row of the temperature block of the logits table),
       // + cN: the table rows hold dnum_j - cN, and sum_j w_j = 1
-      const char* arow = tabL + (MB * 16) * G_::TROW + (16 * cb + 4 * g) * (int)sizeof(T);
+      float av[4];
+      ld4s<T>(av, tabL, 16 * MB, 16 * cb + 4 * g, G_::TROW);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        d[i] += lds_elem<T>(arow, i) * dt;
-        if (states) d[i] += cN[16 * cb + 4 * g + i];
+      for (int i = 0; i < 4; ++i) d[i] += av[i] * dt;
+      if (states) {
+        const f32x4 cn = *reinterpret_cast<const f32x4*>(cN + 16 * cb + 4 * g);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) d[i] += cn[i];
       }
       if (pv) {
         if constexpr (sizeof(T) == 2) {
@@ -904,13 +942,12 @@ __global__ void __launch_bounds__(256) k_slice_bwd(StreamArgs a) {
 #pragma unroll
     for (int cb = 0; cb < G_::CB; ++cb) {
       K16<T> xa;
-      ld_k16_t<T>(xa, xt, G_::XT_ROW, 0, 16 * cb);
+      ld_k16_t<T, true>(xa, xt, G_::XT_ROW, 0, 16 * cb);
       da[cb] += (k16_elem(xa, 0) * dtp[0] + k16_elem(xa, 1) * dtp[1]) +
                 (k16_elem(xa, 2) * dtp[2] + k16_elem(xa, 3) * dtp[3]);
 #pragma unroll
       for (int nb = 0; nb < MB; ++nb) dA[cb][nb] = mma16(xa, lp[nb], dA[cb][nb]);
     }
-    wave_sync();
   }
 
   // lane partials -> wave totals
