@@ -23,19 +23,19 @@ constexpr int kPartialsMax = 256;      // blocks (point chunks) per streaming pa
 template <int SZ, int C, int MB>
 struct Geo {
   static constexpr int M16 = 16 * MB;            // slices padded to 16
-  static constexpr int NB = MB + 1;              // + one temperature block
   static constexpr int XF = C / 32;              // K32 fragments per point row
   static constexpr int CB = C / 16;              // 16-channel blocks
   // table image (bytes); every region starts on a 16-byte boundary
   static constexpr int TROW = C * SZ + 32;       // logits table row: A[:,j] or a
   static constexpr int SROW = M16 * SZ + 16;     // deslice table row: s'[:,c]
   static constexpr int WROW = 2 * C * SZ + 32;   // dw table row: (dnum_j | s'_j)
-  // header (fp32): bias[M16], dden[M16], cN[C], cS[C], sw[M16]: cN and cS are
-  // the den-weighted means over slices of dnum_j and s'_j that the backward
-  // table rows are centred by; sw_j = den_j / sum den are those weights
-  static constexpr int HDR = (3 * M16 + 2 * C) * 4;
+  // header (fp32): bias[M16], dden[M16], cN[C], cS[C], sw[M16], a[C]: cN and
+  // cS are the den-weighted means over slices of dnum_j and s'_j that the
+  // backward table rows are centred by; sw_j = den_j / sum den are those
+  // weights; a is the temperature projection in fp32
+  static constexpr int HDR = (3 * M16 + 3 * C) * 4;
   static constexpr int OFF_L = HDR;
-  static constexpr int SZ_L = NB * 16 * TROW;
+  static constexpr int SZ_L = (M16 + 1) * TROW;  // rows: A[:, j] (j < M16), then a
   static constexpr int OFF_2 = OFF_L + SZ_L;     // second table (S or W)
   static constexpr int SZ_S = C * SROW;
   static constexpr int SZ_W = M16 * WROW;
@@ -51,9 +51,9 @@ struct Geo {
          : (pass == kSliceBwd || pass == kWeightsBwd) ? OFF_2 + SZ_W
          : OFF_2;
   }
+  // per wave: x tile, (dY tile or output staging), Gumbel rows, scratch
   static constexpr int wave_bytes(int pass) {
-    return pass == kSliceBwd ? 2 * XT + GT + SCR
-         : pass == kWeightsBwd ? XT + GT + SCR
+    return (pass == kSliceBwd || pass == kWeightsBwd) ? 2 * XT + GT + SCR
          : pass == kDesliceBwd ? 2 * XT + GT
          : XT + GT;
   }

@@ -27,8 +27,8 @@ static PrepGeo prep_geo(int dtype, int C, int M, int MB) {
   g.TROW = C * g.SZ + 32;
   g.SROW = g.M16 * g.SZ + 16;
   g.WROW = 2 * C * g.SZ + 32;
-  g.OFF_L = (3 * g.M16 + 2 * C) * 4;  // header: bias, dden, cN, cS, sw
-  g.OFF_2 = g.OFF_L + (MB + 1) * 16 * g.TROW;
+  g.OFF_L = (3 * g.M16 + 3 * C) * 4;  // header: bias, dden, cN, cS, sw, a
+  g.OFF_2 = g.OFF_L + (g.M16 + 1) * g.TROW;
   return g;
 }
 
@@ -56,8 +56,9 @@ __global__ void k_prep(PrepGeo g, PrepArgs p) {
   for (int64_t j = tid; j < M16; j += nth) hdr[j] = (j < M && p.b) ? p.b[j] : 0.f;
   if (p.pass != kSliceBwd)
     for (int64_t k = tid; k < 2 * M16 + 2 * C; k += nth) hdr[M16 + k] = 0.f;
-  // logits table: rows j < M16: A[:, j] (0 beyond M); rows M16..M16+15: a
-  const int64_t nL = (int64_t)(M16 + 16) * C;
+  for (int64_t c = tid; c < C; c += nth) hdr[3 * M16 + 2 * C + c] = av ? to_f<T>(av[c]) : 0.f;
+  // logits table: rows j < M16: A[:, j] (0 beyond M); row M16: a
+  const int64_t nL = (int64_t)(M16 + 1) * C;
 #pragma unroll 4
   for (int64_t k = tid; k < nL; k += nth) {
     const int j = (int)(k / C), c = (int)(k - (int64_t)j * C);

@@ -2,7 +2,7 @@
 //
 // Every pass recomputes the slice weights of a 16-point tile on chip:
 //   logits  l = x A + b  and  t = tau0 + b_t + x.a   (one MFMA contraction
-//           over C against the table [A^T ; a a ... a], Eq. 3 and Eq. 4)
+//           over C against the table [A^T ; a], Eq. 3 and Eq. 4)
 //   w       = softmax_j((l + g) / max(t, tau_min))    (Eq. 4, in registers)
 // and then does its own contraction:
 //   kAggregate   num = W^T x, den = 1^T W        (Eq. 1; Section 4.2 partials)
@@ -21,10 +21,13 @@
 // of the iteration, and the next tile's loads are issued into the same
 // registers right away, so they have a whole tile of work to land.  All MFMA
 // operands are then read from LDS (16-byte row reads, or ds_read_b64_tr_b16
-// for the transposed operand of the contractions over points).  Sums over
-// points are accumulated in registers, reduced across the block's waves in
-// LDS in wave order and written as one fp32 record per block; a separate
-// kernel adds the P records in block order.
+// for the transposed operand of the contractions over points); each
+// contraction issues its LDS reads ahead of the MFMAs that consume them.
+// Point outputs (y, dx) are staged in LDS and written back as whole rows, the
+// same 1 KB-per-instruction pattern as the loads.  Sums over points are
+// accumulated in registers, reduced across the block's waves in LDS in wave
+// order and written as one fp32 record per block; a separate kernel adds the
+// P records in block order.
 #pragma once
 
 #include "pa_device.hpp"
@@ -63,11 +66,106 @@ __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Software pipeline over N unrolled steps: the LDS reads of step i + D - 1
+// are issued before the MFMAs of step i (the scheduling barrier keeps the
+// compiler from sinking them back next to their use).
+template <int N, int D, typename F, typename Load, typename Use>
+__device__ __forceinline__ void pipelined(Load load, Use use) {
+  F buf[D];
+#pragma unroll
+  for (int i = 0; i < D - 1; ++i)
+    if (i < N) load(i, buf[i]);
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    if (i + D - 1 < N) load(i + D - 1, buf[(i + D - 1) % D]);
+    __builtin_amdgcn_sched_barrier(0);
+    use(i, buf[i % D]);
+  }
+}
+
 // ---------------------------------------------------------------------------
-// Point tiles: HBM -> registers -> swizzled LDS
+// LDS addressing.  Tables and point tiles have rows padded by 32 bytes and
+// their 16-byte chunks swizzled (chunk ^ bit 3 of the row, swz() in
+// pa_device.hpp).  Every fragment read below is a per-lane base, computed
+// once per kernel, plus a compile-time offset.
 // ---------------------------------------------------------------------------
+// K32 row fragment of lane (r, g): elements [col + 8g, col + 8g + 8) of row
+// row0 + lr (row0 % 16 == 0, col % 32 == 0), at offset row0 * RB + col * sz.
+template <typename T> struct RowBase { int lo, hi; };
+template <typename T>
+__device__ __forceinline__ RowBase<T> row_base(int lr, int RB) {
+  const int g = lane_id() >> 4, b = (lr >> 3) & 1;
+  if constexpr (sizeof(T) == 2) {
+    return {lr * RB + 16 * (g ^ b), 0};
+  } else {
+    return {lr * RB + 32 * g + 16 * b, lr * RB + 32 * g + 16 - 16 * b};
+  }
+}
+template <typename T>
+__device__ __forceinline__ void ld_row(K32<T>& f, const char* a, const RowBase<T>& o, int off) {
+  if constexpr (sizeof(T) == 2) {
+    f.v = *reinterpret_cast<const bf16x8*>(a + o.lo + off);
+  } else {
+    f.lo = *reinterpret_cast<const f32x4*>(a + o.lo + off);
+    f.hi = *reinterpret_cast<const f32x4*>(a + o.hi + off);
+  }
+}
+
+// Transposed K16 fragment: lane (r, g) element i = arr[row0 + 4g + i][col0 + r]
+// at offset row0 * RB + col0 * sz (row0, col0 % 16 == 0).  bf16 uses
+// ds_read_b64_tr_b16: within each 16-lane group, lane 4a+e receives element
+// e of the 8-byte chunks addressed by lanes a, a+4, a+8, a+12, so lane k
+// addresses row 4g + k/4, columns 4 (k%4) .. +3.  fp32 reads four elements.
+template <typename T, bool SWZ>
+__device__ __forceinline__ int tr_base(int RB) {
+  const int r = lane_id() & 15, g = lane_id() >> 4;
+  const int b = SWZ ? (g >> 1) : 0;  // bit 3 of the row
+  if constexpr (sizeof(T) == 2) {
+    return (4 * g + (r >> 2)) * RB + 16 * (((r >> 1) & 1) ^ b) + 8 * (r & 1);
+  } else {
+    return 4 * g * RB + 16 * ((r >> 2) ^ b) + 4 * (r & 3);
+  }
+}
+template <typename T>
+__device__ __forceinline__ void ld_tr(K16<T>& f, const char* a, int base, int off, int RB) {
+  if constexpr (sizeof(T) == 2) {
+    typedef __bf16 v4 __attribute__((__vector_size__(4 * sizeof(__bf16))));
+    v4 v = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+        (__attribute__((address_space(3))) v4*)(a + base + off));
+    f.v = __builtin_bit_cast(bf16x4, v);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) f.v[i] = *reinterpret_cast<const float*>(a + base + off + i * RB);
+  }
+}
+
+// SP-layout output fragment (lane (r, g): channels [c0 + 4g, +4) of point r)
+// into a swizzled tile, at offset c0 * sz (c0 % 16 == 0).
+template <typename T>
+__device__ __forceinline__ int stage_base(int RB) {
+  const int r = lane_id() & 15, g = lane_id() >> 4, b = (r >> 3) & 1;
+  if constexpr (sizeof(T) == 2) {
+    return r * RB + 16 * ((g >> 1) ^ b) + 8 * (g & 1);
+  } else {
+    return r * RB + 16 * (g ^ b);
+  }
+}
+template <typename T>
+__device__ __forceinline__ void stage4(char* tile, int base, int off, const f32x4& d) {
+  if constexpr (sizeof(T) == 2) {
+    bf16x4 o;
+    o[0] = (bf16)d[0]; o[1] = (bf16)d[1]; o[2] = (bf16)d[2]; o[3] = (bf16)d[3];
+    *reinterpret_cast<bf16x4*>(tile + base + off) = o;
+  } else {
+    *reinterpret_cast<f32x4*>(tile + base + off) = d;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Point tiles: HBM -> registers -> swizzled LDS, and staged outputs back.
 // Rows [p0, p0+16) of a [N,C] tensor are 16*C*SZ contiguous bytes; lane l
 // holds 16-byte chunks q = l + 64k.  Rows >= N are zero.
+// ---------------------------------------------------------------------------
 template <typename T, int C>
 struct TileRegs {
   static constexpr int RCH = C * (int)sizeof(T) / 16;  // chunks per row
@@ -80,11 +178,19 @@ __device__ __forceinline__ void load_tile(TileRegs<T, C>& R, const T* base, int6
                                           int64_t N) {
   constexpr int RCH = TileRegs<T, C>::RCH;
   const int lane = lane_id();
+  // uniform 64-bit row address + 32-bit lane offset (scalar-base addressing)
   const char* src = reinterpret_cast<const char*>(base + p0 * C);
+  if (p0 + 16 <= N) {
 #pragma unroll
-  for (int k = 0; k < TileRegs<T, C>::NCH; ++k) {
-    const int q = lane + 64 * k;
-    R.c[k] = (p0 + q / RCH < N) ? ld_global16(src + 16 * q) : uint4{0, 0, 0, 0};
+    for (int k = 0; k < TileRegs<T, C>::NCH; ++k)
+      R.c[k] = ld_global16(src + (uint32_t)(16 * lane + 1024 * k));
+  } else {
+#pragma unroll
+    for (int k = 0; k < TileRegs<T, C>::NCH; ++k) {
+      const int row = (lane + 64 * k) / RCH;
+      R.c[k] = (p0 + row < N) ? ld_global16(src + (uint32_t)(16 * lane + 1024 * k))
+                              : uint4{0, 0, 0, 0};
+    }
   }
 }
 
@@ -101,6 +207,23 @@ __device__ __forceinline__ void store_tile(char* tile, const TileRegs<T, C>& R) 
   }
 }
 
+// Staged output tile (swizzled LDS) -> rows [p0, p0 + nvalid) of dst.
+template <typename T, int C>
+__device__ __forceinline__ void write_tile(T* dst, int64_t p0, const char* tile, int nvalid) {
+  constexpr int RCH = TileRegs<T, C>::RCH;
+  constexpr int NCH = TileRegs<T, C>::NCH;
+  constexpr int ROW = C * (int)sizeof(T) + 32;
+  const int lane = lane_id();
+  char* d = reinterpret_cast<char*>(dst + p0 * C);
+#pragma unroll
+  for (int k = 0; k < NCH; ++k) {
+    const int q = lane + 64 * k;
+    const int row = q / RCH, cc = q - row * RCH;
+    const uint4 v = *reinterpret_cast<const uint4*>(tile + swz(row, 16 * cc, ROW));
+    if (row < nvalid) *reinterpret_cast<uint4*>(d + (uint32_t)(16 * lane + 1024 * k)) = v;
+  }
+}
+
 // The Gumbel rows of a tile: 16*M elements, contiguous in G.  GCH 16-byte
 // chunks per lane cover the largest tile (M = 16*MB).  In LDS each row has
 // stride GROW = 16*MB*sz + 16 bytes (only the first M elements are used).
@@ -114,35 +237,36 @@ struct GRegs {
 template <typename T, int MB>
 __device__ __forceinline__ void load_g(GRegs<T, MB>& gr, const T* G, int64_t p0, int64_t N,
                                        int M, bool hasG) {
+  if (!hasG) return;
   const int lane = lane_id();
   const int nchunk = M * (int)sizeof(T);  // (16 rows * M * sz) / 16
-  const int64_t nvalid = N - p0 < 16 ? N - p0 : 16;
   const char* base = reinterpret_cast<const char*>(G + p0 * M);
+  if (p0 + 16 <= N) {
 #pragma unroll
-  for (int k = 0; k < GRegs<T, MB>::GCH; ++k) {
-    const int q = lane + 64 * k;
-    uint4 v{0, 0, 0, 0};
-    if (hasG && q < nchunk) {
-      if (nvalid == 16) {
-        v = ld_global16(base + 16 * q);
-      } else {
-        // tail tile: element-wise, only elements of valid rows
-        const int64_t nel = nvalid * M;
-        const T* e = reinterpret_cast<const T*>(base + 16 * q);
-        const int64_t e0 = (int64_t)q * 16 / (int)sizeof(T);
-        T tmp[16 / sizeof(T)];
-#pragma unroll
-        for (int u = 0; u < (int)(16 / sizeof(T)); ++u)
-          tmp[u] = (e0 + u < nel) ? e[u] : from_f<T>(0.f);
-        v = *reinterpret_cast<uint4*>(tmp);
-      }
+    for (int k = 0; k < GRegs<T, MB>::GCH; ++k) {
+      const int q = lane + 64 * k;
+      gr.c[k] = q < nchunk ? ld_global16(base + (uint32_t)(16 * q)) : uint4{0, 0, 0, 0};
     }
-    gr.c[k] = v;
+  } else {
+    // tail tile: element-wise, only elements of valid rows
+    const int64_t nel = (N - p0) * M;
+#pragma unroll
+    for (int k = 0; k < GRegs<T, MB>::GCH; ++k) {
+      const int q = lane + 64 * k;
+      const T* e = reinterpret_cast<const T*>(base + 16 * q);
+      const int64_t e0 = (int64_t)q * 16 / (int)sizeof(T);
+      T tmp[16 / sizeof(T)];
+#pragma unroll
+      for (int u = 0; u < (int)(16 / sizeof(T)); ++u)
+        tmp[u] = (q < nchunk && e0 + u < nel) ? e[u] : from_f<T>(0.f);
+      gr.c[k] = *reinterpret_cast<uint4*>(tmp);
+    }
   }
 }
 
 template <typename T, int MB>
-__device__ __forceinline__ void store_g(char* gt, const GRegs<T, MB>& gr, int M) {
+__device__ __forceinline__ void store_g(char* gt, const GRegs<T, MB>& gr, int M, bool hasG) {
+  if (!hasG) return;
   constexpr int SZ = (int)sizeof(T);
   constexpr int GROW = 16 * MB * SZ + 16;
   const int lane = lane_id();
@@ -167,94 +291,56 @@ __device__ __forceinline__ void store_g(char* gt, const GRegs<T, MB>& gr, int M)
 }
 
 // ---------------------------------------------------------------------------
-// LDS operand reads
-// ---------------------------------------------------------------------------
-// K32 fragment of row `row`, elements [col, col+8) of a swizzled array.
-template <typename T>
-__device__ __forceinline__ void ld_k32s(K32<T>& f, const char* base, int row, int col, int RB) {
-  if constexpr (sizeof(T) == 2) {
-    f.v = *reinterpret_cast<const bf16x8*>(base + swz(row, 2 * col, RB));
-  } else {
-    f.lo = *reinterpret_cast<const f32x4*>(base + swz(row, 4 * col, RB));
-    f.hi = *reinterpret_cast<const f32x4*>(base + swz(row, 4 * col + 16, RB));
-  }
-}
-
-// Transposed K16 fragment: lane (r,g) element i = arr[row0 + 4g + i][col0 + r]
-// (row stride RB bytes; swizzled or plain).  bf16 uses ds_read_b64_tr_b16:
-// within each 16-lane group, lane 4a+e receives element e of the 8-byte
-// chunks addressed by lanes a, a+4, a+8, a+12, so lane k addresses row
-// row0 + 4g + k/4, columns col0 + 4 (k%4) .. +3.  fp32 reads the four
-// elements one by one.
-template <typename T, bool SWZ>
-__device__ __forceinline__ void ld_k16_t(K16<T>& f, const char* base, int RB, int row0,
-                                         int col0) {
-  const int r = lane_id() & 15, g = lane_id() >> 4;
-  if constexpr (sizeof(T) == 2) {
-    typedef __bf16 bf16x4v __attribute__((__vector_size__(4 * sizeof(__bf16))));
-    const int row = row0 + 4 * g + (r >> 2), bcol = (col0 + 4 * (r & 3)) * 2;
-    const char* p = base + (SWZ ? swz(row, bcol, RB) : row * RB + bcol);
-    bf16x4v v = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-        (__attribute__((address_space(3))) bf16x4v*)(p));
-    f.v = __builtin_bit_cast(bf16x4, v);
-  } else {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int row = row0 + 4 * g + i, bcol = (col0 + r) * 4;
-      f.v[i] = *reinterpret_cast<const float*>(base + (SWZ ? swz(row, bcol, RB) : row * RB + bcol));
-    }
-  }
-}
-
-// Four consecutive elements [col, col+4) of a swizzled row, as floats.
-template <typename T>
-__device__ __forceinline__ void ld4s(float (&v)[4], const char* base, int row, int col, int RB) {
-  if constexpr (sizeof(T) == 2) {
-    const bf16x4 q = *reinterpret_cast<const bf16x4*>(base + swz(row, 2 * col, RB));
-#pragma unroll
-    for (int i = 0; i < 4; ++i) v[i] = (float)q[i];
-  } else {
-    const f32x4 q = *reinterpret_cast<const f32x4*>(base + swz(row, 4 * col, RB));
-#pragma unroll
-    for (int i = 0; i < 4; ++i) v[i] = q[i];
-  }
-}
-
-template <typename T>
-__device__ __forceinline__ float lds_elem(const char* base, int idx) {
-  return to_f<T>(reinterpret_cast<const T*>(base)[idx]);
-}
-
-// ---------------------------------------------------------------------------
 // Logits and temperature: one contraction over C against the logits table.
 //   PS layout (SP = false): D[point][slice]; lane (r,g) holds point 4g+i,
 //                           slice 16nb+r.
 //   SP layout (SP = true):  D[slice][point]; lane (r,g) holds slice
 //                           16nb+4g+i, point r.
-// bf16: block nb = MB is the temperature block (every row of the table is
-// a), so every lane receives x.a for its point(s).
+// bf16: block nb = MB is the temperature block (every lane reads the single
+// table row a), so every lane receives x.a for its point(s).  The point
+// fragments xa are returned for reuse (the dw contraction of the backward).
 // ---------------------------------------------------------------------------
+template <typename T, int C, int MB>
+struct LogitsBases {
+  RowBase<T> x, t, a;
+};
 template <typename T, int C, int MB, bool SP>
-__device__ __forceinline__ void logits(typename LAcc<T, SP>::v (&acc)[MB + 1], const char* xt,
-                                       const char* tabL) {
+__device__ __forceinline__ LogitsBases<T, C, MB> logits_bases() {
+  using G_ = Geo<sizeof(T), C, MB>;
+  using V = typename LAcc<T, SP>::v;
+  const int r = lane_id() & 15;
+  return {row_base<T>(r, G_::XT_ROW), row_base<T>(SP ? a_row<V>(r) : r, G_::TROW),
+          row_base<T>(0, G_::TROW)};
+}
+
+template <typename T, int C, int MB, bool SP>
+__device__ __forceinline__ void logits(typename LAcc<T, SP>::v (&acc)[MB + 1],
+                                       K32<T> (&xa)[C / 32], const char* xt, const char* tabL,
+                                       const LogitsBases<T, C, MB>& lb) {
   using G_ = Geo<sizeof(T), C, MB>;
   using V = typename LAcc<T, SP>::v;
   constexpr int NT = sizeof(T) == 2 ? MB + 1 : MB;
-  const int r = lane_id() & 15, g = lane_id() >> 4;
-  const int ra = SP ? a_row<V>(r) : r;  // table row supplied by this lane
+  constexpr int SZ = (int)sizeof(T);
 #pragma unroll
   for (int nb = 0; nb <= MB; ++nb) acc[nb] = zero_acc<V>();
 #pragma unroll
-  for (int s = 0; s < C / 32; ++s) {
-    K32<T> xa;
-    ld_k32s<T>(xa, xt, r, 32 * s + 8 * g, G_::XT_ROW);
+  for (int s = 0; s < C / 32; ++s) ld_row<T>(xa[s], xt, lb.x, 32 * s * SZ);
+  struct F { K32<T> t[NT]; };
+  pipelined<C / 32, 2, F>(
+      [&](int s, F& f) {
 #pragma unroll
-    for (int nb = 0; nb < NT; ++nb) {
-      K32<T> t;
-      ld_k32s<T>(t, tabL, nb * 16 + ra, 32 * s + 8 * g, G_::TROW);
-      acc[nb] = SP ? mma_acc(t, xa, acc[nb]) : mma_acc(xa, t, acc[nb]);
-    }
-  }
+        for (int nb = 0; nb < NT; ++nb) {
+          if (nb < MB)
+            ld_row<T>(f.t[nb], tabL, lb.t, 16 * nb * G_::TROW + 32 * s * SZ);
+          else
+            ld_row<T>(f.t[nb], tabL, lb.a, G_::M16 * G_::TROW + 32 * s * SZ);
+        }
+      },
+      [&](int s, F& f) {
+#pragma unroll
+        for (int nb = 0; nb < NT; ++nb)
+          acc[nb] = SP ? mma_acc(f.t[nb], xa[s], acc[nb]) : mma_acc(xa[s], f.t[nb], acc[nb]);
+      });
 }
 
 // Unclamped temperature t = tau0 + b_t + x.a of the lane's own point (row r
@@ -264,23 +350,22 @@ __device__ __forceinline__ void logits(typename LAcc<T, SP>::v (&acc)[MB + 1], c
 // x.a) and the backward scales with 1/tau^2; an fp32 sum would lose about
 // 1e-5 of tau there.
 template <typename T, int C, int MB, typename V>
-__device__ __forceinline__ float temperature_own(const V (&acc)[MB + 1], const char* xt,
-                                                 const char* tabL, double tb) {
+__device__ __forceinline__ float temperature_own(const V (&acc)[MB + 1], const K32<T> (&xa)[C / 32],
+                                                 const char* tabL, const RowBase<T>& ab,
+                                                 double tb) {
   using G_ = Geo<sizeof(T), C, MB>;
   if constexpr (sizeof(T) == 2) {
-    return (float)((double)acc[MB][0] + tb);
+    return (float)acc[MB][0] + (float)tb;
   } else {
-    const int r = lane_id() & 15, g = lane_id() >> 4;
     double s = 0.0;
 #pragma unroll
     for (int q = 0; q < C / 32; ++q) {
-      K32<float> xa, av;
-      ld_k32s<float>(xa, xt, r, 32 * q + 8 * g, G_::XT_ROW);
-      ld_k32s<float>(av, tabL, 16 * MB, 32 * q + 8 * g, G_::TROW);
+      K32<float> av;
+      ld_row<float>(av, tabL, ab, G_::M16 * G_::TROW + 32 * q * 4);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        s = fma((double)xa.lo[e], (double)av.lo[e], s);
-        s = fma((double)xa.hi[e], (double)av.hi[e], s);
+        s = fma((double)xa[q].lo[e], (double)av.lo[e], s);
+        s = fma((double)xa[q].hi[e], (double)av.hi[e], s);
       }
     }
     s = s + __shfl_xor(s, 16);
@@ -291,13 +376,14 @@ __device__ __forceinline__ float temperature_own(const V (&acc)[MB + 1], const c
 
 // PS layout: temperatures of points 4g+i (i = 0..3).
 template <typename T, int C, int MB, typename V>
-__device__ __forceinline__ void temperature_ps(const V (&acc)[MB + 1], const char* xt,
-                                               const char* tabL, double tb, float (&t)[4]) {
+__device__ __forceinline__ void temperature_ps(const V (&acc)[MB + 1], const K32<T> (&xa)[C / 32],
+                                               const char* tabL, const RowBase<T>& ab, double tb,
+                                               float (&t)[4]) {
   if constexpr (sizeof(T) == 2) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) t[i] = (float)((double)acc[MB][i] + tb);
+    for (int i = 0; i < 4; ++i) t[i] = (float)acc[MB][i] + (float)tb;
   } else {
-    const float own = temperature_own<T, C, MB, V>(acc, xt, tabL, tb);
+    const float own = temperature_own<T, C, MB, V>(acc, xa, tabL, ab, tb);
     const int g = lane_id() >> 4;
 #pragma unroll
     for (int i = 0; i < 4; ++i) t[i] = __shfl(own, 4 * g + i);
@@ -311,7 +397,7 @@ __device__ __forceinline__ void temperature_ps(const V (&acc)[MB + 1], const cha
 // and points beyond N get w = 0.  The Gumbel values are read transposed
 // from the padded G tile (rows 4g+i, column 16nb+r).
 template <typename T, int MB, typename V>
-__device__ __forceinline__ void softmax_ps(const V (&acc)[MB + 1], const char* gt,
+__device__ __forceinline__ void softmax_ps(const V (&acc)[MB + 1], const char* gt, int gtr,
                                            const float (&bias)[MB], int M, bool hasG,
                                            const float (&t)[4], float tau_min, int nvalid,
                                            float (&w)[MB][4], float (&tau)[4]) {
@@ -324,8 +410,7 @@ __device__ __forceinline__ void softmax_ps(const V (&acc)[MB + 1], const char* g
     const int j = 16 * nb + r;
     const bool valid = j < M;
     K16<T> gv;
-    if (hasG)
-      ld_k16_t<T, false>(gv, gt, GROW, 0, 16 * nb);
+    if (hasG) ld_tr<T>(gv, gt, gtr, 16 * nb * (int)sizeof(T), GROW);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const float gg = (hasG && valid) ? k16_elem(gv, i) : 0.f;
@@ -335,7 +420,7 @@ __device__ __forceinline__ void softmax_ps(const V (&acc)[MB + 1], const char* g
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     tau[i] = fmaxf(t[i], tau_min);
-    const R k = (R)(kLog2e / tau[i]);
+    const R k = (R)(kLog2e * fast_rcp(tau[i]));
     float m = (float)u[0][i];
 #pragma unroll
     for (int nb = 1; nb < MB; ++nb) m = fmaxf(m, (float)u[nb][i]);
@@ -347,7 +432,7 @@ __device__ __forceinline__ void softmax_ps(const V (&acc)[MB + 1], const char* g
       s += e[nb];
     }
     s = row16_sum(s);
-    const float inv = 1.0f / s;
+    const float inv = fast_rcp(s);
     const bool pv = (4 * g + i) < nvalid;
 #pragma unroll
     for (int nb = 0; nb < MB; ++nb) w[nb][i] = pv ? e[nb] * inv : 0.f;
@@ -368,7 +453,7 @@ __device__ __forceinline__ void softmax_sp(const V (&acc)[MB + 1], const char* g
   constexpr int GROW = 16 * MB * SZ + 16;
   const int r = lane_id() & 15, g = lane_id() >> 4;
   tau = fmaxf(t, tau_min);
-  const R k = (R)(kLog2e / tau);
+  const R k = (R)(kLog2e * fast_rcp(tau));
   R u[MB][4];
   float m = -INFINITY;
 #pragma unroll
@@ -406,7 +491,7 @@ __device__ __forceinline__ void softmax_sp(const V (&acc)[MB + 1], const char* g
       s += e[nb][i];
     }
   s = groups_sum(s);
-  const float inv = 1.0f / s;
+  const float inv = fast_rcp(s);
   const bool pv = r < nvalid;
 #pragma unroll
   for (int nb = 0; nb < MB; ++nb)
@@ -421,10 +506,12 @@ __device__ __forceinline__ void copy_image(char* lds, const void* img, int bytes
   for (int q = threadIdx.x; q < bytes / 16; q += blockDim.x) dst[q] = src[q];
 }
 
-__device__ __forceinline__ void tile_range(int64_t N, int waves, int64_t& t0, int64_t& t1) {
+// (wave: the wave's index in its block, uniform, so the range is scalar)
+__device__ __forceinline__ void tile_range(int64_t N, int waves, int wave, int64_t& t0,
+                                           int64_t& t1) {
   const int64_t tiles = (N + 15) / 16;
   const int64_t tw = (int64_t)gridDim.x * waves;
-  const int64_t gw = (int64_t)blockIdx.x * waves + (threadIdx.x >> 6);
+  const int64_t gw = (int64_t)blockIdx.x * waves + wave;
   t0 = tiles * gw / tw;
   t1 = tiles * (gw + 1) / tw;
 }
@@ -449,8 +536,10 @@ k_aggregate(StreamArgs a) {
   using G_ = Geo<sizeof(T), C, MB>;
   constexpr int PASS = BWD ? kDesliceBwd : kAggregate;
   constexpr int WAVES = G_::waves(PASS);
+  constexpr int SZ = (int)sizeof(T);
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  const int wave = threadIdx.x >> 6, r = lane_id() & 15, g = lane_id() >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int r = lane_id() & 15, g = lane_id() >> 4;
   const bool hasG = a.flags & kHasG;
 
   copy_image(smem, a.img, G_::img_bytes(PASS));
@@ -460,6 +549,9 @@ k_aggregate(StreamArgs a) {
   char* xt = wreg;                          // x tile (logits)
   char* yt = BWD ? wreg + G_::XT : wreg;    // tile contracted over points
   char* gt = wreg + (BWD ? 2 : 1) * G_::XT; // Gumbel rows
+  const auto lb = logits_bases<T, C, MB, false>();
+  const int xtr = tr_base<T, true>(G_::XT_ROW);
+  const int gtr = tr_base<T, false>(G_::GROW);
 
   float bias[MB];
 #pragma unroll
@@ -478,7 +570,7 @@ k_aggregate(StreamArgs a) {
   const T* Y = reinterpret_cast<const T*>(a.dY);
   const T* Gp = reinterpret_cast<const T*>(a.G);
   int64_t t0, t1;
-  tile_range(a.N, WAVES, t0, t1);
+  tile_range(a.N, WAVES, wave, t0, t1);
 
   TileRegs<T, C> xr, yr;
   GRegs<T, MB> gr;
@@ -493,7 +585,7 @@ k_aggregate(StreamArgs a) {
     wave_sync();
     store_tile<T, C>(xt, xr);
     if constexpr (BWD) store_tile<T, C>(yt, yr);
-    store_g<T, MB>(gt, gr, a.M);
+    store_g<T, MB>(gt, gr, a.M, hasG);
     wave_sync();
     if (t + 1 < t1) {
       load_tile<T, C>(xr, X, p0 + 16, a.N);
@@ -502,10 +594,11 @@ k_aggregate(StreamArgs a) {
     }
 
     typename LAcc<T, false>::v lg[MB + 1];
-    logits<T, C, MB, false>(lg, xt, tabL);
+    K32<T> xa[G_::XF];
+    logits<T, C, MB, false>(lg, xa, xt, tabL, lb);
     float w[MB][4], tau[4], tt[4];
-    temperature_ps<T, C, MB>(lg, xt, tabL, a.tb, tt);
-    softmax_ps<T, MB>(lg, gt, bias, a.M, hasG, tt, a.tau_min, nvalid, w, tau);
+    temperature_ps<T, C, MB>(lg, xa, tabL, lb.a, a.tb, tt);
+    softmax_ps<T, MB>(lg, gt, gtr, bias, a.M, hasG, tt, a.tau_min, nvalid, w, tau);
 
     K16<T> wt[MB];
 #pragma unroll
@@ -515,13 +608,13 @@ k_aggregate(StreamArgs a) {
         den[nb] += (k16_elem(wt[nb], 0) + k16_elem(wt[nb], 1)) +
                    (k16_elem(wt[nb], 2) + k16_elem(wt[nb], 3));
     }
+    struct F { K16<T> xb; };
+    pipelined<G_::CB, 8, F>(
+        [&](int cb, F& f) { ld_tr<T>(f.xb, yt, xtr, 16 * cb * SZ, G_::XT_ROW); },
+        [&](int cb, F& f) {
 #pragma unroll
-    for (int cb = 0; cb < G_::CB; ++cb) {
-      K16<T> xb;
-      ld_k16_t<T, true>(xb, yt, G_::XT_ROW, 0, 16 * cb);
-#pragma unroll
-      for (int nb = 0; nb < MB; ++nb) acc[nb][cb] = mma16(wt[nb], xb, acc[nb][cb]);
-    }
+          for (int nb = 0; nb < MB; ++nb) acc[nb][cb] = mma16(wt[nb], f.xb, acc[nb][cb]);
+        });
   }
 
   // den: lane (r,g) holds slice 16nb+r summed over its points -> sum groups
@@ -555,14 +648,17 @@ k_aggregate(StreamArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// kDeslice (SP layout): y = W S'.
+// kDeslice (SP layout): y = W S'.  The y tile is staged in the x tile, which
+// the logits are done with, and written back as whole rows.
 // ---------------------------------------------------------------------------
 template <typename T, int C, int MB>
 __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kDeslice))) k_deslice(StreamArgs a) {
   using G_ = Geo<sizeof(T), C, MB>;
   constexpr int WAVES = G_::waves(kDeslice);
+  constexpr int SZ = (int)sizeof(T);
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  const int wave = threadIdx.x >> 6, r = lane_id() & 15, g = lane_id() >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int r = lane_id() & 15, g = lane_id() >> 4;
   const bool hasG = a.flags & kHasG;
 
   copy_image(smem, a.img, G_::img_bytes(kDeslice));
@@ -571,6 +667,9 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kDeslice)))
   const char* tabS = smem + G_::OFF_2;
   char* xt = smem + G_::img_bytes(kDeslice) + wave * G_::wave_bytes(kDeslice);
   char* gt = xt + G_::XT;
+  const auto lb = logits_bases<T, C, MB, true>();
+  const int sb = r * G_::SROW + 4 * g * SZ;  // S'^T row 16cb + r, slices 16nb + 4g ..
+  const int stb = stage_base<T>(G_::XT_ROW);
 
   float bias[MB][4];
 #pragma unroll
@@ -583,7 +682,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kDeslice)))
   const T* Gp = reinterpret_cast<const T*>(a.G);
   T* Y = reinterpret_cast<T*>(a.out);
   int64_t t0, t1;
-  tile_range(a.N, WAVES, t0, t1);
+  tile_range(a.N, WAVES, wave, t0, t1);
 
   TileRegs<T, C> xr;
   GRegs<T, MB> gr;
@@ -596,7 +695,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kDeslice)))
     const int nvalid = (int)(a.N - p0 < 16 ? a.N - p0 : 16);
     wave_sync();
     store_tile<T, C>(xt, xr);
-    store_g<T, MB>(gt, gr, a.M);
+    store_g<T, MB>(gt, gr, a.M, hasG);
     wave_sync();
     if (t + 1 < t1) {
       load_tile<T, C>(xr, X, p0 + 16, a.N);
@@ -604,35 +703,30 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kDeslice)))
     }
 
     typename LAcc<T, true>::v lg[MB + 1];
-    logits<T, C, MB, true>(lg, xt, tabL);
+    K32<T> xa[G_::XF];
+    logits<T, C, MB, true>(lg, xa, xt, tabL, lb);
     float w[MB][4], zs[MB][4], tau;
-    const float tt = temperature_own<T, C, MB>(lg, xt, tabL, a.tb);
+    const float tt = temperature_own<T, C, MB>(lg, xa, tabL, lb.a, a.tb);
     softmax_sp<T, MB>(lg, gt, bias, a.M, hasG, tt, a.tau_min, nvalid, w, zs, tau);
 
     K16<T> wb[MB];
 #pragma unroll
     for (int nb = 0; nb < MB; ++nb) set_k16(wb[nb], w[nb][0], w[nb][1], w[nb][2], w[nb][3]);
-    const bool pv = r < nvalid;
-    T* yrow = Y + (p0 + r) * C + 4 * g;
+    wave_sync();  // the logits reads of the x tile are done: it becomes the y tile
+    struct F { K16<T> s[MB]; };
+    pipelined<G_::CB, 4, F>(
+        [&](int cb, F& f) {
 #pragma unroll
-    for (int cb = 0; cb < G_::CB; ++cb) {
-      f32x4 d = zero4();
+          for (int nb = 0; nb < MB; ++nb) ld_k16(f.s[nb], tabS + sb + 16 * cb * G_::SROW + 16 * nb * SZ);
+        },
+        [&](int cb, F& f) {
+          f32x4 d = zero4();
 #pragma unroll
-      for (int nb = 0; nb < MB; ++nb) {
-        K16<T> sa;
-        ld_k16(sa, tabS + (16 * cb + r) * G_::SROW + (16 * nb + 4 * g) * (int)sizeof(T));
-        d = mma16(sa, wb[nb], d);
-      }
-      if (pv) {
-        if constexpr (sizeof(T) == 2) {
-          bf16x4 o;
-          o[0] = (bf16)d[0]; o[1] = (bf16)d[1]; o[2] = (bf16)d[2]; o[3] = (bf16)d[3];
-          *reinterpret_cast<bf16x4*>(yrow + 16 * cb) = o;
-        } else {
-          *reinterpret_cast<f32x4*>(yrow + 16 * cb) = d;
-        }
-      }
-    }
+          for (int nb = 0; nb < MB; ++nb) d = mma16(f.s[nb], wb[nb], d);
+          stage4<T>(xt, stb, 16 * cb * SZ, d);
+        });
+    wave_sync();
+    write_tile<T, C>(Y, p0, xt, nvalid);
   }
 }
 
@@ -644,7 +738,8 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kWeights)))
   using G_ = Geo<sizeof(T), C, MB>;
   constexpr int WAVES = G_::waves(kWeights);
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  const int wave = threadIdx.x >> 6, r = lane_id() & 15, g = lane_id() >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int r = lane_id() & 15, g = lane_id() >> 4;
   const bool hasG = a.flags & kHasG;
 
   copy_image(smem, a.img, G_::img_bytes(kWeights));
@@ -652,6 +747,8 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kWeights)))
   const char* tabL = smem + G_::OFF_L;
   char* xt = smem + G_::img_bytes(kWeights) + wave * G_::wave_bytes(kWeights);
   char* gt = xt + G_::XT;
+  const auto lb = logits_bases<T, C, MB, false>();
+  const int gtr = tr_base<T, false>(G_::GROW);
   float bias[MB];
 #pragma unroll
   for (int nb = 0; nb < MB; ++nb) bias[nb] = reinterpret_cast<const float*>(smem)[16 * nb + r];
@@ -660,7 +757,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kWeights)))
   const T* Gp = reinterpret_cast<const T*>(a.G);
   float* W = reinterpret_cast<float*>(a.out);
   int64_t t0, t1;
-  tile_range(a.N, WAVES, t0, t1);
+  tile_range(a.N, WAVES, wave, t0, t1);
   TileRegs<T, C> xr;
   GRegs<T, MB> gr;
   for (int64_t t = t0; t < t1; ++t) {
@@ -670,13 +767,14 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kWeights)))
     const int nvalid = (int)(a.N - p0 < 16 ? a.N - p0 : 16);
     wave_sync();
     store_tile<T, C>(xt, xr);
-    store_g<T, MB>(gt, gr, a.M);
+    store_g<T, MB>(gt, gr, a.M, hasG);
     wave_sync();
     typename LAcc<T, false>::v lg[MB + 1];
-    logits<T, C, MB, false>(lg, xt, tabL);
+    K32<T> xa[G_::XF];
+    logits<T, C, MB, false>(lg, xa, xt, tabL, lb);
     float w[MB][4], tau[4], tt[4];
-    temperature_ps<T, C, MB>(lg, xt, tabL, a.tb, tt);
-    softmax_ps<T, MB>(lg, gt, bias, a.M, hasG, tt, a.tau_min, nvalid, w, tau);
+    temperature_ps<T, C, MB>(lg, xa, tabL, lb.a, a.tb, tt);
+    softmax_ps<T, MB>(lg, gt, gtr, bias, a.M, hasG, tt, a.tau_min, nvalid, w, tau);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int p = 4 * g + i;
@@ -697,22 +795,27 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kWeights)))
 //   dw   = [dY Sp^T] + [x dnum^T] + dden    (kSliceBwd)   or  dW (kWeightsBwd)
 //   dz   = w (dw - <w, dw>)
 //   dl   = dz / tau;  dtau = dtau_in - <dz, z> / tau;  dt = dtau if t > tau_min
-//   dx   = W dnum + A dl + a dt   (W dnum only with the states term)
+//   dx   = W dnum + A dl + a dt
 //   dA  += x^T dl,  db += 1^T dl,  da += x^T dt,  db_t += 1^T dt
 // The backward table rows hold dnum_j - cN and s'_j - cS (a shift common to
 // all slices, which the softmax backward does not see); the header's dden is
-// centred here by its den-weighted mean cD.
+// centred here by its den-weighted mean cD.  Without the states term the
+// dnum rows, cN and dden are zero in the table image; without the deslice
+// term the dY contraction is skipped.  The dx tile is staged in the dY tile
+// (dw is done with it) and written back as whole rows.
 // ---------------------------------------------------------------------------
 template <typename T, int C, int MB, int PASS>
 __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_slice_bwd(StreamArgs a) {
   using G_ = Geo<sizeof(T), C, MB>;
+  using V = typename LAcc<T, true>::v;
   constexpr int WAVES = G_::waves(PASS);
   constexpr int M16 = G_::M16;
+  constexpr int SZ = (int)sizeof(T);
   constexpr int SROWF = M16 + 1;  // dl transpose row stride (floats)
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  const int wave = threadIdx.x >> 6, r = lane_id() & 15, g = lane_id() >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int r = lane_id() & 15, g = lane_id() >> 4;
   const bool hasG = a.flags & kHasG;
-  const bool states = (PASS == kSliceBwd) && (a.flags & kStatesTerm);
   const bool deslice = (PASS == kSliceBwd) && (a.flags & kDesliceTerm);
 
   copy_image(smem, a.img, G_::img_bytes(PASS));
@@ -720,14 +823,22 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
   const float* hdr = reinterpret_cast<const float*>(smem);
   const float* dden_tab = hdr + M16;
   const float* cN = hdr + 2 * M16;
+  const float* af = hdr + 3 * M16 + 2 * C;  // a in fp32
   const char* tabL = smem + G_::OFF_L;
   const char* tabW = smem + G_::OFF_2;
   char* wreg = smem + G_::img_bytes(PASS) + wave * G_::wave_bytes(PASS);
   char* xt = wreg;
-  char* yt = wreg + G_::XT;  // dY tile (kSliceBwd only)
-  char* gt = wreg + (PASS == kSliceBwd ? 2 : 1) * G_::XT;
+  char* yt = wreg + G_::XT;  // dY tile, then the dx staging tile
+  char* gt = wreg + 2 * G_::XT;
   float* scr = reinterpret_cast<float*>(gt + G_::GT);  // [16][M16+1]
   float* scr_dt = scr + 16 * SROWF;                     // [16]
+  const auto lb = logits_bases<T, C, MB, true>();
+  const RowBase<T> yb = row_base<T>(r, G_::XT_ROW);
+  const RowBase<T> wrb = row_base<T>(a_row<V>(r), G_::WROW);
+  const int xtr = tr_base<T, true>(G_::XT_ROW);
+  const int ltr = tr_base<T, true>(G_::TROW);
+  const int wtr = tr_base<T, true>(G_::WROW);
+  const int stb = stage_base<T>(G_::XT_ROW);
 
   // dden_j centred by its den-weighted mean (a shift common to all slices)
   float cD = 0.f;
@@ -763,7 +874,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
   const T* Gp = reinterpret_cast<const T*>(a.G);
   T* DX = reinterpret_cast<T*>(a.out);
   int64_t t0, t1;
-  tile_range(a.N, WAVES, t0, t1);
+  tile_range(a.N, WAVES, wave, t0, t1);
 
   TileRegs<T, C> xr, yr;
   GRegs<T, MB> gr;
@@ -779,7 +890,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
     wave_sync();
     store_tile<T, C>(xt, xr);
     if (deslice) store_tile<T, C>(yt, yr);
-    store_g<T, MB>(gt, gr, a.M);
+    store_g<T, MB>(gt, gr, a.M, hasG);
     wave_sync();
     if (t + 1 < t1) {
       load_tile<T, C>(xr, X, p0 + 16, a.N);
@@ -787,45 +898,45 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
       load_g<T, MB>(gr, Gp, p0 + 16, a.N, a.M, hasG);
     }
 
-    typename LAcc<T, true>::v lg[MB + 1];
-    logits<T, C, MB, true>(lg, xt, tabL);
+    V lg[MB + 1];
+    K32<T> xa[G_::XF];
+    logits<T, C, MB, true>(lg, xa, xt, tabL, lb);
     float w[MB][4], zs[MB][4], tau;
-    const float tt = temperature_own<T, C, MB>(lg, xt, tabL, a.tb);
+    const float tt = temperature_own<T, C, MB>(lg, xa, tabL, lb.a, a.tb);
     softmax_sp<T, MB>(lg, gt, bias, a.M, hasG, tt, a.tau_min, nvalid, w, zs, tau);
 
     // dw in the SP layout
     float dw[MB][4];
     if constexpr (PASS == kSliceBwd) {
-      using V = typename LAcc<T, true>::v;
       V acc[MB];
-      const int ra = a_row<V>(r);
 #pragma unroll
       for (int nb = 0; nb < MB; ++nb) acc[nb] = zero_acc<V>();
-      if (states) {
+      // states term: x . (dnum_j - cN)  (zero rows without the states term)
+      struct FS { K32<T> tw[MB]; };
+      pipelined<G_::XF, 2, FS>(
+          [&](int s, FS& f) {
 #pragma unroll
-        for (int s = 0; s < G_::XF; ++s) {
-          K32<T> xa;
-          ld_k32s<T>(xa, xt, r, 32 * s + 8 * g, G_::XT_ROW);
+            for (int nb = 0; nb < MB; ++nb)
+              ld_row<T>(f.tw[nb], tabW, wrb, 16 * nb * G_::WROW + 32 * s * SZ);
+          },
+          [&](int s, FS& f) {
 #pragma unroll
-          for (int nb = 0; nb < MB; ++nb) {
-            K32<T> tw;
-            ld_k32s<T>(tw, tabW, 16 * nb + ra, 32 * s + 8 * g, G_::WROW);
-            acc[nb] = mma_acc(tw, xa, acc[nb]);
-          }
-        }
-      }
+            for (int nb = 0; nb < MB; ++nb) acc[nb] = mma_acc(f.tw[nb], xa[s], acc[nb]);
+          });
       if (deslice) {
+        // deslice term: dY . (s'_j - cS)
+        struct FD { K32<T> ya; K32<T> tw[MB]; };
+        pipelined<G_::XF, 2, FD>(
+            [&](int s, FD& f) {
+              ld_row<T>(f.ya, yt, yb, 32 * s * SZ);
 #pragma unroll
-        for (int s = 0; s < G_::XF; ++s) {
-          K32<T> ya;
-          ld_k32s<T>(ya, yt, r, 32 * s + 8 * g, G_::XT_ROW);
+              for (int nb = 0; nb < MB; ++nb)
+                ld_row<T>(f.tw[nb], tabW, wrb, 16 * nb * G_::WROW + (C + 32 * s) * SZ);
+            },
+            [&](int s, FD& f) {
 #pragma unroll
-          for (int nb = 0; nb < MB; ++nb) {
-            K32<T> tw;
-            ld_k32s<T>(tw, tabW, 16 * nb + ra, C + 32 * s + 8 * g, G_::WROW);
-            acc[nb] = mma_acc(tw, ya, acc[nb]);
-          }
-        }
+              for (int nb = 0; nb < MB; ++nb) acc[nb] = mma_acc(f.tw[nb], f.ya, acc[nb]);
+            });
       }
 #pragma unroll
       for (int nb = 0; nb < MB; ++nb)
@@ -858,7 +969,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
 #pragma unroll
       for (int i = 0; i < 4; ++i) res += w[nb][i] * (dw[nb][i] - wdw);
     res = groups_sum(res);
-    const float rtau = 1.0f / tau;
+    const float rtau = fast_rcp(tau);
     float dl[MB][4];
     float zdz = 0.f;
 #pragma unroll
@@ -875,48 +986,38 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
     const float dt = (pv && tt > a.tau_min) ? dtau : 0.f;
 
     // dx = [W | dl] [dnum - cN ; A^T] + a dt + cN   (SP: D[channel][point])
-    K16<T> wb[MB], lb[MB];
+    K16<T> wb[MB], lbk[MB];
 #pragma unroll
     for (int nb = 0; nb < MB; ++nb) {
       set_k16(wb[nb], w[nb][0], w[nb][1], w[nb][2], w[nb][3]);
-      set_k16(lb[nb], dl[nb][0], dl[nb][1], dl[nb][2], dl[nb][3]);
+      set_k16(lbk[nb], dl[nb][0], dl[nb][1], dl[nb][2], dl[nb][3]);
     }
-    T* dxrow = DX + (p0 + r) * C + 4 * g;
+    wave_sync();  // the dw reads of the dY tile are done: it becomes the dx tile
+    struct FX { K16<T> ta[MB], tn[MB]; f32x4 av, cn; };
+    pipelined<G_::CB, 2, FX>(
+        [&](int cb, FX& f) {
 #pragma unroll
-    for (int cb = 0; cb < G_::CB; ++cb) {
-      f32x4 d = zero4();
+          for (int nb = 0; nb < MB; ++nb) {
+            // A^T rows of the logits table and (dnum_j - cN) rows of the
+            // backward table, read transposed: [channel][slice]
+            ld_tr<T>(f.ta[nb], tabL, ltr, 16 * nb * G_::TROW + 16 * cb * SZ, G_::TROW);
+            ld_tr<T>(f.tn[nb], tabW, wtr, 16 * nb * G_::WROW + 16 * cb * SZ, G_::WROW);
+          }
+          f.av = *reinterpret_cast<const f32x4*>(af + 16 * cb + 4 * g);
+          f.cn = *reinterpret_cast<const f32x4*>(cN + 16 * cb + 4 * g);
+        },
+        [&](int cb, FX& f) {
+          f32x4 d = zero4();
 #pragma unroll
-      for (int nb = 0; nb < MB; ++nb) {
-        K16<T> ta;  // A^T rows of the logits table, read transposed
-        ld_k16_t<T, true>(ta, tabL, G_::TROW, 16 * nb, 16 * cb);
-        d = mma16(ta, lb[nb], d);
-        if (states) {
-          K16<T> tn;  // (dnum_j - cN) rows of the backward table, transposed
-          ld_k16_t<T, true>(tn, tabW, G_::WROW, 16 * nb, 16 * cb);
-          d = mma16(tn, wb[nb], d);
-        }
-      }
-      // + a dt (a is any row of the temperature block of the logits table),
-      // + cN: the table rows hold dnum_j - cN, and sum_j w_j = 1
-      float av[4];
-      ld4s<T>(av, tabL, 16 * MB, 16 * cb + 4 * g, G_::TROW);
+          for (int nb = 0; nb < MB; ++nb) {
+            d = mma16(f.ta[nb], lbk[nb], d);
+            d = mma16(f.tn[nb], wb[nb], d);
+          }
+          // + a dt, + cN: the table rows hold dnum_j - cN, and sum_j w_j = 1
 #pragma unroll
-      for (int i = 0; i < 4; ++i) d[i] += av[i] * dt;
-      if (states) {
-        const f32x4 cn = *reinterpret_cast<const f32x4*>(cN + 16 * cb + 4 * g);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) d[i] += cn[i];
-      }
-      if (pv) {
-        if constexpr (sizeof(T) == 2) {
-          bf16x4 o;
-          o[0] = (bf16)d[0]; o[1] = (bf16)d[1]; o[2] = (bf16)d[2]; o[3] = (bf16)d[3];
-          *reinterpret_cast<bf16x4*>(dxrow + 16 * cb) = o;
-        } else {
-          *reinterpret_cast<f32x4*>(dxrow + 16 * cb) = d;
-        }
-      }
-    }
+          for (int i = 0; i < 4; ++i) d[i] += f.av[i] * dt + f.cn[i];
+          stage4<T>(yt, stb, 16 * cb * SZ, d);
+        });
 
     // parameter gradients: transpose dl (and dt) to the PS layout
 #pragma unroll
@@ -925,6 +1026,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
       for (int i = 0; i < 4; ++i) scr[r * SROWF + 16 * nb + 4 * g + i] = dl[nb][i];
     if (g == 0) scr_dt[r] = dt;
     wave_sync();
+    write_tile<T, C>(DX, p0, yt, nvalid);
     float dlp[MB][4], dtp[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -939,15 +1041,23 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
       db[nb] += (dlp[nb][0] + dlp[nb][1]) + (dlp[nb][2] + dlp[nb][3]);
     }
     if (g == 0) dbt += dt;
+    const bf16x2 dt01{(bf16)dtp[0], (bf16)dtp[1]}, dt23{(bf16)dtp[2], (bf16)dtp[3]};
+    struct FA { K16<T> xa; };
+    pipelined<G_::CB, 8, FA>(
+        [&](int cb, FA& f) { ld_tr<T>(f.xa, xt, xtr, 16 * cb * SZ, G_::XT_ROW); },
+        [&](int cb, FA& f) {
+          if constexpr (SZ == 2) {
+            da[cb] = __builtin_amdgcn_fdot2_f32_bf16(
+                bf16x2{f.xa.v[2], f.xa.v[3]}, dt23,
+                __builtin_amdgcn_fdot2_f32_bf16(bf16x2{f.xa.v[0], f.xa.v[1]}, dt01, da[cb], false),
+                false);
+          } else {
+            da[cb] += (k16_elem(f.xa, 0) * dtp[0] + k16_elem(f.xa, 1) * dtp[1]) +
+                      (k16_elem(f.xa, 2) * dtp[2] + k16_elem(f.xa, 3) * dtp[3]);
+          }
 #pragma unroll
-    for (int cb = 0; cb < G_::CB; ++cb) {
-      K16<T> xa;
-      ld_k16_t<T, true>(xa, xt, G_::XT_ROW, 0, 16 * cb);
-      da[cb] += (k16_elem(xa, 0) * dtp[0] + k16_elem(xa, 1) * dtp[1]) +
-                (k16_elem(xa, 2) * dtp[2] + k16_elem(xa, 3) * dtp[3]);
-#pragma unroll
-      for (int nb = 0; nb < MB; ++nb) dA[cb][nb] = mma16(xa, lp[nb], dA[cb][nb]);
-    }
+          for (int nb = 0; nb < MB; ++nb) dA[cb][nb] = mma16(f.xa, lp[nb], dA[cb][nb]);
+        });
   }
 
   // lane partials -> wave totals
