@@ -15,11 +15,10 @@ enum Pass { kAggregate = 0, kDeslice = 1, kDesliceBwd = 2, kWeights = 3, kSliceB
 constexpr int kLdsBytes = 160 * 1024;  // LDS per CU on gfx950
 constexpr int kPartialsMax = 256;      // blocks (point chunks) per streaming pass
 
-// LDS rows of the tables and point tiles are padded by 32 bytes and their
-// 16-byte chunks are swizzled (chunk ^ bit 3 of the row; see swz() in
-// pa_device.hpp): row reads of 16 bytes per lane (MFMA operands) and the
-// transposed reads of 8 bytes per lane (ds_read_b64_tr_b16) then hit
-// distinct banks.
+// LDS rows of the tables and point tiles are padded by 32 bytes (lds_off()
+// in pa_device.hpp): row reads of 16 bytes per lane (MFMA operands) over 16
+// rows and the transposed reads of 8 bytes per lane (ds_read_b64_tr_b16)
+// then hit distinct banks.
 template <int SZ, int C, int MB>
 struct Geo {
   static constexpr int M16 = 16 * MB;            // slices padded to 16

@@ -2,7 +2,7 @@
 //   - the per-call table image (logits table [A^T ; a], deslice table S'^T,
 //     backward table [dnum | S'], biases, dden) in the exact byte layout the
 //     streaming kernels copy into LDS (rows of the logits and backward tables
-//     padded and chunk-swizzled as in pa_layout.h);
+//     padded as in pa_layout.h);
 //   - the ordered reduction of per-block partial-sum records (the partial
 //     sums of Section 4.2, here over point chunks of one GPU);
 //   - the states s_j = num_j / max(den_j, eps) (Eq. 1);
@@ -67,7 +67,7 @@ __global__ void k_prep(PrepGeo g, PrepArgs p) {
       v = j < M ? A[(int64_t)c * M + j] : from_f<T>(0.f);
     else
       v = av ? av[c] : from_f<T>(0.f);
-    *reinterpret_cast<T*>(img + g.OFF_L + swz(j, c * g.SZ, g.TROW)) = v;
+    *reinterpret_cast<T*>(img + g.OFF_L + lds_off(j, c * g.SZ, g.TROW)) = v;
   }
   if (p.pass == kDeslice) {
     // S'^T: row c, column j
@@ -99,7 +99,7 @@ __global__ void k_prep(PrepGeo g, PrepArgs p) {
           v = p.Sp[j * C + (cc - C)] - hdr[2 * M16 + C + (cc - C)];
         }
       }
-      *reinterpret_cast<T*>(img + g.OFF_2 + swz(j, cc * g.SZ, g.WROW)) = from_f<T>(v);
+      *reinterpret_cast<T*>(img + g.OFF_2 + lds_off(j, cc * g.SZ, g.WROW)) = from_f<T>(v);
     }
   }
 }

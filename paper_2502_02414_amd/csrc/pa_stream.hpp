@@ -84,22 +84,18 @@ __device__ __forceinline__ void pipelined(Load load, Use use) {
 }
 
 // ---------------------------------------------------------------------------
-// LDS addressing.  Tables and point tiles have rows padded by 32 bytes and
-// their 16-byte chunks swizzled (chunk ^ bit 3 of the row, swz() in
-// pa_device.hpp).  Every fragment read below is a per-lane base, computed
-// once per kernel, plus a compile-time offset.
+// LDS addressing.  Tables and point tiles have rows padded by 32 bytes
+// (lds_off() in pa_device.hpp).  Every fragment read below is a per-lane
+// base, computed once per kernel, plus a compile-time offset.
 // ---------------------------------------------------------------------------
 // K32 row fragment of lane (r, g): elements [col + 8g, col + 8g + 8) of row
-// row0 + lr (row0 % 16 == 0, col % 32 == 0), at offset row0 * RB + col * sz.
+// row0 + lr, at offset row0 * RB + col * sz.
 template <typename T> struct RowBase { int lo, hi; };
 template <typename T>
 __device__ __forceinline__ RowBase<T> row_base(int lr, int RB) {
-  const int g = lane_id() >> 4, b = (lr >> 3) & 1;
-  if constexpr (sizeof(T) == 2) {
-    return {lr * RB + 16 * (g ^ b), 0};
-  } else {
-    return {lr * RB + 32 * g + 16 * b, lr * RB + 32 * g + 16 - 16 * b};
-  }
+  const int g = lane_id() >> 4;
+  constexpr int SZ = (int)sizeof(T);
+  return {lr * RB + 8 * g * SZ, lr * RB + 8 * g * SZ + 16};
 }
 template <typename T>
 __device__ __forceinline__ void ld_row(K32<T>& f, const char* a, const RowBase<T>& o, int off) {
@@ -112,18 +108,17 @@ __device__ __forceinline__ void ld_row(K32<T>& f, const char* a, const RowBase<T
 }
 
 // Transposed K16 fragment: lane (r, g) element i = arr[row0 + 4g + i][col0 + r]
-// at offset row0 * RB + col0 * sz (row0, col0 % 16 == 0).  bf16 uses
-// ds_read_b64_tr_b16: within each 16-lane group, lane 4a+e receives element
-// e of the 8-byte chunks addressed by lanes a, a+4, a+8, a+12, so lane k
-// addresses row 4g + k/4, columns 4 (k%4) .. +3.  fp32 reads four elements.
-template <typename T, bool SWZ>
+// at offset row0 * RB + col0 * sz.  bf16 uses ds_read_b64_tr_b16: within
+// each 16-lane group, lane 4a+e receives element e of the 8-byte chunks
+// addressed by lanes a, a+4, a+8, a+12, so lane k addresses row 4g + k/4,
+// columns 4 (k%4) .. +3.  fp32 reads four elements.
+template <typename T>
 __device__ __forceinline__ int tr_base(int RB) {
   const int r = lane_id() & 15, g = lane_id() >> 4;
-  const int b = SWZ ? (g >> 1) : 0;  // bit 3 of the row
   if constexpr (sizeof(T) == 2) {
-    return (4 * g + (r >> 2)) * RB + 16 * (((r >> 1) & 1) ^ b) + 8 * (r & 1);
+    return (4 * g + (r >> 2)) * RB + 8 * (r & 3);
   } else {
-    return 4 * g * RB + 16 * ((r >> 2) ^ b) + 4 * (r & 3);
+    return 4 * g * RB + 4 * r;
   }
 }
 template <typename T>
@@ -140,15 +135,11 @@ __device__ __forceinline__ void ld_tr(K16<T>& f, const char* a, int base, int of
 }
 
 // SP-layout output fragment (lane (r, g): channels [c0 + 4g, +4) of point r)
-// into a swizzled tile, at offset c0 * sz (c0 % 16 == 0).
+// into a tile, at offset c0 * sz.
 template <typename T>
 __device__ __forceinline__ int stage_base(int RB) {
-  const int r = lane_id() & 15, g = lane_id() >> 4, b = (r >> 3) & 1;
-  if constexpr (sizeof(T) == 2) {
-    return r * RB + 16 * ((g >> 1) ^ b) + 8 * (g & 1);
-  } else {
-    return r * RB + 16 * (g ^ b);
-  }
+  const int r = lane_id() & 15, g = lane_id() >> 4;
+  return r * RB + 4 * g * (int)sizeof(T);
 }
 template <typename T>
 __device__ __forceinline__ void stage4(char* tile, int base, int off, const f32x4& d) {
@@ -162,7 +153,7 @@ __device__ __forceinline__ void stage4(char* tile, int base, int off, const f32x
 }
 
 // ---------------------------------------------------------------------------
-// Point tiles: HBM -> registers -> swizzled LDS, and staged outputs back.
+// Point tiles: HBM -> registers -> padded LDS rows, and staged outputs back.
 // Rows [p0, p0+16) of a [N,C] tensor are 16*C*SZ contiguous bytes; lane l
 // holds 16-byte chunks q = l + 64k.  Rows >= N are zero.
 // ---------------------------------------------------------------------------
@@ -203,11 +194,11 @@ __device__ __forceinline__ void store_tile(char* tile, const TileRegs<T, C>& R) 
   for (int k = 0; k < TileRegs<T, C>::NCH; ++k) {
     const int q = lane + 64 * k;
     const int row = q / RCH, cc = q - row * RCH;
-    *reinterpret_cast<uint4*>(tile + swz(row, 16 * cc, ROW)) = R.c[k];
+    *reinterpret_cast<uint4*>(tile + lds_off(row, 16 * cc, ROW)) = R.c[k];
   }
 }
 
-// Staged output tile (swizzled LDS) -> rows [p0, p0 + nvalid) of dst.
+// Staged output tile (padded LDS rows) -> rows [p0, p0 + nvalid) of dst.
 template <typename T, int C>
 __device__ __forceinline__ void write_tile(T* dst, int64_t p0, const char* tile, int nvalid) {
   constexpr int RCH = TileRegs<T, C>::RCH;
@@ -219,7 +210,7 @@ __device__ __forceinline__ void write_tile(T* dst, int64_t p0, const char* tile,
   for (int k = 0; k < NCH; ++k) {
     const int q = lane + 64 * k;
     const int row = q / RCH, cc = q - row * RCH;
-    const uint4 v = *reinterpret_cast<const uint4*>(tile + swz(row, 16 * cc, ROW));
+    const uint4 v = *reinterpret_cast<const uint4*>(tile + lds_off(row, 16 * cc, ROW));
     if (row < nvalid) *reinterpret_cast<uint4*>(d + (uint32_t)(16 * lane + 1024 * k)) = v;
   }
 }
@@ -550,8 +541,8 @@ k_aggregate(StreamArgs a) {
   char* yt = BWD ? wreg + G_::XT : wreg;    // tile contracted over points
   char* gt = wreg + (BWD ? 2 : 1) * G_::XT; // Gumbel rows
   const auto lb = logits_bases<T, C, MB, false>();
-  const int xtr = tr_base<T, true>(G_::XT_ROW);
-  const int gtr = tr_base<T, false>(G_::GROW);
+  const int xtr = tr_base<T>(G_::XT_ROW);
+  const int gtr = tr_base<T>(G_::GROW);
 
   float bias[MB];
 #pragma unroll
@@ -748,7 +739,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kWeights)))
   char* xt = smem + G_::img_bytes(kWeights) + wave * G_::wave_bytes(kWeights);
   char* gt = xt + G_::XT;
   const auto lb = logits_bases<T, C, MB, false>();
-  const int gtr = tr_base<T, false>(G_::GROW);
+  const int gtr = tr_base<T>(G_::GROW);
   float bias[MB];
 #pragma unroll
   for (int nb = 0; nb < MB; ++nb) bias[nb] = reinterpret_cast<const float*>(smem)[16 * nb + r];
@@ -835,9 +826,9 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
   const auto lb = logits_bases<T, C, MB, true>();
   const RowBase<T> yb = row_base<T>(r, G_::XT_ROW);
   const RowBase<T> wrb = row_base<T>(a_row<V>(r), G_::WROW);
-  const int xtr = tr_base<T, true>(G_::XT_ROW);
-  const int ltr = tr_base<T, true>(G_::TROW);
-  const int wtr = tr_base<T, true>(G_::WROW);
+  const int xtr = tr_base<T>(G_::XT_ROW);
+  const int ltr = tr_base<T>(G_::TROW);
+  const int wtr = tr_base<T>(G_::WROW);
   const int stb = stage_base<T>(G_::XT_ROW);
 
   // dden_j centred by its den-weighted mean (a shift common to all slices)
