@@ -177,18 +177,32 @@ __device__ __forceinline__ float row16_sum(float v) {
   v += dpp<kMirror>(v);
   return v;
 }
-// Reduction over the four lane groups (lanes l, l^16, l^32, l^48).
+// Reduction over the four lane groups (lanes l, l^16, l^32, l^48) with the
+// gfx950 lane-swap instructions (VALU, no LDS round trip).  With both
+// operands equal to v, v_permlane16_swap leaves in each lane the values of
+// rows (2k, 2k+1) as the two operands (lower row first), and
+// v_permlane32_swap does the same for the two halves, so every lane forms
+// (v0 + v1) + (v2 + v3) in the same order: the result is bitwise equal on
+// the four lanes.  s_nop 1 covers the VALU-write to lane-swap-read hazard.
+__device__ __forceinline__ void lane_swap16(float& a, float& b) {
+  asm volatile("s_nop 1\n\tv_permlane16_swap_b32 %0, %1" : "+v"(a), "+v"(b));
+}
+__device__ __forceinline__ void lane_swap32(float& a, float& b) {
+  asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1" : "+v"(a), "+v"(b));
+}
 __device__ __forceinline__ float groups_max(float v) {
-  v = fmaxf(v, __shfl_xor(v, 16));
-  v = fmaxf(v, __shfl_xor(v, 32));
-  return v;
+  float a = v, b = v;
+  lane_swap16(a, b);
+  float c = fmaxf(a, b), d = c;
+  lane_swap32(c, d);
+  return fmaxf(c, d);
 }
 __device__ __forceinline__ float groups_sum(float v) {
-  // (a + b) + (c + d) on every lane, in the same association order.
-  float o16 = __shfl_xor(v, 16);
-  float lo = (lane_id() & 16) ? o16 + v : v + o16;
-  float o32 = __shfl_xor(lo, 32);
-  return (lane_id() & 32) ? o32 + lo : lo + o32;
+  float a = v, b = v;
+  lane_swap16(a, b);
+  float c = a + b, d = c;
+  lane_swap32(c, d);
+  return c + d;
 }
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }

@@ -53,7 +53,8 @@ __global__ void k_prep(PrepGeo g, PrepArgs p) {
   // header: bias[M16]; the backward pass's dden, cN, cS come from
   // k_prep_center (run first); other passes get zeros
   float* hdr = reinterpret_cast<float*>(img);
-  for (int64_t j = tid; j < M16; j += nth) hdr[j] = (j < M && p.b) ? p.b[j] : 0.f;
+  // padded slices j >= M get bias -inf: their softmax weight is exactly 0
+  for (int64_t j = tid; j < M16; j += nth) hdr[j] = j < M ? (p.b ? p.b[j] : 0.f) : -INFINITY;
   if (p.pass != kSliceBwd)
     for (int64_t k = tid; k < 2 * M16 + 2 * C; k += nth) hdr[M16 + k] = 0.f;
   for (int64_t c = tid; c < C; c += nth) hdr[3 * M16 + 2 * C + c] = av ? to_f<T>(av[c]) : 0.f;

@@ -228,7 +228,11 @@ struct GRegs {
 template <typename T, int MB>
 __device__ __forceinline__ void load_g(GRegs<T, MB>& gr, const T* G, int64_t p0, int64_t N,
                                        int M, bool hasG) {
-  if (!hasG) return;
+  if (!hasG) {  // no Gumbel noise: the tile's M columns are written as zeros
+#pragma unroll
+    for (int k = 0; k < GRegs<T, MB>::GCH; ++k) gr.c[k] = uint4{0, 0, 0, 0};
+    return;
+  }
   const int lane = lane_id();
   const int nchunk = M * (int)sizeof(T);  // (16 rows * M * sz) / 16
   const char* base = reinterpret_cast<const char*>(G + p0 * M);
@@ -257,7 +261,6 @@ __device__ __forceinline__ void load_g(GRegs<T, MB>& gr, const T* G, int64_t p0,
 
 template <typename T, int MB>
 __device__ __forceinline__ void store_g(char* gt, const GRegs<T, MB>& gr, int M, bool hasG) {
-  if (!hasG) return;
   constexpr int SZ = (int)sizeof(T);
   constexpr int GROW = 16 * MB * SZ + 16;
   const int lane = lane_id();
@@ -304,7 +307,7 @@ __device__ __forceinline__ LogitsBases<T, C, MB> logits_bases() {
           row_base<T>(0, G_::TROW)};
 }
 
-template <typename T, int C, int MB, bool SP>
+template <typename T, int C, int MB, bool SP, bool KEEP_X = true>
 __device__ __forceinline__ void logits(typename LAcc<T, SP>::v (&acc)[MB + 1],
                                        K32<T> (&xa)[C / 32], const char* xt, const char* tabL,
                                        const LogitsBases<T, C, MB>& lb) {
@@ -314,11 +317,17 @@ __device__ __forceinline__ void logits(typename LAcc<T, SP>::v (&acc)[MB + 1],
   constexpr int SZ = (int)sizeof(T);
 #pragma unroll
   for (int nb = 0; nb <= MB; ++nb) acc[nb] = zero_acc<V>();
+  // KEEP_X: all point fragments are read up front and returned in xa (for
+  // reuse by the caller); otherwise each is read with its step's table
+  // fragments and dropped after use (fewer live registers).
+  if constexpr (KEEP_X) {
 #pragma unroll
-  for (int s = 0; s < C / 32; ++s) ld_row<T>(xa[s], xt, lb.x, 32 * s * SZ);
-  struct F { K32<T> t[NT]; };
+    for (int s = 0; s < C / 32; ++s) ld_row<T>(xa[s], xt, lb.x, 32 * s * SZ);
+  }
+  struct F { K32<T> t[NT]; K32<T> x; };
   pipelined<C / 32, 2, F>(
       [&](int s, F& f) {
+        if constexpr (!KEEP_X) ld_row<T>(f.x, xt, lb.x, 32 * s * SZ);
 #pragma unroll
         for (int nb = 0; nb < NT; ++nb) {
           if (nb < MB)
@@ -328,9 +337,10 @@ __device__ __forceinline__ void logits(typename LAcc<T, SP>::v (&acc)[MB + 1],
         }
       },
       [&](int s, F& f) {
+        const K32<T>& x = KEEP_X ? xa[s] : f.x;
 #pragma unroll
         for (int nb = 0; nb < NT; ++nb)
-          acc[nb] = SP ? mma_acc(f.t[nb], xa[s], acc[nb]) : mma_acc(xa[s], f.t[nb], acc[nb]);
+          acc[nb] = SP ? mma_acc(f.t[nb], x, acc[nb]) : mma_acc(x, f.t[nb], acc[nb]);
       });
 }
 
@@ -384,29 +394,26 @@ __device__ __forceinline__ void temperature_ps(const V (&acc)[MB + 1], const K32
 // Softmax over slices, PS layout.  u = l + b + g (the noisy logit), m its
 // row maximum; the base-2 exponent zs = (u - m) log2(e) / tau is formed
 // after the shift, so its error is relative to u - m (not to u / tau, which
-// is large when tau is clamped); w = 2^zs / sum.  Invalid slices (j >= M)
-// and points beyond N get w = 0.  The Gumbel values are read transposed
-// from the padded G tile (rows 4g+i, column 16nb+r).
+// is large when tau is clamped); w = 2^zs / sum.  Padded slices (j >= M)
+// have bias -inf in the table header and Gumbel 0 (the G tile starts zeroed
+// and only its first M columns are ever written), so they get w = 0; points
+// beyond N get w = 0.  The Gumbel values are read transposed from the G tile
+// (rows 4g+i, column 16nb+r).
 template <typename T, int MB, typename V>
 __device__ __forceinline__ void softmax_ps(const V (&acc)[MB + 1], const char* gt, int gtr,
-                                           const float (&bias)[MB], int M, bool hasG,
-                                           const float (&t)[4], float tau_min, int nvalid,
-                                           float (&w)[MB][4], float (&tau)[4]) {
+                                           const float (&bias)[MB], const float (&t)[4],
+                                           float tau_min, int nvalid, float (&w)[MB][4],
+                                           float (&tau)[4]) {
   using R = decltype(acc[0][0] + 0.f);
   constexpr int GROW = 16 * MB * (int)sizeof(T) + 16;
-  const int r = lane_id() & 15, g = lane_id() >> 4;
+  const int g = lane_id() >> 4;
   R u[MB][4];
 #pragma unroll
   for (int nb = 0; nb < MB; ++nb) {
-    const int j = 16 * nb + r;
-    const bool valid = j < M;
     K16<T> gv;
-    if (hasG) ld_tr<T>(gv, gt, gtr, 16 * nb * (int)sizeof(T), GROW);
+    ld_tr<T>(gv, gt, gtr, 16 * nb * (int)sizeof(T), GROW);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float gg = (hasG && valid) ? k16_elem(gv, i) : 0.f;
-      u[nb][i] = valid ? (R)acc[nb][i] + (R)bias[nb] + (R)gg : (R)-INFINITY;
-    }
+    for (int i = 0; i < 4; ++i) u[nb][i] = (R)acc[nb][i] + (R)bias[nb] + (R)k16_elem(gv, i);
   }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -423,22 +430,23 @@ __device__ __forceinline__ void softmax_ps(const V (&acc)[MB + 1], const char* g
       s += e[nb];
     }
     s = row16_sum(s);
-    const float inv = fast_rcp(s);
-    const bool pv = (4 * g + i) < nvalid;
+    const float inv = (4 * g + i) < nvalid ? fast_rcp(s) : 0.f;
 #pragma unroll
-    for (int nb = 0; nb < MB; ++nb) w[nb][i] = pv ? e[nb] * inv : 0.f;
+    for (int nb = 0; nb < MB; ++nb) w[nb][i] = e[nb] * inv;
   }
 }
 
 // Softmax over slices, SP layout (the lane's point is r).  Also returns the
 // shifted base-2 exponents zs (the natural logit is zs ln 2 + const) for
 // the temperature gradient.  The Gumbel values are four consecutive
-// elements of row r of the G tile.
+// elements of row r of the G tile.  With bf16 storage the exponent is one
+// fma, u k - m k (its rounding error, relative to u k, stays far below the
+// bf16 tolerance); fp32 storage keeps the shift before the scale.
 template <typename T, int MB, typename V>
 __device__ __forceinline__ void softmax_sp(const V (&acc)[MB + 1], const char* gt,
-                                           const float (&bias)[MB][4], int M, bool hasG, float t,
-                                           float tau_min, int nvalid, float (&w)[MB][4],
-                                           float (&zs)[MB][4], float& tau) {
+                                           const float (&bias)[MB][4], float t, float tau_min,
+                                           int nvalid, float (&w)[MB][4], float (&zs)[MB][4],
+                                           float& tau) {
   using R = decltype(acc[0][0] + 0.f);
   constexpr int SZ = (int)sizeof(T);
   constexpr int GROW = 16 * MB * SZ + 16;
@@ -449,45 +457,49 @@ __device__ __forceinline__ void softmax_sp(const V (&acc)[MB + 1], const char* g
   float m = -INFINITY;
 #pragma unroll
   for (int nb = 0; nb < MB; ++nb) {
-    float gv[4] = {0.f, 0.f, 0.f, 0.f};
-    if (hasG) {
-      const char* p = gt + r * GROW + (16 * nb + 4 * g) * SZ;
-      if constexpr (SZ == 2) {
-        const bf16x4 q = *reinterpret_cast<const bf16x4*>(p);
+    float gv[4];
+    const char* p = gt + r * GROW + (16 * nb + 4 * g) * SZ;
+    if constexpr (SZ == 2) {
+      const bf16x4 q = *reinterpret_cast<const bf16x4*>(p);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) gv[i] = (float)q[i];
-      } else {
-        const f32x4 q = *reinterpret_cast<const f32x4*>(p);
+      for (int i = 0; i < 4; ++i) gv[i] = (float)q[i];
+    } else {
+      const f32x4 q = *reinterpret_cast<const f32x4*>(p);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) gv[i] = q[i];
-      }
+      for (int i = 0; i < 4; ++i) gv[i] = q[i];
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int j = 16 * nb + 4 * g + i;
-      const bool valid = j < M;
-      u[nb][i] = valid ? (R)acc[nb][i] + (R)bias[nb][i] + (R)gv[i] : (R)-INFINITY;
+      u[nb][i] = (R)acc[nb][i] + (R)bias[nb][i] + (R)gv[i];
       m = fmaxf(m, (float)u[nb][i]);
     }
   }
   m = groups_max(m);
   float s = 0.f;
   float e[MB][4];
+  const float mk = (float)((R)m * k);
 #pragma unroll
   for (int nb = 0; nb < MB; ++nb)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      zs[nb][i] = (float)((u[nb][i] - (R)m) * k);
+      if constexpr (SZ == 2)
+        zs[nb][i] = fmaf((float)u[nb][i], (float)k, -mk);
+      else
+        zs[nb][i] = (float)((u[nb][i] - (R)m) * k);
       e[nb][i] = fast_exp2(zs[nb][i]);
       s += e[nb][i];
     }
   s = groups_sum(s);
-  const float inv = fast_rcp(s);
-  const bool pv = r < nvalid;
+  const float inv = r < nvalid ? fast_rcp(s) : 0.f;
 #pragma unroll
   for (int nb = 0; nb < MB; ++nb)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) w[nb][i] = pv ? e[nb][i] * inv : 0.f;
+    for (int i = 0; i < 4; ++i) w[nb][i] = e[nb][i] * inv;
+}
+
+// Zero a wave-private LDS region (16-byte multiple).
+__device__ __forceinline__ void zero_lds(char* p, int bytes) {
+  for (int q = lane_id(); q < bytes / 16; q += 64) reinterpret_cast<uint4*>(p)[q] = uint4{0, 0, 0, 0};
 }
 
 // Copy the table image from global memory into LDS (all threads).
@@ -519,7 +531,12 @@ __device__ __forceinline__ void block_ordered_reduce(int waves, Put put) {
 }
 
 // ---------------------------------------------------------------------------
-// kAggregate and kDesliceBwd (PS layout): W^T x (with den) or W^T dY.
+// kAggregate and kDesliceBwd: W^T x (with den = W^T 1) or W^T dY.  The
+// weights come out of the softmax in the SP layout (lane: one point, 4
+// slices per block); they are staged in the G tile (consumed by then) and
+// read back transposed, which gives the contraction over points its A
+// operand (lane: one slice, 4 points).  den is the same contraction against
+// a B operand of ones, so it uses exactly the rounded weights of num.
 // ---------------------------------------------------------------------------
 template <typename T, int C, int MB, bool BWD>
 __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(BWD ? kDesliceBwd : kAggregate)))
@@ -539,23 +556,29 @@ k_aggregate(StreamArgs a) {
   char* wreg = smem + G_::img_bytes(PASS) + wave * G_::wave_bytes(PASS);
   char* xt = wreg;                          // x tile (logits)
   char* yt = BWD ? wreg + G_::XT : wreg;    // tile contracted over points
-  char* gt = wreg + (BWD ? 2 : 1) * G_::XT; // Gumbel rows
-  const auto lb = logits_bases<T, C, MB, false>();
+  char* gt = wreg + (BWD ? 2 : 1) * G_::XT; // Gumbel rows, then the weights
+  zero_lds(gt, G_::GT);
+  const auto lb = logits_bases<T, C, MB, true>();
   const int xtr = tr_base<T>(G_::XT_ROW);
-  const int gtr = tr_base<T>(G_::GROW);
+  const int wtr = tr_base<T>(G_::GROW);
+  const int wsb = r * G_::GROW + 4 * g * SZ;  // SP weights of point r, slices 16nb + 4g ..
 
-  float bias[MB];
-#pragma unroll
-  for (int nb = 0; nb < MB; ++nb) bias[nb] = reinterpret_cast<const float*>(smem)[16 * nb + r];
-
-  f32x4 acc[MB][G_::CB];
+  float bias[MB][4];
 #pragma unroll
   for (int nb = 0; nb < MB; ++nb)
 #pragma unroll
-    for (int cb = 0; cb < G_::CB; ++cb) acc[nb][cb] = zero4();
-  float den[MB];
+    for (int i = 0; i < 4; ++i)
+      bias[nb][i] = reinterpret_cast<const float*>(smem)[16 * nb + 4 * g + i];
+
+  f32x4 acc[MB][G_::CB], dacc[MB];
 #pragma unroll
-  for (int nb = 0; nb < MB; ++nb) den[nb] = 0.f;
+  for (int nb = 0; nb < MB; ++nb) {
+    dacc[nb] = zero4();
+#pragma unroll
+    for (int cb = 0; cb < G_::CB; ++cb) acc[nb][cb] = zero4();
+  }
+  K16<T> ones;
+  set_k16(ones, 1.f, 1.f, 1.f, 1.f);
 
   const T* X = reinterpret_cast<const T*>(a.x);
   const T* Y = reinterpret_cast<const T*>(a.dY);
@@ -584,33 +607,36 @@ k_aggregate(StreamArgs a) {
       load_g<T, MB>(gr, Gp, p0 + 16, a.N, a.M, hasG);
     }
 
-    typename LAcc<T, false>::v lg[MB + 1];
+    typename LAcc<T, true>::v lg[MB + 1];
     K32<T> xa[G_::XF];
-    logits<T, C, MB, false>(lg, xa, xt, tabL, lb);
-    float w[MB][4], tau[4], tt[4];
-    temperature_ps<T, C, MB>(lg, xa, tabL, lb.a, a.tb, tt);
-    softmax_ps<T, MB>(lg, gt, gtr, bias, a.M, hasG, tt, a.tau_min, nvalid, w, tau);
+    logits<T, C, MB, true, (SZ == 4)>(lg, xa, xt, tabL, lb);
+    float w[MB][4], zs[MB][4], tau;
+    const float tt = temperature_own<T, C, MB>(lg, xa, tabL, lb.a, a.tb);
+    softmax_sp<T, MB>(lg, gt, bias, tt, a.tau_min, nvalid, w, zs, tau);
 
-    K16<T> wt[MB];
+    // SP -> PS through the G tile (the softmax has read its Gumbel values)
+    wave_sync();
 #pragma unroll
     for (int nb = 0; nb < MB; ++nb) {
-      set_k16(wt[nb], w[nb][0], w[nb][1], w[nb][2], w[nb][3]);
-      if (!BWD)
-        den[nb] += (k16_elem(wt[nb], 0) + k16_elem(wt[nb], 1)) +
-                   (k16_elem(wt[nb], 2) + k16_elem(wt[nb], 3));
+      f32x4 v{w[nb][0], w[nb][1], w[nb][2], w[nb][3]};
+      stage4<T>(gt, wsb, 16 * nb * SZ, v);
+    }
+    wave_sync();
+    K16<T> wt[MB];
+#pragma unroll
+    for (int nb = 0; nb < MB; ++nb) ld_tr<T>(wt[nb], gt, wtr, 16 * nb * SZ, G_::GROW);
+    if constexpr (!BWD) {
+#pragma unroll
+      for (int nb = 0; nb < MB; ++nb) dacc[nb] = mma16(wt[nb], ones, dacc[nb]);
     }
     struct F { K16<T> xb; };
-    pipelined<G_::CB, 8, F>(
+    pipelined<G_::CB, 4, F>(
         [&](int cb, F& f) { ld_tr<T>(f.xb, yt, xtr, 16 * cb * SZ, G_::XT_ROW); },
         [&](int cb, F& f) {
 #pragma unroll
           for (int nb = 0; nb < MB; ++nb) acc[nb][cb] = mma16(wt[nb], f.xb, acc[nb][cb]);
         });
   }
-
-  // den: lane (r,g) holds slice 16nb+r summed over its points -> sum groups
-#pragma unroll
-  for (int nb = 0; nb < MB; ++nb) den[nb] = groups_sum(den[nb]);
 
   __syncthreads();  // every wave is done with the tables and tiles
   float* red = reinterpret_cast<float*>(smem);  // [M16][C] then den [M16]
@@ -624,12 +650,14 @@ k_aggregate(StreamArgs a) {
           float* d = red + (16 * nb + 4 * g + i) * C + 16 * cb + r;
           *d = first ? acc[nb][cb][i] : *d + acc[nb][cb][i];
         }
-    if (!BWD && g == 0)
+    if (!BWD && r == 0)
 #pragma unroll
-      for (int nb = 0; nb < MB; ++nb) {
-        float* d = red + G_::M16 * C + 16 * nb + r;
-        *d = first ? den[nb] : *d + den[nb];
-      }
+      for (int nb = 0; nb < MB; ++nb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float* d = red + G_::M16 * C + 16 * nb + 4 * g + i;
+          *d = first ? dacc[nb][i] : *d + dacc[nb][i];
+        }
   });
   float* rec = a.partials + (int64_t)blockIdx.x * a.rec;
   const int MC = a.M * C;
@@ -658,6 +686,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kDeslice)))
   const char* tabS = smem + G_::OFF_2;
   char* xt = smem + G_::img_bytes(kDeslice) + wave * G_::wave_bytes(kDeslice);
   char* gt = xt + G_::XT;
+  zero_lds(gt, G_::GT);
   const auto lb = logits_bases<T, C, MB, true>();
   const int sb = r * G_::SROW + 4 * g * SZ;  // S'^T row 16cb + r, slices 16nb + 4g ..
   const int stb = stage_base<T>(G_::XT_ROW);
@@ -698,7 +727,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kDeslice)))
     logits<T, C, MB, true>(lg, xa, xt, tabL, lb);
     float w[MB][4], zs[MB][4], tau;
     const float tt = temperature_own<T, C, MB>(lg, xa, tabL, lb.a, a.tb);
-    softmax_sp<T, MB>(lg, gt, bias, a.M, hasG, tt, a.tau_min, nvalid, w, zs, tau);
+    softmax_sp<T, MB>(lg, gt, bias, tt, a.tau_min, nvalid, w, zs, tau);
 
     K16<T> wb[MB];
 #pragma unroll
@@ -738,6 +767,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kWeights)))
   const char* tabL = smem + G_::OFF_L;
   char* xt = smem + G_::img_bytes(kWeights) + wave * G_::wave_bytes(kWeights);
   char* gt = xt + G_::XT;
+  zero_lds(gt, G_::GT);
   const auto lb = logits_bases<T, C, MB, false>();
   const int gtr = tr_base<T>(G_::GROW);
   float bias[MB];
@@ -765,7 +795,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kWeights)))
     logits<T, C, MB, false>(lg, xa, xt, tabL, lb);
     float w[MB][4], tau[4], tt[4];
     temperature_ps<T, C, MB>(lg, xa, tabL, lb.a, a.tb, tt);
-    softmax_ps<T, MB>(lg, gt, gtr, bias, a.M, hasG, tt, a.tau_min, nvalid, w, tau);
+    softmax_ps<T, MB>(lg, gt, gtr, bias, tt, a.tau_min, nvalid, w, tau);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int p = 4 * g + i;
@@ -821,6 +851,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
   char* xt = wreg;
   char* yt = wreg + G_::XT;  // dY tile, then the dx staging tile
   char* gt = wreg + 2 * G_::XT;
+  zero_lds(gt, G_::GT);
   float* scr = reinterpret_cast<float*>(gt + G_::GT);  // [16][M16+1]
   float* scr_dt = scr + 16 * SROWF;                     // [16]
   const auto lb = logits_bases<T, C, MB, true>();
@@ -894,7 +925,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
     logits<T, C, MB, true>(lg, xa, xt, tabL, lb);
     float w[MB][4], zs[MB][4], tau;
     const float tt = temperature_own<T, C, MB>(lg, xa, tabL, lb.a, a.tb);
-    softmax_sp<T, MB>(lg, gt, bias, a.M, hasG, tt, a.tau_min, nvalid, w, zs, tau);
+    softmax_sp<T, MB>(lg, gt, bias, tt, a.tau_min, nvalid, w, zs, tau);
 
     // dw in the SP layout
     float dw[MB][4];
