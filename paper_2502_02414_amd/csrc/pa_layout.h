@@ -67,10 +67,7 @@ struct Geo {
   // SIMD hide each other's latency); the accumulating passes, and fp32
   // storage (whose tiles take twice the registers), run 4
   static constexpr int max_waves(int pass) {
-    return ((pass == kDeslice || pass == kWeights) && SZ == 2) ||
-                   (pass == kAggregate && SZ == 2 && MB <= 2)
-               ? 8
-               : 4;
+    return (pass == kDeslice || pass == kWeights) && SZ == 2 ? 8 : 4;
   }
   static constexpr int waves(int pass) {
     return (max_waves(pass) >= 8 && img_bytes(pass) + 8 * wave_bytes(pass) <= kLdsBytes) ? 8

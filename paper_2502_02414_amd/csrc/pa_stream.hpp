@@ -56,6 +56,12 @@ struct StreamArgs {
 
 enum Flags { kHasG = 1, kStatesTerm = 2, kDesliceTerm = 4 };
 
+// Tiles of loads in flight per wave (register stages) in each streaming pass:
+// two for the bf16 forward passes, whose registers allow it.
+template <typename T, bool BWD> constexpr int agg_depth() { return sizeof(T) == 2 && !BWD ? 2 : 1; }
+template <typename T> constexpr int des_depth() { return sizeof(T) == 2 ? 2 : 1; }
+constexpr int kBwdDepth = 1;
+
 __device__ __forceinline__ uint4 ld_global16(const void* p) {
   return *reinterpret_cast<const uint4*>(p);
 }
@@ -216,8 +222,10 @@ __device__ __forceinline__ void write_tile(T* dst, int64_t p0, const char* tile,
 }
 
 // The Gumbel rows of a tile: 16*M elements, contiguous in G.  GCH 16-byte
-// chunks per lane cover the largest tile (M = 16*MB).  In LDS each row has
-// stride GROW = 16*MB*sz + 16 bytes (only the first M elements are used).
+// chunks per lane cover the largest tile (M = 16*MB).  In LDS they keep the
+// same layout, element (row, j) at (row*M + j)*sz; reads of a padded slice
+// j >= M land on finite data (the next row, or the tile's zeroed tail) and
+// are masked by the -inf bias.
 template <typename T, int MB>
 struct GRegs {
   static constexpr int BYTES = 16 * 16 * MB * (int)sizeof(T);
@@ -237,48 +245,85 @@ __device__ __forceinline__ void load_g(GRegs<T, MB>& gr, const T* G, int64_t p0,
   const int nchunk = M * (int)sizeof(T);  // (16 rows * M * sz) / 16
   const char* base = reinterpret_cast<const char*>(G + p0 * M);
   if (p0 + 16 <= N) {
+    // lanes past the tile's chunks re-read its last chunk (never stored):
+    // selecting on the loaded data would make the compiler wait for it here,
+    // which would serialize the prefetch of the whole next tile
 #pragma unroll
     for (int k = 0; k < GRegs<T, MB>::GCH; ++k) {
-      const int q = lane + 64 * k;
-      gr.c[k] = q < nchunk ? ld_global16(base + (uint32_t)(16 * q)) : uint4{0, 0, 0, 0};
+      const int q = lane + 64 * k < nchunk ? lane + 64 * k : nchunk - 1;
+      gr.c[k] = ld_global16(base + (uint32_t)(16 * q));
     }
   } else {
-    // tail tile: element-wise, only elements of valid rows
+    // tail tile: element-wise, only elements of valid rows (assembled as
+    // 32-bit words, so that the full-tile path's data stay whole words)
     const int64_t nel = (N - p0) * M;
 #pragma unroll
     for (int k = 0; k < GRegs<T, MB>::GCH; ++k) {
       const int q = lane + 64 * k;
-      const T* e = reinterpret_cast<const T*>(base + 16 * q);
       const int64_t e0 = (int64_t)q * 16 / (int)sizeof(T);
-      T tmp[16 / sizeof(T)];
+      uint32_t wd[4];
 #pragma unroll
-      for (int u = 0; u < (int)(16 / sizeof(T)); ++u)
-        tmp[u] = (q < nchunk && e0 + u < nel) ? e[u] : from_f<T>(0.f);
-      gr.c[k] = *reinterpret_cast<uint4*>(tmp);
+      for (int d = 0; d < 4; ++d) {
+        if constexpr (sizeof(T) == 2) {
+          const unsigned short* e = reinterpret_cast<const unsigned short*>(G + p0 * M + e0 + 2 * d);
+          const uint32_t lo = (q < nchunk && e0 + 2 * d < nel) ? e[0] : 0u;
+          const uint32_t hi = (q < nchunk && e0 + 2 * d + 1 < nel) ? e[1] : 0u;
+          wd[d] = lo | (hi << 16);
+        } else {
+          const uint32_t* e = reinterpret_cast<const uint32_t*>(G + p0 * M + e0 + d);
+          wd[d] = (q < nchunk && e0 + d < nel) ? e[0] : 0u;
+        }
+        // opaque word: keeps the compiler from splitting the merge of the two
+        // paths into 16-bit halves (which would need the full-tile path's
+        // loaded data at the merge point, i.e. wait for the prefetch)
+        asm volatile("" : "+v"(wd[d]));
+      }
+      gr.c[k] = uint4{wd[0], wd[1], wd[2], wd[3]};
     }
   }
 }
 
 template <typename T, int MB>
 __device__ __forceinline__ void store_g(char* gt, const GRegs<T, MB>& gr, int M, bool hasG) {
-  constexpr int SZ = (int)sizeof(T);
-  constexpr int GROW = 16 * MB * SZ + 16;
+  // the tile is the 16 rows' 16*M contiguous elements, copied chunk by chunk
   const int lane = lane_id();
-  const int nchunk = M * SZ;
-  const int rch = (M * SZ) / 16;  // chunks per row when rows are 16-byte multiples
+  const int nchunk = M * (int)sizeof(T);
 #pragma unroll
   for (int k = 0; k < GRegs<T, MB>::GCH; ++k) {
     const int q = lane + 64 * k;
-    if (q >= nchunk) continue;
-    if ((M * SZ) % 16 == 0) {
-      const int row = q / rch, cc = q - row * rch;
-      *reinterpret_cast<uint4*>(gt + row * GROW + 16 * cc) = gr.c[k];
-    } else {
-      const T* e = reinterpret_cast<const T*>(&gr.c[k]);
+    if (q < nchunk) *reinterpret_cast<uint4*>(gt + 16 * q) = gr.c[k];
+  }
+}
+
+// One tile's rows in registers: x, dY (unused registers are dropped by the
+// compiler in the passes that do not read dY), and the Gumbel rows.
+template <typename T, int C, int MB>
+struct TileStage {
+  TileRegs<T, C> x, y;
+  GRegs<T, MB> g;
+};
+
+// Streams tiles [t0, t1) with DEPTH register stages: at the top of tile t
+// its stage is written to the wave's LDS tiles and immediately reloaded
+// with tile t + DEPTH, so DEPTH tiles of loads are in flight while body(t)
+// computes.  load(stage, tile) / store(stage) / body(tile).
+template <int DEPTH, typename Stage, typename Load, typename Store, typename Body>
+__device__ __forceinline__ void stream_tiles(int64_t t0, int64_t t1, Load load, Store store,
+                                             Body body) {
+  Stage st[DEPTH];
 #pragma unroll
-      for (int u = 0; u < 16 / SZ; ++u) {
-        const int el = q * (16 / SZ) + u, row = el / M, col = el - row * M;
-        *reinterpret_cast<T*>(gt + row * GROW + col * SZ) = e[u];
+  for (int d = 0; d < DEPTH; ++d)
+    if (t0 + d < t1) load(st[d], t0 + d);
+  for (int64_t t = t0; t < t1; t += DEPTH) {
+#pragma unroll
+    for (int d = 0; d < DEPTH; ++d) {
+      const int64_t tt = t + d;
+      if (tt < t1) {
+        wave_sync();
+        store(st[d]);
+        wave_sync();
+        if (tt + DEPTH < t1) load(st[d], tt + DEPTH);
+        body(tt);
       }
     }
   }
@@ -400,21 +445,21 @@ __device__ __forceinline__ void temperature_ps(const V (&acc)[MB + 1], const K32
 // beyond N get w = 0.  The Gumbel values are read transposed from the G tile
 // (rows 4g+i, column 16nb+r).
 template <typename T, int MB, typename V>
-__device__ __forceinline__ void softmax_ps(const V (&acc)[MB + 1], const char* gt, int gtr,
+__device__ __forceinline__ void softmax_ps(const V (&acc)[MB + 1], const char* gt, int M,
                                            const float (&bias)[MB], const float (&t)[4],
                                            float tau_min, int nvalid, float (&w)[MB][4],
                                            float (&tau)[4]) {
   using R = decltype(acc[0][0] + 0.f);
-  constexpr int GROW = 16 * MB * (int)sizeof(T) + 16;
   const int g = lane_id() >> 4;
+  const int r = lane_id() & 15;
   R u[MB][4];
 #pragma unroll
-  for (int nb = 0; nb < MB; ++nb) {
-    K16<T> gv;
-    ld_tr<T>(gv, gt, gtr, 16 * nb * (int)sizeof(T), GROW);
+  for (int nb = 0; nb < MB; ++nb)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) u[nb][i] = (R)acc[nb][i] + (R)bias[nb] + (R)k16_elem(gv, i);
-  }
+    for (int i = 0; i < 4; ++i) {
+      const float gv = to_f<T>(reinterpret_cast<const T*>(gt)[(4 * g + i) * M + 16 * nb + r]);
+      u[nb][i] = (R)acc[nb][i] + (R)bias[nb] + (R)gv;
+    }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     tau[i] = fmaxf(t[i], tau_min);
@@ -443,13 +488,12 @@ __device__ __forceinline__ void softmax_ps(const V (&acc)[MB + 1], const char* g
 // fma, u k - m k (its rounding error, relative to u k, stays far below the
 // bf16 tolerance); fp32 storage keeps the shift before the scale.
 template <typename T, int MB, typename V>
-__device__ __forceinline__ void softmax_sp(const V (&acc)[MB + 1], const char* gt,
+__device__ __forceinline__ void softmax_sp(const V (&acc)[MB + 1], const char* gt, int M,
                                            const float (&bias)[MB][4], float t, float tau_min,
                                            int nvalid, float (&w)[MB][4], float (&zs)[MB][4],
                                            float& tau) {
   using R = decltype(acc[0][0] + 0.f);
   constexpr int SZ = (int)sizeof(T);
-  constexpr int GROW = 16 * MB * SZ + 16;
   const int r = lane_id() & 15, g = lane_id() >> 4;
   tau = fmaxf(t, tau_min);
   const R k = (R)(kLog2e * fast_rcp(tau));
@@ -458,15 +502,20 @@ __device__ __forceinline__ void softmax_sp(const V (&acc)[MB + 1], const char* g
 #pragma unroll
   for (int nb = 0; nb < MB; ++nb) {
     float gv[4];
-    const char* p = gt + r * GROW + (16 * nb + 4 * g) * SZ;
-    if constexpr (SZ == 2) {
-      const bf16x4 q = *reinterpret_cast<const bf16x4*>(p);
+    const int e = r * M + 16 * nb + 4 * g;  // element index in the G tile
+    if (M % 4 == 0) {                        // 4 aligned elements
+      if constexpr (SZ == 2) {
+        const bf16x4 q = *reinterpret_cast<const bf16x4*>(gt + e * SZ);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) gv[i] = (float)q[i];
+        for (int i = 0; i < 4; ++i) gv[i] = (float)q[i];
+      } else {
+        const f32x4 q = *reinterpret_cast<const f32x4*>(gt + e * SZ);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) gv[i] = q[i];
+      }
     } else {
-      const f32x4 q = *reinterpret_cast<const f32x4*>(p);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) gv[i] = q[i];
+      for (int i = 0; i < 4; ++i) gv[i] = to_f<T>(reinterpret_cast<const T*>(gt)[e + i]);
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -586,33 +635,27 @@ k_aggregate(StreamArgs a) {
   int64_t t0, t1;
   tile_range(a.N, WAVES, wave, t0, t1);
 
-  TileRegs<T, C> xr, yr;
-  GRegs<T, MB> gr;
-  if (t0 < t1) {
-    load_tile<T, C>(xr, X, t0 * 16, a.N);
-    if constexpr (BWD) load_tile<T, C>(yr, Y, t0 * 16, a.N);
-    load_g<T, MB>(gr, Gp, t0 * 16, a.N, a.M, hasG);
-  }
-  for (int64_t t = t0; t < t1; ++t) {
+  using Stage = TileStage<T, C, MB>;
+  auto load = [&](Stage& st, int64_t tile) {
+    load_tile<T, C>(st.x, X, tile * 16, a.N);
+    if constexpr (BWD) load_tile<T, C>(st.y, Y, tile * 16, a.N);
+    load_g<T, MB>(st.g, Gp, tile * 16, a.N, a.M, hasG);
+  };
+  auto store = [&](const Stage& st) {
+    store_tile<T, C>(xt, st.x);
+    if constexpr (BWD) store_tile<T, C>(yt, st.y);
+    store_g<T, MB>(gt, st.g, a.M, hasG);
+  };
+  stream_tiles<agg_depth<T, BWD>(), Stage>(t0, t1, load, store, [&](int64_t t) {
     const int64_t p0 = t * 16;
     const int nvalid = (int)(a.N - p0 < 16 ? a.N - p0 : 16);
-    wave_sync();
-    store_tile<T, C>(xt, xr);
-    if constexpr (BWD) store_tile<T, C>(yt, yr);
-    store_g<T, MB>(gt, gr, a.M, hasG);
-    wave_sync();
-    if (t + 1 < t1) {
-      load_tile<T, C>(xr, X, p0 + 16, a.N);
-      if constexpr (BWD) load_tile<T, C>(yr, Y, p0 + 16, a.N);
-      load_g<T, MB>(gr, Gp, p0 + 16, a.N, a.M, hasG);
-    }
 
     typename LAcc<T, true>::v lg[MB + 1];
     K32<T> xa[G_::XF];
     logits<T, C, MB, true, (SZ == 4)>(lg, xa, xt, tabL, lb);
     float w[MB][4], zs[MB][4], tau;
     const float tt = temperature_own<T, C, MB>(lg, xa, tabL, lb.a, a.tb);
-    softmax_sp<T, MB>(lg, gt, bias, tt, a.tau_min, nvalid, w, zs, tau);
+    softmax_sp<T, MB>(lg, gt, a.M, bias, tt, a.tau_min, nvalid, w, zs, tau);
 
     // SP -> PS through the G tile (the softmax has read its Gumbel values)
     wave_sync();
@@ -636,7 +679,7 @@ k_aggregate(StreamArgs a) {
 #pragma unroll
           for (int nb = 0; nb < MB; ++nb) acc[nb][cb] = mma16(wt[nb], f.xb, acc[nb][cb]);
         });
-  }
+  });
 
   __syncthreads();  // every wave is done with the tables and tiles
   float* red = reinterpret_cast<float*>(smem);  // [M16][C] then den [M16]
@@ -704,30 +747,25 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kDeslice)))
   int64_t t0, t1;
   tile_range(a.N, WAVES, wave, t0, t1);
 
-  TileRegs<T, C> xr;
-  GRegs<T, MB> gr;
-  if (t0 < t1) {
-    load_tile<T, C>(xr, X, t0 * 16, a.N);
-    load_g<T, MB>(gr, Gp, t0 * 16, a.N, a.M, hasG);
-  }
-  for (int64_t t = t0; t < t1; ++t) {
+  using Stage = TileStage<T, C, MB>;
+  auto load = [&](Stage& st, int64_t tile) {
+    load_tile<T, C>(st.x, X, tile * 16, a.N);
+    load_g<T, MB>(st.g, Gp, tile * 16, a.N, a.M, hasG);
+  };
+  auto store = [&](const Stage& st) {
+    store_tile<T, C>(xt, st.x);
+    store_g<T, MB>(gt, st.g, a.M, hasG);
+  };
+  stream_tiles<des_depth<T>(), Stage>(t0, t1, load, store, [&](int64_t t) {
     const int64_t p0 = t * 16;
     const int nvalid = (int)(a.N - p0 < 16 ? a.N - p0 : 16);
-    wave_sync();
-    store_tile<T, C>(xt, xr);
-    store_g<T, MB>(gt, gr, a.M, hasG);
-    wave_sync();
-    if (t + 1 < t1) {
-      load_tile<T, C>(xr, X, p0 + 16, a.N);
-      load_g<T, MB>(gr, Gp, p0 + 16, a.N, a.M, hasG);
-    }
 
     typename LAcc<T, true>::v lg[MB + 1];
     K32<T> xa[G_::XF];
     logits<T, C, MB, true>(lg, xa, xt, tabL, lb);
     float w[MB][4], zs[MB][4], tau;
     const float tt = temperature_own<T, C, MB>(lg, xa, tabL, lb.a, a.tb);
-    softmax_sp<T, MB>(lg, gt, bias, tt, a.tau_min, nvalid, w, zs, tau);
+    softmax_sp<T, MB>(lg, gt, a.M, bias, tt, a.tau_min, nvalid, w, zs, tau);
 
     K16<T> wb[MB];
 #pragma unroll
@@ -747,7 +785,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kDeslice)))
         });
     wave_sync();
     write_tile<T, C>(Y, p0, xt, nvalid);
-  }
+  });
 }
 
 // ---------------------------------------------------------------------------
@@ -769,7 +807,6 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kWeights)))
   char* gt = xt + G_::XT;
   zero_lds(gt, G_::GT);
   const auto lb = logits_bases<T, C, MB, false>();
-  const int gtr = tr_base<T>(G_::GROW);
   float bias[MB];
 #pragma unroll
   for (int nb = 0; nb < MB; ++nb) bias[nb] = reinterpret_cast<const float*>(smem)[16 * nb + r];
@@ -795,7 +832,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kWeights)))
     logits<T, C, MB, false>(lg, xa, xt, tabL, lb);
     float w[MB][4], tau[4], tt[4];
     temperature_ps<T, C, MB>(lg, xa, tabL, lb.a, a.tb, tt);
-    softmax_ps<T, MB>(lg, gt, gtr, bias, tt, a.tau_min, nvalid, w, tau);
+    softmax_ps<T, MB>(lg, gt, a.M, bias, tt, a.tau_min, nvalid, w, tau);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int p = 4 * g + i;
@@ -898,34 +935,28 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
   int64_t t0, t1;
   tile_range(a.N, WAVES, wave, t0, t1);
 
-  TileRegs<T, C> xr, yr;
-  GRegs<T, MB> gr;
-  if (t0 < t1) {
-    load_tile<T, C>(xr, X, t0 * 16, a.N);
-    if (deslice) load_tile<T, C>(yr, Y, t0 * 16, a.N);
-    load_g<T, MB>(gr, Gp, t0 * 16, a.N, a.M, hasG);
-  }
-  for (int64_t t = t0; t < t1; ++t) {
+  using Stage = TileStage<T, C, MB>;
+  auto load = [&](Stage& st, int64_t tile) {
+    load_tile<T, C>(st.x, X, tile * 16, a.N);
+    if (deslice) load_tile<T, C>(st.y, Y, tile * 16, a.N);
+    load_g<T, MB>(st.g, Gp, tile * 16, a.N, a.M, hasG);
+  };
+  auto store = [&](const Stage& st) {
+    store_tile<T, C>(xt, st.x);
+    if (deslice) store_tile<T, C>(yt, st.y);
+    store_g<T, MB>(gt, st.g, a.M, hasG);
+  };
+  stream_tiles<kBwdDepth, Stage>(t0, t1, load, store, [&](int64_t t) {
     const int64_t p0 = t * 16;
     const int nvalid = (int)(a.N - p0 < 16 ? a.N - p0 : 16);
     const bool pv = r < nvalid;
-    wave_sync();
-    store_tile<T, C>(xt, xr);
-    if (deslice) store_tile<T, C>(yt, yr);
-    store_g<T, MB>(gt, gr, a.M, hasG);
-    wave_sync();
-    if (t + 1 < t1) {
-      load_tile<T, C>(xr, X, p0 + 16, a.N);
-      if (deslice) load_tile<T, C>(yr, Y, p0 + 16, a.N);
-      load_g<T, MB>(gr, Gp, p0 + 16, a.N, a.M, hasG);
-    }
 
     V lg[MB + 1];
     K32<T> xa[G_::XF];
     logits<T, C, MB, true>(lg, xa, xt, tabL, lb);
     float w[MB][4], zs[MB][4], tau;
     const float tt = temperature_own<T, C, MB>(lg, xa, tabL, lb.a, a.tb);
-    softmax_sp<T, MB>(lg, gt, bias, tt, a.tau_min, nvalid, w, zs, tau);
+    softmax_sp<T, MB>(lg, gt, a.M, bias, tt, a.tau_min, nvalid, w, zs, tau);
 
     // dw in the SP layout
     float dw[MB][4];
@@ -1080,7 +1111,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
 #pragma unroll
           for (int nb = 0; nb < MB; ++nb) dA[cb][nb] = mma16(f.xa, lp[nb], dA[cb][nb]);
         });
-  }
+  });
 
   // lane partials -> wave totals
 #pragma unroll
