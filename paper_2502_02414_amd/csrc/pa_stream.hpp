@@ -66,10 +66,13 @@ __device__ __forceinline__ uint4 ld_global16(const void* p) {
   return *reinterpret_cast<const uint4*>(p);
 }
 
+// Orders a wave's LDS accesses across lanes: its LDS writes have completed
+// (lgkmcnt) before any later LDS access, and the compiler moves no memory
+// access across it.  (A wavefront-scope fence would also wait for every
+// outstanding global load, i.e. for the tiles being prefetched.)
 __device__ __forceinline__ void wave_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
   __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
 // Software pipeline over N unrolled steps: the LDS reads of step i + D - 1
@@ -603,10 +606,9 @@ k_aggregate(StreamArgs a) {
   __syncthreads();
   const char* tabL = smem + G_::OFF_L;
   char* wreg = smem + G_::img_bytes(PASS) + wave * G_::wave_bytes(PASS);
-  char* xt = wreg;                          // x tile (logits)
-  char* yt = BWD ? wreg + G_::XT : wreg;    // tile contracted over points
-  char* gt = wreg + (BWD ? 2 : 1) * G_::XT; // Gumbel rows, then the weights
-  zero_lds(gt, G_::GT);
+  // x tile, (dY tile), Gumbel rows (then the transposed weights)
+  char* const wbuf = wreg + (BWD ? 2 : 1) * G_::XT;
+  zero_lds(wbuf, G_::GT);
   const auto lb = logits_bases<T, C, MB, true>();
   const int xtr = tr_base<T>(G_::XT_ROW);
   const int wtr = tr_base<T>(G_::GROW);
@@ -635,18 +637,8 @@ k_aggregate(StreamArgs a) {
   int64_t t0, t1;
   tile_range(a.N, WAVES, wave, t0, t1);
 
-  using Stage = TileStage<T, C, MB>;
-  auto load = [&](Stage& st, int64_t tile) {
-    load_tile<T, C>(st.x, X, tile * 16, a.N);
-    if constexpr (BWD) load_tile<T, C>(st.y, Y, tile * 16, a.N);
-    load_g<T, MB>(st.g, Gp, tile * 16, a.N, a.M, hasG);
-  };
-  auto store = [&](const Stage& st) {
-    store_tile<T, C>(xt, st.x);
-    if constexpr (BWD) store_tile<T, C>(yt, st.y);
-    store_g<T, MB>(gt, st.g, a.M, hasG);
-  };
-  stream_tiles<agg_depth<T, BWD>(), Stage>(t0, t1, load, store, [&](int64_t t) {
+  // one tile: xt (logits), yt (contracted over points), gt (Gumbel rows)
+  auto tile_body = [&](int64_t t, const char* xt, const char* yt, const char* gt) {
     const int64_t p0 = t * 16;
     const int nvalid = (int)(a.N - p0 < 16 ? a.N - p0 : 16);
 
@@ -657,17 +649,17 @@ k_aggregate(StreamArgs a) {
     const float tt = temperature_own<T, C, MB>(lg, xa, tabL, lb.a, a.tb);
     softmax_sp<T, MB>(lg, gt, a.M, bias, tt, a.tau_min, nvalid, w, zs, tau);
 
-    // SP -> PS through the G tile (the softmax has read its Gumbel values)
+    // SP -> PS through the weights buffer
     wave_sync();
 #pragma unroll
     for (int nb = 0; nb < MB; ++nb) {
       f32x4 v{w[nb][0], w[nb][1], w[nb][2], w[nb][3]};
-      stage4<T>(gt, wsb, 16 * nb * SZ, v);
+      stage4<T>(wbuf, wsb, 16 * nb * SZ, v);
     }
     wave_sync();
     K16<T> wt[MB];
 #pragma unroll
-    for (int nb = 0; nb < MB; ++nb) ld_tr<T>(wt[nb], gt, wtr, 16 * nb * SZ, G_::GROW);
+    for (int nb = 0; nb < MB; ++nb) ld_tr<T>(wt[nb], wbuf, wtr, 16 * nb * SZ, G_::GROW);
     if constexpr (!BWD) {
 #pragma unroll
       for (int nb = 0; nb < MB; ++nb) dacc[nb] = mma16(wt[nb], ones, dacc[nb]);
@@ -679,7 +671,26 @@ k_aggregate(StreamArgs a) {
 #pragma unroll
           for (int nb = 0; nb < MB; ++nb) acc[nb][cb] = mma16(wt[nb], f.xb, acc[nb][cb]);
         });
-  });
+  };
+
+  {
+    char* xt = wreg;
+    char* yt = BWD ? wreg + G_::XT : wreg;
+    char* gt = wbuf;  // the Gumbel rows are consumed before the weights are staged
+    using Stage = TileStage<T, C, MB>;
+    auto load = [&](Stage& st, int64_t tile) {
+      load_tile<T, C>(st.x, X, tile * 16, a.N);
+      if constexpr (BWD) load_tile<T, C>(st.y, Y, tile * 16, a.N);
+      load_g<T, MB>(st.g, Gp, tile * 16, a.N, a.M, hasG);
+    };
+    auto store = [&](const Stage& st) {
+      store_tile<T, C>(xt, st.x);
+      if constexpr (BWD) store_tile<T, C>(yt, st.y);
+      store_g<T, MB>(gt, st.g, a.M, hasG);
+    };
+    stream_tiles<agg_depth<T, BWD>(), Stage>(t0, t1, load, store,
+                                             [&](int64_t t) { tile_body(t, xt, yt, gt); });
+  }
 
   __syncthreads();  // every wave is done with the tables and tiles
   float* red = reinterpret_cast<float*>(smem);  // [M16][C] then den [M16]
