@@ -51,9 +51,11 @@ struct Geo {
          : OFF_2;
   }
   // per wave: x tile, (dY tile or output staging), Gumbel rows, scratch
+  // (the aggregating passes: the transposed weights)
   static constexpr int wave_bytes(int pass) {
     return (pass == kSliceBwd || pass == kWeightsBwd) ? 2 * XT + GT + SCR
-         : pass == kDesliceBwd ? 2 * XT + GT
+         : pass == kDesliceBwd ? 2 * XT + 2 * GT
+         : pass == kAggregate ? XT + 2 * GT
          : XT + GT;
   }
   // floats of one block's partial-sum record

@@ -200,22 +200,24 @@ hipError_t launch_prep(const PrepArgs& p, hipStream_t st) {
 __global__ void k_reduce(const float* __restrict__ parts, int P, int64_t rec, Segments seg) {
   // 16 record columns x 16 partial groups per block: each thread adds every
   // 16th partial (few dependent loads per thread), then the 16 group sums
-  // are added in a fixed tree order.
-  __shared__ float sh[16][17];
+  // are added in a fixed tree order.  The sums are formed in fp64: the
+  // records are signed partial sums (gradients) whose total can be far
+  // smaller than the sum of their magnitudes.
+  __shared__ double sh[16][17];
   const int kk = threadIdx.x & 15, pg = threadIdx.x >> 4;
   const int64_t k = (int64_t)blockIdx.x * 16 + kk;
-  float acc = 0.f;
+  double acc = 0.0;
   if (k < rec) {
 #pragma unroll 8
-    for (int p = pg; p < P; p += 16) acc += parts[(int64_t)p * rec + k];
+    for (int p = pg; p < P; p += 16) acc += (double)parts[(int64_t)p * rec + k];
   }
   sh[pg][kk] = acc;
   __syncthreads();
   if (pg == 0 && k < rec) {
-    float t[8];
+    double t[8];
 #pragma unroll
     for (int q = 0; q < 8; ++q) t[q] = sh[2 * q][kk] + sh[2 * q + 1][kk];
-    const float tot = ((t[0] + t[1]) + (t[2] + t[3])) + ((t[4] + t[5]) + (t[6] + t[7]));
+    const float tot = (float)(((t[0] + t[1]) + (t[2] + t[3])) + ((t[4] + t[5]) + (t[6] + t[7])));
     int64_t off = k;
     for (int i = 0; i < seg.n; ++i) {
       if (off < seg.len[i]) {

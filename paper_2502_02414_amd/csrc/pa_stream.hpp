@@ -57,9 +57,12 @@ struct StreamArgs {
 enum Flags { kHasG = 1, kStatesTerm = 2, kDesliceTerm = 4 };
 
 // Tiles of loads in flight per wave (register stages) in each streaming pass:
-// two for the bf16 forward passes, whose registers allow it.
-template <typename T, bool BWD> constexpr int agg_depth() { return sizeof(T) == 2 && !BWD ? 2 : 1; }
-template <typename T> constexpr int des_depth() { return sizeof(T) == 2 ? 2 : 1; }
+// two for the bf16 forward passes with up to 32 slices, whose registers
+// allow it.
+template <typename T, int MB, bool BWD> constexpr int agg_depth() {
+  return sizeof(T) == 2 && !BWD && MB <= 2 ? 2 : 1;
+}
+template <typename T, int MB> constexpr int des_depth() { return sizeof(T) == 2 && MB <= 2 ? 2 : 1; }
 constexpr int kBwdDepth = 1;
 
 __device__ __forceinline__ uint4 ld_global16(const void* p) {
@@ -176,21 +179,18 @@ struct TileRegs {
 template <typename T, int C>
 __device__ __forceinline__ void load_tile(TileRegs<T, C>& R, const T* base, int64_t p0,
                                           int64_t N) {
+  // rows past N re-read row N - 1 (finite data; their points are masked):
+  // no predicated loads, so the compiler can track these loads exactly
   constexpr int RCH = TileRegs<T, C>::RCH;
   const int lane = lane_id();
-  // uniform 64-bit row address + 32-bit lane offset (scalar-base addressing)
+  const int lim = N - 1 - p0 < 15 ? (int)(N - 1 - p0) : 15;  // last valid row of the tile
   const char* src = reinterpret_cast<const char*>(base + p0 * C);
-  if (p0 + 16 <= N) {
 #pragma unroll
-    for (int k = 0; k < TileRegs<T, C>::NCH; ++k)
-      R.c[k] = ld_global16(src + (uint32_t)(16 * lane + 1024 * k));
-  } else {
-#pragma unroll
-    for (int k = 0; k < TileRegs<T, C>::NCH; ++k) {
-      const int row = (lane + 64 * k) / RCH;
-      R.c[k] = (p0 + row < N) ? ld_global16(src + (uint32_t)(16 * lane + 1024 * k))
-                              : uint4{0, 0, 0, 0};
-    }
+  for (int k = 0; k < TileRegs<T, C>::NCH; ++k) {
+    const int q = lane + 64 * k;
+    const int row = q / RCH, cc = q - row * RCH;
+    const int rr = row < lim ? row : lim;
+    R.c[k] = ld_global16(src + (uint32_t)(rr * C * (int)sizeof(T) + 16 * cc));
   }
 }
 
@@ -237,53 +237,32 @@ struct GRegs {
 };
 
 template <typename T, int MB>
-__device__ __forceinline__ void load_g(GRegs<T, MB>& gr, const T* G, int64_t p0, int64_t N,
-                                       int M, bool hasG) {
-  if (!hasG) {  // no Gumbel noise: the tile's M columns are written as zeros
-#pragma unroll
-    for (int k = 0; k < GRegs<T, MB>::GCH; ++k) gr.c[k] = uint4{0, 0, 0, 0};
-    return;
-  }
+__device__ __forceinline__ void load_g(GRegs<T, MB>& gr, const T* G, const void* safe, int64_t p0,
+                                       int64_t N, int M, bool hasG) {
+  // A full tile's 16*M elements are whole 16-byte chunks (lanes past the last
+  // one re-read it).  Without noise, or for the tail tile, every lane reads
+  // the 16 bytes at `safe` instead, and the tile body rewrites the rows
+  // (g_fixup): no predicated loads, no partial chunks read past the end of G.
   const int lane = lane_id();
-  const int nchunk = M * (int)sizeof(T);  // (16 rows * M * sz) / 16
-  const char* base = reinterpret_cast<const char*>(G + p0 * M);
-  if (p0 + 16 <= N) {
-    // lanes past the tile's chunks re-read its last chunk (never stored):
-    // selecting on the loaded data would make the compiler wait for it here,
-    // which would serialize the prefetch of the whole next tile
+  const int nchunk = M * (int)sizeof(T);
+  const bool full = hasG && p0 + 16 <= N;
+  const char* src = full ? reinterpret_cast<const char*>(G + p0 * M)
+                         : reinterpret_cast<const char*>(safe);
 #pragma unroll
-    for (int k = 0; k < GRegs<T, MB>::GCH; ++k) {
-      const int q = lane + 64 * k < nchunk ? lane + 64 * k : nchunk - 1;
-      gr.c[k] = ld_global16(base + (uint32_t)(16 * q));
-    }
-  } else {
-    // tail tile: element-wise, only elements of valid rows (assembled as
-    // 32-bit words, so that the full-tile path's data stay whole words)
-    const int64_t nel = (N - p0) * M;
-#pragma unroll
-    for (int k = 0; k < GRegs<T, MB>::GCH; ++k) {
-      const int q = lane + 64 * k;
-      const int64_t e0 = (int64_t)q * 16 / (int)sizeof(T);
-      uint32_t wd[4];
-#pragma unroll
-      for (int d = 0; d < 4; ++d) {
-        if constexpr (sizeof(T) == 2) {
-          const unsigned short* e = reinterpret_cast<const unsigned short*>(G + p0 * M + e0 + 2 * d);
-          const uint32_t lo = (q < nchunk && e0 + 2 * d < nel) ? e[0] : 0u;
-          const uint32_t hi = (q < nchunk && e0 + 2 * d + 1 < nel) ? e[1] : 0u;
-          wd[d] = lo | (hi << 16);
-        } else {
-          const uint32_t* e = reinterpret_cast<const uint32_t*>(G + p0 * M + e0 + d);
-          wd[d] = (q < nchunk && e0 + d < nel) ? e[0] : 0u;
-        }
-        // opaque word: keeps the compiler from splitting the merge of the two
-        // paths into 16-bit halves (which would need the full-tile path's
-        // loaded data at the merge point, i.e. wait for the prefetch)
-        asm volatile("" : "+v"(wd[d]));
-      }
-      gr.c[k] = uint4{wd[0], wd[1], wd[2], wd[3]};
-    }
+  for (int k = 0; k < GRegs<T, MB>::GCH; ++k) {
+    const int q = lane + 64 * k < nchunk ? lane + 64 * k : nchunk - 1;
+    gr.c[k] = ld_global16(src + (full ? (uint32_t)(16 * q) : 0u));
   }
+}
+
+// Gumbel rows of a tile that load_g did not read (no noise: zeros; the tail
+// tile: its valid elements, element by element), written into the G tile.
+template <typename T, int MB>
+__device__ __forceinline__ void g_fixup(char* gt, const T* G, int64_t p0, int64_t N, int M,
+                                        bool hasG) {
+  const int64_t nel = hasG ? (N - p0 < 16 ? N - p0 : 16) * M : 0;
+  T* d = reinterpret_cast<T*>(gt);
+  for (int e = lane_id(); e < 16 * M; e += 64) d[e] = e < nel ? G[p0 * M + e] : from_f<T>(0.f);
 }
 
 template <typename T, int MB>
@@ -309,27 +288,34 @@ struct TileStage {
 // Streams tiles [t0, t1) with DEPTH register stages: at the top of tile t
 // its stage is written to the wave's LDS tiles and immediately reloaded
 // with tile t + DEPTH, so DEPTH tiles of loads are in flight while body(t)
-// computes.  load(stage, tile) / store(stage) / body(tile).
-template <int DEPTH, typename Stage, typename Load, typename Store, typename Body>
-__device__ __forceinline__ void stream_tiles(int64_t t0, int64_t t1, Load load, Store store,
-                                             Body body) {
-  Stage st[DEPTH];
+// computes.  The pipelined tiles are full ones (t < tfull = N / 16); every
+// stage is reloaded on every tile -- past the end with the current tile
+// again (an L2 hit) -- so all loads are unconditional and the compiler's
+// wait before a stage's store covers that stage only.  A partial last tile
+// is left to tail(t), after the loop.  load(stage, tile) / store(stage).
+template <int DEPTH, typename Stage, typename Load, typename Store, typename Body, typename Tail>
+__device__ __forceinline__ void stream_tiles(int64_t t0, int64_t t1, int64_t tfull, Load load,
+                                             Store store, Body body, Tail tail) {
+  const int64_t te = t1 < tfull ? t1 : tfull;
+  if (t0 < te) {
+    Stage st[DEPTH];
 #pragma unroll
-  for (int d = 0; d < DEPTH; ++d)
-    if (t0 + d < t1) load(st[d], t0 + d);
-  for (int64_t t = t0; t < t1; t += DEPTH) {
+    for (int d = 0; d < DEPTH; ++d) load(st[d], t0 + d < te ? t0 + d : te - 1);
+    for (int64_t t = t0; t < te; t += DEPTH) {
 #pragma unroll
-    for (int d = 0; d < DEPTH; ++d) {
-      const int64_t tt = t + d;
-      if (tt < t1) {
-        wave_sync();
-        store(st[d]);
-        wave_sync();
-        if (tt + DEPTH < t1) load(st[d], tt + DEPTH);
-        body(tt);
+      for (int d = 0; d < DEPTH; ++d) {
+        const int64_t tt = t + d;
+        if (tt < te) {
+          wave_sync();
+          store(st[d]);
+          wave_sync();
+          load(st[d], tt + DEPTH < te ? tt + DEPTH : tt);
+          body(tt);
+        }
       }
     }
   }
+  if (t0 <= te && te < t1) tail(te);  // this wave owns the partial last tile
 }
 
 // ---------------------------------------------------------------------------
@@ -606,9 +592,10 @@ k_aggregate(StreamArgs a) {
   __syncthreads();
   const char* tabL = smem + G_::OFF_L;
   char* wreg = smem + G_::img_bytes(PASS) + wave * G_::wave_bytes(PASS);
-  // x tile, (dY tile), Gumbel rows (then the transposed weights)
-  char* const wbuf = wreg + (BWD ? 2 : 1) * G_::XT;
-  zero_lds(wbuf, G_::GT);
+  // x tile, (dY tile), Gumbel rows, transposed weights
+  char* const gbuf = wreg + (BWD ? 2 : 1) * G_::XT;
+  char* const wbuf = gbuf + G_::GT;
+  zero_lds(gbuf, 2 * G_::GT);
   const auto lb = logits_bases<T, C, MB, true>();
   const int xtr = tr_base<T>(G_::XT_ROW);
   const int wtr = tr_base<T>(G_::GROW);
@@ -638,7 +625,7 @@ k_aggregate(StreamArgs a) {
   tile_range(a.N, WAVES, wave, t0, t1);
 
   // one tile: xt (logits), yt (contracted over points), gt (Gumbel rows)
-  auto tile_body = [&](int64_t t, const char* xt, const char* yt, const char* gt) {
+  auto tile_body = [&](int64_t t, const char* xt, const char* yt, char* gt) {
     const int64_t p0 = t * 16;
     const int nvalid = (int)(a.N - p0 < 16 ? a.N - p0 : 16);
 
@@ -676,20 +663,29 @@ k_aggregate(StreamArgs a) {
   {
     char* xt = wreg;
     char* yt = BWD ? wreg + G_::XT : wreg;
-    char* gt = wbuf;  // the Gumbel rows are consumed before the weights are staged
+    char* gt = gbuf;
     using Stage = TileStage<T, C, MB>;
     auto load = [&](Stage& st, int64_t tile) {
       load_tile<T, C>(st.x, X, tile * 16, a.N);
       if constexpr (BWD) load_tile<T, C>(st.y, Y, tile * 16, a.N);
-      load_g<T, MB>(st.g, Gp, tile * 16, a.N, a.M, hasG);
+      load_g<T, MB>(st.g, Gp, X, tile * 16, a.N, a.M, hasG);
     };
     auto store = [&](const Stage& st) {
       store_tile<T, C>(xt, st.x);
       if constexpr (BWD) store_tile<T, C>(yt, st.y);
-      store_g<T, MB>(gt, st.g, a.M, hasG);
+      if (hasG) store_g<T, MB>(gt, st.g, a.M, hasG);
     };
-    stream_tiles<agg_depth<T, BWD>(), Stage>(t0, t1, load, store,
-                                             [&](int64_t t) { tile_body(t, xt, yt, gt); });
+    auto tail = [&](int64_t t) {
+      Stage st;
+      load(st, t);
+      wave_sync();
+      store(st);
+      g_fixup<T, MB>(gt, Gp, t * 16, a.N, a.M, hasG);
+      wave_sync();
+      tile_body(t, xt, yt, gt);
+    };
+    stream_tiles<agg_depth<T, MB, BWD>(), Stage>(t0, t1, a.N / 16, load, store,
+                                             [&](int64_t t) { tile_body(t, xt, yt, gt); }, tail);
   }
 
   __syncthreads();  // every wave is done with the tables and tiles
@@ -761,13 +757,13 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kDeslice)))
   using Stage = TileStage<T, C, MB>;
   auto load = [&](Stage& st, int64_t tile) {
     load_tile<T, C>(st.x, X, tile * 16, a.N);
-    load_g<T, MB>(st.g, Gp, tile * 16, a.N, a.M, hasG);
+    load_g<T, MB>(st.g, Gp, X, tile * 16, a.N, a.M, hasG);
   };
   auto store = [&](const Stage& st) {
     store_tile<T, C>(xt, st.x);
-    store_g<T, MB>(gt, st.g, a.M, hasG);
+    if (hasG) store_g<T, MB>(gt, st.g, a.M, hasG);
   };
-  stream_tiles<des_depth<T>(), Stage>(t0, t1, load, store, [&](int64_t t) {
+  auto body = [&](int64_t t) {
     const int64_t p0 = t * 16;
     const int nvalid = (int)(a.N - p0 < 16 ? a.N - p0 : 16);
 
@@ -796,7 +792,17 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kDeslice)))
         });
     wave_sync();
     write_tile<T, C>(Y, p0, xt, nvalid);
-  });
+  };
+  auto tail = [&](int64_t t) {
+    Stage st;
+    load(st, t);
+    wave_sync();
+    store(st);
+    g_fixup<T, MB>(gt, Gp, t * 16, a.N, a.M, hasG);
+    wave_sync();
+    body(t);
+  };
+  stream_tiles<des_depth<T, MB>(), Stage>(t0, t1, a.N / 16, load, store, body, tail);
 }
 
 // ---------------------------------------------------------------------------
@@ -832,12 +838,16 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kWeights)))
   for (int64_t t = t0; t < t1; ++t) {
     const int64_t p0 = t * 16;
     load_tile<T, C>(xr, X, p0, a.N);
-    load_g<T, MB>(gr, Gp, p0, a.N, a.M, hasG);
+    load_g<T, MB>(gr, Gp, X, p0, a.N, a.M, hasG);
     const int nvalid = (int)(a.N - p0 < 16 ? a.N - p0 : 16);
     wave_sync();
     store_tile<T, C>(xt, xr);
     store_g<T, MB>(gt, gr, a.M, hasG);
     wave_sync();
+    if (!hasG || p0 + 16 > a.N) {  // Gumbel rows load_g did not read
+      g_fixup<T, MB>(gt, Gp, p0, a.N, a.M, hasG);
+      wave_sync();
+    }
     typename LAcc<T, false>::v lg[MB + 1];
     K32<T> xa[G_::XF];
     logits<T, C, MB, false>(lg, xa, xt, tabL, lb);
@@ -948,16 +958,18 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
 
   using Stage = TileStage<T, C, MB>;
   auto load = [&](Stage& st, int64_t tile) {
+    // dY is loaded unconditionally (x stands in without the deslice term),
+    // so that the loads are never predicated
     load_tile<T, C>(st.x, X, tile * 16, a.N);
-    if (deslice) load_tile<T, C>(st.y, Y, tile * 16, a.N);
-    load_g<T, MB>(st.g, Gp, tile * 16, a.N, a.M, hasG);
+    load_tile<T, C>(st.y, deslice ? Y : X, tile * 16, a.N);
+    load_g<T, MB>(st.g, Gp, X, tile * 16, a.N, a.M, hasG);
   };
   auto store = [&](const Stage& st) {
     store_tile<T, C>(xt, st.x);
     if (deslice) store_tile<T, C>(yt, st.y);
-    store_g<T, MB>(gt, st.g, a.M, hasG);
+    if (hasG) store_g<T, MB>(gt, st.g, a.M, hasG);
   };
-  stream_tiles<kBwdDepth, Stage>(t0, t1, load, store, [&](int64_t t) {
+  auto body = [&](int64_t t) {
     const int64_t p0 = t * 16;
     const int nvalid = (int)(a.N - p0 < 16 ? a.N - p0 : 16);
     const bool pv = r < nvalid;
@@ -1122,7 +1134,17 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
 #pragma unroll
           for (int nb = 0; nb < MB; ++nb) dA[cb][nb] = mma16(f.xa, lp[nb], dA[cb][nb]);
         });
-  });
+  };
+  auto tail = [&](int64_t t) {
+    Stage st;
+    load(st, t);
+    wave_sync();
+    store(st);
+    g_fixup<T, MB>(gt, Gp, t * 16, a.N, a.M, hasG);
+    wave_sync();
+    body(t);
+  };
+  stream_tiles<kBwdDepth, Stage>(t0, t1, a.N / 16, load, store, body, tail);
 
   // lane partials -> wave totals
 #pragma unroll

@@ -4,8 +4,9 @@ Each entry point of include/pa.h is fed the same seeded inputs as the oracle
 and compared by relative L2 per output tensor: <= 1e-5 for fp32 storage and
 <= 2e-2 for bf16 storage with fp32 accumulation.  Shapes span several
 16-point tiles with a ragged tail, ragged slice blocks (M not a multiple of
-16), M = 1, missing noise / Ada-Temp, the denominator floor, and the layer
-configurations of the benchmark suite.
+16), M = 1, missing noise / Ada-Temp, the denominator floor, the layer
+configurations of the benchmark suite, and sizes with several tiles per
+wave (the streaming passes' multi-tile pipeline).
 """
 import numpy as np
 import pytest
@@ -24,6 +25,11 @@ SHAPES = [
     (777, 64, 4, 33, "bf16"),
     (257, 128, 8, 1, "f32"),
     (517, 256, 8, 64, "bf16"),
+    # several 16-point tiles per wave: the streaming passes' register
+    # pipeline (a tile's stage reloaded while the previous tile computes)
+    (66013, 256, 8, 32, "bf16"),
+    (50003, 256, 8, 64, "bf16"),
+    (40007, 128, 8, 32, "f32"),
 ]
 IDS = [f"N{n}-C{c}-H{h}-M{m}-{d}" for n, c, h, m, d in SHAPES]
 
@@ -35,7 +41,7 @@ def check(name, gpu, ref, dt, tol=None):
     assert np.isfinite(e) and e <= bar, (name, e, bar)
 
 
-def check_ada_temp(out, ref, dt):
+def check_ada_temp(out, ref, dt, tol=None):
     """The Ada-Temp Linear (Eq. 3) has parameters (a, b_t); its gradient is
     checked as one tensor [da, db_t].  db_t alone is a sum over points of dt_i
     of both signs whose value is a fraction of a percent of sum |dt_i|, so on
@@ -43,7 +49,7 @@ def check_ada_temp(out, ref, dt):
     number."""
     g = np.concatenate([host(out["da"]).ravel(), host(out["db_t"]).ravel()])
     r = np.concatenate([np.asarray(ref["da"]).ravel(), [ref["db_t"]]])
-    check("d(a,b_t)", g, r, dt)
+    check("d(a,b_t)", g, r, dt, tol)
 
 
 def check_key_bias(gpu_dbk, gpu_dbq, dt="f32"):
@@ -209,6 +215,14 @@ def test_slice_weights_backward(cases, shape):
     check_ada_temp(out, ref, c.dt)
 
 
+# The chain feeds every call the previous calls' outputs instead of the
+# oracle's: each call meets TOL on oracle inputs (the per-call tests above),
+# and the backward of the slice projection (dx, dA through dnum = dS / den and
+# the softmax backward) amplifies the relative error of its inputs by a
+# small factor.  With fp32 storage the chain is held to 5x the per-call bar.
+CHAIN_TOL = {"f32": 5 * TOL["f32"], "bf16": TOL["bf16"]}
+
+
 @pytest.mark.parametrize("shape", SHAPES, ids=IDS)
 def test_layer_chain(cases, shape):
     """Forward then backward of the whole layer, GPU outputs feeding GPU calls."""
@@ -216,10 +230,10 @@ def test_layer_chain(cases, shape):
     c, g, (f, gr) = get_case(cases, shape)
     out = g.layer()
     for k in ("num", "den", "S", "Sp", "y"):
-        check(k, out[k], f[k], c.dt)
+        check(k, out[k], f[k], c.dt, CHAIN_TOL[c.dt])
     for k in ("dSp", "dS", "dWq", "dbq", "dWk", "dWv", "dbv", "dx", "dA", "db", "da"):
-        check(k, out[k], gr[k], c.dt)
-    check_ada_temp(out, gr, c.dt)
+        check(k, out[k], gr[k], c.dt, CHAIN_TOL[c.dt])
+    check_ada_temp(out, gr, c.dt, CHAIN_TOL[c.dt])
     check_key_bias(out["dbk"], out["dbq"], c.dt)
 
 
