@@ -63,7 +63,7 @@ template <typename T, int MB, bool BWD> constexpr int agg_depth() {
   return sizeof(T) == 2 && !BWD && MB <= 2 ? 2 : 1;
 }
 template <typename T, int MB> constexpr int des_depth() { return sizeof(T) == 2 && MB <= 2 ? 2 : 1; }
-constexpr int kBwdDepth = 1;
+template <typename T, int MB> constexpr int bwd_depth() { return 1; }
 
 __device__ __forceinline__ uint4 ld_global16(const void* p) {
   return *reinterpret_cast<const uint4*>(p);
@@ -1144,7 +1144,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
     wave_sync();
     body(t);
   };
-  stream_tiles<kBwdDepth, Stage>(t0, t1, a.N / 16, load, store, body, tail);
+  stream_tiles<bwd_depth<T, MB>(), Stage>(t0, t1, a.N / 16, load, store, body, tail);
 
   // lane partials -> wave totals
 #pragma unroll
