@@ -226,8 +226,12 @@ pa_status pa_slice_aggregate(const pa_dims* dims, const void* x, const void* G,
   seg.dst[0] = num; seg.len[0] = (int64_t)dims->M * dims->C;
   seg.dst[1] = den; seg.len[1] = dims->M;
   seg.n = 2;
+  seg.S = S;
+  seg.nS = (int64_t)dims->M * dims->C;
+  seg.den_col = seg.nS;
+  seg.C = dims->C;
+  seg.eps = dims->eps;
   PA_HIP(pa::launch_reduce(L.partials, L.P, L.rec, seg, st), "reduce");
-  PA_HIP(pa::launch_states(num, den, S, dims->M, dims->C, dims->eps, st), "states");
   return PA_OK;
 }
 
@@ -403,12 +407,9 @@ pa_status reduce_slice_grads(const pa_dims& d, const pa::StreamLaunch& L,
   seg.dst[0] = gr->dA; seg.len[0] = (int64_t)d.C * d.M;
   seg.dst[1] = gr->db; seg.len[1] = d.M;
   seg.dst[2] = gr->da; seg.len[2] = d.C;
-  seg.dst[3] = gr->db_t ? gr->db_t : gr->dtau0; seg.len[3] = 1;
+  seg.dst[3] = gr->db_t; seg.dst2[3] = gr->dtau0; seg.len[3] = 1;  // d tau0 = d b_t
   seg.n = 4;
   PA_HIP(pa::launch_reduce(L.partials, L.P, L.rec, seg, st), "reduce");
-  if (gr->db_t && gr->dtau0)
-    PA_HIP(hipMemcpyAsync(gr->dtau0, gr->db_t, sizeof(float), hipMemcpyDeviceToDevice, st),
-           "dtau0 copy");
   return PA_OK;
 }
 

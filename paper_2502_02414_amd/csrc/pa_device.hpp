@@ -105,6 +105,20 @@ __device__ __forceinline__ f32x4 mma16(const K16<float>& a, const K16<float>& b,
   return c;
 }
 
+// Two K16 products as one: the concatenated fragments pair the same
+// elements (lane group g: a0 with b0, a1 with b1), so one K32 MFMA gives the
+// sum of both products (bf16); fp32 runs the two products.
+__device__ __forceinline__ f32x4 mma16x2(const K16<bf16>& a0, const K16<bf16>& b0,
+                                         const K16<bf16>& a1, const K16<bf16>& b1, f32x4 c) {
+  const bf16x8 a = __builtin_shufflevector(a0.v, a1.v, 0, 1, 2, 3, 4, 5, 6, 7);
+  const bf16x8 b = __builtin_shufflevector(b0.v, b1.v, 0, 1, 2, 3, 4, 5, 6, 7);
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mma16x2(const K16<float>& a0, const K16<float>& b0,
+                                         const K16<float>& a1, const K16<float>& b1, f32x4 c) {
+  return mma16(a1, b1, mma16(a0, b0, c));
+}
+
 // K16 fragment from four floats (rounded to the operand type).
 __device__ __forceinline__ void set_k16(K16<bf16>& f, float a, float b, float c, float d) {
   f.v[0] = (bf16)a; f.v[1] = (bf16)b; f.v[2] = (bf16)c; f.v[3] = (bf16)d;

@@ -54,17 +54,21 @@ hipError_t launch_prep(const PrepArgs& p, hipStream_t st);
 size_t image_bytes(int pass, int dtype, int C, int MB);
 
 // out[k] = sum_{p < P} partials[p * rec + k] (k < rec), in order p = 0..P-1,
-// scattered into up to 6 destination segments.
+// scattered into up to 6 destination segments (each written to dst[i] and,
+// if given, also to dst2[i]).  With S set, the first nS columns are the
+// numerators [M,C] of Eq. 1 and the states S = num / max(den, eps) are
+// written too, den_j being column den_col + j reduced in the same order.
 struct Segments {
   float* dst[6];
+  float* dst2[6];
   int64_t len[6];
   int n;
+  float* S;
+  int64_t nS, den_col;
+  int C;
+  float eps;
 };
 hipError_t launch_reduce(const float* partials, int P, int64_t rec, const Segments& seg,
-                         hipStream_t st);
-
-// S = num / max(den, eps)
-hipError_t launch_states(const float* num, const float* den, float* S, int M, int C, float eps,
                          hipStream_t st);
 
 // Token-side products (fp32, M <= 64 rows):

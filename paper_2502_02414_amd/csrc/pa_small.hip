@@ -5,7 +5,7 @@
 //     padded as in pa_layout.h);
 //   - the ordered reduction of per-block partial-sum records (the partial
 //     sums of Section 4.2, here over point chunks of one GPU);
-//   - the states s_j = num_j / max(den_j, eps) (Eq. 1);
+//     with the states s_j = num_j / max(den_j, eps) (Eq. 1) formed there;
 // (token attention lives in pa_tokens.hip).
 #include "pa_device.hpp"
 #include "pa_internal.h"
@@ -195,36 +195,56 @@ hipError_t launch_prep(const PrepArgs& p, hipStream_t st) {
 }
 
 // ---------------------------------------------------------------------------
-// Ordered reduction of partial records
+// Ordered reduction of partial records (and the states of Eq. 1)
 // ---------------------------------------------------------------------------
+// Fixed-order sum of the 16 group sums of one column.
+__device__ __forceinline__ float group_total(const double (&t16)[16]) {
+  double t[8];
+#pragma unroll
+  for (int q = 0; q < 8; ++q) t[q] = t16[2 * q] + t16[2 * q + 1];
+  return (float)(((t[0] + t[1]) + (t[2] + t[3])) + ((t[4] + t[5]) + (t[6] + t[7])));
+}
+
 __global__ void k_reduce(const float* __restrict__ parts, int P, int64_t rec, Segments seg) {
   // 16 record columns x 16 partial groups per block: each thread adds every
   // 16th partial (few dependent loads per thread), then the 16 group sums
   // are added in a fixed tree order.  The sums are formed in fp64: the
   // records are signed partial sums (gradients) whose total can be far
-  // smaller than the sum of their magnitudes.
-  __shared__ double sh[16][17];
+  // smaller than the sum of their magnitudes.  A block of numerator columns
+  // (16 columns of one slice j, as 16 divides C) also forms den_j, in the
+  // same order as den_j's own block, for the states.
+  __shared__ double sh[17][16];
   const int kk = threadIdx.x & 15, pg = threadIdx.x >> 4;
-  const int64_t k = (int64_t)blockIdx.x * 16 + kk;
+  const int64_t k0 = (int64_t)blockIdx.x * 16, k = k0 + kk;
+  const bool states = seg.S != nullptr && k0 < seg.nS;
   double acc = 0.0;
   if (k < rec) {
 #pragma unroll 8
     for (int p = pg; p < P; p += 16) acc += (double)parts[(int64_t)p * rec + k];
   }
-  sh[pg][kk] = acc;
+  sh[kk][pg] = acc;
+  if (states && kk == 0) {
+    const int64_t dc = seg.den_col + k0 / seg.C;
+    double ad = 0.0;
+#pragma unroll 8
+    for (int p = pg; p < P; p += 16) ad += (double)parts[(int64_t)p * rec + dc];
+    sh[16][pg] = ad;
+  }
   __syncthreads();
   if (pg == 0 && k < rec) {
-    double t[8];
-#pragma unroll
-    for (int q = 0; q < 8; ++q) t[q] = sh[2 * q][kk] + sh[2 * q + 1][kk];
-    const float tot = (float)(((t[0] + t[1]) + (t[2] + t[3])) + ((t[4] + t[5]) + (t[6] + t[7])));
+    const float tot = group_total(sh[kk]);
     int64_t off = k;
     for (int i = 0; i < seg.n; ++i) {
       if (off < seg.len[i]) {
         if (seg.dst[i]) seg.dst[i][off] = tot;
+        if (seg.dst2[i]) seg.dst2[i][off] = tot;
         break;
       }
       off -= seg.len[i];
+    }
+    if (states && k < seg.nS) {
+      const float den = group_total(sh[16]);
+      seg.S[k] = tot / (den >= seg.eps ? den : seg.eps);
     }
   }
 }
@@ -232,28 +252,11 @@ __global__ void k_reduce(const float* __restrict__ parts, int P, int64_t rec, Se
 hipError_t launch_reduce(const float* partials, int P, int64_t rec, const Segments& seg,
                          hipStream_t st) {
   if (!partials || P < 1 || rec < 1) return hipErrorInvalidValue;
+  if (seg.S && (seg.C < 16 || seg.C % 16 || seg.nS > rec || seg.den_col < 0 ||
+                seg.den_col + seg.nS / seg.C > rec))
+    return hipErrorInvalidValue;
   const int blocks = (int)((rec + 15) / 16);
   hipLaunchKernelGGL(k_reduce, dim3(blocks), dim3(256), 0, st, partials, P, rec, seg);
-  return hipGetLastError();
-}
-
-// ---------------------------------------------------------------------------
-// States
-// ---------------------------------------------------------------------------
-__global__ void k_states(const float* num, const float* den, float* S, int M, int C, float eps) {
-  const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (k >= (int64_t)M * C) return;
-  const int j = (int)(k / C);
-  const float d = den[j] >= eps ? den[j] : eps;
-  S[k] = num[k] / d;
-}
-
-hipError_t launch_states(const float* num, const float* den, float* S, int M, int C, float eps,
-                         hipStream_t st) {
-  if (!num || !den || !S) return hipErrorInvalidValue;
-  const int64_t n = (int64_t)M * C;
-  hipLaunchKernelGGL(k_states, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, num, den, S,
-                     M, C, eps);
   return hipGetLastError();
 }
 

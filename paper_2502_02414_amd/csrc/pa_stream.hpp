@@ -787,7 +787,20 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kDeslice)))
         [&](int cb, F& f) {
           f32x4 d = zero4();
 #pragma unroll
-          for (int nb = 0; nb < MB; ++nb) d = mma16(f.s[nb], wb[nb], d);
+          for (int nb = 0; nb + 1 < MB; nb += 2)
+            d = mma16x2(f.s[nb], wb[nb], f.s[nb + 1], wb[nb + 1], d);
+          if constexpr (MB % 2 == 1) {
+            // the odd product stays a K32 MFMA (zero second half): one MFMA
+            // shape per accumulator chain (a 16x16x16 MFMA taking the
+            // accumulator of a preceding 16x16x32 one gave wrong sums)
+            if constexpr (SZ == 2) {
+              K16<T> z;
+              set_k16(z, 0.f, 0.f, 0.f, 0.f);
+              d = mma16x2(f.s[MB - 1], wb[MB - 1], z, z, d);
+            } else {
+              d = mma16(f.s[MB - 1], wb[MB - 1], d);
+            }
+          }
           stage4<T>(xt, stb, 16 * cb * SZ, d);
         });
     wave_sync();
@@ -1083,12 +1096,12 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
           f.cn = *reinterpret_cast<const f32x4*>(cN + 16 * cb + 4 * g);
         },
         [&](int cb, FX& f) {
+          // the 2 MB products [A^T | dnum - cN] x [dl ; w], two per MFMA
+          auto fa = [&](int q) -> const K16<T>& { return q < MB ? f.ta[q] : f.tn[q - MB]; };
+          auto fb = [&](int q) -> const K16<T>& { return q < MB ? lbk[q] : wb[q - MB]; };
           f32x4 d = zero4();
 #pragma unroll
-          for (int nb = 0; nb < MB; ++nb) {
-            d = mma16(f.ta[nb], lbk[nb], d);
-            d = mma16(f.tn[nb], wb[nb], d);
-          }
+          for (int q = 0; q < 2 * MB; q += 2) d = mma16x2(fa(q), fb(q), fa(q + 1), fb(q + 1), d);
           // + a dt, + cN: the table rows hold dnum_j - cN, and sum_j w_j = 1
 #pragma unroll
           for (int i = 0; i < 4; ++i) d[i] += f.av[i] * dt + f.cn[i];
