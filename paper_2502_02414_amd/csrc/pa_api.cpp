@@ -265,8 +265,10 @@ AttnWs attn_ws(const pa_dims& d, void* ws) {
   return a;
 }
 
-pa_status attn_forward(const pa_dims& d, const float* S, const pa_attn_params* ap, float* Sp,
-                       const AttnWs& w, hipStream_t st) {
+// General path (heads too large for the fused kernel): Q, K, V, P, O in the
+// workspace, O -> Sp when Sp is wanted and there is no output projection.
+pa_status attn_forward_general(const pa_dims& d, const float* S, const pa_attn_params* ap,
+                               float* Sp, const AttnWs& w, hipStream_t st) {
   const int M = d.M, C = d.C;
   pa::Proj q{};
   q.n = 3; q.M = M; q.Cin = C; q.Cout = C;
@@ -275,18 +277,18 @@ pa_status attn_forward(const pa_dims& d, const float* S, const pa_attn_params* a
   q.b[0] = ap->bq; q.b[1] = ap->bk; q.b[2] = ap->bv;
   q.out[0] = w.Q; q.out[1] = w.K; q.out[2] = w.V;
   PA_HIP(pa::launch_proj(q, st), "QKV projection");
-  // the heads' output goes straight to Sp only when Sp is wanted and there is
-  // no output projection; otherwise (and for the backward's recompute, which
-  // passes Sp = NULL) it goes to the workspace.
   float* O = (ap->Wo || !Sp) ? w.O : Sp;
   PA_HIP(pa::launch_attn_core(w.Q, w.K, w.V, w.P, O, M, C, d.H, st), "attention core");
-  if (ap->Wo && Sp) {
-    pa::Proj o{};
-    o.n = 1; o.M = M; o.Cin = C; o.Cout = C;
-    o.in[0] = w.O; o.W[0] = ap->Wo; o.b[0] = ap->bo; o.out[0] = Sp;
-    PA_HIP(pa::launch_proj(o, st), "output projection");
-  }
   return PA_OK;
+}
+
+pa::HeadArgs head_args(const pa_dims& d, const float* S, const pa_attn_params* ap) {
+  pa::HeadArgs h{};
+  h.S = S;
+  h.W[0] = ap->Wq; h.W[1] = ap->Wk; h.W[2] = ap->Wv;
+  h.b[0] = ap->bq; h.b[1] = ap->bk; h.b[2] = ap->bv;
+  h.geo.M = d.M; h.geo.C = d.C; h.geo.H = d.H;
+  return h;
 }
 }  // namespace
 
@@ -295,7 +297,25 @@ pa_status pa_token_attention(const pa_dims* dims, const float* S, const pa_attn_
   PA_TRY(check_attn(dims, S, ap));
   PA_TRY(check_ptr(Sp, "Sp", true));
   PA_TRY(check_ws(*dims, ws, ws_bytes));
-  return attn_forward(*dims, S, ap, Sp, attn_ws(*dims, ws), as_stream(stream));
+  hipStream_t st = as_stream(stream);
+  const pa_dims& d = *dims;
+  const AttnWs w = attn_ws(d, ws);
+  // the heads' output: straight to Sp without an output projection
+  float* O = ap->Wo ? w.O : Sp;
+  if (pa::head_fits(d.M, d.C, d.H)) {
+    pa::HeadArgs h = head_args(d, S, ap);
+    h.O = O;
+    PA_HIP(pa::launch_head(h, false, st), "attention heads");
+  } else {
+    PA_TRY(attn_forward_general(d, S, ap, Sp, w, st));
+  }
+  if (ap->Wo) {
+    pa::Proj o{};
+    o.n = 1; o.M = d.M; o.Cin = d.C; o.Cout = d.C;
+    o.in[0] = w.O; o.W[0] = ap->Wo; o.b[0] = ap->bo; o.out[0] = Sp;
+    PA_HIP(pa::launch_proj(o, st), "output projection");
+  }
+  return PA_OK;
 }
 
 pa_status pa_token_attention_backward(const pa_dims* dims, const float* S,
@@ -311,9 +331,9 @@ pa_status pa_token_attention_backward(const pa_dims* dims, const float* S,
   }
   PA_TRY(check_ws(*dims, ws, ws_bytes));
   hipStream_t st = as_stream(stream);
-  const int M = dims->M, C = dims->C;
-  const AttnWs w = attn_ws(*dims, ws);
-  PA_TRY(attn_forward(*dims, S, ap, nullptr, w, st));  // Q, K, V, P, O
+  const pa_dims& d = *dims;
+  const int M = d.M, C = d.C;
+  const AttnWs w = attn_ws(d, ws);
   const float* dO = dSp;
   if (ap->Wo) {
     pa::Proj q{};  // dO = dSp Wo^T
@@ -321,41 +341,38 @@ pa_status pa_token_attention_backward(const pa_dims* dims, const float* S,
     q.in[0] = dSp; q.W[0] = ap->Wo; q.out[0] = w.dO;
     PA_HIP(pa::launch_proj(q, st), "dO");
     dO = w.dO;
-    if (ag && ag->dWo) {
-      pa::Outer o{};
-      o.n = 1; o.M = M; o.C = C; o.S = w.O; o.dX[0] = dSp; o.out[0] = ag->dWo;
-      PA_HIP(pa::launch_outer(o, st), "dWo");
-    }
-    if (ag && ag->dbo) {
-      pa::ColSum cs{};
-      cs.n = 1; cs.M = M; cs.C = C; cs.in[0] = dSp; cs.out[0] = ag->dbo;
-      PA_HIP(pa::launch_colsum(cs, st), "dbo");
-    }
   }
-  PA_HIP(pa::launch_attn_core_bwd(w.Q, w.K, w.V, w.P, dO, w.dQ, w.dK, w.dV, M, C, dims->H, st),
-         "attention core backward");
-  {
-    pa::Proj q{};  // dS = dQ Wq^T + dK Wk^T + dV Wv^T
-    q.n = 3; q.M = M; q.Cin = C; q.Cout = C; q.transW = 1; q.sum = 1;
-    q.in[0] = w.dQ; q.in[1] = w.dK; q.in[2] = w.dV;
-    q.W[0] = ap->Wq; q.W[1] = ap->Wk; q.W[2] = ap->Wv;
-    q.out[0] = dS;
-    PA_HIP(pa::launch_proj(q, st), "dS");
+  const bool wantWo = ag && ap->Wo && (ag->dWo || ag->dbo);
+  if (pa::head_fits(M, C, d.H)) {
+    pa::HeadArgs h = head_args(d, S, ap);  // recomputes the forward per head
+    h.dO = dO;
+    h.O = wantWo ? w.O : nullptr;
+    h.dX[0] = w.dQ; h.dX[1] = w.dK; h.dX[2] = w.dV;
+    PA_HIP(pa::launch_head(h, true, st), "attention heads backward");
+  } else {
+    PA_TRY(attn_forward_general(d, S, ap, nullptr, w, st));  // Q, K, V, P, O
+    PA_HIP(pa::launch_attn_core_bwd(w.Q, w.K, w.V, w.P, dO, w.dQ, w.dK, w.dV, M, C, d.H, st),
+           "attention core backward");
   }
+  // dS = dQ Wq^T + dK Wk^T + dV Wv^T; dW = S^T dX, db = 1^T dX; dWo = O^T dSp
+  pa::GradArgs g{};
+  g.M = M; g.C = C;
+  g.nS = 3; g.dS = dS;
+  g.X[0] = w.dQ; g.X[1] = w.dK; g.X[2] = w.dV;
+  g.W[0] = ap->Wq; g.W[1] = ap->Wk; g.W[2] = ap->Wv;
   if (ag) {
-    float* dW3[3] = {ag->dWq, ag->dWk, ag->dWv};
-    float* db3[3] = {ag->dbq, ag->dbk, ag->dbv};
-    const float* d3[3] = {w.dQ, w.dK, w.dV};
-    pa::Outer o{};
-    o.M = M; o.C = C; o.S = S;
-    for (int t = 0; t < 3; ++t)
-      if (dW3[t]) { o.dX[o.n] = d3[t]; o.out[o.n] = dW3[t]; ++o.n; }
-    if (o.n) PA_HIP(pa::launch_outer(o, st), "dW");
-    pa::ColSum cs{};
-    cs.n = 3; cs.M = M; cs.C = C;
-    for (int t = 0; t < 3; ++t) { cs.in[t] = d3[t]; cs.out[t] = db3[t]; }
-    if (db3[0] || db3[1] || db3[2]) PA_HIP(pa::launch_colsum(cs, st), "db");
+    float* dW4[4] = {ag->dWq, ag->dWk, ag->dWv, ag->dWo};
+    float* db4[4] = {ag->dbq, ag->dbk, ag->dbv, ag->dbo};
+    const float* B4[4] = {w.dQ, w.dK, w.dV, dSp};
+    const float* A4[4] = {S, S, S, w.O};
+    for (int t = 0; t < 4; ++t) {
+      if (!dW4[t] && !db4[t]) continue;
+      if (t == 3 && !ap->Wo) continue;
+      g.A[g.nO] = A4[t]; g.B[g.nO] = B4[t]; g.dW[g.nO] = dW4[t]; g.db[g.nO] = db4[t];
+      ++g.nO;
+    }
   }
+  PA_HIP(pa::launch_token_grads(g, st), "token gradients");
   return PA_OK;
 }
 

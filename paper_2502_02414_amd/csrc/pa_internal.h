@@ -83,21 +83,47 @@ struct Proj {
   int n, M, Cin, Cout, transW, sum;
 };
 hipError_t launch_proj(const Proj& q, hipStream_t st);
-// out_p [C,C] = S^T [C,M] dX_p [M,C]   (weight gradients)
-struct Outer {
-  const float* S;
-  const float* dX[3];
-  float* out[3];
-  int n, M, C;
+// Fused per-head token attention (one block per head, channels [hD, hD+D)):
+//   forward:  O_h = softmax(Q_h K_h^T / sqrt(D)) V_h with [Q|K|V]_h = S W_h + b_h
+//   backward: the same forward, then dQ_h, dK_h, dV_h from dO_h (and O_h if
+//             O is given).
+// M, C, H are set by the caller; launch_head fills the rest of the geometry
+// and returns hipErrorInvalidConfiguration when a head does not fit on chip
+// (head_fits tells beforehand).
+struct HeadGeo {
+  int M, C, H, D;
+  int M16, D16, MT, NT, T;  // padded rows / head columns, projection tiles
+  int KC, SR;               // K chunk, chunk row stride (floats)
+  size_t lds;
 };
-hipError_t launch_outer(const Outer& q, hipStream_t st);
-// out_p [C] = column sums of in_p [M,C]   (bias gradients; NULL out skipped)
-struct ColSum {
-  const float* in[3];
-  float* out[3];
-  int n, M, C;
+struct HeadArgs {
+  const float* S;     // [M,C]
+  const float* W[3];  // Wq, Wk, Wv [C,C]
+  const float* b[3];  // [C], nullable
+  const float* dO;    // [M,C] (backward)
+  float* O;           // [M,C] forward output; backward: nullable
+  float* dX[3];       // dQ, dK, dV [M,C] (backward)
+  HeadGeo geo;
 };
-hipError_t launch_colsum(const ColSum& q, hipStream_t st);
+bool head_fits(int M, int C, int H);
+hipError_t launch_head(HeadArgs a, bool bwd, hipStream_t st);
+// Parameter-side products of the token backward, one launch:
+//   dS = sum_{p < nS} X_p W_p^T           (X_p [M,C], W_p [C,C]; dS [M,C])
+//   dW_p = A_p^T B_p, db_p = 1^T B_p      (p < nO; A_p, B_p [M,C]; NULL
+//                                          outputs skipped)
+struct GradArgs {
+  const float* X[3];
+  const float* W[3];
+  int nS;
+  float* dS;
+  const float* A[4];
+  const float* B[4];
+  float* dW[4];
+  float* db[4];
+  int nO;
+  int M, C;
+};
+hipError_t launch_token_grads(const GradArgs& a, hipStream_t st);
 // Per-head attention core: P_h = softmax(Q_h K_h^T * scale), O_h = P_h V_h.
 hipError_t launch_attn_core(const float* Q, const float* K, const float* V, float* P, float* O,
                             int M, int C, int H, hipStream_t st);

@@ -159,6 +159,30 @@ def test_token_attention_backward(cases, shape):
     check_key_bias(ga["dbk"], ga["dbq"])
 
 
+# heads too large (D = C) or too narrow (D = 2) for the fused per-head
+# kernels: the general projection + core kernels
+GENERAL_HEADS = [(300, 128, 1, 64, "f32"), (300, 32, 16, 8, "f32")]
+
+
+@pytest.mark.parametrize("shape", GENERAL_HEADS,
+                         ids=[f"C{c}-H{h}-M{m}" for _, c, h, m, _ in GENERAL_HEADS])
+def test_token_attention_general_heads(cases, shape):
+    say(f"token_attention (general heads) {shape}")
+    c, g, (f, _) = get_case(cases, shape)
+    S = g.torch.from_numpy(f["S"].astype(np.float32)).cuda()
+    p = oracle_params(c)
+    check("Sp", g.attention(S), f["Sp"], "f32")
+    rng = np.random.default_rng(6)
+    dSp = g.torch.from_numpy(rng.standard_normal((c.M, c.C)).astype(np.float32)).cuda()
+    ga = g.attention_backward(S, dSp)
+    ref = oracle.token_attention_backward(S.cpu().numpy(), c.H, p["Wq"], p.get("bq"), p["Wk"],
+                                          p.get("bk"), p["Wv"], p.get("bv"), None, None,
+                                          dSp.cpu().numpy())
+    for k in ("dS", "dWq", "dbq", "dWk", "dWv", "dbv"):
+        check(k, ga[k], ref[k], "f32")
+    check_key_bias(ga["dbk"], ga["dbq"])
+
+
 def _slice_backward_ref(c, f, dS, Sp, use_dY):
     """Oracle of pa_slice_aggregate_backward for the given dS / Sp / dY."""
     p = oracle_params(c)
