@@ -57,16 +57,22 @@ struct StreamArgs {
 enum Flags { kHasG = 1, kStatesTerm = 2, kDesliceTerm = 4 };
 
 // Tiles of loads in flight per wave (register stages) in each streaming pass:
-// two for the bf16 forward passes with up to 32 slices, whose registers
-// allow it.
-template <typename T, int MB, bool BWD> constexpr int agg_depth() {
-  return sizeof(T) == 2 && !BWD && MB <= 2 ? 2 : 1;
-}
+// two for the bf16 deslice with up to 32 slices, whose registers allow it;
+// the aggregating passes stream 32-point tiles there (one stage holds as
+// many points as two).
+template <typename T, int MB, bool BWD> constexpr int agg_depth() { return 1; }
 template <typename T, int MB> constexpr int des_depth() { return sizeof(T) == 2 && MB <= 2 ? 2 : 1; }
 template <typename T, int MB> constexpr int bwd_depth() { return 1; }
 
+// Point-side tensors are streamed once per pass: their 16-byte loads and
+// stores are non-temporal (they neither displace nor leave dirty data in the
+// caches, so a pass does not pay for the previous pass's write-backs).
+typedef unsigned int nt_u32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ uint4 ld_global16(const void* p) {
-  return *reinterpret_cast<const uint4*>(p);
+  return __builtin_bit_cast(uint4, __builtin_nontemporal_load(reinterpret_cast<const nt_u32x4*>(p)));
+}
+__device__ __forceinline__ void st_global16(void* p, const uint4& v) {
+  __builtin_nontemporal_store(__builtin_bit_cast(nt_u32x4, v), reinterpret_cast<nt_u32x4*>(p));
 }
 
 // Orders a wave's LDS accesses across lanes: its LDS writes have completed
@@ -166,27 +172,33 @@ __device__ __forceinline__ void stage4(char* tile, int base, int off, const f32x
 
 // ---------------------------------------------------------------------------
 // Point tiles: HBM -> registers -> padded LDS rows, and staged outputs back.
-// Rows [p0, p0+16) of a [N,C] tensor are 16*C*SZ contiguous bytes; lane l
-// holds 16-byte chunks q = l + 64k.  Rows >= N are zero.
+// Rows [p0, p0+ROWS) of a [N,C] tensor are ROWS*C*SZ contiguous bytes; lane
+// l holds 16-byte chunks q = l + 64k.  Rows >= N re-read row N - 1 (finite
+// data; their points are masked).
 // ---------------------------------------------------------------------------
-template <typename T, int C>
+template <typename T, int C, int ROWS = 16>
 struct TileRegs {
   static constexpr int RCH = C * (int)sizeof(T) / 16;  // chunks per row
-  static constexpr int NCH = 16 * RCH / 64;            // chunks per lane
+  static constexpr int NCH = ROWS * RCH / 64;          // chunks per lane
   uint4 c[NCH];
 };
 
-template <typename T, int C>
-__device__ __forceinline__ void load_tile(TileRegs<T, C>& R, const T* base, int64_t p0,
+// Last valid row of the tile at p0 (at most ROWS - 1).
+template <int ROWS>
+__device__ __forceinline__ int last_row(int64_t p0, int64_t N) {
+  return N - 1 - p0 < ROWS - 1 ? (int)(N - 1 - p0) : ROWS - 1;
+}
+
+template <typename T, int C, int ROWS = 16>
+__device__ __forceinline__ void load_tile(TileRegs<T, C, ROWS>& R, const T* base, int64_t p0,
                                           int64_t N) {
-  // rows past N re-read row N - 1 (finite data; their points are masked):
   // no predicated loads, so the compiler can track these loads exactly
-  constexpr int RCH = TileRegs<T, C>::RCH;
+  constexpr int RCH = TileRegs<T, C, ROWS>::RCH;
   const int lane = lane_id();
-  const int lim = N - 1 - p0 < 15 ? (int)(N - 1 - p0) : 15;  // last valid row of the tile
+  const int lim = last_row<ROWS>(p0, N);
   const char* src = reinterpret_cast<const char*>(base + p0 * C);
 #pragma unroll
-  for (int k = 0; k < TileRegs<T, C>::NCH; ++k) {
+  for (int k = 0; k < TileRegs<T, C, ROWS>::NCH; ++k) {
     const int q = lane + 64 * k;
     const int row = q / RCH, cc = q - row * RCH;
     const int rr = row < lim ? row : lim;
@@ -194,13 +206,13 @@ __device__ __forceinline__ void load_tile(TileRegs<T, C>& R, const T* base, int6
   }
 }
 
-template <typename T, int C>
-__device__ __forceinline__ void store_tile(char* tile, const TileRegs<T, C>& R) {
-  constexpr int RCH = TileRegs<T, C>::RCH;
+template <typename T, int C, int ROWS = 16>
+__device__ __forceinline__ void store_tile(char* tile, const TileRegs<T, C, ROWS>& R) {
+  constexpr int RCH = TileRegs<T, C, ROWS>::RCH;
   constexpr int ROW = C * (int)sizeof(T) + 32;
   const int lane = lane_id();
 #pragma unroll
-  for (int k = 0; k < TileRegs<T, C>::NCH; ++k) {
+  for (int k = 0; k < TileRegs<T, C, ROWS>::NCH; ++k) {
     const int q = lane + 64 * k;
     const int row = q / RCH, cc = q - row * RCH;
     *reinterpret_cast<uint4*>(tile + lds_off(row, 16 * cc, ROW)) = R.c[k];
@@ -208,10 +220,10 @@ __device__ __forceinline__ void store_tile(char* tile, const TileRegs<T, C>& R) 
 }
 
 // Staged output tile (padded LDS rows) -> rows [p0, p0 + nvalid) of dst.
-template <typename T, int C>
+template <typename T, int C, int ROWS = 16>
 __device__ __forceinline__ void write_tile(T* dst, int64_t p0, const char* tile, int nvalid) {
-  constexpr int RCH = TileRegs<T, C>::RCH;
-  constexpr int NCH = TileRegs<T, C>::NCH;
+  constexpr int RCH = TileRegs<T, C, ROWS>::RCH;
+  constexpr int NCH = TileRegs<T, C, ROWS>::NCH;
   constexpr int ROW = C * (int)sizeof(T) + 32;
   const int lane = lane_id();
   char* d = reinterpret_cast<char*>(dst + p0 * C);
@@ -220,36 +232,76 @@ __device__ __forceinline__ void write_tile(T* dst, int64_t p0, const char* tile,
     const int q = lane + 64 * k;
     const int row = q / RCH, cc = q - row * RCH;
     const uint4 v = *reinterpret_cast<const uint4*>(tile + lds_off(row, 16 * cc, ROW));
-    if (row < nvalid) *reinterpret_cast<uint4*>(d + (uint32_t)(16 * lane + 1024 * k)) = v;
+    if (row < nvalid) st_global16(d + (uint32_t)(16 * lane + 1024 * k), v);
   }
 }
 
-// The Gumbel rows of a tile: 16*M elements, contiguous in G.  GCH 16-byte
+// The lane's K32 row fragments of a tile, straight from HBM in the MFMA
+// layout (the B operand of the logits): half h (rows 16h..16h+15), step s:
+// lane (r, g) holds elements [32s + 8g, +8) of row 16h + r, 16 or 32 bytes.
+template <typename T, int C, int ROWS>
+struct FragRegs {
+  static constexpr int XF = C / 32;
+  static constexpr int PER = 8 * (int)sizeof(T) / 16;  // 16-byte chunks per fragment
+  uint4 c[ROWS / 16][XF][PER];
+};
+
+template <typename T, int C, int ROWS>
+__device__ __forceinline__ void load_frags(FragRegs<T, C, ROWS>& F, const T* base, int64_t p0,
+                                           int64_t N) {
+  constexpr int SZ = (int)sizeof(T);
+  const int r = lane_id() & 15, g = lane_id() >> 4;
+  const int lim = last_row<ROWS>(p0, N);
+  const char* src = reinterpret_cast<const char*>(base + p0 * C);
+#pragma unroll
+  for (int h = 0; h < ROWS / 16; ++h) {
+    const int row = 16 * h + r < lim ? 16 * h + r : lim;
+#pragma unroll
+    for (int s = 0; s < C / 32; ++s)
+#pragma unroll
+      for (int q = 0; q < FragRegs<T, C, ROWS>::PER; ++q)
+        F.c[h][s][q] = ld_global16(src + (uint32_t)(row * C * SZ + (32 * s + 8 * g) * SZ + 16 * q));
+  }
+}
+
+template <typename T, int C, int ROWS>
+__device__ __forceinline__ K32<T> frag_of(const FragRegs<T, C, ROWS>& F, int h, int s) {
+  K32<T> k;
+  if constexpr (sizeof(T) == 2) {
+    k.v = __builtin_bit_cast(bf16x8, F.c[h][s][0]);
+  } else {
+    k.lo = __builtin_bit_cast(f32x4, F.c[h][s][0]);
+    k.hi = __builtin_bit_cast(f32x4, F.c[h][s][1]);
+  }
+  return k;
+}
+
+// The Gumbel rows of a tile: ROWS*M elements, contiguous in G.  GCH 16-byte
 // chunks per lane cover the largest tile (M = 16*MB).  In LDS they keep the
 // same layout, element (row, j) at (row*M + j)*sz; reads of a padded slice
 // j >= M land on finite data (the next row, or the tile's zeroed tail) and
 // are masked by the -inf bias.
-template <typename T, int MB>
+template <typename T, int MB, int ROWS = 16>
 struct GRegs {
-  static constexpr int BYTES = 16 * 16 * MB * (int)sizeof(T);
+  static constexpr int BYTES = ROWS * 16 * MB * (int)sizeof(T);
   static constexpr int GCH = (BYTES / 16 + 63) / 64;
   uint4 c[GCH];
 };
 
-template <typename T, int MB>
-__device__ __forceinline__ void load_g(GRegs<T, MB>& gr, const T* G, const void* safe, int64_t p0,
-                                       int64_t N, int M, bool hasG) {
-  // A full tile's 16*M elements are whole 16-byte chunks (lanes past the last
-  // one re-read it).  Without noise, or for the tail tile, every lane reads
-  // the 16 bytes at `safe` instead, and the tile body rewrites the rows
+template <typename T, int MB, int ROWS = 16>
+__device__ __forceinline__ void load_g(GRegs<T, MB, ROWS>& gr, const T* G, const void* safe,
+                                       int64_t p0, int64_t N, int M, bool hasG) {
+  // A full tile's ROWS*M elements are whole 16-byte chunks (lanes past the
+  // last one re-read it).  Without noise, or for the tail tile, every lane
+  // reads the 16 bytes at `safe` instead, and the tile body rewrites the rows
   // (g_fixup): no predicated loads, no partial chunks read past the end of G.
   const int lane = lane_id();
-  const int nchunk = M * (int)sizeof(T);
-  const bool full = hasG && p0 + 16 <= N;
+  const int nchunk = ROWS * M * (int)sizeof(T) / 16;
+  const bool full = hasG && p0 + ROWS <= N;
   const char* src = full ? reinterpret_cast<const char*>(G + p0 * M)
                          : reinterpret_cast<const char*>(safe);
 #pragma unroll
-  for (int k = 0; k < GRegs<T, MB>::GCH; ++k) {
+  for (int k = 0; k < GRegs<T, MB, ROWS>::GCH; ++k) {
     const int q = lane + 64 * k < nchunk ? lane + 64 * k : nchunk - 1;
     gr.c[k] = ld_global16(src + (full ? (uint32_t)(16 * q) : 0u));
   }
@@ -257,21 +309,21 @@ __device__ __forceinline__ void load_g(GRegs<T, MB>& gr, const T* G, const void*
 
 // Gumbel rows of a tile that load_g did not read (no noise: zeros; the tail
 // tile: its valid elements, element by element), written into the G tile.
-template <typename T, int MB>
+template <typename T, int MB, int ROWS = 16>
 __device__ __forceinline__ void g_fixup(char* gt, const T* G, int64_t p0, int64_t N, int M,
                                         bool hasG) {
-  const int64_t nel = hasG ? (N - p0 < 16 ? N - p0 : 16) * M : 0;
+  const int64_t nel = hasG ? (N - p0 < ROWS ? N - p0 : ROWS) * M : 0;
   T* d = reinterpret_cast<T*>(gt);
-  for (int e = lane_id(); e < 16 * M; e += 64) d[e] = e < nel ? G[p0 * M + e] : from_f<T>(0.f);
+  for (int e = lane_id(); e < ROWS * M; e += 64) d[e] = e < nel ? G[p0 * M + e] : from_f<T>(0.f);
 }
 
-template <typename T, int MB>
-__device__ __forceinline__ void store_g(char* gt, const GRegs<T, MB>& gr, int M, bool hasG) {
-  // the tile is the 16 rows' 16*M contiguous elements, copied chunk by chunk
+template <typename T, int MB, int ROWS = 16>
+__device__ __forceinline__ void store_g(char* gt, const GRegs<T, MB, ROWS>& gr, int M, bool hasG) {
+  // the tile is the rows' ROWS*M contiguous elements, copied chunk by chunk
   const int lane = lane_id();
-  const int nchunk = M * (int)sizeof(T);
+  const int nchunk = ROWS * M * (int)sizeof(T) / 16;
 #pragma unroll
-  for (int k = 0; k < GRegs<T, MB>::GCH; ++k) {
+  for (int k = 0; k < GRegs<T, MB, ROWS>::GCH; ++k) {
     const int q = lane + 64 * k;
     if (q < nchunk) *reinterpret_cast<uint4*>(gt + 16 * q) = gr.c[k];
   }
@@ -288,11 +340,15 @@ struct TileStage {
 // Streams tiles [t0, t1) with DEPTH register stages: at the top of tile t
 // its stage is written to the wave's LDS tiles and immediately reloaded
 // with tile t + DEPTH, so DEPTH tiles of loads are in flight while body(t)
-// computes.  The pipelined tiles are full ones (t < tfull = N / 16); every
-// stage is reloaded on every tile -- past the end with the current tile
-// again (an L2 hit) -- so all loads are unconditional and the compiler's
-// wait before a stage's store covers that stage only.  A partial last tile
-// is left to tail(t), after the loop.  load(stage, tile) / store(stage).
+// computes; body(t, stage) also gets the stage's registers as they were
+// before the reload (for operands used straight from registers).  The
+// pipelined tiles are full ones (t < tfull).  The main loop runs whole rounds
+// of DEPTH tiles with every stage reloaded on every tile -- past the end with
+// the current tile again (an L2 hit) -- so all loads are unconditional and
+// every path into the loop head has issued the stages in the same order:
+// the compiler's wait before a stage's store then covers that stage only.
+// The last (fewer than DEPTH) tiles, already loaded, follow the loop; a
+// partial last tile is left to tail(t).  load(stage, tile) / store(stage).
 template <int DEPTH, typename Stage, typename Load, typename Store, typename Body, typename Tail>
 __device__ __forceinline__ void stream_tiles(int64_t t0, int64_t t1, int64_t tfull, Load load,
                                              Store store, Body body, Tail tail) {
@@ -301,17 +357,26 @@ __device__ __forceinline__ void stream_tiles(int64_t t0, int64_t t1, int64_t tfu
     Stage st[DEPTH];
 #pragma unroll
     for (int d = 0; d < DEPTH; ++d) load(st[d], t0 + d < te ? t0 + d : te - 1);
-    for (int64_t t = t0; t < te; t += DEPTH) {
+    int64_t t = t0;
+    for (; t + DEPTH <= te; t += DEPTH) {
 #pragma unroll
       for (int d = 0; d < DEPTH; ++d) {
         const int64_t tt = t + d;
-        if (tt < te) {
-          wave_sync();
-          store(st[d]);
-          wave_sync();
-          load(st[d], tt + DEPTH < te ? tt + DEPTH : tt);
-          body(tt);
-        }
+        wave_sync();
+        store(st[d]);
+        wave_sync();
+        const Stage cur = st[d];
+        load(st[d], tt + DEPTH < te ? tt + DEPTH : tt);
+        body(tt, cur);
+      }
+    }
+#pragma unroll
+    for (int d = 0; d + 1 < DEPTH; ++d) {
+      if (t + d < te) {
+        wave_sync();
+        store(st[d]);
+        wave_sync();
+        body(t + d, st[d]);
       }
     }
   }
@@ -375,6 +440,39 @@ __device__ __forceinline__ void logits(typename LAcc<T, SP>::v (&acc)[MB + 1],
 #pragma unroll
         for (int nb = 0; nb < NT; ++nb)
           acc[nb] = SP ? mma_acc(f.t[nb], x, acc[nb]) : mma_acc(x, f.t[nb], acc[nb]);
+      });
+}
+
+// Logits (SP layout, bf16) of H 16-point halves in one pass over the table:
+// each table fragment feeds every half.  xfrag(h, s, f) gives the point
+// fragment of half h at step s.  Block MB is the temperature block.
+template <typename T, int C, int MB, int H, typename XFrag>
+__device__ __forceinline__ void logits_h(f32x4 (&acc)[H][MB + 1], const char* tabL,
+                                         const LogitsBases<T, C, MB>& lb, XFrag xfrag) {
+  using G_ = Geo<sizeof(T), C, MB>;
+  constexpr int SZ = (int)sizeof(T);
+#pragma unroll
+  for (int h = 0; h < H; ++h)
+#pragma unroll
+    for (int nb = 0; nb <= MB; ++nb) acc[h][nb] = zero4();
+  struct F { K32<T> t[MB + 1]; K32<T> x[H]; };
+  pipelined<C / 32, 2, F>(
+      [&](int s, F& f) {
+#pragma unroll
+        for (int h = 0; h < H; ++h) xfrag(h, s, f.x[h]);
+#pragma unroll
+        for (int nb = 0; nb <= MB; ++nb) {
+          if (nb < MB)
+            ld_row<T>(f.t[nb], tabL, lb.t, 16 * nb * G_::TROW + 32 * s * SZ);
+          else
+            ld_row<T>(f.t[nb], tabL, lb.a, G_::M16 * G_::TROW + 32 * s * SZ);
+        }
+      },
+      [&](int s, F& f) {
+#pragma unroll
+        for (int h = 0; h < H; ++h)
+#pragma unroll
+          for (int nb = 0; nb <= MB; ++nb) acc[h][nb] = mma_acc(f.t[nb], f.x[h], acc[h][nb]);
       });
 }
 
@@ -549,8 +647,8 @@ __device__ __forceinline__ void copy_image(char* lds, const void* img, int bytes
 
 // (wave: the wave's index in its block, uniform, so the range is scalar)
 __device__ __forceinline__ void tile_range(int64_t N, int waves, int wave, int64_t& t0,
-                                           int64_t& t1) {
-  const int64_t tiles = (N + 15) / 16;
+                                           int64_t& t1, int rows = 16) {
+  const int64_t tiles = (N + rows - 1) / rows;
   const int64_t tw = (int64_t)gridDim.x * waves;
   const int64_t gw = (int64_t)blockIdx.x * waves + wave;
   t0 = tiles * gw / tw;
@@ -571,18 +669,32 @@ __device__ __forceinline__ void block_ordered_reduce(int waves, Put put) {
 // ---------------------------------------------------------------------------
 // kAggregate and kDesliceBwd: W^T x (with den = W^T 1) or W^T dY.  The
 // weights come out of the softmax in the SP layout (lane: one point, 4
-// slices per block); they are staged in the G tile (consumed by then) and
-// read back transposed, which gives the contraction over points its A
-// operand (lane: one slice, 4 points).  den is the same contraction against
-// a B operand of ones, so it uses exactly the rounded weights of num.
+// slices per block); they are staged in LDS and read back transposed, which
+// gives the contraction over points its A operand (lane: one slice, 4
+// points).  den is the same contraction against a B operand of ones, so it
+// uses exactly the rounded weights of num.  With 32-row tiles the two
+// 16-point halves share the logits' table reads and their contractions over
+// points pair into K32 MFMAs; the backward's x then goes from HBM straight
+// into the logits' MFMA fragments (XREG), only dY passes through LDS.
 // ---------------------------------------------------------------------------
+template <typename T, int C, int MB, int ROWS, bool XREG, bool BWD>
+struct AggStage {
+  TileRegs<T, C, ROWS> x;   // x rows (LDS), unless XREG
+  TileRegs<T, C, ROWS> y;   // dY rows (BWD)
+  FragRegs<T, C, ROWS> xf;  // x fragments (XREG)
+  GRegs<T, MB, ROWS> g;
+};
+
 template <typename T, int C, int MB, bool BWD>
 __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(BWD ? kDesliceBwd : kAggregate)))
 k_aggregate(StreamArgs a) {
   using G_ = Geo<sizeof(T), C, MB>;
   constexpr int PASS = BWD ? kDesliceBwd : kAggregate;
   constexpr int WAVES = G_::waves(PASS);
+  constexpr int ROWS = G_::rows(PASS), H = ROWS / 16;
+  constexpr bool XREG = BWD && ROWS == 32;
   constexpr int SZ = (int)sizeof(T);
+  using V = typename LAcc<T, true>::v;
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r = lane_id() & 15, g = lane_id() >> 4;
@@ -592,10 +704,13 @@ k_aggregate(StreamArgs a) {
   __syncthreads();
   const char* tabL = smem + G_::OFF_L;
   char* wreg = smem + G_::img_bytes(PASS) + wave * G_::wave_bytes(PASS);
-  // x tile, (dY tile), Gumbel rows, transposed weights
-  char* const gbuf = wreg + (BWD ? 2 : 1) * G_::XT;
-  char* const wbuf = gbuf + G_::GT;
-  zero_lds(gbuf, 2 * G_::GT);
+  // x tile (logits; not with XREG), contracted tile (x, or dY), Gumbel rows,
+  // transposed weights
+  char* const xt = wreg;
+  char* const yt = (BWD && !XREG) ? wreg + G_::XT : wreg;
+  char* const gbuf = wreg + ((BWD && !XREG) ? 2 : 1) * H * G_::XT;
+  char* const wbuf = gbuf + H * G_::GT;
+  zero_lds(gbuf, 2 * H * G_::GT);
   const auto lb = logits_bases<T, C, MB, true>();
   const int xtr = tr_base<T>(G_::XT_ROW);
   const int wtr = tr_base<T>(G_::GROW);
@@ -622,71 +737,106 @@ k_aggregate(StreamArgs a) {
   const T* Y = reinterpret_cast<const T*>(a.dY);
   const T* Gp = reinterpret_cast<const T*>(a.G);
   int64_t t0, t1;
-  tile_range(a.N, WAVES, wave, t0, t1);
+  tile_range(a.N, WAVES, wave, t0, t1, ROWS);
+  using Stage = AggStage<T, C, MB, ROWS, XREG, BWD>;
 
-  // one tile: xt (logits), yt (contracted over points), gt (Gumbel rows)
-  auto tile_body = [&](int64_t t, const char* xt, const char* yt, char* gt) {
-    const int64_t p0 = t * 16;
-    const int nvalid = (int)(a.N - p0 < 16 ? a.N - p0 : 16);
-
-    typename LAcc<T, true>::v lg[MB + 1];
-    K32<T> xa[G_::XF];
-    logits<T, C, MB, true, (SZ == 4)>(lg, xa, xt, tabL, lb);
-    float w[MB][4], zs[MB][4], tau;
-    const float tt = temperature_own<T, C, MB>(lg, xa, tabL, lb.a, a.tb);
-    softmax_sp<T, MB>(lg, gt, a.M, bias, tt, a.tau_min, nvalid, w, zs, tau);
+  auto tile_body = [&](int64_t t, const Stage& cur) {
+    const int64_t p0 = t * ROWS;
+    int nv[H];
+#pragma unroll
+    for (int h = 0; h < H; ++h) {
+      const int64_t rem = a.N - p0 - 16 * h;
+      nv[h] = rem < 0 ? 0 : rem > 16 ? 16 : (int)rem;
+    }
+    V lg[H][MB + 1];
+    float tt[H];
+    if constexpr (H == 1) {
+      K32<T> xa[G_::XF];
+      logits<T, C, MB, true, (SZ == 4)>(lg[0], xa, xt, tabL, lb);
+      tt[0] = temperature_own<T, C, MB>(lg[0], xa, tabL, lb.a, a.tb);
+    } else {
+      logits_h<T, C, MB, H>(lg, tabL, lb, [&](int h, int s, K32<T>& f) {
+        if constexpr (XREG)
+          f = frag_of<T, C, ROWS>(cur.xf, h, s);
+        else
+          ld_row<T>(f, xt, lb.x, h * 16 * G_::XT_ROW + 32 * s * SZ);
+      });
+#pragma unroll
+      for (int h = 0; h < H; ++h) tt[h] = (float)lg[h][MB][0] + (float)a.tb;
+    }
+    float w[H][MB][4], zs[MB][4], tau;
+#pragma unroll
+    for (int h = 0; h < H; ++h)
+      softmax_sp<T, MB>(lg[h], gbuf + h * 16 * a.M * SZ, a.M, bias, tt[h], a.tau_min, nv[h], w[h],
+                        zs, tau);
 
     // SP -> PS through the weights buffer
     wave_sync();
 #pragma unroll
-    for (int nb = 0; nb < MB; ++nb) {
-      f32x4 v{w[nb][0], w[nb][1], w[nb][2], w[nb][3]};
-      stage4<T>(wbuf, wsb, 16 * nb * SZ, v);
-    }
-    wave_sync();
-    K16<T> wt[MB];
+    for (int h = 0; h < H; ++h)
 #pragma unroll
-    for (int nb = 0; nb < MB; ++nb) ld_tr<T>(wt[nb], wbuf, wtr, 16 * nb * SZ, G_::GROW);
+      for (int nb = 0; nb < MB; ++nb) {
+        f32x4 v{w[h][nb][0], w[h][nb][1], w[h][nb][2], w[h][nb][3]};
+        stage4<T>(wbuf, wsb + h * 16 * G_::GROW, 16 * nb * SZ, v);
+      }
+    wave_sync();
+    K16<T> wt[H][MB];
+#pragma unroll
+    for (int h = 0; h < H; ++h)
+#pragma unroll
+      for (int nb = 0; nb < MB; ++nb)
+        ld_tr<T>(wt[h][nb], wbuf, wtr, h * 16 * G_::GROW + 16 * nb * SZ, G_::GROW);
     if constexpr (!BWD) {
 #pragma unroll
-      for (int nb = 0; nb < MB; ++nb) dacc[nb] = mma16(wt[nb], ones, dacc[nb]);
+      for (int nb = 0; nb < MB; ++nb) {
+        if constexpr (H == 2)
+          dacc[nb] = mma16x2(wt[0][nb], ones, wt[1][nb], ones, dacc[nb]);
+        else
+          dacc[nb] = mma16(wt[0][nb], ones, dacc[nb]);
+      }
     }
-    struct F { K16<T> xb; };
+    struct F { K16<T> xb[H]; };
     pipelined<G_::CB, 4, F>(
-        [&](int cb, F& f) { ld_tr<T>(f.xb, yt, xtr, 16 * cb * SZ, G_::XT_ROW); },
         [&](int cb, F& f) {
 #pragma unroll
-          for (int nb = 0; nb < MB; ++nb) acc[nb][cb] = mma16(wt[nb], f.xb, acc[nb][cb]);
+          for (int h = 0; h < H; ++h)
+            ld_tr<T>(f.xb[h], yt, xtr, h * 16 * G_::XT_ROW + 16 * cb * SZ, G_::XT_ROW);
+        },
+        [&](int cb, F& f) {
+#pragma unroll
+          for (int nb = 0; nb < MB; ++nb) {
+            if constexpr (H == 2)
+              acc[nb][cb] = mma16x2(wt[0][nb], f.xb[0], wt[1][nb], f.xb[1], acc[nb][cb]);
+            else
+              acc[nb][cb] = mma16(wt[0][nb], f.xb[0], acc[nb][cb]);
+          }
         });
   };
 
-  {
-    char* xt = wreg;
-    char* yt = BWD ? wreg + G_::XT : wreg;
-    char* gt = gbuf;
-    using Stage = TileStage<T, C, MB>;
-    auto load = [&](Stage& st, int64_t tile) {
-      load_tile<T, C>(st.x, X, tile * 16, a.N);
-      if constexpr (BWD) load_tile<T, C>(st.y, Y, tile * 16, a.N);
-      load_g<T, MB>(st.g, Gp, X, tile * 16, a.N, a.M, hasG);
-    };
-    auto store = [&](const Stage& st) {
-      store_tile<T, C>(xt, st.x);
-      if constexpr (BWD) store_tile<T, C>(yt, st.y);
-      if (hasG) store_g<T, MB>(gt, st.g, a.M, hasG);
-    };
-    auto tail = [&](int64_t t) {
-      Stage st;
-      load(st, t);
-      wave_sync();
-      store(st);
-      g_fixup<T, MB>(gt, Gp, t * 16, a.N, a.M, hasG);
-      wave_sync();
-      tile_body(t, xt, yt, gt);
-    };
-    stream_tiles<agg_depth<T, MB, BWD>(), Stage>(t0, t1, a.N / 16, load, store,
-                                             [&](int64_t t) { tile_body(t, xt, yt, gt); }, tail);
-  }
+  auto load = [&](Stage& st, int64_t tile) {
+    const int64_t p0 = tile * ROWS;
+    if constexpr (XREG)
+      load_frags<T, C, ROWS>(st.xf, X, p0, a.N);
+    else
+      load_tile<T, C, ROWS>(st.x, X, p0, a.N);
+    if constexpr (BWD) load_tile<T, C, ROWS>(st.y, Y, p0, a.N);
+    load_g<T, MB, ROWS>(st.g, Gp, X, p0, a.N, a.M, hasG);
+  };
+  auto store = [&](const Stage& st) {
+    if constexpr (!XREG) store_tile<T, C, ROWS>(xt, st.x);
+    if constexpr (BWD) store_tile<T, C, ROWS>(yt, st.y);
+    if (hasG) store_g<T, MB, ROWS>(gbuf, st.g, a.M, hasG);
+  };
+  auto tail = [&](int64_t t) {
+    Stage st;
+    load(st, t);
+    wave_sync();
+    store(st);
+    g_fixup<T, MB, ROWS>(gbuf, Gp, t * ROWS, a.N, a.M, hasG);
+    wave_sync();
+    tile_body(t, st);
+  };
+  stream_tiles<agg_depth<T, MB, BWD>(), Stage>(t0, t1, a.N / ROWS, load, store, tile_body, tail);
 
   __syncthreads();  // every wave is done with the tables and tiles
   float* red = reinterpret_cast<float*>(smem);  // [M16][C] then den [M16]
@@ -763,7 +913,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kDeslice)))
     store_tile<T, C>(xt, st.x);
     if (hasG) store_g<T, MB>(gt, st.g, a.M, hasG);
   };
-  auto body = [&](int64_t t) {
+  auto body = [&](int64_t t, const auto&...) {
     const int64_t p0 = t * 16;
     const int nvalid = (int)(a.N - p0 < 16 ? a.N - p0 : 16);
 
@@ -982,7 +1132,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
     if (deslice) store_tile<T, C>(yt, st.y);
     if (hasG) store_g<T, MB>(gt, st.g, a.M, hasG);
   };
-  auto body = [&](int64_t t) {
+  auto body = [&](int64_t t, const auto&...) {
     const int64_t p0 = t * 16;
     const int nvalid = (int)(a.N - p0 < 16 ? a.N - p0 : 16);
     const bool pv = r < nvalid;
