@@ -45,11 +45,13 @@ struct Geo {
   static constexpr int GT = 16 * GROW;
   static constexpr int SCR = 16 * (M16 + 1) * 4 + 64;  // dl transpose + dt
 
-  // points per streamed tile: the aggregating passes with bf16 storage and
-  // up to 32 slices take two 16-point halves at once (more independent work
-  // per wave; their contraction over points pairs into K32 MFMAs)
+  // points per streamed tile: the forward aggregate with bf16 storage and up
+  // to 32 slices takes two 16-point halves at once (more independent work
+  // per wave; its contraction over points pairs into K32 MFMAs); the
+  // backward aggregate, with two streamed tensors, measured faster with
+  // 16-point tiles (fewer loads in flight per wave)
   static constexpr int rows(int pass) {
-    return (pass == kAggregate || pass == kDesliceBwd) && SZ == 2 && MB <= 2 ? 32 : 16;
+    return pass == kAggregate && SZ == 2 && MB <= 2 ? 32 : 16;
   }
   static constexpr int img_bytes(int pass) {
     return pass == kDeslice ? OFF_2 + SZ_S
@@ -57,12 +59,11 @@ struct Geo {
          : OFF_2;
   }
   // per wave: x tile, (dY tile or output staging), Gumbel rows, scratch
-  // (the aggregating passes: the transposed weights).  32-row tiles: the
-  // contracted tile (x, or dY) and Gumbel / weight rows for 32 points; the
-  // backward's x then comes from HBM straight into MFMA fragments.
+  // (the aggregating passes: the transposed weights); 32-row tiles hold x,
+  // Gumbel and weight rows for 32 points
   static constexpr int wave_bytes(int pass) {
     return (pass == kSliceBwd || pass == kWeightsBwd) ? 2 * XT + GT + SCR
-         : (pass == kDesliceBwd || pass == kAggregate) && rows(pass) == 32 ? 2 * XT + 4 * GT
+         : pass == kAggregate && rows(pass) == 32 ? 2 * XT + 4 * GT
          : pass == kDesliceBwd ? 2 * XT + 2 * GT
          : pass == kAggregate ? XT + 2 * GT
          : XT + GT;

@@ -236,46 +236,6 @@ __device__ __forceinline__ void write_tile(T* dst, int64_t p0, const char* tile,
   }
 }
 
-// The lane's K32 row fragments of a tile, straight from HBM in the MFMA
-// layout (the B operand of the logits): half h (rows 16h..16h+15), step s:
-// lane (r, g) holds elements [32s + 8g, +8) of row 16h + r, 16 or 32 bytes.
-template <typename T, int C, int ROWS>
-struct FragRegs {
-  static constexpr int XF = C / 32;
-  static constexpr int PER = 8 * (int)sizeof(T) / 16;  // 16-byte chunks per fragment
-  uint4 c[ROWS / 16][XF][PER];
-};
-
-template <typename T, int C, int ROWS>
-__device__ __forceinline__ void load_frags(FragRegs<T, C, ROWS>& F, const T* base, int64_t p0,
-                                           int64_t N) {
-  constexpr int SZ = (int)sizeof(T);
-  const int r = lane_id() & 15, g = lane_id() >> 4;
-  const int lim = last_row<ROWS>(p0, N);
-  const char* src = reinterpret_cast<const char*>(base + p0 * C);
-#pragma unroll
-  for (int h = 0; h < ROWS / 16; ++h) {
-    const int row = 16 * h + r < lim ? 16 * h + r : lim;
-#pragma unroll
-    for (int s = 0; s < C / 32; ++s)
-#pragma unroll
-      for (int q = 0; q < FragRegs<T, C, ROWS>::PER; ++q)
-        F.c[h][s][q] = ld_global16(src + (uint32_t)(row * C * SZ + (32 * s + 8 * g) * SZ + 16 * q));
-  }
-}
-
-template <typename T, int C, int ROWS>
-__device__ __forceinline__ K32<T> frag_of(const FragRegs<T, C, ROWS>& F, int h, int s) {
-  K32<T> k;
-  if constexpr (sizeof(T) == 2) {
-    k.v = __builtin_bit_cast(bf16x8, F.c[h][s][0]);
-  } else {
-    k.lo = __builtin_bit_cast(f32x4, F.c[h][s][0]);
-    k.hi = __builtin_bit_cast(f32x4, F.c[h][s][1]);
-  }
-  return k;
-}
-
 // The Gumbel rows of a tile: ROWS*M elements, contiguous in G.  GCH 16-byte
 // chunks per lane cover the largest tile (M = 16*MB).  In LDS they keep the
 // same layout, element (row, j) at (row*M + j)*sz; reads of a padded slice
@@ -340,9 +300,7 @@ struct TileStage {
 // Streams tiles [t0, t1) with DEPTH register stages: at the top of tile t
 // its stage is written to the wave's LDS tiles and immediately reloaded
 // with tile t + DEPTH, so DEPTH tiles of loads are in flight while body(t)
-// computes; body(t, stage) also gets the stage's registers as they were
-// before the reload (for operands used straight from registers).  The
-// pipelined tiles are full ones (t < tfull).  The main loop runs whole rounds
+// computes.  The pipelined tiles are full ones (t < tfull).  The main loop runs whole rounds
 // of DEPTH tiles with every stage reloaded on every tile -- past the end with
 // the current tile again (an L2 hit) -- so all loads are unconditional and
 // every path into the loop head has issued the stages in the same order:
@@ -365,9 +323,8 @@ __device__ __forceinline__ void stream_tiles(int64_t t0, int64_t t1, int64_t tfu
         wave_sync();
         store(st[d]);
         wave_sync();
-        const Stage cur = st[d];
         load(st[d], tt + DEPTH < te ? tt + DEPTH : tt);
-        body(tt, cur);
+        body(tt);
       }
     }
 #pragma unroll
@@ -376,7 +333,7 @@ __device__ __forceinline__ void stream_tiles(int64_t t0, int64_t t1, int64_t tfu
         wave_sync();
         store(st[d]);
         wave_sync();
-        body(t + d, st[d]);
+        body(t + d);
       }
     }
   }
@@ -674,14 +631,12 @@ __device__ __forceinline__ void block_ordered_reduce(int waves, Put put) {
 // points).  den is the same contraction against a B operand of ones, so it
 // uses exactly the rounded weights of num.  With 32-row tiles the two
 // 16-point halves share the logits' table reads and their contractions over
-// points pair into K32 MFMAs; the backward's x then goes from HBM straight
-// into the logits' MFMA fragments (XREG), only dY passes through LDS.
+// points pair into K32 MFMAs.
 // ---------------------------------------------------------------------------
-template <typename T, int C, int MB, int ROWS, bool XREG, bool BWD>
+template <typename T, int C, int MB, int ROWS, bool BWD>
 struct AggStage {
-  TileRegs<T, C, ROWS> x;   // x rows (LDS), unless XREG
-  TileRegs<T, C, ROWS> y;   // dY rows (BWD)
-  FragRegs<T, C, ROWS> xf;  // x fragments (XREG)
+  TileRegs<T, C, ROWS> x;  // x rows
+  TileRegs<T, C, ROWS> y;  // dY rows (BWD)
   GRegs<T, MB, ROWS> g;
 };
 
@@ -692,7 +647,6 @@ k_aggregate(StreamArgs a) {
   constexpr int PASS = BWD ? kDesliceBwd : kAggregate;
   constexpr int WAVES = G_::waves(PASS);
   constexpr int ROWS = G_::rows(PASS), H = ROWS / 16;
-  constexpr bool XREG = BWD && ROWS == 32;
   constexpr int SZ = (int)sizeof(T);
   using V = typename LAcc<T, true>::v;
   extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -704,11 +658,11 @@ k_aggregate(StreamArgs a) {
   __syncthreads();
   const char* tabL = smem + G_::OFF_L;
   char* wreg = smem + G_::img_bytes(PASS) + wave * G_::wave_bytes(PASS);
-  // x tile (logits; not with XREG), contracted tile (x, or dY), Gumbel rows,
-  // transposed weights
+  // x tile (logits), contracted tile (x, or dY), Gumbel rows, transposed
+  // weights
   char* const xt = wreg;
-  char* const yt = (BWD && !XREG) ? wreg + G_::XT : wreg;
-  char* const gbuf = wreg + ((BWD && !XREG) ? 2 : 1) * H * G_::XT;
+  char* const yt = BWD ? wreg + H * G_::XT : wreg;
+  char* const gbuf = wreg + (BWD ? 2 : 1) * H * G_::XT;
   char* const wbuf = gbuf + H * G_::GT;
   zero_lds(gbuf, 2 * H * G_::GT);
   const auto lb = logits_bases<T, C, MB, true>();
@@ -738,9 +692,9 @@ k_aggregate(StreamArgs a) {
   const T* Gp = reinterpret_cast<const T*>(a.G);
   int64_t t0, t1;
   tile_range(a.N, WAVES, wave, t0, t1, ROWS);
-  using Stage = AggStage<T, C, MB, ROWS, XREG, BWD>;
+  using Stage = AggStage<T, C, MB, ROWS, BWD>;
 
-  auto tile_body = [&](int64_t t, const Stage& cur) {
+  auto tile_body = [&](int64_t t) {
     const int64_t p0 = t * ROWS;
     int nv[H];
 #pragma unroll
@@ -756,10 +710,7 @@ k_aggregate(StreamArgs a) {
       tt[0] = temperature_own<T, C, MB>(lg[0], xa, tabL, lb.a, a.tb);
     } else {
       logits_h<T, C, MB, H>(lg, tabL, lb, [&](int h, int s, K32<T>& f) {
-        if constexpr (XREG)
-          f = frag_of<T, C, ROWS>(cur.xf, h, s);
-        else
-          ld_row<T>(f, xt, lb.x, h * 16 * G_::XT_ROW + 32 * s * SZ);
+        ld_row<T>(f, xt, lb.x, h * 16 * G_::XT_ROW + 32 * s * SZ);
       });
 #pragma unroll
       for (int h = 0; h < H; ++h) tt[h] = (float)lg[h][MB][0] + (float)a.tb;
@@ -815,15 +766,12 @@ k_aggregate(StreamArgs a) {
 
   auto load = [&](Stage& st, int64_t tile) {
     const int64_t p0 = tile * ROWS;
-    if constexpr (XREG)
-      load_frags<T, C, ROWS>(st.xf, X, p0, a.N);
-    else
-      load_tile<T, C, ROWS>(st.x, X, p0, a.N);
+    load_tile<T, C, ROWS>(st.x, X, p0, a.N);
     if constexpr (BWD) load_tile<T, C, ROWS>(st.y, Y, p0, a.N);
     load_g<T, MB, ROWS>(st.g, Gp, X, p0, a.N, a.M, hasG);
   };
   auto store = [&](const Stage& st) {
-    if constexpr (!XREG) store_tile<T, C, ROWS>(xt, st.x);
+    store_tile<T, C, ROWS>(xt, st.x);
     if constexpr (BWD) store_tile<T, C, ROWS>(yt, st.y);
     if (hasG) store_g<T, MB, ROWS>(gbuf, st.g, a.M, hasG);
   };
@@ -834,7 +782,7 @@ k_aggregate(StreamArgs a) {
     store(st);
     g_fixup<T, MB, ROWS>(gbuf, Gp, t * ROWS, a.N, a.M, hasG);
     wave_sync();
-    tile_body(t, st);
+    tile_body(t);
   };
   stream_tiles<agg_depth<T, MB, BWD>(), Stage>(t0, t1, a.N / ROWS, load, store, tile_body, tail);
 
@@ -913,7 +861,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kDeslice)))
     store_tile<T, C>(xt, st.x);
     if (hasG) store_g<T, MB>(gt, st.g, a.M, hasG);
   };
-  auto body = [&](int64_t t, const auto&...) {
+  auto body = [&](int64_t t) {
     const int64_t p0 = t * 16;
     const int nvalid = (int)(a.N - p0 < 16 ? a.N - p0 : 16);
 
@@ -1132,7 +1080,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
     if (deslice) store_tile<T, C>(yt, st.y);
     if (hasG) store_g<T, MB>(gt, st.g, a.M, hasG);
   };
-  auto body = [&](int64_t t, const auto&...) {
+  auto body = [&](int64_t t) {
     const int64_t p0 = t * 16;
     const int nvalid = (int)(a.N - p0 < 16 ? a.N - p0 : 16);
     const bool pv = r < nvalid;
