@@ -68,12 +68,16 @@ struct Geo {
          : pass == kAggregate ? XT + 2 * GT
          : XT + GT;
   }
-  // floats of one block's partial-sum record
-  static constexpr int red_floats(int pass) {
-    return pass == kAggregate ? M16 * C + M16
-         : pass == kDesliceBwd ? M16 * C
-         : (pass == kSliceBwd || pass == kWeightsBwd) ? C * M16 + M16 + C + 1
+  // f32x4 per lane of a wave's partial sums (the cross-wave reduction)
+  static constexpr int red_vecs(int pass) {
+    return pass == kAggregate ? MB * CB + MB
+         : pass == kDesliceBwd ? MB * CB
+         : (pass == kSliceBwd || pass == kWeightsBwd) ? CB * MB + (CB + 3) / 4 + (MB + 4) / 4
          : 0;
+  }
+  // LDS of the cross-wave reduction: waves/2 slots of red_vecs x 64 lanes
+  static constexpr int red_bytes(int pass, int waves) {
+    return (waves / 2 > 0 ? waves / 2 : 1) * red_vecs(pass) * 64 * 16;
   }
   // the light passes run 8 waves per block with bf16 storage (two waves per
   // SIMD hide each other's latency); the accumulating passes, and fp32
@@ -87,12 +91,13 @@ struct Geo {
          : (img_bytes(pass) + 2 * wave_bytes(pass) <= kLdsBytes) ? 2 : 1;
   }
   static constexpr int lds_bytes(int pass) {
-    return (img_bytes(pass) + waves(pass) * wave_bytes(pass)) > red_floats(pass) * 4
+    return (img_bytes(pass) + waves(pass) * wave_bytes(pass)) > red_bytes(pass, waves(pass))
                ? img_bytes(pass) + waves(pass) * wave_bytes(pass)
-               : red_floats(pass) * 4;
+               : red_bytes(pass, waves(pass));
   }
   static constexpr bool fits(int pass) {
-    return img_bytes(pass) + wave_bytes(pass) <= kLdsBytes && red_floats(pass) * 4 <= kLdsBytes;
+    return img_bytes(pass) + wave_bytes(pass) <= kLdsBytes &&
+           red_bytes(pass, waves(pass)) <= kLdsBytes;
   }
 };
 

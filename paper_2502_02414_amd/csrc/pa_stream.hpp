@@ -63,6 +63,9 @@ enum Flags { kHasG = 1, kStatesTerm = 2, kDesliceTerm = 4 };
 template <typename T, int MB, bool BWD> constexpr int agg_depth() { return 1; }
 template <typename T, int MB> constexpr int des_depth() { return sizeof(T) == 2 && MB <= 2 ? 2 : 1; }
 template <typename T, int MB> constexpr int bwd_depth() { return 1; }
+// Passes that walk their tile ranges backwards (alternating with the passes
+// before and after them in a layer step).
+constexpr bool kRevDeslice = false, kRevSliceBwd = false;
 
 // Point-side tensors are streamed once per pass: their 16-byte loads and
 // stores are non-temporal (they neither displace nor leave dirty data in the
@@ -306,15 +309,24 @@ struct TileStage {
 // every path into the loop head has issued the stages in the same order:
 // the compiler's wait before a stage's store then covers that stage only.
 // The last (fewer than DEPTH) tiles, already loaded, follow the loop; a
-// partial last tile is left to tail(t).  load(stage, tile) / store(stage).
-template <int DEPTH, typename Stage, typename Load, typename Store, typename Body, typename Tail>
+// partial last tile is left to tail(t).  load(stage, tile) / store(stage);
+// init() is the block's set-up (tables into LDS), run by every wave once the
+// first stages' loads are in flight.
+template <int DEPTH, typename Stage, bool REV = false, typename Load, typename Store,
+          typename Body, typename Tail, typename Init>
 __device__ __forceinline__ void stream_tiles(int64_t t0, int64_t t1, int64_t tfull, Load load,
-                                             Store store, Body body, Tail tail) {
+                                             Store store, Body body, Tail tail, Init init) {
   const int64_t te = t1 < tfull ? t1 : tfull;
+  // REV walks the range from its end: tile(i) for i = t0 .. te - 1
+  auto tile = [&](int64_t i) { return REV ? t0 + te - 1 - i : i; };
+  Stage st[DEPTH];
   if (t0 < te) {
-    Stage st[DEPTH];
 #pragma unroll
-    for (int d = 0; d < DEPTH; ++d) load(st[d], t0 + d < te ? t0 + d : te - 1);
+    for (int d = 0; d < DEPTH; ++d) load(st[d], tile(t0 + d < te ? t0 + d : te - 1));
+  }
+  init();  // the block's set-up (every wave), while the first tiles load
+  if (REV && t0 <= te && te < t1) tail(te);  // this wave owns the partial last tile
+  if (t0 < te) {
     int64_t t = t0;
     for (; t + DEPTH <= te; t += DEPTH) {
 #pragma unroll
@@ -323,8 +335,8 @@ __device__ __forceinline__ void stream_tiles(int64_t t0, int64_t t1, int64_t tfu
         wave_sync();
         store(st[d]);
         wave_sync();
-        load(st[d], tt + DEPTH < te ? tt + DEPTH : tt);
-        body(tt);
+        load(st[d], tile(tt + DEPTH < te ? tt + DEPTH : tt));
+        body(tile(tt));
       }
     }
 #pragma unroll
@@ -333,11 +345,11 @@ __device__ __forceinline__ void stream_tiles(int64_t t0, int64_t t1, int64_t tfu
         wave_sync();
         store(st[d]);
         wave_sync();
-        body(t + d);
+        body(tile(t + d));
       }
     }
   }
-  if (t0 <= te && te < t1) tail(te);  // this wave owns the partial last tile
+  if (!REV && t0 <= te && te < t1) tail(te);  // this wave owns the partial last tile
 }
 
 // ---------------------------------------------------------------------------
@@ -612,14 +624,28 @@ __device__ __forceinline__ void tile_range(int64_t N, int waves, int wave, int64
   t1 = tiles * (gw + 1) / tw;
 }
 
-// Ordered (wave 0, 1, ...) sum of per-wave register partials into an LDS
-// region; `put(first)` writes (first) or adds this wave's values.
-template <typename Put>
-__device__ __forceinline__ void block_ordered_reduce(int waves, Put put) {
-  const int wave = threadIdx.x >> 6;
-  for (int w = 0; w < waves; ++w) {
-    if (wave == w) put(w == 0);
+// Sum of per-wave register partials over the block's waves, pairwise in a
+// fixed order (((w0 + w1) + (w2 + w3)) + ...), through LDS slots (the
+// tables and tiles are dead by then; WAVES/2 slots of NV f32x4 per lane at
+// lds); wave 0 ends with the block total.  visit(f) calls f(f32x4&) on every
+// partial vector, always in the same order.
+template <int WAVES, int NV, typename Visit>
+__device__ __forceinline__ void block_tree_reduce(char* lds, Visit visit) {
+  const int wave = threadIdx.x >> 6, lane = lane_id();
+  f32x4* slots = reinterpret_cast<f32x4*>(lds);
+#pragma unroll
+  for (int span = 1; span < WAVES; span *= 2) {
+    __syncthreads();  // the LDS is free (main loop, or the previous round, done)
+    f32x4* slot = slots + (wave / (2 * span)) * NV * 64;
+    if ((wave & (2 * span - 1)) == span) {
+      int k = 0;
+      visit([&](f32x4& v) { slot[64 * k++ + lane] = v; });
+    }
     __syncthreads();
+    if ((wave & (2 * span - 1)) == 0) {
+      int k = 0;
+      visit([&](f32x4& v) { v += slot[64 * k++ + lane]; });
+    }
   }
 }
 
@@ -654,8 +680,6 @@ k_aggregate(StreamArgs a) {
   const int r = lane_id() & 15, g = lane_id() >> 4;
   const bool hasG = a.flags & kHasG;
 
-  copy_image(smem, a.img, G_::img_bytes(PASS));
-  __syncthreads();
   const char* tabL = smem + G_::OFF_L;
   char* wreg = smem + G_::img_bytes(PASS) + wave * G_::wave_bytes(PASS);
   // x tile (logits), contracted tile (x, or dY), Gumbel rows, transposed
@@ -664,18 +688,22 @@ k_aggregate(StreamArgs a) {
   char* const yt = BWD ? wreg + H * G_::XT : wreg;
   char* const gbuf = wreg + (BWD ? 2 : 1) * H * G_::XT;
   char* const wbuf = gbuf + H * G_::GT;
-  zero_lds(gbuf, 2 * H * G_::GT);
   const auto lb = logits_bases<T, C, MB, true>();
   const int xtr = tr_base<T>(G_::XT_ROW);
   const int wtr = tr_base<T>(G_::GROW);
   const int wsb = r * G_::GROW + 4 * g * SZ;  // SP weights of point r, slices 16nb + 4g ..
 
   float bias[MB][4];
+  auto init = [&]() {
+    copy_image(smem, a.img, G_::img_bytes(PASS));
+    __syncthreads();
+    zero_lds(gbuf, 2 * H * G_::GT);
 #pragma unroll
-  for (int nb = 0; nb < MB; ++nb)
+    for (int nb = 0; nb < MB; ++nb)
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      bias[nb][i] = reinterpret_cast<const float*>(smem)[16 * nb + 4 * g + i];
+      for (int i = 0; i < 4; ++i)
+        bias[nb][i] = reinterpret_cast<const float*>(smem)[16 * nb + 4 * g + i];
+  };
 
   f32x4 acc[MB][G_::CB], dacc[MB];
 #pragma unroll
@@ -784,34 +812,34 @@ k_aggregate(StreamArgs a) {
     wave_sync();
     tile_body(t);
   };
-  stream_tiles<agg_depth<T, MB, BWD>(), Stage>(t0, t1, a.N / ROWS, load, store, tile_body, tail);
+  stream_tiles<agg_depth<T, MB, BWD>(), Stage>(t0, t1, a.N / ROWS, load, store, tile_body, tail,
+                                             init);
 
-  __syncthreads();  // every wave is done with the tables and tiles
-  float* red = reinterpret_cast<float*>(smem);  // [M16][C] then den [M16]
-  block_ordered_reduce(WAVES, [&](bool first) {
+  // block total in wave 0, written as this block's record: num [M][C]
+  // (or dS' [M][C]), then den [M]
+  block_tree_reduce<WAVES, MB * G_::CB + (BWD ? 0 : MB)>(smem, [&](auto f) {
 #pragma unroll
     for (int nb = 0; nb < MB; ++nb)
 #pragma unroll
-      for (int cb = 0; cb < G_::CB; ++cb)
+      for (int cb = 0; cb < G_::CB; ++cb) f(acc[nb][cb]);
+    if constexpr (!BWD)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float* d = red + (16 * nb + 4 * g + i) * C + 16 * cb + r;
-          *d = first ? acc[nb][cb][i] : *d + acc[nb][cb][i];
-        }
-    if (!BWD && r == 0)
-#pragma unroll
-      for (int nb = 0; nb < MB; ++nb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float* d = red + G_::M16 * C + 16 * nb + 4 * g + i;
-          *d = first ? dacc[nb][i] : *d + dacc[nb][i];
-        }
+      for (int nb = 0; nb < MB; ++nb) f(dacc[nb]);
   });
-  float* rec = a.partials + (int64_t)blockIdx.x * a.rec;
-  const int MC = a.M * C;
-  for (int k = threadIdx.x; k < MC; k += blockDim.x) rec[k] = red[k];
-  if (!BWD)
-    for (int j = threadIdx.x; j < a.M; j += blockDim.x) rec[MC + j] = red[G_::M16 * C + j];
+  if (wave == 0) {
+    float* rec = a.partials + (int64_t)blockIdx.x * a.rec;
+#pragma unroll
+    for (int nb = 0; nb < MB; ++nb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int j = 16 * nb + 4 * g + i;
+        if (j < a.M) {
+#pragma unroll
+          for (int cb = 0; cb < G_::CB; ++cb) rec[j * C + 16 * cb + r] = acc[nb][cb][i];
+          if (!BWD && r == 0) rec[a.M * C + j] = dacc[nb][i];
+        }
+      }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -828,23 +856,25 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kDeslice)))
   const int r = lane_id() & 15, g = lane_id() >> 4;
   const bool hasG = a.flags & kHasG;
 
-  copy_image(smem, a.img, G_::img_bytes(kDeslice));
-  __syncthreads();
   const char* tabL = smem + G_::OFF_L;
   const char* tabS = smem + G_::OFF_2;
   char* xt = smem + G_::img_bytes(kDeslice) + wave * G_::wave_bytes(kDeslice);
   char* gt = xt + G_::XT;
-  zero_lds(gt, G_::GT);
   const auto lb = logits_bases<T, C, MB, true>();
   const int sb = r * G_::SROW + 4 * g * SZ;  // S'^T row 16cb + r, slices 16nb + 4g ..
   const int stb = stage_base<T>(G_::XT_ROW);
 
   float bias[MB][4];
+  auto init = [&]() {
+    copy_image(smem, a.img, G_::img_bytes(kDeslice));
+    __syncthreads();
+    zero_lds(gt, G_::GT);
 #pragma unroll
-  for (int nb = 0; nb < MB; ++nb)
+    for (int nb = 0; nb < MB; ++nb)
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      bias[nb][i] = reinterpret_cast<const float*>(smem)[16 * nb + 4 * g + i];
+      for (int i = 0; i < 4; ++i)
+        bias[nb][i] = reinterpret_cast<const float*>(smem)[16 * nb + 4 * g + i];
+  };
 
   const T* X = reinterpret_cast<const T*>(a.x);
   const T* Gp = reinterpret_cast<const T*>(a.G);
@@ -913,7 +943,8 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kDeslice)))
     wave_sync();
     body(t);
   };
-  stream_tiles<des_depth<T, MB>(), Stage>(t0, t1, a.N / 16, load, store, body, tail);
+  stream_tiles<des_depth<T, MB>(), Stage, kRevDeslice>(t0, t1, a.N / 16, load, store, body, tail,
+                                                     init);
 }
 
 // ---------------------------------------------------------------------------
@@ -1008,8 +1039,6 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
   const bool hasG = a.flags & kHasG;
   const bool deslice = (PASS == kSliceBwd) && (a.flags & kDesliceTerm);
 
-  copy_image(smem, a.img, G_::img_bytes(PASS));
-  __syncthreads();
   const float* hdr = reinterpret_cast<const float*>(smem);
   const float* dden_tab = hdr + M16;
   const float* cN = hdr + 2 * M16;
@@ -1020,7 +1049,6 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
   char* xt = wreg;
   char* yt = wreg + G_::XT;  // dY tile, then the dx staging tile
   char* gt = wreg + 2 * G_::XT;
-  zero_lds(gt, G_::GT);
   float* scr = reinterpret_cast<float*>(gt + G_::GT);  // [16][M16+1]
   float* scr_dt = scr + 16 * SROWF;                     // [16]
   const auto lb = logits_bases<T, C, MB, true>();
@@ -1031,21 +1059,24 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
   const int wtr = tr_base<T>(G_::WROW);
   const int stb = stage_base<T>(G_::XT_ROW);
 
-  // dden_j centred by its den-weighted mean (a shift common to all slices)
-  float cD = 0.f;
-  {
+  float bias[MB][4], dden[MB][4];
+  auto init = [&]() {
+    copy_image(smem, a.img, G_::img_bytes(PASS));
+    __syncthreads();
+    zero_lds(gt, G_::GT);
+    // dden_j centred by its den-weighted mean (a shift common to all slices)
+    float cD = 0.f;
     const float* sw = hdr + 2 * M16 + 2 * C;
     for (int j = 0; j < a.M; ++j) cD += sw[j] * dden_tab[j];
-  }
-  float bias[MB][4], dden[MB][4];
 #pragma unroll
-  for (int nb = 0; nb < MB; ++nb)
+    for (int nb = 0; nb < MB; ++nb)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int j = 16 * nb + 4 * g + i;
-      bias[nb][i] = hdr[j];
-      dden[nb][i] = j < a.M ? dden_tab[j] - cD : 0.f;
-    }
+      for (int i = 0; i < 4; ++i) {
+        const int j = 16 * nb + 4 * g + i;
+        bias[nb][i] = hdr[j];
+        dden[nb][i] = j < a.M ? dden_tab[j] - cD : 0.f;
+      }
+  };
 
   f32x4 dA[G_::CB][MB];
   float da[G_::CB];
@@ -1255,7 +1286,8 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
     wave_sync();
     body(t);
   };
-  stream_tiles<bwd_depth<T, MB>(), Stage>(t0, t1, a.N / 16, load, store, body, tail);
+  stream_tiles<bwd_depth<T, MB>(), Stage, kRevSliceBwd>(t0, t1, a.N / 16, load, store, body, tail,
+                                                       init);
 
   // lane partials -> wave totals
 #pragma unroll
@@ -1264,44 +1296,44 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
   for (int cb = 0; cb < G_::CB; ++cb) da[cb] = groups_sum(da[cb]);
   dbt = row16_sum(dbt);  // only g == 0 lanes carry values; sum their row
 
-  __syncthreads();
-  float* red = reinterpret_cast<float*>(smem);  // dA [C][M16], db [M16], da [C], dbt
-  block_ordered_reduce(WAVES, [&](bool first) {
+  // block total in wave 0, written as this block's record: dA [C][M],
+  // db [M], da [C], db_t
+  constexpr int NDA = (G_::CB + 3) / 4, NSC = (MB + 1 + 3) / 4;
+  f32x4 dav[NDA], scv[NSC];
+#pragma unroll
+  for (int k = 0; k < 4 * NDA; ++k) dav[k / 4][k % 4] = k < G_::CB ? da[k] : 0.f;
+#pragma unroll
+  for (int k = 0; k < 4 * NSC; ++k) scv[k / 4][k % 4] = k < MB ? db[k] : k == MB ? dbt : 0.f;
+  block_tree_reduce<WAVES, G_::CB * MB + NDA + NSC>(smem, [&](auto f) {
 #pragma unroll
     for (int cb = 0; cb < G_::CB; ++cb)
 #pragma unroll
-      for (int nb = 0; nb < MB; ++nb)
+      for (int nb = 0; nb < MB; ++nb) f(dA[cb][nb]);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float* d = red + (16 * cb + 4 * g + i) * M16 + 16 * nb + r;
-          *d = first ? dA[cb][nb][i] : *d + dA[cb][nb][i];
-        }
-    if (g == 0) {
+    for (int k = 0; k < NDA; ++k) f(dav[k]);
 #pragma unroll
-      for (int nb = 0; nb < MB; ++nb) {
-        float* d = red + C * M16 + 16 * nb + r;
-        *d = first ? db[nb] : *d + db[nb];
-      }
+    for (int k = 0; k < NSC; ++k) f(scv[k]);
+  });
+  if (wave == 0) {
+    float* rec = a.partials + (int64_t)blockIdx.x * a.rec;
+    const int M = a.M;
 #pragma unroll
-      for (int cb = 0; cb < G_::CB; ++cb) {
-        float* d = red + C * M16 + M16 + 16 * cb + r;
-        *d = first ? da[cb] : *d + da[cb];
-      }
-      if (r == 0) {
-        float* d = red + C * M16 + M16 + C;
-        *d = first ? dbt : *d + dbt;
+    for (int nb = 0; nb < MB; ++nb) {
+      const int j = 16 * nb + r;
+      if (j < M) {
+#pragma unroll
+        for (int cb = 0; cb < G_::CB; ++cb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) rec[(16 * cb + 4 * g + i) * M + j] = dA[cb][nb][i];
+        if (g == 0) rec[C * M + j] = scv[nb / 4][nb % 4];
       }
     }
-  });
-  float* rec = a.partials + (int64_t)blockIdx.x * a.rec;
-  const int M = a.M;
-  for (int k = threadIdx.x; k < C * M; k += blockDim.x) {
-    const int c = k / M, j = k - c * M;
-    rec[k] = red[c * M16 + j];
+    if (g == 0) {
+#pragma unroll
+      for (int cb = 0; cb < G_::CB; ++cb) rec[C * M + M + 16 * cb + r] = dav[cb / 4][cb % 4];
+      if (r == 0) rec[C * M + M + C] = scv[MB / 4][MB % 4];
+    }
   }
-  for (int j = threadIdx.x; j < M; j += blockDim.x) rec[C * M + j] = red[C * M16 + j];
-  for (int c = threadIdx.x; c < C; c += blockDim.x) rec[C * M + M + c] = red[C * M16 + M16 + c];
-  if (threadIdx.x == 0) rec[C * M + M + C] = red[C * M16 + M16 + C];
 }
 
 // ---------------------------------------------------------------------------
