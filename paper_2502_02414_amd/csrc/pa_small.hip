@@ -1,8 +1,8 @@
 // Small kernels around the streaming passes (gfx950):
 //   - the per-call table image (logits table [A^T ; a], deslice table S'^T,
-//     backward table [dnum | S'], biases, dden) in the exact byte layout the
-//     streaming kernels copy into LDS (rows of the logits and backward tables
-//     padded as in pa_layout.h);
+//     backward table [dnum | S'] with its centres, biases, dden) in the exact
+//     byte layout the streaming kernels copy into LDS (rows of the logits and
+//     backward tables padded as in pa_layout.h), one launch per call;
 //   - the ordered reduction of per-block partial-sum records (the partial
 //     sums of Section 4.2, here over point chunks of one GPU);
 //     with the states s_j = num_j / max(den_j, eps) (Eq. 1) formed there;
@@ -39,24 +39,117 @@ size_t image_bytes(int pass, int dtype, int C, int MB) {
   return (size_t)g.OFF_2;
 }
 
+// The backward header and table (kSliceBwd, kWeightsBwd), block `bid` of
+// M + ceil(2C/256):
+//   blocks [0, M): dden_j (chain rule of Eq. 1; 0 when den_j < eps), reduced
+//     over C in a fixed tree, and sw_j = w_j / sum w;
+//   the others: one column cc of the backward table per thread (dnum for
+//     cc < C, s' beyond), its centre cN[c] / cS[c] and its M16 rows.
+// Any centre common to all slices leaves the softmax backward unchanged;
+// the mean weighted by w_j = max(den_j, 0) (the slices' share of the points)
+// keeps a slice with a tiny or floored denominator -- whose dnum_j =
+// dS_j / max(den_j, eps) can be huge -- from dragging the centre away from
+// the rows that carry weight, and keeps the small differences between nearly
+// equal rows out of the rounding.  Without the states term den is not given
+// and the weights are uniform; kWeightsBwd has neither term (zeros).
 template <typename T>
-__global__ void k_prep(PrepGeo g, PrepArgs p) {
+__device__ __forceinline__ void prep_back(const PrepGeo& g, const PrepArgs& p, int bid,
+                                          float* red) {
+  char* img = reinterpret_cast<char*>(p.img);
+  float* hdr = reinterpret_cast<float*>(img);
+  const int C = g.C, M = g.M, M16 = g.M16;
+  const bool states = p.dS != nullptr && p.pass == kSliceBwd;
+  const bool desl = p.Sp != nullptr && p.pass == kSliceBwd;
+  if (bid < M) {
+    const int j = bid;
+    // loads first: den_j, row j of dS and num (one element per thread for
+    // C <= 256), and in wave 0 the weights w_k (one slice per lane)
+    const float dj = states ? p.den[j] : 1.f;
+    float s = 0.f;
+    for (int c = threadIdx.x; c < C; c += 256) {
+      const float dv = states ? p.dS[j * C + c] : 0.f, nv = states ? p.num[j * C + c] : 0.f;
+      s += dv * (nv / dj);
+    }
+    const int k = threadIdx.x < 64 ? (int)threadIdx.x : 0;
+    const float wk = k < M ? (states ? fmaxf(p.den[k < M ? k : 0], 0.f) : 1.f) : 0.f;
+    const bool live = states && dj >= p.eps;
+    red[threadIdx.x] = live ? s : 0.f;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+      if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+      __syncthreads();
+    }
+    float wsum = wk;  // wave 0: fixed-order butterfly over the slices
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) wsum += __shfl_xor(wsum, o);
+    if (threadIdx.x == 0) {
+      hdr[M16 + j] = live ? -red[0] / dj : 0.f;
+      hdr[2 * M16 + 2 * C + j] = (states ? fmaxf(dj, 0.f) : 1.f) / wsum;
+    }
+    if (j == 0)
+      for (int q = M + threadIdx.x; q < M16; q += blockDim.x) {
+        hdr[M16 + q] = 0.f;
+        hdr[2 * M16 + 2 * C + q] = 0.f;
+      }
+    return;
+  }
+  const int cc = (bid - M) * blockDim.x + threadIdx.x;
+  if (cc >= 2 * C) return;
+  const bool first = cc < C;
+  const int c = first ? cc : cc - C;
+  const bool on = first ? states : desl;
+  // the column's values and weights, all loads issued at once (M <= 64)
+  float v[64], w[64];
+#pragma unroll
+  for (int j = 0; j < 64; ++j) {
+    const int jj = j < M ? j : M - 1;
+    v[j] = on ? (first ? p.dS[jj * C + c] : p.Sp[jj * C + c]) : 0.f;
+    w[j] = states ? p.den[jj] : 1.f;
+  }
+  float wsum = 0.f, sum = 0.f;
+#pragma unroll
+  for (int j = 0; j < 64; ++j) {
+    if (j < M) {
+      if (first) v[j] = v[j] / (w[j] >= p.eps ? w[j] : p.eps);  // dnum_j
+      const float wj = states ? fmaxf(w[j], 0.f) : 1.f;
+      wsum += wj;
+      sum += wj * v[j];
+    }
+  }
+  const float ctr = on && wsum > 0.f ? sum * (1.0f / wsum) : 0.f;
+  hdr[2 * M16 + cc] = ctr;  // cN[c] (cc < C), then cS[c]
+#pragma unroll
+  for (int j = 0; j < 64; ++j)
+    if (j < M16)
+      *reinterpret_cast<T*>(img + g.OFF_2 + lds_off(j, cc * g.SZ, g.WROW)) =
+          from_f<T>(on && j < M ? v[j] - ctr : 0.f);
+}
+
+// The table image of a pass: for the backward passes the blocks
+// [0, M + ceil(2C/256)) build the backward header and table (prep_back),
+// the rest (grid-stride) the bias and a header, the logits table [A^T ; a]
+// and, for kDeslice, S'^T.
+template <typename T>
+__global__ void __launch_bounds__(256) k_prep(PrepGeo g, PrepArgs p) {
+  __shared__ float red[256];
+  const bool back = p.pass == kSliceBwd || p.pass == kWeightsBwd;
+  const int nback = back ? g.M + (2 * g.C + 255) / 256 : 0;
+  if ((int)blockIdx.x < nback) {
+    prep_back<T>(g, p, blockIdx.x, red);
+    return;
+  }
   char* img = reinterpret_cast<char*>(p.img);
   const T* A = reinterpret_cast<const T*>(p.A);
   const T* av = reinterpret_cast<const T*>(p.a);
   const int C = g.C, M = g.M, M16 = g.M16;
-  const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t nth = (int64_t)gridDim.x * blockDim.x;
-  const bool states = p.dS != nullptr && p.pass == kSliceBwd;
-  const bool desl = p.Sp != nullptr && (p.pass == kSliceBwd || p.pass == kDeslice);
+  const int64_t tid = (int64_t)(blockIdx.x - nback) * blockDim.x + threadIdx.x;
+  const int64_t nth = (int64_t)(gridDim.x - nback) * blockDim.x;
 
-  // header: bias[M16]; the backward pass's dden, cN, cS come from
-  // k_prep_center (run first); other passes get zeros
   float* hdr = reinterpret_cast<float*>(img);
   // padded slices j >= M get bias -inf: their softmax weight is exactly 0
   for (int64_t j = tid; j < M16; j += nth) hdr[j] = j < M ? (p.b ? p.b[j] : 0.f) : -INFINITY;
-  if (p.pass != kSliceBwd)
-    for (int64_t k = tid; k < 2 * M16 + 2 * C; k += nth) hdr[M16 + k] = 0.f;
+  if (!back)
+    for (int64_t k = tid; k < 2 * M16 + 2 * C; k += nth) hdr[M16 + k] = 0.f;  // dden, cN, cS, sw
   for (int64_t c = tid; c < C; c += nth) hdr[3 * M16 + 2 * C + c] = av ? to_f<T>(av[c]) : 0.f;
   // logits table: rows j < M16: A[:, j] (0 beyond M); row M16: a
   const int64_t nL = (int64_t)(M16 + 1) * C;
@@ -80,100 +173,6 @@ __global__ void k_prep(PrepGeo g, PrepArgs p) {
       *reinterpret_cast<T*>(img + g.OFF_2 + c * g.SROW + j * g.SZ) = from_f<T>(v);
     }
   }
-  if (p.pass == kSliceBwd || p.pass == kWeightsBwd) {
-    // row j: (dnum_j | s'_j)
-    const int64_t nW = (int64_t)M16 * 2 * C;
-#pragma unroll 4
-    for (int64_t k = tid; k < nW; k += nth) {
-      const int j = (int)(k / (2 * C)), cc = (int)(k - (int64_t)j * 2 * C);
-      // rows centred by cN / cS: a shift common to all slices leaves the
-      // softmax backward unchanged and keeps the small differences between
-      // nearly equal tokens out of the rounding
-      float v = 0.f;
-      if (j < M) {
-        if (cc < C) {
-          if (states) {
-            const float d = p.den[j] >= p.eps ? p.den[j] : p.eps;
-            v = p.dS[j * C + cc] / d - hdr[2 * M16 + cc];
-          }
-        } else if (desl) {
-          v = p.Sp[j * C + (cc - C)] - hdr[2 * M16 + C + (cc - C)];
-        }
-      }
-      *reinterpret_cast<T*>(img + g.OFF_2 + lds_off(j, cc * g.SZ, g.WROW)) = from_f<T>(v);
-    }
-  }
-}
-
-// Backward header: dden_j (chain rule of Eq. 1; 0 when den_j < eps), the
-// normalised slice weights sw_j = den_j / sum den, and the centres cN, cS of
-// dnum_j, s'_j over slices.  Any centre common to all slices leaves the
-// softmax backward unchanged; the mean weighted by den_j (the slices' share
-// of the points) keeps a slice with a tiny or floored denominator -- whose
-// dnum_j = dS_j / max(den_j, eps) can be huge -- from dragging the centre
-// away from the rows that carry weight.  Without the states term den is not
-// given and the weights are uniform.  Blocks [0, M) reduce dden_j over C;
-// the others compute the centres of 256 channels each.
-__global__ void k_prep_center(PrepGeo g, PrepArgs p) {
-  __shared__ float red[256];
-  float* hdr = reinterpret_cast<float*>(p.img);
-  const int C = g.C, M = g.M, M16 = g.M16;
-  const bool states = p.dS != nullptr;
-  const bool desl = p.Sp != nullptr;
-  if ((int)blockIdx.x < M) {
-    const int j = blockIdx.x;
-    float s = 0.f;
-    if (states && p.den[j] >= p.eps) {
-      const float d = p.den[j];
-      for (int c = threadIdx.x; c < C; c += 256) s += p.dS[j * C + c] * (p.num[j * C + c] / d);
-    }
-    red[threadIdx.x] = s;
-    __syncthreads();
-    for (int w = 128; w > 0; w >>= 1) {
-      if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
-      __syncthreads();
-    }
-    if (threadIdx.x == 0) {
-      const float dd = (states && p.den[j] >= p.eps) ? -red[0] / p.den[j] : 0.f;
-      hdr[M16 + j] = dd;
-      float wsum = 0.f;
-#pragma unroll 8
-      for (int k = 0; k < M; ++k) wsum += states ? fmaxf(p.den[k], 0.f) : 1.f;
-      hdr[2 * M16 + 2 * C + j] = (states ? fmaxf(p.den[j], 0.f) : 1.f) / wsum;
-    }
-    if (j == 0)
-      for (int k = M + threadIdx.x; k < M16; k += blockDim.x) {
-        hdr[M16 + k] = 0.f;
-        hdr[2 * M16 + 2 * C + k] = 0.f;
-      }
-    return;
-  }
-  const int c = (blockIdx.x - M) * blockDim.x + threadIdx.x;
-  if (c >= C) return;
-  float wsum = 0.f, sn = 0.f, ss = 0.f;
-  // weights and values for 8 slices at a time, loads first
-  for (int j0 = 0; j0 < M; j0 += 8) {
-    float wj[8], dv[8], sv[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int j = j0 + u < M ? j0 + u : M - 1;
-      wj[u] = states ? p.den[j] : 1.f;
-      dv[u] = states ? p.dS[j * C + c] : 0.f;
-      sv[u] = desl ? p.Sp[j * C + c] : 0.f;
-    }
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      if (j0 + u >= M) break;
-      const float w = states ? fmaxf(wj[u], 0.f) : 1.f;
-      const float d = wj[u] >= p.eps ? wj[u] : p.eps;
-      wsum += w;
-      sn += w * (dv[u] / d);
-      ss += w * sv[u];
-    }
-  }
-  const float inv = wsum > 0.f ? 1.0f / wsum : 0.f;
-  hdr[2 * M16 + c] = sn * inv;
-  hdr[2 * M16 + C + c] = ss * inv;
 }
 
 hipError_t launch_prep(const PrepArgs& p, hipStream_t st) {
@@ -181,12 +180,8 @@ hipError_t launch_prep(const PrepArgs& p, hipStream_t st) {
   if (p.pass == kDeslice && !p.Sp) return hipErrorInvalidValue;
   if (p.pass == kSliceBwd && p.dS && (!p.num || !p.den)) return hipErrorInvalidValue;
   PrepGeo g = prep_geo(p.dtype, p.C, p.M, p.MB);
-  if (p.pass == kSliceBwd) {
-    hipLaunchKernelGGL(k_prep_center, dim3(p.M + (p.C + 255) / 256), dim3(256), 0, st, g, p);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
-  const int blocks = 64;
+  const bool back = p.pass == kSliceBwd || p.pass == kWeightsBwd;
+  const int blocks = 64 + (back ? p.M + (2 * p.C + 255) / 256 : 0);
   if (p.dtype == 1)
     hipLaunchKernelGGL(k_prep<bf16>, dim3(blocks), dim3(256), 0, st, g, p);
   else

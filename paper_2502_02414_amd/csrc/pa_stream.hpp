@@ -310,8 +310,8 @@ struct TileStage {
 // the compiler's wait before a stage's store then covers that stage only.
 // The last (fewer than DEPTH) tiles, already loaded, follow the loop; a
 // partial last tile is left to tail(t).  load(stage, tile) / store(stage);
-// init() is the block's set-up (tables into LDS), run by every wave once the
-// first stages' loads are in flight.
+// init() is the block's set-up (tables into LDS), run by every wave first
+// (its loads then do not queue behind the tiles').
 template <int DEPTH, typename Stage, bool REV = false, typename Load, typename Store,
           typename Body, typename Tail, typename Init>
 __device__ __forceinline__ void stream_tiles(int64_t t0, int64_t t1, int64_t tfull, Load load,
@@ -320,11 +320,11 @@ __device__ __forceinline__ void stream_tiles(int64_t t0, int64_t t1, int64_t tfu
   // REV walks the range from its end: tile(i) for i = t0 .. te - 1
   auto tile = [&](int64_t i) { return REV ? t0 + te - 1 - i : i; };
   Stage st[DEPTH];
+  init();  // the block's set-up (every wave)
   if (t0 < te) {
 #pragma unroll
     for (int d = 0; d < DEPTH; ++d) load(st[d], tile(t0 + d < te ? t0 + d : te - 1));
   }
-  init();  // the block's set-up (every wave), while the first tiles load
   if (REV && t0 <= te && te < t1) tail(te);  // this wave owns the partial last tile
   if (t0 < te) {
     int64_t t = t0;
