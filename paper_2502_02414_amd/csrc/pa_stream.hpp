@@ -63,16 +63,28 @@ enum Flags { kHasG = 1, kStatesTerm = 2, kDesliceTerm = 4 };
 template <typename T, int MB, bool BWD> constexpr int agg_depth() { return 1; }
 template <typename T, int MB> constexpr int des_depth() { return sizeof(T) == 2 && MB <= 2 ? 2 : 1; }
 template <typename T, int MB> constexpr int bwd_depth() { return 1; }
-// Passes that walk their tile ranges backwards (alternating with the passes
-// before and after them in a layer step).
-constexpr bool kRevDeslice = false, kRevSliceBwd = false;
+// Cache reuse between the passes of a layer step: the aggregate's loads of
+// x and G keep their lines in the last-level cache, and the deslice (which
+// reads the same x and G next) walks its tile ranges backwards, so it starts
+// on the lines the aggregate read last (measured: deslice -41 us, aggregate
+// +12 us at N = 1M).  The other passes stream non-temporally in the forward
+// direction (keeping their loads too cost more than their successors gained).
+constexpr bool kRevDeslice = true, kRevSliceBwd = false;
+template <int PASS> constexpr bool keep_loads() { return PASS == kAggregate; }
 
-// Point-side tensors are streamed once per pass: their 16-byte loads and
-// stores are non-temporal (they neither displace nor leave dirty data in the
-// caches, so a pass does not pay for the previous pass's write-backs).
+// Point-side tensors are streamed once per pass: their 16-byte stores are
+// non-temporal (no dirty data is left in the caches, so a pass does not pay
+// for the previous pass's write-backs), and so are the loads of a pass
+// unless it is marked as feeding the next pass through the last-level cache
+// (NT = false: the lines it reads last stay cached for a next pass that
+// walks the points in the opposite direction).
 typedef unsigned int nt_u32x4 __attribute__((ext_vector_type(4)));
+template <bool NT = true>
 __device__ __forceinline__ uint4 ld_global16(const void* p) {
-  return __builtin_bit_cast(uint4, __builtin_nontemporal_load(reinterpret_cast<const nt_u32x4*>(p)));
+  if constexpr (NT)
+    return __builtin_bit_cast(uint4, __builtin_nontemporal_load(reinterpret_cast<const nt_u32x4*>(p)));
+  else
+    return *reinterpret_cast<const uint4*>(p);
 }
 __device__ __forceinline__ void st_global16(void* p, const uint4& v) {
   __builtin_nontemporal_store(__builtin_bit_cast(nt_u32x4, v), reinterpret_cast<nt_u32x4*>(p));
@@ -192,7 +204,7 @@ __device__ __forceinline__ int last_row(int64_t p0, int64_t N) {
   return N - 1 - p0 < ROWS - 1 ? (int)(N - 1 - p0) : ROWS - 1;
 }
 
-template <typename T, int C, int ROWS = 16>
+template <typename T, int C, int ROWS = 16, bool NT = true>
 __device__ __forceinline__ void load_tile(TileRegs<T, C, ROWS>& R, const T* base, int64_t p0,
                                           int64_t N) {
   // no predicated loads, so the compiler can track these loads exactly
@@ -205,7 +217,7 @@ __device__ __forceinline__ void load_tile(TileRegs<T, C, ROWS>& R, const T* base
     const int q = lane + 64 * k;
     const int row = q / RCH, cc = q - row * RCH;
     const int rr = row < lim ? row : lim;
-    R.c[k] = ld_global16(src + (uint32_t)(rr * C * (int)sizeof(T) + 16 * cc));
+    R.c[k] = ld_global16<NT>(src + (uint32_t)(rr * C * (int)sizeof(T) + 16 * cc));
   }
 }
 
@@ -251,7 +263,7 @@ struct GRegs {
   uint4 c[GCH];
 };
 
-template <typename T, int MB, int ROWS = 16>
+template <typename T, int MB, int ROWS = 16, bool NT = true>
 __device__ __forceinline__ void load_g(GRegs<T, MB, ROWS>& gr, const T* G, const void* safe,
                                        int64_t p0, int64_t N, int M, bool hasG) {
   // A full tile's ROWS*M elements are whole 16-byte chunks (lanes past the
@@ -266,7 +278,7 @@ __device__ __forceinline__ void load_g(GRegs<T, MB, ROWS>& gr, const T* G, const
 #pragma unroll
   for (int k = 0; k < GRegs<T, MB, ROWS>::GCH; ++k) {
     const int q = lane + 64 * k < nchunk ? lane + 64 * k : nchunk - 1;
-    gr.c[k] = ld_global16(src + (full ? (uint32_t)(16 * q) : 0u));
+    gr.c[k] = ld_global16<NT>(src + (full ? (uint32_t)(16 * q) : 0u));
   }
 }
 
@@ -794,9 +806,10 @@ k_aggregate(StreamArgs a) {
 
   auto load = [&](Stage& st, int64_t tile) {
     const int64_t p0 = tile * ROWS;
-    load_tile<T, C, ROWS>(st.x, X, p0, a.N);
-    if constexpr (BWD) load_tile<T, C, ROWS>(st.y, Y, p0, a.N);
-    load_g<T, MB, ROWS>(st.g, Gp, X, p0, a.N, a.M, hasG);
+    constexpr bool NT = !keep_loads<PASS>();
+    load_tile<T, C, ROWS, NT>(st.x, X, p0, a.N);
+    if constexpr (BWD) load_tile<T, C, ROWS, NT>(st.y, Y, p0, a.N);
+    load_g<T, MB, ROWS, NT>(st.g, Gp, X, p0, a.N, a.M, hasG);
   };
   auto store = [&](const Stage& st) {
     store_tile<T, C, ROWS>(xt, st.x);
@@ -884,8 +897,9 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kDeslice)))
 
   using Stage = TileStage<T, C, MB>;
   auto load = [&](Stage& st, int64_t tile) {
-    load_tile<T, C>(st.x, X, tile * 16, a.N);
-    load_g<T, MB>(st.g, Gp, X, tile * 16, a.N, a.M, hasG);
+    constexpr bool NT = !keep_loads<kDeslice>();
+    load_tile<T, C, 16, NT>(st.x, X, tile * 16, a.N);
+    load_g<T, MB, 16, NT>(st.g, Gp, X, tile * 16, a.N, a.M, hasG);
   };
   auto store = [&](const Stage& st) {
     store_tile<T, C>(xt, st.x);
@@ -1102,9 +1116,10 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
   auto load = [&](Stage& st, int64_t tile) {
     // dY is loaded unconditionally (x stands in without the deslice term),
     // so that the loads are never predicated
-    load_tile<T, C>(st.x, X, tile * 16, a.N);
-    load_tile<T, C>(st.y, deslice ? Y : X, tile * 16, a.N);
-    load_g<T, MB>(st.g, Gp, X, tile * 16, a.N, a.M, hasG);
+    constexpr bool NT = !keep_loads<PASS>();
+    load_tile<T, C, 16, NT>(st.x, X, tile * 16, a.N);
+    load_tile<T, C, 16, NT>(st.y, deslice ? Y : X, tile * 16, a.N);
+    load_g<T, MB, 16, NT>(st.g, Gp, X, tile * 16, a.N, a.M, hasG);
   };
   auto store = [&](const Stage& st) {
     store_tile<T, C>(xt, st.x);
