@@ -93,27 +93,35 @@ __device__ __forceinline__ void prep_back(const PrepGeo& g, const PrepArgs& p, i
       }
     return;
   }
+  // per slice (once per block, in LDS): the weight w_j and 1 / max(den_j, eps)
+  float* wl = red;
+  float* rl = red + 64;
+  if (threadIdx.x < 64) {
+    const int j = threadIdx.x < M ? (int)threadIdx.x : M - 1;
+    const float dj = states ? p.den[j] : 1.f;
+    wl[threadIdx.x] = states ? fmaxf(dj, 0.f) : 1.f;
+    rl[threadIdx.x] = 1.0f / (dj >= p.eps ? dj : p.eps);
+  }
+  __syncthreads();
   const int cc = (bid - M) * blockDim.x + threadIdx.x;
   if (cc >= 2 * C) return;
   const bool first = cc < C;
   const int c = first ? cc : cc - C;
   const bool on = first ? states : desl;
-  // the column's values and weights, all loads issued at once (M <= 64)
-  float v[64], w[64];
+  // the column's values, all loads issued at once (M <= 64)
+  float v[64];
 #pragma unroll
   for (int j = 0; j < 64; ++j) {
     const int jj = j < M ? j : M - 1;
     v[j] = on ? (first ? p.dS[jj * C + c] : p.Sp[jj * C + c]) : 0.f;
-    w[j] = states ? p.den[jj] : 1.f;
   }
   float wsum = 0.f, sum = 0.f;
 #pragma unroll
   for (int j = 0; j < 64; ++j) {
     if (j < M) {
-      if (first) v[j] = v[j] / (w[j] >= p.eps ? w[j] : p.eps);  // dnum_j
-      const float wj = states ? fmaxf(w[j], 0.f) : 1.f;
-      wsum += wj;
-      sum += wj * v[j];
+      if (first) v[j] *= rl[j];  // dnum_j
+      wsum += wl[j];
+      sum += wl[j] * v[j];
     }
   }
   const float ctr = on && wsum > 0.f ? sum * (1.0f / wsum) : 0.f;
