@@ -64,11 +64,12 @@ template <typename T, int MB, bool BWD> constexpr int agg_depth() { return 1; }
 template <typename T, int MB> constexpr int des_depth() { return sizeof(T) == 2 && MB <= 2 ? 2 : 1; }
 template <typename T, int MB> constexpr int bwd_depth() { return 1; }
 // Cache reuse between the passes of a layer step: the aggregate's loads of
-// x and G keep their lines in the last-level cache, and the deslice (which
-// reads the same x and G next) walks its tile ranges backwards, so it starts
-// on the lines the aggregate read last (measured: deslice -41 us, aggregate
-// +12 us at N = 1M).  The other passes stream non-temporally in the forward
-// direction (keeping their loads too cost more than their successors gained).
+// x keep their lines in the last-level cache, and the deslice (which reads
+// the same x next) walks its tile ranges backwards, so it starts on the lines
+// the aggregate read last (measured at N = 1M: deslice -41 us, aggregate
+// +9 us; keeping G as well gained nothing).  The other passes stream
+// non-temporally in the forward direction (keeping their loads too cost more
+// than their successors gained).
 constexpr bool kRevDeslice = true, kRevSliceBwd = false;
 template <int PASS> constexpr bool keep_loads() { return PASS == kAggregate; }
 
@@ -809,7 +810,7 @@ k_aggregate(StreamArgs a) {
     constexpr bool NT = !keep_loads<PASS>();
     load_tile<T, C, ROWS, NT>(st.x, X, p0, a.N);
     if constexpr (BWD) load_tile<T, C, ROWS, NT>(st.y, Y, p0, a.N);
-    load_g<T, MB, ROWS, NT>(st.g, Gp, X, p0, a.N, a.M, hasG);
+    load_g<T, MB, ROWS, true>(st.g, Gp, X, p0, a.N, a.M, hasG);  // G: streamed either way
   };
   auto store = [&](const Stage& st) {
     store_tile<T, C, ROWS>(xt, st.x);
