@@ -10,9 +10,11 @@ the timed region.  Prints one JSON line (rank 0).
 
     python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--no-cpu-baseline]
 
-Roofline: the dominant call is timed with HIP events (torch.cuda.Event on
-the stream the library launches on) over every timed step; its achieved
-bandwidth is its algorithmic bytes per call over that time.  Traffic (HBM
+Roofline: the streaming kernel of the dominant call is timed with HIP events
+over every timed step: the library records them on the stream it launches on,
+right around that kernel (pa_time_kernel), so the duration is the kernel's
+own, as rocprofv3 reports it.  Its achieved bandwidth is its algorithmic
+bytes per launch over that duration.  Traffic (HBM
 bytes per call from the rocprofv3 FETCH_SIZE / WRITE_SIZE counters) is read
 from profiles/traffic_*.txt when that file was measured on the current
 kernel sources, else null.
@@ -44,6 +46,15 @@ def algo_bytes_per_point(C, M, b, g):
         "pa_token_attention": 0,
         "pa_token_attention_backward": 0,
     }
+
+
+# The streaming kernel each call launches (one per call).
+STREAM_KERNEL = {
+    "pa_slice_aggregate": "aggregate",          # k_aggregate, forward
+    "pa_deslice": "deslice",                    # k_deslice
+    "pa_deslice_backward": "deslice_bwd",       # k_aggregate, deslice backward
+    "pa_slice_aggregate_backward": "slice_bwd",  # k_slice_bwd
+}
 
 
 def kernel_sources_sha() -> str:
@@ -139,53 +150,52 @@ def main():
          lambda: B.pa_slice_aggregate_backward(dims, x, G, sp, num, den, dS, Sp, dY, dx, sgr, ws)),
     ]
 
-    def step(events=None, only=None):
+    def step(events=None):
         for k, (name, fn) in enumerate(calls):
-            ev = events is not None and (only is None or k == only)
-            if ev:
+            if events is not None:
                 events[k][0].record()
             fn()
-            if ev:
+            if events is not None:
                 events[k][1].record()
 
-    def event_pairs():
-        return [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-                 for _ in calls] for _ in range(args.steps)]
+    def event_pair():
+        return B.HipEvent(), B.HipEvent()
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
 
     # Per-call breakdown, in its own pass: an event pair around every call
-    # leaves the GPU idle for a few microseconds at each record, so these
-    # events stay out of the timed region.
+    # costs the GPU a little idle time at each record, so these events stay
+    # out of the timed region.
     per_call = {name: 0.0 for name, _ in calls}
-    evs = event_pairs()
+    evs = [[event_pair() for _ in calls] for _ in range(args.steps)]
     for s in range(args.steps):
         step(evs[s])
     torch.cuda.synchronize()
     for s in range(args.steps):
         for k, (name, _) in enumerate(calls):
-            per_call[name] += evs[s][k][0].elapsed_time(evs[s][k][1]) / args.steps
+            per_call[name] += evs[s][k][0].elapsed_ms(evs[s][k][1]) / args.steps
     bpp = algo_bytes_per_point(C, M, 2, 2)
     dom = max((n for n in per_call if bpp[n] > 0), key=lambda n: per_call[n])
-    kdom = [name for name, _ in calls].index(dom)
 
-    # Timed region: K whole steps; only the dominant call is bracketed by
-    # events (its duration for the roofline).
-    evs = event_pairs()
+    # Timed region: K whole steps; in each, the library brackets the streaming
+    # kernel of the dominant call with one event pair (its duration for the
+    # roofline).
+    kev = [event_pair() for _ in range(args.steps)]
+    start, end = event_pair()
     torch.cuda.synchronize()
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t_wall = time.perf_counter()
     start.record()
     for s in range(args.steps):
-        step(evs[s], only=kdom)
+        B.pa_time_kernel(dom, *kev[s])
+        step()
     end.record()
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall
-    total_ms = start.elapsed_time(end)
-    dom_ms = sum(evs[s][kdom][0].elapsed_time(evs[s][kdom][1]) for s in range(args.steps))
-    dom_ms /= args.steps
+    B.pa_time_kernel(None)
+    total_ms = start.elapsed_ms(end)
+    kernel_ms = sum(e0.elapsed_ms(e1) for e0, e1 in kev) / args.steps
     ms_per_step = total_ms / args.steps
     value = N / (ms_per_step * 1e-3)
 
@@ -198,12 +208,13 @@ def main():
         del src, dst
 
     dom_bytes = bpp[dom] * N
-    achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
+    achieved = dom_bytes / (kernel_ms * 1e-3) / 1e9
     step_bytes = sum(bpp.values()) * N
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                "traffic": read_traffic("slice_bwd"), "kernel": dom,
-                "algo_bytes_per_call": dom_bytes, "call_ms": round(dom_ms, 4)}
+                "traffic": read_traffic(STREAM_KERNEL[dom]), "call": dom,
+                "kernel": STREAM_KERNEL[dom], "algo_bytes_per_launch": dom_bytes,
+                "kernel_ms": round(kernel_ms, 4), "call_ms": round(per_call[dom], 4)}
 
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "points/s", "n_gpus": 1,

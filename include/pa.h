@@ -191,6 +191,21 @@ pa_status pa_slice_weights_backward(const pa_dims* dims, const void* x,
                                     void* dx, const pa_slice_grads* gr,
                                     void* ws, size_t ws_bytes, void* stream);
 
+/* Diagnostics: time the streaming kernel of one entry point with the
+ * caller's HIP events (hipEvent_t passed as void*), without a profiler.
+ * While armed, every later call on this thread of the entry point named
+ * `call` (pa_slice_weights, pa_slice_aggregate, pa_deslice,
+ * pa_deslice_backward, pa_slice_aggregate_backward or
+ * pa_slice_weights_backward) records `start` on its stream right before
+ * its streaming kernel and `stop` right after it, so hipEventElapsedTime
+ * gives that kernel's duration alone (without the table set-up and the
+ * partial-sum reduction around it).  The events stay owned by the caller
+ * and must outlive the calls they time; re-arming replaces the pair.
+ * call = NULL disarms.  An unknown name or a NULL event returns
+ * PA_ERR_INVALID and leaves the hook as it was.  Host-only: it launches
+ * nothing. */
+pa_status pa_time_kernel(const char* call, void* start, void* stop);
+
 #ifdef __cplusplus
 }
 #endif

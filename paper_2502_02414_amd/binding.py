@@ -28,7 +28,7 @@ SYMBOLS = (
     "pa_version", "pa_last_error", "pa_workspace_size", "pa_slice_weights",
     "pa_slice_aggregate", "pa_token_attention", "pa_deslice", "pa_deslice_backward",
     "pa_token_attention_backward", "pa_slice_aggregate_backward",
-    "pa_slice_weights_backward",
+    "pa_slice_weights_backward", "pa_time_kernel",
 )
 
 
@@ -90,6 +90,7 @@ def load(path: str = LIB_PATH):
     lib.pa_token_attention_backward.argtypes = [D, P, APp, P, P, AGp, P, S, P]
     lib.pa_slice_aggregate_backward.argtypes = [D, P, P, SPp, P, P, P, P, P, P, SGp, P, S, P]
     lib.pa_slice_weights_backward.argtypes = [D, P, P, SPp, P, P, P, SGp, P, S, P]
+    lib.pa_time_kernel.argtypes = [ctypes.c_char_p, P, P]
     for name in SYMBOLS:
         if name not in ("pa_version", "pa_last_error"):
             getattr(lib, name).restype = ctypes.c_int
@@ -208,3 +209,62 @@ def pa_slice_weights_backward(dims, x, G, sp, dW, dtau, dx, gr, ws, stream=None)
     _check(load().pa_slice_weights_backward(
         ctypes.byref(dims), _ptr(x), _ptr(G), ctypes.byref(sp), _ptr(dW), _ptr(dtau), _ptr(dx),
         ctypes.byref(gr) if gr is not None else None, _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def pa_time_kernel(call: Optional[str], start=None, stop=None):
+    """Arm (or, with call None, disarm) the kernel timing hook of this thread:
+    ``start`` / ``stop`` are ``HipEvent`` objects."""
+    _check(load().pa_time_kernel(call.encode() if call is not None else None,
+                                 start.handle if start is not None else None,
+                                 stop.handle if stop is not None else None))
+
+
+# HIP events straight from the HIP runtime (the library times its kernels on
+# the caller's stream with these; torch.cuda.Event cannot be handed over).
+HIP_EVENT_DISABLE_SYSTEM_FENCE = 0x20000000
+_hip = None
+
+
+def _hip_rt():
+    global _hip
+    if _hip is None:
+        h = ctypes.CDLL("libamdhip64.so")
+        h.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+        h.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        h.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                          ctypes.c_void_p]
+        h.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        for f in ("hipEventCreateWithFlags", "hipEventRecord", "hipEventElapsedTime",
+                  "hipEventDestroy"):
+            getattr(h, f).restype = ctypes.c_int
+        _hip = h
+    return _hip
+
+
+class HipEvent:
+    """A timing HIP event.  By default it is recorded with a device-scope
+    fence only (hipEventDisableSystemFence): no write-back of the caches to
+    the host at each record, so timing a kernel disturbs the next one less."""
+
+    def __init__(self, flags: int = HIP_EVENT_DISABLE_SYSTEM_FENCE):
+        self.handle = ctypes.c_void_p()
+        e = _hip_rt().hipEventCreateWithFlags(ctypes.byref(self.handle), flags)
+        if e != 0:
+            raise RuntimeError(f"hipEventCreateWithFlags failed ({e})")
+
+    def record(self, stream=None):
+        e = _hip_rt().hipEventRecord(self.handle, _stream(stream))
+        if e != 0:
+            raise RuntimeError(f"hipEventRecord failed ({e})")
+
+    def elapsed_ms(self, end: "HipEvent") -> float:
+        ms = ctypes.c_float()
+        e = _hip_rt().hipEventElapsedTime(ctypes.byref(ms), self.handle, end.handle)
+        if e != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed ({e})")
+        return ms.value
+
+    def __del__(self):
+        if self.handle and _hip is not None:
+            _hip.hipEventDestroy(self.handle)
+            self.handle = ctypes.c_void_p()

@@ -175,6 +175,27 @@ pa_status check_slice(const pa_dims* dims, const void* x, const void* G,
 
 hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 
+// pa_time_kernel's hook: the pass whose streaming kernel is bracketed by the
+// caller's events on this thread (-1: disarmed).
+struct KernelTimer {
+  int pass = -1;
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+thread_local KernelTimer g_timer;
+
+// Launches the streaming kernel of a pass, between the armed events when it
+// is the timed pass.
+hipError_t run_stream(int pass, const pa_dims& d, const pa::StreamLaunch& L, hipStream_t st) {
+  const bool timed = g_timer.pass == pass;
+  if (timed) {
+    hipError_t e = hipEventRecord(g_timer.start, st);
+    if (e != hipSuccess) return e;
+  }
+  hipError_t e = pa::launch_stream(pass, d.dtype, d.C, mblocks(d.M), L, st);
+  if (e == hipSuccess && timed) e = hipEventRecord(g_timer.stop, st);
+  return e;
+}
+
 }  // namespace
 
 extern "C" {
@@ -182,6 +203,30 @@ extern "C" {
 int pa_version(void) { return PA_VERSION; }
 
 const char* pa_last_error(void) { return g_err.c_str(); }
+
+pa_status pa_time_kernel(const char* call, void* start, void* stop) {
+  if (!call) {
+    g_timer = KernelTimer{};
+    return PA_OK;
+  }
+  static const struct { const char* name; int pass; } kCalls[] = {
+      {"pa_slice_weights", pa::kWeights},
+      {"pa_slice_aggregate", pa::kAggregate},
+      {"pa_deslice", pa::kDeslice},
+      {"pa_deslice_backward", pa::kDesliceBwd},
+      {"pa_slice_aggregate_backward", pa::kSliceBwd},
+      {"pa_slice_weights_backward", pa::kWeightsBwd},
+  };
+  int pass = -1;
+  for (const auto& c : kCalls)
+    if (std::strcmp(call, c.name) == 0) pass = c.pass;
+  if (pass < 0) return fail(PA_ERR_INVALID, "pa_time_kernel: no streaming kernel in '%s'", call);
+  if (!start || !stop) return fail(PA_ERR_INVALID, "pa_time_kernel: start and stop are required");
+  g_timer.pass = pass;
+  g_timer.start = static_cast<hipEvent_t>(start);
+  g_timer.stop = static_cast<hipEvent_t>(stop);
+  return PA_OK;
+}
 
 pa_status pa_workspace_size(const pa_dims* dims, size_t* bytes) {
   PA_TRY(check_dims(dims));
@@ -203,7 +248,7 @@ pa_status pa_slice_weights(const pa_dims* dims, const void* x, const void* G,
   pa::StreamLaunch L = stream_of(*dims, pa::kWeights, x, G, sp, ws);
   L.out = W;
   L.tau_out = tau;
-  PA_HIP(pa::launch_stream(pa::kWeights, dims->dtype, dims->C, mblocks(dims->M), L, st),
+  PA_HIP(run_stream(pa::kWeights, *dims, L, st),
          "slice weights");
   return PA_OK;
 }
@@ -220,7 +265,7 @@ pa_status pa_slice_aggregate(const pa_dims* dims, const void* x, const void* G,
   hipStream_t st = as_stream(stream);
   PA_HIP(pa::launch_prep(prep_of(*dims, pa::kAggregate, sp, ws), st), "prep");
   pa::StreamLaunch L = stream_of(*dims, pa::kAggregate, x, G, sp, ws);
-  PA_HIP(pa::launch_stream(pa::kAggregate, dims->dtype, dims->C, mblocks(dims->M), L, st),
+  PA_HIP(run_stream(pa::kAggregate, *dims, L, st),
          "slice aggregate");
   pa::Segments seg{};
   seg.dst[0] = num; seg.len[0] = (int64_t)dims->M * dims->C;
@@ -390,7 +435,7 @@ pa_status pa_deslice(const pa_dims* dims, const void* x, const void* G,
   PA_HIP(pa::launch_prep(p, st), "prep");
   pa::StreamLaunch L = stream_of(*dims, pa::kDeslice, x, G, sp, ws);
   L.out = y;
-  PA_HIP(pa::launch_stream(pa::kDeslice, dims->dtype, dims->C, mblocks(dims->M), L, st),
+  PA_HIP(run_stream(pa::kDeslice, *dims, L, st),
          "deslice");
   return PA_OK;
 }
@@ -407,7 +452,7 @@ pa_status pa_deslice_backward(const pa_dims* dims, const void* x, const void* G,
   PA_HIP(pa::launch_prep(prep_of(*dims, pa::kDesliceBwd, sp, ws), st), "prep");
   pa::StreamLaunch L = stream_of(*dims, pa::kDesliceBwd, x, G, sp, ws);
   L.dY = dY;
-  PA_HIP(pa::launch_stream(pa::kDesliceBwd, dims->dtype, dims->C, mblocks(dims->M), L, st),
+  PA_HIP(run_stream(pa::kDesliceBwd, *dims, L, st),
          "deslice backward");
   pa::Segments seg{};
   seg.dst[0] = dSp; seg.len[0] = (int64_t)dims->M * dims->C;
@@ -472,7 +517,7 @@ pa_status pa_slice_aggregate_backward(const pa_dims* dims, const void* x, const 
   L.out = dx;
   L.states = dS != nullptr;
   L.deslice = Sp != nullptr;
-  PA_HIP(pa::launch_stream(pa::kSliceBwd, dims->dtype, dims->C, mblocks(dims->M), L, st),
+  PA_HIP(run_stream(pa::kSliceBwd, *dims, L, st),
          "slice backward");
   return reduce_slice_grads(*dims, L, gr, st);
 }
@@ -494,7 +539,7 @@ pa_status pa_slice_weights_backward(const pa_dims* dims, const void* x, const vo
   L.dW = dW;
   L.dtau = dtau;
   L.out = dx;
-  PA_HIP(pa::launch_stream(pa::kWeightsBwd, dims->dtype, dims->C, mblocks(dims->M), L, st),
+  PA_HIP(run_stream(pa::kWeightsBwd, *dims, L, st),
          "slice weights backward");
   return reduce_slice_grads(*dims, L, gr, st);
 }

@@ -32,7 +32,7 @@ def _declared_symbols():
 
 def test_every_declared_symbol_is_exported(lib):
     declared = _declared_symbols()
-    assert len(declared) == 11
+    assert len(declared) == 12
     assert sorted(B.SYMBOLS) == declared
     for name in declared:
         assert hasattr(lib, name), name
@@ -137,3 +137,14 @@ def test_unserved_table_shape_is_unsupported(lib):
     st = lib.pa_slice_aggregate_backward(ctypes.byref(d), FAKE, None, ctypes.byref(sp), FAKE,
                                          FAKE, FAKE, None, None, FAKE, None, FAKE, n, None)
     assert st == B.PA_ERR_UNSUPPORTED
+
+
+def test_kernel_timing_hook_checks(lib):
+    # host-only: arming records nothing until a call launches its kernel
+    assert lib.pa_time_kernel(None, None, None) == B.PA_OK
+    assert lib.pa_time_kernel(b"pa_token_attention", FAKE, FAKE) == B.PA_ERR_INVALID
+    assert "no streaming kernel" in lib.pa_last_error().decode()
+    assert lib.pa_time_kernel(b"pa_deslice", FAKE, None) == B.PA_ERR_INVALID
+    assert lib.pa_time_kernel(b"pa_slice_aggregate_backward", FAKE, FAKE) == B.PA_OK
+    assert lib.pa_time_kernel(None, None, None) == B.PA_OK
+

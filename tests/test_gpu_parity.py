@@ -270,6 +270,31 @@ def test_deterministic(cases):
         assert g.torch.equal(a[k], b[k]), k
 
 
+def test_kernel_timing_hook(cases):
+    """pa_time_kernel brackets exactly one streaming kernel per call with the
+    caller's events and changes no output."""
+    from paper_2502_02414_amd import binding as B
+    shape = (66013, 256, 8, 32, "bf16")
+    c, g, _ = get_case(cases, shape)
+    a = g.layer()
+    for call in ("pa_slice_aggregate", "pa_deslice", "pa_deslice_backward",
+                 "pa_slice_aggregate_backward"):
+        e0, e1, c0, c1 = B.HipEvent(), B.HipEvent(), B.HipEvent(), B.HipEvent()
+        B.pa_time_kernel(call, e0, e1)
+        try:
+            c0.record()
+            b = g.layer()
+            c1.record()
+            g.torch.cuda.synchronize()
+        finally:
+            B.pa_time_kernel(None)
+        kernel_ms, layer_ms = e0.elapsed_ms(e1), c0.elapsed_ms(c1)
+        say(f"  {call}: kernel {kernel_ms * 1e3:.1f} us of a {layer_ms * 1e3:.1f} us layer")
+        assert 0.0 < kernel_ms < layer_ms
+        for k in a:
+            assert g.torch.equal(a[k], b[k]), (call, k)
+
+
 @pytest.mark.parametrize("variant", ["no_noise", "no_adatemp", "single_point", "empty_slice"])
 def test_edge_cases(variant):
     say(f"edge {variant}")
