@@ -191,12 +191,41 @@ pa_status pa_slice_weights_backward(const pa_dims* dims, const void* x,
                                     void* dx, const pa_slice_grads* gr,
                                     void* ws, size_t ws_bytes, void* stream);
 
+/* Stored-weights variant of the forward and of the deslice backward.
+ * Algorithm 1 computes the weights once and reuses them in the deslice;
+ * the calls above recompute them from x and G in every pass instead.
+ * These three calls store them once: W [N,M] in dtype (row-major, exactly
+ * the weights the aggregate contracted, i.e. rounded to dtype), written by
+ * pa_slice_aggregate_w, then read by pa_deslice_w and pa_deslice_backward_w
+ * in place of x and G (64 B per point at M = 32 in bf16 instead of 576).
+ * pa_slice_aggregate_backward needs x anyway and recomputes them as before.
+ * W is caller-owned device memory, 16-byte aligned, and must not alias any
+ * other argument.  Results equal those of the recomputing calls up to the
+ * fp32 accumulation order.
+ *
+ * pa_slice_aggregate_w: pa_slice_aggregate, plus W written. */
+pa_status pa_slice_aggregate_w(const pa_dims* dims, const void* x, const void* G,
+                               const pa_slice_params* sp, float* num, float* den,
+                               float* S, void* W, void* ws, size_t ws_bytes,
+                               void* stream);
+
+/* pa_deslice_w: y = W Sp (the deslice of Section 3) from a stored W [N,M]
+ * dtype; y [N,C] dtype.  dims->tau0, tau_min and eps are not used. */
+pa_status pa_deslice_w(const pa_dims* dims, const void* W, const float* Sp, void* y,
+                       void* ws, size_t ws_bytes, void* stream);
+
+/* pa_deslice_backward_w: dSp [M,C] fp32 = W^T dY from a stored W [N,M]
+ * dtype and dY [N,C] dtype. */
+pa_status pa_deslice_backward_w(const pa_dims* dims, const void* W, const void* dY,
+                                float* dSp, void* ws, size_t ws_bytes, void* stream);
+
 /* Diagnostics: time the streaming kernel of one entry point with the
  * caller's HIP events (hipEvent_t passed as void*), without a profiler.
  * While armed, every later call on this thread of the entry point named
  * `call` (pa_slice_weights, pa_slice_aggregate, pa_deslice,
- * pa_deslice_backward, pa_slice_aggregate_backward or
- * pa_slice_weights_backward) records `start` on its stream right before
+ * pa_deslice_backward, pa_slice_aggregate_backward,
+ * pa_slice_weights_backward, pa_slice_aggregate_w, pa_deslice_w or
+ * pa_deslice_backward_w) records `start` on its stream right before
  * its streaming kernel and `stop` right after it, so hipEventElapsedTime
  * gives that kernel's duration alone (without the table set-up and the
  * partial-sum reduction around it).  The events stay owned by the caller

@@ -28,7 +28,8 @@ SYMBOLS = (
     "pa_version", "pa_last_error", "pa_workspace_size", "pa_slice_weights",
     "pa_slice_aggregate", "pa_token_attention", "pa_deslice", "pa_deslice_backward",
     "pa_token_attention_backward", "pa_slice_aggregate_backward",
-    "pa_slice_weights_backward", "pa_time_kernel",
+    "pa_slice_weights_backward", "pa_time_kernel", "pa_slice_aggregate_w", "pa_deslice_w",
+    "pa_deslice_backward_w",
 )
 
 
@@ -91,6 +92,9 @@ def load(path: str = LIB_PATH):
     lib.pa_slice_aggregate_backward.argtypes = [D, P, P, SPp, P, P, P, P, P, P, SGp, P, S, P]
     lib.pa_slice_weights_backward.argtypes = [D, P, P, SPp, P, P, P, SGp, P, S, P]
     lib.pa_time_kernel.argtypes = [ctypes.c_char_p, P, P]
+    lib.pa_slice_aggregate_w.argtypes = [D, P, P, SPp, P, P, P, P, P, S, P]
+    lib.pa_deslice_w.argtypes = [D, P, P, P, P, S, P]
+    lib.pa_deslice_backward_w.argtypes = [D, P, P, P, P, S, P]
     for name in SYMBOLS:
         if name not in ("pa_version", "pa_last_error"):
             getattr(lib, name).restype = ctypes.c_int
@@ -209,6 +213,22 @@ def pa_slice_weights_backward(dims, x, G, sp, dW, dtau, dx, gr, ws, stream=None)
     _check(load().pa_slice_weights_backward(
         ctypes.byref(dims), _ptr(x), _ptr(G), ctypes.byref(sp), _ptr(dW), _ptr(dtau), _ptr(dx),
         ctypes.byref(gr) if gr is not None else None, _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def pa_slice_aggregate_w(dims, x, G, sp, num, den, S, W, ws, stream=None):
+    _check(load().pa_slice_aggregate_w(ctypes.byref(dims), _ptr(x), _ptr(G), ctypes.byref(sp),
+                                       _ptr(num), _ptr(den), _ptr(S), _ptr(W), _ptr(ws),
+                                       ws.numel(), _stream(stream)))
+
+
+def pa_deslice_w(dims, W, Sp, y, ws, stream=None):
+    _check(load().pa_deslice_w(ctypes.byref(dims), _ptr(W), _ptr(Sp), _ptr(y), _ptr(ws),
+                               ws.numel(), _stream(stream)))
+
+
+def pa_deslice_backward_w(dims, W, dY, dSp, ws, stream=None):
+    _check(load().pa_deslice_backward_w(ctypes.byref(dims), _ptr(W), _ptr(dY), _ptr(dSp),
+                                        _ptr(ws), ws.numel(), _stream(stream)))
 
 
 def pa_time_kernel(call: Optional[str], start=None, stop=None):

@@ -15,7 +15,7 @@ LIB = os.path.join(HERE, "libpa.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 SOURCES = ["pa_stream.hip", "pa_stream_agg.hip", "pa_stream_des.hip", "pa_stream_desbwd.hip",
            "pa_stream_wts.hip", "pa_stream_slbwd.hip", "pa_stream_wtsbwd.hip", "pa_small.hip",
-           "pa_tokens.hip",
+           "pa_stream_aggw.hip", "pa_stream_desw.hip", "pa_stream_desbwdw.hip", "pa_tokens.hip",
            "pa_api.cpp"]
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-fPIC", "-std=c++17",

@@ -56,7 +56,7 @@ Layout layout_of(const pa_dims& d) {
   Layout L{};
   const int MB = mblocks(d.M);
   size_t img = 0;
-  for (int pass = pa::kAggregate; pass <= pa::kWeightsBwd; ++pass) {
+  for (int pass = 0; pass < pa::kNumPasses; ++pass) {
     size_t b = pa::image_bytes(pass, d.dtype, d.C, MB);
     if (b > img) img = b;
   }
@@ -136,9 +136,11 @@ pa::PrepArgs prep_of(const pa_dims& d, int pass, const pa_slice_params* sp, void
   p.M = d.M;
   p.MB = mblocks(d.M);
   p.eps = d.eps;
-  p.A = sp->A;
-  p.b = sp->b;
-  p.a = sp->a;
+  if (sp) {  // (the stored-weights deslice builds no logits table)
+    p.A = sp->A;
+    p.b = sp->b;
+    p.a = sp->a;
+  }
   p.img = wsb(ws) + layout_of(d).img;
   return p;
 }
@@ -155,7 +157,7 @@ pa::StreamLaunch stream_of(const pa_dims& d, int pass, const void* x, const void
   L.M = d.M;
   L.rec = (int)pa::record_floats(pass, d.C, d.M);
   L.P = chunks(d, pass);
-  L.tb = (double)d.tau0 + (double)sp->b_t;
+  L.tb = (double)d.tau0 + (sp ? (double)sp->b_t : 0.0);
   L.tau_min = d.tau_min;
   return L;
 }
@@ -216,6 +218,9 @@ pa_status pa_time_kernel(const char* call, void* start, void* stop) {
       {"pa_deslice_backward", pa::kDesliceBwd},
       {"pa_slice_aggregate_backward", pa::kSliceBwd},
       {"pa_slice_weights_backward", pa::kWeightsBwd},
+      {"pa_slice_aggregate_w", pa::kAggregateW},
+      {"pa_deslice_w", pa::kDesliceW},
+      {"pa_deslice_backward_w", pa::kDesliceBwdW},
   };
   int pass = -1;
   for (const auto& c : kCalls)
@@ -253,20 +258,25 @@ pa_status pa_slice_weights(const pa_dims* dims, const void* x, const void* G,
   return PA_OK;
 }
 
-pa_status pa_slice_aggregate(const pa_dims* dims, const void* x, const void* G,
-                             const pa_slice_params* sp, float* num, float* den, float* S,
-                             void* ws, size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+// pa_slice_aggregate and pa_slice_aggregate_w (which also writes W).
+pa_status slice_aggregate(int pass, const pa_dims* dims, const void* x, const void* G,
+                          const pa_slice_params* sp, float* num, float* den, float* S, void* W,
+                          void* ws, size_t ws_bytes, void* stream) {
   PA_TRY(check_slice(dims, x, G, sp));
   PA_TRY(check_ptr(num, "num", true));
   PA_TRY(check_ptr(den, "den", true));
   PA_TRY(check_ptr(S, "S", true));
-  PA_TRY(check_pass(*dims, pa::kAggregate));
+  PA_TRY(check_ptr(W, "W", pass == pa::kAggregateW));
+  PA_TRY(check_pass(*dims, pass));
   PA_TRY(check_ws(*dims, ws, ws_bytes));
   hipStream_t st = as_stream(stream);
-  PA_HIP(pa::launch_prep(prep_of(*dims, pa::kAggregate, sp, ws), st), "prep");
-  pa::StreamLaunch L = stream_of(*dims, pa::kAggregate, x, G, sp, ws);
-  PA_HIP(run_stream(pa::kAggregate, *dims, L, st),
-         "slice aggregate");
+  PA_HIP(pa::launch_prep(prep_of(*dims, pass, sp, ws), st), "prep");
+  pa::StreamLaunch L = stream_of(*dims, pass, x, G, sp, ws);
+  L.out = W;
+  PA_HIP(run_stream(pass, *dims, L, st), "slice aggregate");
   pa::Segments seg{};
   seg.dst[0] = num; seg.len[0] = (int64_t)dims->M * dims->C;
   seg.dst[1] = den; seg.len[1] = dims->M;
@@ -276,6 +286,59 @@ pa_status pa_slice_aggregate(const pa_dims* dims, const void* x, const void* G,
   seg.den_col = seg.nS;
   seg.C = dims->C;
   seg.eps = dims->eps;
+  PA_HIP(pa::launch_reduce(L.partials, L.P, L.rec, seg, st), "reduce");
+  return PA_OK;
+}
+}  // namespace
+
+extern "C" {
+
+pa_status pa_slice_aggregate(const pa_dims* dims, const void* x, const void* G,
+                             const pa_slice_params* sp, float* num, float* den, float* S,
+                             void* ws, size_t ws_bytes, void* stream) {
+  return slice_aggregate(pa::kAggregate, dims, x, G, sp, num, den, S, nullptr, ws, ws_bytes,
+                         stream);
+}
+
+pa_status pa_slice_aggregate_w(const pa_dims* dims, const void* x, const void* G,
+                               const pa_slice_params* sp, float* num, float* den, float* S,
+                               void* W, void* ws, size_t ws_bytes, void* stream) {
+  return slice_aggregate(pa::kAggregateW, dims, x, G, sp, num, den, S, W, ws, ws_bytes, stream);
+}
+
+pa_status pa_deslice_w(const pa_dims* dims, const void* W, const float* Sp, void* y, void* ws,
+                       size_t ws_bytes, void* stream) {
+  PA_TRY(check_dims(dims));
+  PA_TRY(check_ptr(W, "W", true));
+  PA_TRY(check_ptr(Sp, "Sp", true));
+  PA_TRY(check_ptr(y, "y", true));
+  PA_TRY(check_pass(*dims, pa::kDesliceW));
+  PA_TRY(check_ws(*dims, ws, ws_bytes));
+  hipStream_t st = as_stream(stream);
+  pa::PrepArgs p = prep_of(*dims, pa::kDesliceW, nullptr, ws);
+  p.Sp = Sp;
+  PA_HIP(pa::launch_prep(p, st), "prep");
+  pa::StreamLaunch L = stream_of(*dims, pa::kDesliceW, nullptr, W, nullptr, ws);
+  L.out = y;
+  PA_HIP(run_stream(pa::kDesliceW, *dims, L, st), "deslice (stored weights)");
+  return PA_OK;
+}
+
+pa_status pa_deslice_backward_w(const pa_dims* dims, const void* W, const void* dY, float* dSp,
+                                void* ws, size_t ws_bytes, void* stream) {
+  PA_TRY(check_dims(dims));
+  PA_TRY(check_ptr(W, "W", true));
+  PA_TRY(check_ptr(dY, "dY", true));
+  PA_TRY(check_ptr(dSp, "dSp", true));
+  PA_TRY(check_pass(*dims, pa::kDesliceBwdW));
+  PA_TRY(check_ws(*dims, ws, ws_bytes));
+  hipStream_t st = as_stream(stream);
+  pa::StreamLaunch L = stream_of(*dims, pa::kDesliceBwdW, nullptr, W, nullptr, ws);
+  L.dY = dY;
+  PA_HIP(run_stream(pa::kDesliceBwdW, *dims, L, st), "deslice backward (stored weights)");
+  pa::Segments seg{};
+  seg.dst[0] = dSp; seg.len[0] = (int64_t)dims->M * dims->C;
+  seg.n = 1;
   PA_HIP(pa::launch_reduce(L.partials, L.P, L.rec, seg, st), "reduce");
   return PA_OK;
 }

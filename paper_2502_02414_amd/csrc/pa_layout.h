@@ -9,8 +9,15 @@
 
 namespace pa {
 
+// The stored-weights passes follow Algorithm 1's dataflow, where the weights
+// are computed once and the deslice reuses them: kAggregateW is kAggregate
+// that also writes W [N,M] (storage dtype); kDesliceW and kDesliceBwdW read
+// that W in place of recomputing it from x and G.
 enum Pass { kAggregate = 0, kDeslice = 1, kDesliceBwd = 2, kWeights = 3, kSliceBwd = 4,
-            kWeightsBwd = 5 };
+            kWeightsBwd = 5, kAggregateW = 6, kDesliceW = 7, kDesliceBwdW = 8 };
+constexpr int kNumPasses = 9;
+constexpr bool agg_fwd(int pass) { return pass == kAggregate || pass == kAggregateW; }
+constexpr bool agg_bwd(int pass) { return pass == kDesliceBwd || pass == kDesliceBwdW; }
 
 constexpr int kLdsBytes = 160 * 1024;  // LDS per CU on gfx950
 constexpr int kPartialsMax = 256;      // blocks (point chunks) per streaming pass
@@ -51,10 +58,14 @@ struct Geo {
   // backward aggregate, with two streamed tensors, measured faster with
   // 16-point tiles (fewer loads in flight per wave)
   static constexpr int rows(int pass) {
-    return pass == kAggregate && SZ == 2 && MB <= 2 ? 32 : 16;
+    return agg_fwd(pass) && SZ == 2 && MB <= 2 ? 32 : 16;
   }
+  // LDS image of a pass: the stored-weights deslice holds only the deslice
+  // table (at offset 0), its backward no table at all
   static constexpr int img_bytes(int pass) {
     return pass == kDeslice ? OFF_2 + SZ_S
+         : pass == kDesliceW ? SZ_S
+         : pass == kDesliceBwdW ? 0
          : (pass == kSliceBwd || pass == kWeightsBwd) ? OFF_2 + SZ_W
          : OFF_2;
   }
@@ -63,15 +74,15 @@ struct Geo {
   // Gumbel and weight rows for 32 points
   static constexpr int wave_bytes(int pass) {
     return (pass == kSliceBwd || pass == kWeightsBwd) ? 2 * XT + GT + SCR
-         : pass == kAggregate && rows(pass) == 32 ? 2 * XT + 4 * GT
-         : pass == kDesliceBwd ? 2 * XT + 2 * GT
-         : pass == kAggregate ? XT + 2 * GT
+         : agg_fwd(pass) && rows(pass) == 32 ? 2 * XT + 4 * GT
+         : agg_bwd(pass) ? 2 * XT + 2 * GT
+         : agg_fwd(pass) ? XT + 2 * GT
          : XT + GT;
   }
   // f32x4 per lane of a wave's partial sums (the cross-wave reduction)
   static constexpr int red_vecs(int pass) {
-    return pass == kAggregate ? MB * CB + MB
-         : pass == kDesliceBwd ? MB * CB
+    return agg_fwd(pass) ? MB * CB + MB
+         : agg_bwd(pass) ? MB * CB
          : (pass == kSliceBwd || pass == kWeightsBwd) ? CB * MB + (CB + 3) / 4 + (MB + 4) / 4
          : 0;
   }
@@ -83,7 +94,7 @@ struct Geo {
   // SIMD hide each other's latency); the accumulating passes, and fp32
   // storage (whose tiles take twice the registers), run 4
   static constexpr int max_waves(int pass) {
-    return (pass == kDeslice || pass == kWeights) && SZ == 2 ? 8 : 4;
+    return (pass == kDeslice || pass == kDesliceW || pass == kWeights) && SZ == 2 ? 8 : 4;
   }
   static constexpr int waves(int pass) {
     return (max_waves(pass) >= 8 && img_bytes(pass) + 8 * wave_bytes(pass) <= kLdsBytes) ? 8
@@ -112,8 +123,10 @@ inline int num_chunks(int64_t N, int waves) {
 // Floats in the record a pass writes per block (valid slices only).
 inline int64_t record_floats(int pass, int C, int M) {
   switch (pass) {
-    case kAggregate: return (int64_t)M * C + M;
-    case kDesliceBwd: return (int64_t)M * C;
+    case kAggregate:
+    case kAggregateW: return (int64_t)M * C + M;
+    case kDesliceBwd:
+    case kDesliceBwdW: return (int64_t)M * C;
     case kSliceBwd:
     case kWeightsBwd: return (int64_t)C * M + M + C + 1;
     default: return 0;

@@ -34,7 +34,8 @@ static PrepGeo prep_geo(int dtype, int C, int M, int MB) {
 
 size_t image_bytes(int pass, int dtype, int C, int MB) {
   PrepGeo g = prep_geo(dtype, C, 16 * MB, MB);
-  if (pass == kDeslice) return (size_t)g.OFF_2 + (size_t)C * g.SROW;
+  if (pass == kDeslice || pass == kDesliceW) return (size_t)g.OFF_2 + (size_t)C * g.SROW;
+  if (pass == kDesliceBwdW) return 0;
   if (pass == kSliceBwd || pass == kWeightsBwd) return (size_t)g.OFF_2 + (size_t)g.M16 * g.WROW;
   return (size_t)g.OFF_2;
 }
@@ -137,6 +138,20 @@ __device__ __forceinline__ void prep_back(const PrepGeo& g, const PrepArgs& p, i
 // [0, M + ceil(2C/256)) build the backward header and table (prep_back),
 // the rest (grid-stride) the bias and a header, the logits table [A^T ; a]
 // and, for kDeslice, S'^T.
+// The deslice table S'^T (row c, column j; columns j >= M zero) at OFF_2.
+template <typename T>
+__device__ __forceinline__ void prep_deslice_table(const PrepGeo& g, const PrepArgs& p, char* img,
+                                                   int64_t tid, int64_t nth) {
+  const int C = g.C, M = g.M, M16 = g.M16;
+  const int64_t nS = (int64_t)C * M16;
+#pragma unroll 4
+  for (int64_t k = tid; k < nS; k += nth) {
+    const int c = (int)(k / M16), j = (int)(k - (int64_t)c * M16);
+    const float v = (j < M) ? p.Sp[j * C + c] : 0.f;
+    *reinterpret_cast<T*>(img + g.OFF_2 + c * g.SROW + j * g.SZ) = from_f<T>(v);
+  }
+}
+
 template <typename T>
 __global__ void __launch_bounds__(256) k_prep(PrepGeo g, PrepArgs p) {
   __shared__ float red[256];
@@ -154,6 +169,10 @@ __global__ void __launch_bounds__(256) k_prep(PrepGeo g, PrepArgs p) {
   const int64_t nth = (int64_t)(gridDim.x - nback) * blockDim.x;
 
   float* hdr = reinterpret_cast<float*>(img);
+  if (p.pass == kDesliceW) {  // the stored-weights deslice: its S'^T table only
+    prep_deslice_table<T>(g, p, img, tid, nth);
+    return;
+  }
   // padded slices j >= M get bias -inf: their softmax weight is exactly 0
   for (int64_t j = tid; j < M16; j += nth) hdr[j] = j < M ? (p.b ? p.b[j] : 0.f) : -INFINITY;
   if (!back)
@@ -171,21 +190,12 @@ __global__ void __launch_bounds__(256) k_prep(PrepGeo g, PrepArgs p) {
       v = av ? av[c] : from_f<T>(0.f);
     *reinterpret_cast<T*>(img + g.OFF_L + lds_off(j, c * g.SZ, g.TROW)) = v;
   }
-  if (p.pass == kDeslice) {
-    // S'^T: row c, column j
-    const int64_t nS = (int64_t)C * M16;
-#pragma unroll 4
-    for (int64_t k = tid; k < nS; k += nth) {
-      const int c = (int)(k / M16), j = (int)(k - (int64_t)c * M16);
-      const float v = (j < M) ? p.Sp[j * C + c] : 0.f;
-      *reinterpret_cast<T*>(img + g.OFF_2 + c * g.SROW + j * g.SZ) = from_f<T>(v);
-    }
-  }
+  if (p.pass == kDeslice) prep_deslice_table<T>(g, p, img, tid, nth);
 }
 
 hipError_t launch_prep(const PrepArgs& p, hipStream_t st) {
-  if (!p.img || !p.A) return hipErrorInvalidValue;
-  if (p.pass == kDeslice && !p.Sp) return hipErrorInvalidValue;
+  if (!p.img || (!p.A && p.pass != kDesliceW)) return hipErrorInvalidValue;
+  if ((p.pass == kDeslice || p.pass == kDesliceW) && !p.Sp) return hipErrorInvalidValue;
   if (p.pass == kSliceBwd && p.dS && (!p.num || !p.den)) return hipErrorInvalidValue;
   PrepGeo g = prep_geo(p.dtype, p.C, p.M, p.MB);
   const bool back = p.pass == kSliceBwd || p.pass == kWeightsBwd;

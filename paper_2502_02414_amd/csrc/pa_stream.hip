@@ -24,13 +24,16 @@ hipError_t launch_stream(int pass, int dtype, int C, int MB, const StreamLaunch&
                          hipStream_t st) {
   // every pointer a pass dereferences must be there (a NULL is an error here,
   // never a device fault)
-  if (!L.x || !L.img || L.N < 1 || L.M < 1 || L.M > 16 * MB || L.P < 1) return hipErrorInvalidValue;
-  const bool reduces = pass == kAggregate || pass == kDesliceBwd || pass == kSliceBwd ||
-                       pass == kWeightsBwd;
-  if (reduces && !L.partials) return hipErrorInvalidValue;
-  if ((pass == kDeslice || pass == kWeights || pass == kSliceBwd || pass == kWeightsBwd) && !L.out)
+  // (the stored-weights passes read W, given as G, in place of x and G)
+  const bool win = pass == kDesliceW || pass == kDesliceBwdW;
+  if ((win ? !L.G : !L.x) || !L.img || L.N < 1 || L.M < 1 || L.M > 16 * MB || L.P < 1)
     return hipErrorInvalidValue;
-  if (pass == kDesliceBwd && !L.dY) return hipErrorInvalidValue;
+  const bool reduces = agg_fwd(pass) || agg_bwd(pass) || pass == kSliceBwd || pass == kWeightsBwd;
+  if (reduces && !L.partials) return hipErrorInvalidValue;
+  if ((pass == kDeslice || pass == kDesliceW || pass == kWeights || pass == kSliceBwd ||
+       pass == kWeightsBwd || pass == kAggregateW) && !L.out)
+    return hipErrorInvalidValue;
+  if (agg_bwd(pass) && !L.dY) return hipErrorInvalidValue;
   if (pass == kSliceBwd && L.deslice && !L.dY) return hipErrorInvalidValue;
   if (pass == kWeightsBwd && !L.dW) return hipErrorInvalidValue;
   StreamArgs a;
@@ -45,6 +48,9 @@ hipError_t launch_stream(int pass, int dtype, int C, int MB, const StreamLaunch&
     case kWeights: return launch_weights_pass(dtype, C, MB, a, L.P, st);
     case kSliceBwd: return launch_slice_bwd_pass(dtype, C, MB, a, L.P, st);
     case kWeightsBwd: return launch_weights_bwd_pass(dtype, C, MB, a, L.P, st);
+    case kAggregateW: return launch_aggregate_w_pass(dtype, C, MB, a, L.P, st);
+    case kDesliceW: return launch_deslice_w_pass(dtype, C, MB, a, L.P, st);
+    case kDesliceBwdW: return launch_deslice_bwd_w_pass(dtype, C, MB, a, L.P, st);
     default: return hipErrorInvalidValue;
   }
 }

@@ -615,6 +615,62 @@ __device__ __forceinline__ void softmax_sp(const V (&acc)[MB + 1], const char* g
     for (int i = 0; i < 4; ++i) w[nb][i] = e[nb][i] * inv;
 }
 
+// Stored weights of a tile's points -- a [16][M] tile laid out like the
+// Gumbel rows (W has G's shape and dtype) -- in the SP layout softmax_sp
+// returns: lane (r, g) gets slices 16nb + 4g + i of point r.  Slices >= M
+// and points >= nvalid are 0 (selected, so whatever the padding holds).
+template <typename T, int MB>
+__device__ __forceinline__ void w_tile(const char* wt, int M, int nvalid, float (&w)[MB][4]) {
+  constexpr int SZ = (int)sizeof(T);
+  const int r = lane_id() & 15, g = lane_id() >> 4;
+#pragma unroll
+  for (int nb = 0; nb < MB; ++nb) {
+    const int j0 = 16 * nb + 4 * g, e = r * M + j0;
+    float v[4];
+    if (M % 4 == 0) {  // 4 aligned elements
+      if constexpr (SZ == 2) {
+        const bf16x4 q = *reinterpret_cast<const bf16x4*>(wt + e * SZ);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = (float)q[i];
+      } else {
+        const f32x4 q = *reinterpret_cast<const f32x4*>(wt + e * SZ);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = q[i];
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] = to_f<T>(reinterpret_cast<const T*>(wt)[e + i]);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) w[nb][i] = (r < nvalid && j0 + i < M) ? v[i] : 0.f;
+  }
+}
+
+// The weights of a tile's first nvalid points, staged in LDS as rows of
+// stride `rowb` bytes (slices contiguous), written to rows [p0, p0 + nvalid)
+// of W [N,M]: 16-byte non-temporal stores when a row is a whole number of
+// 16-byte chunks (the rows are then one contiguous run), else element by
+// element.
+template <typename T>
+__device__ __forceinline__ void write_w_rows(T* W, int64_t p0, int nvalid, const char* wl, int M,
+                                             int rowb) {
+  constexpr int SZ = (int)sizeof(T);
+  const int lane = lane_id();
+  char* d = reinterpret_cast<char*>(W + p0 * M);
+  if ((M * SZ) % 16 == 0) {
+    const int cpr = M * SZ / 16;
+    for (int q = lane; q < nvalid * cpr; q += 64) {
+      const int row = q / cpr, c = q - row * cpr;
+      st_global16(d + (int64_t)16 * q, *reinterpret_cast<const uint4*>(wl + row * rowb + 16 * c));
+    }
+  } else {
+    for (int e = lane; e < nvalid * M; e += 64) {
+      const int row = e / M, j = e - row * M;
+      reinterpret_cast<T*>(d)[e] = *reinterpret_cast<const T*>(wl + row * rowb + j * SZ);
+    }
+  }
+}
+
 // Zero a wave-private LDS region (16-byte multiple).
 __device__ __forceinline__ void zero_lds(char* p, int bytes) {
   for (int q = lane_id(); q < bytes / 16; q += 64) reinterpret_cast<uint4*>(p)[q] = uint4{0, 0, 0, 0};
@@ -679,11 +735,19 @@ struct AggStage {
   GRegs<T, MB, ROWS> g;
 };
 
-template <typename T, int C, int MB, bool BWD>
-__global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(BWD ? kDesliceBwd : kAggregate)))
+// WV (stored weights): the forward also writes the weights it contracts
+// (kAggregateW); the backward reads them from W (given as a.G) instead of
+// recomputing them from x and G (kDesliceBwdW: no table, no x tile).
+constexpr int agg_pass(bool bwd, bool wv) {
+  return bwd ? (wv ? kDesliceBwdW : kDesliceBwd) : (wv ? kAggregateW : kAggregate);
+}
+
+template <typename T, int C, int MB, bool BWD, bool WV = false>
+__global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(agg_pass(BWD, WV))))
 k_aggregate(StreamArgs a) {
   using G_ = Geo<sizeof(T), C, MB>;
-  constexpr int PASS = BWD ? kDesliceBwd : kAggregate;
+  constexpr int PASS = agg_pass(BWD, WV);
+  constexpr bool WIN = BWD && WV, WOUT = !BWD && WV;
   constexpr int WAVES = G_::waves(PASS);
   constexpr int ROWS = G_::rows(PASS), H = ROWS / 16;
   constexpr int SZ = (int)sizeof(T);
@@ -691,12 +755,12 @@ k_aggregate(StreamArgs a) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r = lane_id() & 15, g = lane_id() >> 4;
-  const bool hasG = a.flags & kHasG;
+  const bool hasG = WIN || (a.flags & kHasG);  // WIN: the Gumbel rows' buffer holds W
 
   const char* tabL = smem + G_::OFF_L;
   char* wreg = smem + G_::img_bytes(PASS) + wave * G_::wave_bytes(PASS);
-  // x tile (logits), contracted tile (x, or dY), Gumbel rows, transposed
-  // weights
+  // x tile (logits), contracted tile (x, or dY), Gumbel rows (or stored
+  // weights), transposed weights
   char* const xt = wreg;
   char* const yt = BWD ? wreg + H * G_::XT : wreg;
   char* const gbuf = wreg + (BWD ? 2 : 1) * H * G_::XT;
@@ -708,14 +772,16 @@ k_aggregate(StreamArgs a) {
 
   float bias[MB][4];
   auto init = [&]() {
-    copy_image(smem, a.img, G_::img_bytes(PASS));
-    __syncthreads();
+    if constexpr (!WIN) {
+      copy_image(smem, a.img, G_::img_bytes(PASS));
+      __syncthreads();
+    }
     zero_lds(gbuf, 2 * H * G_::GT);
 #pragma unroll
     for (int nb = 0; nb < MB; ++nb)
 #pragma unroll
       for (int i = 0; i < 4; ++i)
-        bias[nb][i] = reinterpret_cast<const float*>(smem)[16 * nb + 4 * g + i];
+        bias[nb][i] = WIN ? 0.f : reinterpret_cast<const float*>(smem)[16 * nb + 4 * g + i];
   };
 
   f32x4 acc[MB][G_::CB], dacc[MB];
@@ -743,24 +809,30 @@ k_aggregate(StreamArgs a) {
       const int64_t rem = a.N - p0 - 16 * h;
       nv[h] = rem < 0 ? 0 : rem > 16 ? 16 : (int)rem;
     }
-    V lg[H][MB + 1];
-    float tt[H];
-    if constexpr (H == 1) {
-      K32<T> xa[G_::XF];
-      logits<T, C, MB, true, (SZ == 4)>(lg[0], xa, xt, tabL, lb);
-      tt[0] = temperature_own<T, C, MB>(lg[0], xa, tabL, lb.a, a.tb);
+    float w[H][MB][4];
+    if constexpr (WIN) {
+#pragma unroll
+      for (int h = 0; h < H; ++h) w_tile<T, MB>(gbuf + h * 16 * a.M * SZ, a.M, nv[h], w[h]);
     } else {
-      logits_h<T, C, MB, H>(lg, tabL, lb, [&](int h, int s, K32<T>& f) {
-        ld_row<T>(f, xt, lb.x, h * 16 * G_::XT_ROW + 32 * s * SZ);
-      });
+      V lg[H][MB + 1];
+      float tt[H];
+      if constexpr (H == 1) {
+        K32<T> xa[G_::XF];
+        logits<T, C, MB, true, (SZ == 4)>(lg[0], xa, xt, tabL, lb);
+        tt[0] = temperature_own<T, C, MB>(lg[0], xa, tabL, lb.a, a.tb);
+      } else {
+        logits_h<T, C, MB, H>(lg, tabL, lb, [&](int h, int s, K32<T>& f) {
+          ld_row<T>(f, xt, lb.x, h * 16 * G_::XT_ROW + 32 * s * SZ);
+        });
 #pragma unroll
-      for (int h = 0; h < H; ++h) tt[h] = (float)lg[h][MB][0] + (float)a.tb;
+        for (int h = 0; h < H; ++h) tt[h] = (float)lg[h][MB][0] + (float)a.tb;
+      }
+      float zs[MB][4], tau;
+#pragma unroll
+      for (int h = 0; h < H; ++h)
+        softmax_sp<T, MB>(lg[h], gbuf + h * 16 * a.M * SZ, a.M, bias, tt[h], a.tau_min, nv[h],
+                          w[h], zs, tau);
     }
-    float w[H][MB][4], zs[MB][4], tau;
-#pragma unroll
-    for (int h = 0; h < H; ++h)
-      softmax_sp<T, MB>(lg[h], gbuf + h * 16 * a.M * SZ, a.M, bias, tt[h], a.tau_min, nv[h], w[h],
-                        zs, tau);
 
     // SP -> PS through the weights buffer
     wave_sync();
@@ -772,6 +844,14 @@ k_aggregate(StreamArgs a) {
         stage4<T>(wbuf, wsb + h * 16 * G_::GROW, 16 * nb * SZ, v);
       }
     wave_sync();
+    // the rows just staged are the tile's weights as the contraction rounds
+    // them (point rows, slices contiguous)
+    if constexpr (WOUT) {
+      int nvt = 0;
+#pragma unroll
+      for (int h = 0; h < H; ++h) nvt += nv[h];
+      write_w_rows<T>(reinterpret_cast<T*>(a.out), p0, nvt, wbuf, a.M, G_::GROW);
+    }
     K16<T> wt[H][MB];
 #pragma unroll
     for (int h = 0; h < H; ++h)
@@ -808,12 +888,14 @@ k_aggregate(StreamArgs a) {
   auto load = [&](Stage& st, int64_t tile) {
     const int64_t p0 = tile * ROWS;
     constexpr bool NT = !keep_loads<PASS>();
-    load_tile<T, C, ROWS, NT>(st.x, X, p0, a.N);
+    if constexpr (!WIN) load_tile<T, C, ROWS, NT>(st.x, X, p0, a.N);
     if constexpr (BWD) load_tile<T, C, ROWS, NT>(st.y, Y, p0, a.N);
-    load_g<T, MB, ROWS, true>(st.g, Gp, X, p0, a.N, a.M, hasG);  // G: streamed either way
+    // G (or W): streamed either way; `safe` is any readable 16 bytes
+    const void* safe = WIN ? a.img : static_cast<const void*>(X);
+    load_g<T, MB, ROWS, true>(st.g, Gp, safe, p0, a.N, a.M, hasG);
   };
   auto store = [&](const Stage& st) {
-    store_tile<T, C, ROWS>(xt, st.x);
+    if constexpr (!WIN) store_tile<T, C, ROWS>(xt, st.x);
     if constexpr (BWD) store_tile<T, C, ROWS>(yt, st.y);
     if (hasG) store_g<T, MB, ROWS>(gbuf, st.g, a.M, hasG);
   };
@@ -860,19 +942,23 @@ k_aggregate(StreamArgs a) {
 // kDeslice (SP layout): y = W S'.  The y tile is staged in the x tile, which
 // the logits are done with, and written back as whole rows.
 // ---------------------------------------------------------------------------
-template <typename T, int C, int MB>
-__global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kDeslice))) k_deslice(StreamArgs a) {
+// WIN (kDesliceW): the weights are read from W (given as a.G, in the Gumbel
+// rows' buffer) instead of recomputed; only the deslice table is in LDS.
+template <typename T, int C, int MB, bool WIN = false>
+__global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(WIN ? kDesliceW : kDeslice)))
+k_deslice(StreamArgs a) {
   using G_ = Geo<sizeof(T), C, MB>;
-  constexpr int WAVES = G_::waves(kDeslice);
+  constexpr int PASS = WIN ? kDesliceW : kDeslice;
+  constexpr int WAVES = G_::waves(PASS);
   constexpr int SZ = (int)sizeof(T);
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r = lane_id() & 15, g = lane_id() >> 4;
-  const bool hasG = a.flags & kHasG;
+  const bool hasG = WIN || (a.flags & kHasG);
 
   const char* tabL = smem + G_::OFF_L;
-  const char* tabS = smem + G_::OFF_2;
-  char* xt = smem + G_::img_bytes(kDeslice) + wave * G_::wave_bytes(kDeslice);
+  const char* tabS = smem + (WIN ? 0 : G_::OFF_2);
+  char* xt = smem + G_::img_bytes(PASS) + wave * G_::wave_bytes(PASS);
   char* gt = xt + G_::XT;
   const auto lb = logits_bases<T, C, MB, true>();
   const int sb = r * G_::SROW + 4 * g * SZ;  // S'^T row 16cb + r, slices 16nb + 4g ..
@@ -880,14 +966,17 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kDeslice)))
 
   float bias[MB][4];
   auto init = [&]() {
-    copy_image(smem, a.img, G_::img_bytes(kDeslice));
+    if constexpr (WIN)  // the deslice table part of the image only
+      copy_image(smem, reinterpret_cast<const char*>(a.img) + G_::OFF_2, G_::SZ_S);
+    else
+      copy_image(smem, a.img, G_::img_bytes(kDeslice));
     __syncthreads();
     zero_lds(gt, G_::GT);
 #pragma unroll
     for (int nb = 0; nb < MB; ++nb)
 #pragma unroll
       for (int i = 0; i < 4; ++i)
-        bias[nb][i] = reinterpret_cast<const float*>(smem)[16 * nb + 4 * g + i];
+        bias[nb][i] = WIN ? 0.f : reinterpret_cast<const float*>(smem)[16 * nb + 4 * g + i];
   };
 
   const T* X = reinterpret_cast<const T*>(a.x);
@@ -898,24 +987,33 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kDeslice)))
 
   using Stage = TileStage<T, C, MB>;
   auto load = [&](Stage& st, int64_t tile) {
-    constexpr bool NT = !keep_loads<kDeslice>();
-    load_tile<T, C, 16, NT>(st.x, X, tile * 16, a.N);
-    load_g<T, MB, 16, NT>(st.g, Gp, X, tile * 16, a.N, a.M, hasG);
+    constexpr bool NT = !keep_loads<PASS>();
+    if constexpr (WIN) {
+      load_g<T, MB, 16, NT>(st.g, Gp, a.img, tile * 16, a.N, a.M, hasG);
+    } else {
+      load_tile<T, C, 16, NT>(st.x, X, tile * 16, a.N);
+      load_g<T, MB, 16, NT>(st.g, Gp, X, tile * 16, a.N, a.M, hasG);
+    }
   };
   auto store = [&](const Stage& st) {
-    store_tile<T, C>(xt, st.x);
+    if constexpr (!WIN) store_tile<T, C>(xt, st.x);
     if (hasG) store_g<T, MB>(gt, st.g, a.M, hasG);
   };
   auto body = [&](int64_t t) {
     const int64_t p0 = t * 16;
     const int nvalid = (int)(a.N - p0 < 16 ? a.N - p0 : 16);
 
-    typename LAcc<T, true>::v lg[MB + 1];
-    K32<T> xa[G_::XF];
-    logits<T, C, MB, true>(lg, xa, xt, tabL, lb);
-    float w[MB][4], zs[MB][4], tau;
-    const float tt = temperature_own<T, C, MB>(lg, xa, tabL, lb.a, a.tb);
-    softmax_sp<T, MB>(lg, gt, a.M, bias, tt, a.tau_min, nvalid, w, zs, tau);
+    float w[MB][4];
+    if constexpr (WIN) {
+      w_tile<T, MB>(gt, a.M, nvalid, w);
+    } else {
+      typename LAcc<T, true>::v lg[MB + 1];
+      K32<T> xa[G_::XF];
+      logits<T, C, MB, true>(lg, xa, xt, tabL, lb);
+      float zs[MB][4], tau;
+      const float tt = temperature_own<T, C, MB>(lg, xa, tabL, lb.a, a.tb);
+      softmax_sp<T, MB>(lg, gt, a.M, bias, tt, a.tau_min, nvalid, w, zs, tau);
+    }
 
     K16<T> wb[MB];
 #pragma unroll
@@ -1366,10 +1464,16 @@ static hipError_t launch_t(const StreamArgs& a, int P, hipStream_t st) {
     const size_t lds = (size_t)G_::lds_bytes(PASS);
     if constexpr (PASS == kAggregate)
       hipLaunchKernelGGL((k_aggregate<T, C, MB, false>), dim3(P), dim3(threads), lds, st, a);
+    else if constexpr (PASS == kAggregateW)
+      hipLaunchKernelGGL((k_aggregate<T, C, MB, false, true>), dim3(P), dim3(threads), lds, st, a);
     else if constexpr (PASS == kDesliceBwd)
       hipLaunchKernelGGL((k_aggregate<T, C, MB, true>), dim3(P), dim3(threads), lds, st, a);
+    else if constexpr (PASS == kDesliceBwdW)
+      hipLaunchKernelGGL((k_aggregate<T, C, MB, true, true>), dim3(P), dim3(threads), lds, st, a);
     else if constexpr (PASS == kDeslice)
       hipLaunchKernelGGL((k_deslice<T, C, MB>), dim3(P), dim3(threads), lds, st, a);
+    else if constexpr (PASS == kDesliceW)
+      hipLaunchKernelGGL((k_deslice<T, C, MB, true>), dim3(P), dim3(threads), lds, st, a);
     else if constexpr (PASS == kWeights)
       hipLaunchKernelGGL((k_weights<T, C, MB>), dim3(P), dim3(threads), lds, st, a);
     else
@@ -1417,5 +1521,8 @@ hipError_t launch_deslice_bwd_pass(int dtype, int C, int MB, const StreamArgs& a
 hipError_t launch_weights_pass(int dtype, int C, int MB, const StreamArgs& a, int P, hipStream_t st);
 hipError_t launch_slice_bwd_pass(int dtype, int C, int MB, const StreamArgs& a, int P, hipStream_t st);
 hipError_t launch_weights_bwd_pass(int dtype, int C, int MB, const StreamArgs& a, int P, hipStream_t st);
+hipError_t launch_aggregate_w_pass(int dtype, int C, int MB, const StreamArgs& a, int P, hipStream_t st);
+hipError_t launch_deslice_w_pass(int dtype, int C, int MB, const StreamArgs& a, int P, hipStream_t st);
+hipError_t launch_deslice_bwd_w_pass(int dtype, int C, int MB, const StreamArgs& a, int P, hipStream_t st);
 
 }  // namespace pa

@@ -180,6 +180,38 @@ class Gpu:
         g["dx"] = dx
         return g
 
+    def aggregate_w(self):
+        """pa_slice_aggregate_w: num, den, S and the stored weights W."""
+        c = self.c
+        num, den, S = self.empty(c.M, c.C), self.empty(c.M), self.empty(c.M, c.C)
+        W = self.empty(c.N, c.M, dt=c.dt)
+        B.pa_slice_aggregate_w(self.dims, self.x, self.G, self.sp, num, den, S, W, self.ws)
+        return num, den, S, W
+
+    def deslice_w(self, W, Sp):
+        y = self.empty(self.c.N, self.c.C, dt=self.c.dt)
+        B.pa_deslice_w(self.dims, W, Sp, y, self.ws)
+        return y
+
+    def deslice_backward_w(self, W):
+        dSp = self.empty(self.c.M, self.c.C)
+        B.pa_deslice_backward_w(self.dims, W, self.dY, dSp, self.ws)
+        return dSp
+
+    def layer_w(self):
+        """The layer with stored weights: the aggregate writes W, the deslice
+        and its backward read it; the slice backward recomputes as always."""
+        num, den, S, W = self.aggregate_w()
+        Sp = self.attention(S)
+        y = self.deslice_w(W, Sp)
+        dSp = self.deslice_backward_w(W)
+        ga = self.attention_backward(S, dSp)
+        gs = self.slice_backward(num, den, ga["dS"], Sp)
+        out = {"num": num, "den": den, "S": S, "W": W, "Sp": Sp, "y": y, "dSp": dSp}
+        out.update(ga)
+        out.update(gs)
+        return out
+
     def layer(self):
         """Forward then backward of the whole layer through the C ABI."""
         num, den, S = self.aggregate()

@@ -32,7 +32,7 @@ def _declared_symbols():
 
 def test_every_declared_symbol_is_exported(lib):
     declared = _declared_symbols()
-    assert len(declared) == 12
+    assert len(declared) == 15
     assert sorted(B.SYMBOLS) == declared
     for name in declared:
         assert hasattr(lib, name), name
@@ -147,4 +147,19 @@ def test_kernel_timing_hook_checks(lib):
     assert lib.pa_time_kernel(b"pa_deslice", FAKE, None) == B.PA_ERR_INVALID
     assert lib.pa_time_kernel(b"pa_slice_aggregate_backward", FAKE, FAKE) == B.PA_OK
     assert lib.pa_time_kernel(None, None, None) == B.PA_OK
+
+
+def test_stored_weights_argument_checks(lib):
+    d = _dims()
+    _, n = _ws_size(lib, d)
+    assert lib.pa_deslice_w(ctypes.byref(d), None, FAKE, FAKE, FAKE, n, None) == B.PA_ERR_INVALID
+    assert "W" in lib.pa_last_error().decode()
+    assert lib.pa_deslice_backward_w(ctypes.byref(d), FAKE, None, FAKE, FAKE, n, None) == \
+        B.PA_ERR_INVALID
+    assert lib.pa_deslice_w(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, 16, None) == \
+        B.PA_ERR_WORKSPACE
+    sp = B.pa_slice_params(FAKE, None, None, 0.0)
+    st = lib.pa_slice_aggregate_w(ctypes.byref(d), FAKE, None, ctypes.byref(sp), FAKE, FAKE,
+                                  FAKE, None, FAKE, n, None)
+    assert st == B.PA_ERR_INVALID and "W" in lib.pa_last_error().decode()
 

@@ -1,10 +1,11 @@
 """HIP path vs the CPU oracle at the workloads' full sizes, through the C ABI.
 
 * The million-point car-surface workload (N = 1,000,000, C = 256, H = 8,
-  M = 32, bf16 storage): the exact inputs and call sequence that bench.py
-  times.  The oracle evaluates the whole layer forward + backward in float64
-  on the host cores (about half a minute), so every output tensor is compared
-  in full, by relative L2.
+  M = 32, bf16 storage): the exact inputs and call sequences that bench.py
+  times (weights recomputed in every pass, and stored once).  The oracle
+  evaluates the whole layer forward + backward in float64 on the host cores
+  (about half a minute), so every output tensor is compared in full, by
+  relative L2.
 * The largest single-layer shape, the aircraft-surface workload (N = 2.5M,
   C = 256, H = 8, M = 64, bf16): the layer must fit and run on one GPU.  The
   oracle computes every quantity that sums over all points (num, den, S, S',
@@ -34,21 +35,24 @@ def test_full_size_bench_workload():
     say(f"full size {w.name}: N={w.N} C={w.C} H={w.H} M={w.M} {w.dtype}")
     c = make_case(w.N, w.C, w.H, w.M, w.dtype, biases=False, workload=w)
     g = Gpu(c)
-    out = g.layer()
+    outs = {"recomputed weights": g.layer(), "stored weights": g.layer_w()}
     g.torch.cuda.synchronize()
-    say("  gpu layer done; oracle forward + backward ...")
+    say("  gpu layers done; oracle forward + backward ...")
     p = oracle_params(c)
     f = oracle.layer_forward(c.x, c.G, p, c.tau0, c.tau_min, c.eps, c.H)
     gr = oracle.layer_backward(c.x, c.G, p, c.tau0, c.tau_min, c.eps, c.H, f, c.dY)
-    for k in ("num", "den", "S", "Sp", "y"):
-        check(k, host(out[k]), f[k], c.dt)
-    del f
-    for k in ("dSp", "dS", "dWq", "dbq", "dWk", "dWv", "dbv", "dx", "dA", "db"):
-        check(k, host(out[k]), gr[k], c.dt)
-    # the Ada-Temp parameters (a, b_t) as one gradient (as in the per-call tests)
-    da = np.concatenate([host(out["da"]).ravel(), host(out["db_t"]).ravel()])
-    check("d(a,b_t)", da, np.concatenate([gr["da"].ravel(), [gr["db_t"]]]), c.dt)
-    assert float(host(out["dtau0"])[0]) == float(host(out["db_t"])[0])
+    for name, out in outs.items():
+        say(f" {name}")
+        for k in ("num", "den", "S", "Sp", "y"):
+            check(k, host(out[k]), f[k], c.dt)
+        if "W" in out:
+            check("W", host(out["W"]), f["W"], c.dt)
+        for k in ("dSp", "dS", "dWq", "dbq", "dWk", "dWv", "dbv", "dx", "dA", "db"):
+            check(k, host(out[k]), gr[k], c.dt)
+        # the Ada-Temp parameters (a, b_t) as one gradient (as in the per-call tests)
+        da = np.concatenate([host(out["da"]).ravel(), host(out["db_t"]).ravel()])
+        check("d(a,b_t)", da, np.concatenate([gr["da"].ravel(), [gr["db_t"]]]), c.dt)
+        assert float(host(out["dtau0"])[0]) == float(host(out["db_t"])[0])
 
 
 def test_max_size_layer_fits_and_matches_sampled_rows():

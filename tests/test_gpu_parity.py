@@ -12,7 +12,7 @@ import numpy as np
 import pytest
 
 import oracle
-from pa_cases import TOL, Gpu, host, make_case, oracle_layer, oracle_params, rel_l2, say
+from pa_cases import TOL, Gpu, dev, host, make_case, oracle_layer, oracle_params, rel_l2, say
 
 pytestmark = pytest.mark.gpu
 
@@ -270,20 +270,70 @@ def test_deterministic(cases):
         assert g.torch.equal(a[k], b[k]), k
 
 
+@pytest.mark.parametrize("shape", SHAPES, ids=IDS)
+def test_slice_aggregate_w(cases, shape):
+    """The stored-weights aggregate: num, den, S bitwise those of
+    pa_slice_aggregate (same contraction), and W the oracle's weights
+    (Eq. 3, 4) rounded to the storage dtype."""
+    say(f"slice_aggregate_w {shape}")
+    c, g, (f, _) = get_case(cases, shape)
+    num, den, S = g.aggregate()
+    num_w, den_w, S_w, W = g.aggregate_w()
+    for k, a, b in (("num", num, num_w), ("den", den, den_w), ("S", S, S_w)):
+        assert g.torch.equal(a, b), k
+    check("W", W, f["W"], c.dt)
+    check("num", num_w, f["num"], c.dt)
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=IDS)
+def test_deslice_w(cases, shape):
+    say(f"deslice_w {shape}")
+    c, g, (f, _) = get_case(cases, shape)
+    W = dev(f["W"].astype(np.float32), c.dt)  # the oracle's weights, in the storage dtype
+    Sp = dev(f["Sp"].astype(np.float32))
+    y = g.deslice_w(W, Sp)
+    check("y", y, oracle.deslice(host(W), host(Sp)), c.dt)
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=IDS)
+def test_deslice_backward_w(cases, shape):
+    say(f"deslice_backward_w {shape}")
+    c, g, (f, _) = get_case(cases, shape)
+    W = dev(f["W"].astype(np.float32), c.dt)
+    dSp = g.deslice_backward_w(W)
+    check("dSp", dSp, oracle.deslice_backward(host(W), f["Sp"], c.dY)[0], c.dt)
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=IDS)
+def test_layer_chain_w(cases, shape):
+    """The whole layer with stored weights, GPU outputs feeding GPU calls."""
+    say(f"layer_w {shape}")
+    c, g, (f, gr) = get_case(cases, shape)
+    out = g.layer_w()
+    for k in ("num", "den", "S", "Sp", "y"):
+        check(k, out[k], f[k], c.dt, CHAIN_TOL[c.dt])
+    for k in ("dSp", "dS", "dWq", "dbq", "dWk", "dWv", "dbv", "dx", "dA", "db", "da"):
+        check(k, out[k], gr[k], c.dt, CHAIN_TOL[c.dt])
+    check_ada_temp(out, gr, c.dt, CHAIN_TOL[c.dt])
+
+
 def test_kernel_timing_hook(cases):
     """pa_time_kernel brackets exactly one streaming kernel per call with the
     caller's events and changes no output."""
     from paper_2502_02414_amd import binding as B
     shape = (66013, 256, 8, 32, "bf16")
     c, g, _ = get_case(cases, shape)
-    a = g.layer()
+    a, aw = g.layer(), g.layer_w()
     for call in ("pa_slice_aggregate", "pa_deslice", "pa_deslice_backward",
-                 "pa_slice_aggregate_backward"):
+                 "pa_slice_aggregate_backward", "pa_slice_aggregate_w", "pa_deslice_w",
+                 "pa_deslice_backward_w"):
         e0, e1, c0, c1 = B.HipEvent(), B.HipEvent(), B.HipEvent(), B.HipEvent()
         B.pa_time_kernel(call, e0, e1)
+        run = g.layer_w if call.endswith("_w") else g.layer
+        ref = aw if call.endswith("_w") else a
         try:
             c0.record()
-            b = g.layer()
+            b = run()
             c1.record()
             g.torch.cuda.synchronize()
         finally:
@@ -291,8 +341,8 @@ def test_kernel_timing_hook(cases):
         kernel_ms, layer_ms = e0.elapsed_ms(e1), c0.elapsed_ms(c1)
         say(f"  {call}: kernel {kernel_ms * 1e3:.1f} us of a {layer_ms * 1e3:.1f} us layer")
         assert 0.0 < kernel_ms < layer_ms
-        for k in a:
-            assert g.torch.equal(a[k], b[k]), (call, k)
+        for k in ref:
+            assert g.torch.equal(ref[k], b[k]), (call, k)
 
 
 @pytest.mark.parametrize("variant", ["no_noise", "no_adatemp", "single_point", "empty_slice"])
@@ -314,8 +364,8 @@ def test_edge_cases(variant):
     f, gr = oracle_layer(c)
     if variant == "empty_slice":
         assert f["den"][2] < c.eps
-    out = g.layer()
-    for k in ("num", "den", "S", "Sp", "y"):
-        check(k, out[k], f[k], c.dt)
-    for k in ("dSp", "dS", "dx", "dA", "db", "da"):
-        check(k, out[k], gr[k], c.dt)
+    for out in (g.layer(), g.layer_w()):  # recomputed, then stored weights
+        for k in ("num", "den", "S", "Sp", "y"):
+            check(k, out[k], f[k], c.dt)
+        for k in ("dSp", "dS", "dx", "dA", "db", "da"):
+            check(k, out[k], gr[k], c.dt)
