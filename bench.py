@@ -6,7 +6,10 @@ A step is one pass of the whole hot path over one batch of synthetic input:
                         -> pa_slice_aggregate_backward           (backward)
 on the million-point car-surface workload (N = 1,000,000, C = 256, H = 8,
 M = 32, bf16 storage, fp32 accumulation).  Inputs are resident in HBM before
-the timed region.  Prints one JSON line (rank 0).
+the timed region.  Prints one JSON line (rank 0).  The headline is this
+sequence, which recomputes the slice weights in every pass; the line also
+reports, under "stored_weights", the same step with the weights written once
+by pa_slice_aggregate_w and read by pa_deslice_w / pa_deslice_backward_w.
 
     python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--no-cpu-baseline]
 
@@ -45,6 +48,10 @@ def algo_bytes_per_point(C, M, b, g):
         "pa_slice_aggregate_backward": 3 * C * b + M * g,  # x, G, dY, dx
         "pa_token_attention": 0,
         "pa_token_attention_backward": 0,
+        # stored weights: W [N,M] written once, read in place of x and G
+        "pa_slice_aggregate_w": C * b + M * g + M * b,   # x, G read; W written
+        "pa_deslice_w": M * b + C * b,                  # W read; y written
+        "pa_deslice_backward_w": M * b + C * b,         # W, dY read
     }
 
 
@@ -54,6 +61,9 @@ STREAM_KERNEL = {
     "pa_deslice": "deslice",                    # k_deslice
     "pa_deslice_backward": "deslice_bwd",       # k_aggregate, deslice backward
     "pa_slice_aggregate_backward": "slice_bwd",  # k_slice_bwd
+    "pa_slice_aggregate_w": "aggregate_w",
+    "pa_deslice_w": "deslice_w",
+    "pa_deslice_backward_w": "deslice_bwd_w",
 }
 
 
@@ -150,6 +160,77 @@ def main():
          lambda: B.pa_slice_aggregate_backward(dims, x, G, sp, num, den, dS, Sp, dY, dx, sgr, ws)),
     ]
 
+    Wst = torch.empty(N, M, dtype=bf, device=dev)  # stored weights (variant)
+    calls_w = [
+        ("pa_slice_aggregate_w",
+         lambda: B.pa_slice_aggregate_w(dims, x, G, sp, num, den, S, Wst, ws)),
+        calls[1],
+        ("pa_deslice_w", lambda: B.pa_deslice_w(dims, Wst, Sp, y, ws)),
+        ("pa_deslice_backward_w", lambda: B.pa_deslice_backward_w(dims, Wst, dY, dSp, ws)),
+        calls[4],
+        calls[5],
+    ]
+
+    bpp = algo_bytes_per_point(C, M, 2, 2)
+    headline = time_steps(calls, bpp, args, B, torch)
+    variant = time_steps(calls_w, bpp, args, B, torch)
+    dom, per_call, kernel_ms = headline["dom"], headline["per_call"], headline["kernel_ms"]
+    ms_per_step, t_wall = headline["ms_per_step"], headline["wall_s"]
+    value = N / (ms_per_step * 1e-3)
+
+    if args.copy_calibration:
+        src = torch.empty(1 << 28, dtype=torch.float32, device=dev)  # 1 GiB
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    dom_bytes = bpp[dom] * N
+    achieved = dom_bytes / (kernel_ms * 1e-3) / 1e9
+    step_bytes = sum(bpp[n] for n, _ in calls) * N
+    w_bytes = sum(bpp[n] for n, _ in calls_w) * N
+    w_ms = variant["ms_per_step"]
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": read_traffic(STREAM_KERNEL[dom]), "call": dom,
+                "kernel": STREAM_KERNEL[dom], "algo_bytes_per_launch": dom_bytes,
+                "kernel_ms": round(kernel_ms, 4), "call_ms": round(per_call[dom], 4)}
+
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "points/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": WORKLOAD, "N": N, "C": C, "H": H, "M": M, "tau0": w.tau0,
+                   "tau_min": w.tau_min, "storage": "bf16", "accumulate": "fp32",
+                   "pass": "forward+backward"},
+        "roofline": roofline,
+        "step_hbm": {"algo_bytes": step_bytes,
+                     "achieved_GBs": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
+                     "frac": round(step_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
+        "per_call_ms": {k: round(v, 4) for k, v in per_call.items()},
+        "wall_s_timed": round(t_wall, 4),
+        # Algorithm 1's dataflow: the weights stored once by the aggregate and
+        # read by the deslice and its backward (same workload and outputs)
+        "stored_weights": {
+            "value": round(N / (w_ms * 1e-3), 1), "ms_per_step": round(w_ms, 4),
+            "algo_bytes": w_bytes,
+            "achieved_GBs": round(w_bytes / (w_ms * 1e-3) / 1e9, 1),
+            "frac": round(w_bytes / (w_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "per_call_ms": {k: round(v, 4) for k, v in variant["per_call"].items()}},
+    }
+
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(x_np, G_np, dY_np, p, w)
+    print(json.dumps(out), flush=True)
+
+
+def time_steps(calls, bpp, args, B, torch):
+    """Warm-up, a per-call breakdown pass, then the timed region of K whole
+    steps of `calls`; in each timed step the library brackets the streaming
+    kernel of the dominant call with one event pair (its duration for the
+    roofline)."""
     def step(events=None):
         for k, (name, fn) in enumerate(calls):
             if events is not None:
@@ -176,12 +257,8 @@ def main():
     for s in range(args.steps):
         for k, (name, _) in enumerate(calls):
             per_call[name] += evs[s][k][0].elapsed_ms(evs[s][k][1]) / args.steps
-    bpp = algo_bytes_per_point(C, M, 2, 2)
     dom = max((n for n in per_call if bpp[n] > 0), key=lambda n: per_call[n])
 
-    # Timed region: K whole steps; in each, the library brackets the streaming
-    # kernel of the dominant call with one event pair (its duration for the
-    # roofline).
     kev = [event_pair() for _ in range(args.steps)]
     start, end = event_pair()
     torch.cuda.synchronize()
@@ -194,47 +271,9 @@ def main():
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall
     B.pa_time_kernel(None)
-    total_ms = start.elapsed_ms(end)
-    kernel_ms = sum(e0.elapsed_ms(e1) for e0, e1 in kev) / args.steps
-    ms_per_step = total_ms / args.steps
-    value = N / (ms_per_step * 1e-3)
-
-    if args.copy_calibration:
-        src = torch.empty(1 << 28, dtype=torch.float32, device=dev)  # 1 GiB
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
-
-    dom_bytes = bpp[dom] * N
-    achieved = dom_bytes / (kernel_ms * 1e-3) / 1e9
-    step_bytes = sum(bpp.values()) * N
-    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                "traffic": read_traffic(STREAM_KERNEL[dom]), "call": dom,
-                "kernel": STREAM_KERNEL[dom], "algo_bytes_per_launch": dom_bytes,
-                "kernel_ms": round(kernel_ms, 4), "call_ms": round(per_call[dom], 4)}
-
-    out = {
-        "metric": METRIC, "value": round(value, 1), "unit": "points/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
-        "data": "synthetic",
-        "config": {"workload": WORKLOAD, "N": N, "C": C, "H": H, "M": M, "tau0": w.tau0,
-                   "tau_min": w.tau_min, "storage": "bf16", "accumulate": "fp32",
-                   "pass": "forward+backward"},
-        "roofline": roofline,
-        "step_hbm": {"algo_bytes": step_bytes,
-                     "achieved_GBs": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
-                     "frac": round(step_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
-        "per_call_ms": {k: round(v, 4) for k, v in per_call.items()},
-        "wall_s_timed": round(t_wall, 4),
-    }
-
-    if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(x_np, G_np, dY_np, p, w)
-    print(json.dumps(out), flush=True)
+    return {"dom": dom, "per_call": per_call, "ms_per_step": start.elapsed_ms(end) / args.steps,
+            "kernel_ms": sum(e0.elapsed_ms(e1) for e0, e1 in kev) / args.steps,
+            "wall_s": t_wall}
 
 
 def cpu_baseline(x_np, G_np, dY_np, p, w, target_s: float = 10.0):

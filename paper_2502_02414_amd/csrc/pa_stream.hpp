@@ -648,25 +648,40 @@ __device__ __forceinline__ void w_tile(const char* wt, int M, int nvalid, float 
 
 // The weights of a tile's first nvalid points, staged in LDS as rows of
 // stride `rowb` bytes (slices contiguous), written to rows [p0, p0 + nvalid)
-// of W [N,M]: 16-byte non-temporal stores when a row is a whole number of
-// 16-byte chunks (the rows are then one contiguous run), else element by
-// element.
-template <typename T>
+// of W [N,M]: 16-byte stores when a row is a whole number of 16-byte chunks
+// (the rows are then one contiguous run), else element by element.  These
+// stores go through the caches, unlike the other streamed outputs: the
+// deslice reads W next, walking backwards onto the lines written last
+// (measured at N = 1M: aggregate -8 us, deslice -16 us against non-temporal
+// stores).  Each lane issues a fixed number of (masked) stores: the vector
+// memory counter also counts stores, and with a data-dependent number of
+// them the compiler can only wait for the prefetched tile by waiting for
+// everything.
+template <typename T, int ROWS, int M16>
 __device__ __forceinline__ void write_w_rows(T* W, int64_t p0, int nvalid, const char* wl, int M,
                                              int rowb) {
   constexpr int SZ = (int)sizeof(T);
   const int lane = lane_id();
   char* d = reinterpret_cast<char*>(W + p0 * M);
   if ((M * SZ) % 16 == 0) {
-    const int cpr = M * SZ / 16;
-    for (int q = lane; q < nvalid * cpr; q += 64) {
+    constexpr int K = (ROWS * M16 * SZ / 16 + 63) / 64;
+    const int cpr = M * SZ / 16, n = nvalid * cpr;
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      const int q = lane + 64 * k;
       const int row = q / cpr, c = q - row * cpr;
-      st_global16(d + (int64_t)16 * q, *reinterpret_cast<const uint4*>(wl + row * rowb + 16 * c));
+      if (q < n)
+        *reinterpret_cast<uint4*>(d + (int64_t)16 * q) =
+            *reinterpret_cast<const uint4*>(wl + row * rowb + 16 * c);
     }
   } else {
-    for (int e = lane; e < nvalid * M; e += 64) {
+    constexpr int K = (ROWS * M16 + 63) / 64;
+    const int n = nvalid * M;
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      const int e = lane + 64 * k;
       const int row = e / M, j = e - row * M;
-      reinterpret_cast<T*>(d)[e] = *reinterpret_cast<const T*>(wl + row * rowb + j * SZ);
+      if (e < n) reinterpret_cast<T*>(d)[e] = *reinterpret_cast<const T*>(wl + row * rowb + j * SZ);
     }
   }
 }
@@ -850,7 +865,7 @@ k_aggregate(StreamArgs a) {
       int nvt = 0;
 #pragma unroll
       for (int h = 0; h < H; ++h) nvt += nv[h];
-      write_w_rows<T>(reinterpret_cast<T*>(a.out), p0, nvt, wbuf, a.M, G_::GROW);
+      write_w_rows<T, ROWS, G_::M16>(reinterpret_cast<T*>(a.out), p0, nvt, wbuf, a.M, G_::GROW);
     }
     K16<T> wt[H][MB];
 #pragma unroll
