@@ -38,6 +38,12 @@ def _load():
         lib.pao_aggregate_backward.argtypes = [I64, I32, I32, D, P, P, P, P, P, P, P]
         lib.pao_slice_weights_backward.argtypes = (
             [I64, I32, I32, D, D, P, P, P, P, P, D, P, P, P, P, P, P, P, P])
+        lib.pao_layernorm.argtypes = [I64, I32, D, P, P, P, P, P, P]
+        lib.pao_layernorm_backward.argtypes = [I64, I32, D, P, P, P, P, P, P]
+        lib.pao_gelu.argtypes = [I64, P, P]
+        lib.pao_gelu_backward.argtypes = [I64, P, P, P]
+        lib.pao_linear.argtypes = [I64, I32, I32, P, P, P, P]
+        lib.pao_linear_backward.argtypes = [I64, I32, I32, P, P, P, P, P, P]
         lib.pao_shard_points.restype = I32
         lib.pao_num_threads.restype = I32
         lib.pao_set_num_threads.argtypes = [I32]
@@ -201,3 +207,122 @@ def layer_backward(x, G, p, tau0, tau_min, eps, H, fwd, dY):
     out.update({"dSp": dSp, "dx": dx_agg + sw["dx"], "dA": sw["dA"], "db": sw["db"],
                 "da": sw["da"], "db_t": sw["db_t"], "dtau0": sw["dtau0"]})
     return out
+
+
+# ---------------------------------------------------------------------------
+# Block stack: the Transolver++ block around the layer (Section 3: the
+# Transformer block with Physics-Attention in place of attention; block
+# diagram of Figure 2a), read as pre-norm with residual adds:
+#     x1 = x + PA(LN1(x)),   x2 = x1 + MLP(LN2(x1)),
+#     MLP(h) = GELU(h W1 + b1) W2 + b2 (exact GELU),
+# and PA with Algorithm 1's Project step applied explicitly:
+#     x_proj = LN1(x) Wp + bp, then the layer on x_proj (to_out = Wo, bo).
+# ---------------------------------------------------------------------------
+LN_EPS = 1e-5
+
+
+def layernorm(x, g, b, eps=LN_EPS):
+    """Per-row LayerNorm (biased variance).  Returns (y, mean, rstd)."""
+    x, g, b = map(_in, (x, g, b))
+    N, C = x.shape
+    y, mean, rstd = np.empty((N, C)), np.empty(N), np.empty(N)
+    _load().pao_layernorm(N, C, float(eps), _p(x), _p(g), _p(b), _p(y), _p(mean), _p(rstd))
+    return y, mean, rstd
+
+
+def layernorm_backward(x, g, dy, eps=LN_EPS):
+    """Chain rule of layernorm.  Returns (dx, dg, db)."""
+    x, g, dy = map(_in, (x, g, dy))
+    N, C = x.shape
+    dx, dg, db = np.empty((N, C)), np.empty(C), np.empty(C)
+    _load().pao_layernorm_backward(N, C, float(eps), _p(x), _p(g), _p(dy), _p(dx), _p(dg),
+                                   _p(db))
+    return dx, dg, db
+
+
+def gelu(x):
+    """Exact GELU x Phi(x)."""
+    x = _in(x)
+    y = np.empty_like(x)
+    _load().pao_gelu(x.size, _p(x), _p(y))
+    return y
+
+
+def gelu_backward(x, dy):
+    x, dy = _in(x), _in(dy)
+    dx = np.empty_like(x)
+    _load().pao_gelu_backward(x.size, _p(x), _p(dy), _p(dx))
+    return dx
+
+
+def linear(x, W, b=None):
+    """y = x W + b."""
+    x, W, b = map(_in, (x, W, b))
+    N, Cin = x.shape
+    Cout = W.shape[1]
+    y = np.empty((N, Cout))
+    _load().pao_linear(N, Cin, Cout, _p(x), _p(W), _p(b), _p(y))
+    return y
+
+
+def linear_backward(x, W, dy):
+    """Chain rule of linear.  Returns (dx, dW, db)."""
+    x, W, dy = map(_in, (x, W, dy))
+    N, Cin = x.shape
+    Cout = W.shape[1]
+    dx, dW, db = np.empty((N, Cin)), np.empty((Cin, Cout)), np.empty(Cout)
+    _load().pao_linear_backward(N, Cin, Cout, _p(x), _p(W), _p(dy), _p(dx), _p(dW), _p(db))
+    return dx, dW, db
+
+
+def block_forward(x, G, p, tau0, tau_min, eps, H, ln_eps=LN_EPS):
+    """One block.  ``p`` holds the layer's parameters (A, b, a, b_t, Wq, bq,
+    Wk, bk, Wv, bv, optional Wo, bo) plus ln1_g, ln1_b, Wp, bp, ln2_g, ln2_b,
+    W1, b1, W2, b2.  Returns (x2, cache)."""
+    h, _, _ = layernorm(x, p["ln1_g"], p["ln1_b"], ln_eps)
+    xp = linear(h, p["Wp"], p["bp"])
+    pa = layer_forward(xp, G, p, tau0, tau_min, eps, H)
+    x1 = _in(x) + pa["y"]
+    h2, _, _ = layernorm(x1, p["ln2_g"], p["ln2_b"], ln_eps)
+    u = linear(h2, p["W1"], p["b1"])
+    v = linear(gelu(u), p["W2"], p["b2"])
+    x2 = x1 + v
+    return x2, {"x": _in(x), "h": h, "xp": xp, "pa": pa, "x1": x1, "h2": h2, "u": u}
+
+
+def block_backward(dx2, G, p, tau0, tau_min, eps, H, cache, ln_eps=LN_EPS):
+    """Chain rule of block_forward.  Returns (dx, grads) with a gradient for
+    every parameter of ``p`` (the layer's as in layer_backward)."""
+    c = cache
+    dx2 = _in(dx2)
+    dgu, dW2, db2 = linear_backward(gelu(c["u"]), p["W2"], dx2)
+    du = gelu_backward(c["u"], dgu)
+    dh2, dW1, db1 = linear_backward(c["h2"], p["W1"], du)
+    dx1_ln, dg2, db2n = layernorm_backward(c["x1"], p["ln2_g"], dh2, ln_eps)
+    dx1 = dx2 + dx1_ln
+    g = layer_backward(c["xp"], G, p, tau0, tau_min, eps, H, c["pa"], dx1)
+    dh, dWp, dbp = linear_backward(c["h"], p["Wp"], g["dx"])
+    dx_ln, dg1, db1n = layernorm_backward(c["x"], p["ln1_g"], dh, ln_eps)
+    grads = {k: v for k, v in g.items() if k not in ("dx", "dSp", "dS")}
+    grads.update({"dW2": dW2, "db2": db2, "dW1": dW1, "db1": db1, "dln2_g": dg2,
+                  "dln2_b": db2n, "dWp": dWp, "dbp": dbp, "dln1_g": dg1, "dln1_b": db1n})
+    return dx1 + dx_ln, grads
+
+
+def stack_forward(x, Gs, ps, tau0, tau_min, eps, H, ln_eps=LN_EPS):
+    """len(ps) blocks in sequence (layer l uses noise Gs[l]).  Returns
+    (output, caches)."""
+    caches = []
+    for G, p in zip(Gs, ps):
+        x, cache = block_forward(x, G, p, tau0, tau_min, eps, H, ln_eps)
+        caches.append(cache)
+    return x, caches
+
+
+def stack_backward(dy, Gs, ps, tau0, tau_min, eps, H, caches, ln_eps=LN_EPS):
+    """Chain rule of stack_forward.  Returns (dx, [grads per layer])."""
+    grads = [None] * len(ps)
+    for l in reversed(range(len(ps))):
+        dy, grads[l] = block_backward(dy, Gs[l], ps[l], tau0, tau_min, eps, H, caches[l], ln_eps)
+    return dy, grads
+

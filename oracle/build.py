@@ -7,19 +7,19 @@ import os
 import subprocess
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-SRC = os.path.join(HERE, "pa_oracle.c")
+SRCS = [os.path.join(HERE, "pa_oracle.c"), os.path.join(HERE, "pa_oracle_block.c")]
 LIB = os.path.join(HERE, "libpa_oracle.so")
 
 
 def build(verbose: bool = False) -> str:
-    """Compile oracle/pa_oracle.c into oracle/libpa_oracle.so and return its path.
+    """Compile the oracle's C sources into oracle/libpa_oracle.so and return its path.
 
     Portable flags only (no -march=native): the library is built here and
     also loaded on other hosts.
     """
     tmp = LIB + ".tmp"
     cmd = ["gcc", "-std=c11", "-O2", "-fopenmp", "-fPIC", "-shared",
-           "-Wall", "-Wextra", "-o", tmp, SRC, "-lm"]
+           "-Wall", "-Wextra", "-o", tmp, *SRCS, "-lm"]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)

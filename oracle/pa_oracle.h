@@ -114,6 +114,26 @@ void pao_slice_weights_backward(int64_t N, int C, int M, double tau0,
                                 double* dx, double* dA, double* db, double* da,
                                 double* db_t, double* dtau0);
 
+/* ---- Block stack (pa_oracle_block.c): the parts of a Transolver++ block
+ * around the layer (pre-norm Transformer block with Physics-Attention in
+ * place of attention, Section 3 and Figure 2a). */
+
+/* LayerNorm per row over C channels, biased variance; g, b nullable (1, 0);
+ * mean, rstd [N] nullable. */
+void pao_layernorm(int64_t N, int C, double eps, const double* x, const double* g,
+                   const double* b, double* y, double* mean, double* rstd);
+/* Its chain rule: dx [N,C], dg [C], db [C] (each nullable). */
+void pao_layernorm_backward(int64_t N, int C, double eps, const double* x, const double* g,
+                            const double* dy, double* dx, double* dg, double* db);
+/* Exact GELU x Phi(x) and its chain rule. */
+void pao_gelu(int64_t n, const double* x, double* y);
+void pao_gelu_backward(int64_t n, const double* x, const double* dy, double* dx);
+/* y = x W + b and its chain rule (dx, dW, db nullable). */
+void pao_linear(int64_t N, int Cin, int Cout, const double* x, const double* W, const double* b,
+                double* y);
+void pao_linear_backward(int64_t N, int Cin, int Cout, const double* x, const double* W,
+                         const double* dy, double* dx, double* dW, double* db);
+
 #ifdef __cplusplus
 }
 #endif
