@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define PA_VERSION 1
+#define PA_VERSION 2
 
 typedef enum { PA_F32 = 0, PA_BF16 = 1 } pa_dtype;
 
@@ -85,6 +85,9 @@ typedef struct {
   const float* b; /* [M] fp32, nullable (0)                       */
   const void* a;  /* [C] dtype, nullable (0)                      */
   float b_t;      /* scalar bias of the Ada-Temp projection       */
+  const float* b_t_dev; /* nullable: a device fp32 scalar added to b_t
+                           (e.g. the bias term of a folded Project step,
+                           pa_project_fold), read by the streaming kernels */
 } pa_slice_params;
 
 /* Token attention parameters (Eq. 2), all fp32 [C,C] / [C]. */
@@ -234,6 +237,90 @@ pa_status pa_deslice_backward_w(const pa_dims* dims, const void* W, const void* 
  * PA_ERR_INVALID and leaves the hook as it was.  Host-only: it launches
  * nothing. */
 pa_status pa_time_kernel(const char* call, void* start, void* stop);
+
+/* ---------------------------------------------------------------------
+ * Block-stack primitives.  A Transolver++ block is the Transformer block
+ * with Physics-Attention in place of attention (Section 3; the block
+ * diagram of Figure 2a), read here as pre-norm with residual adds:
+ *   x1 = x + PA(LN1(x)),  x2 = x1 + GELU(LN2(x1) W1 + b1) W2 + b2,
+ * where PA starts with Algorithm 1's Project step x_proj = h Wp + bp.  The
+ * stack runner (paper_2502_02414_amd/stack.py) composes these calls with
+ * the layer's calls above.  Same conventions as above (device pointers,
+ * 16-byte aligned, asynchronous on `stream`, host validation first);
+ * parameters are fp32 unless said otherwise; "dtype" tensors are bf16 or
+ * fp32.  Sums over rows are per-block partial sums added in block order
+ * (bitwise deterministic), except inside hipBLASLt.
+ * --------------------------------------------------------------------- */
+
+/* Row-major D[m,n] = alpha op(A) op(B) + beta C (+ bias[n] added to every
+ * row), op(X) = X^T when trans; A is [m,k] ([k,m] when transA), B [k,n]
+ * ([n,k] when transB); C [m,n] in D's dtype (nullable: C = D, in place;
+ * a residual add when it is another tensor and beta = 1).  The plain GEMMs of the MLP and the linear layers,
+ * on hipBLASLt (fp32 accumulation).  The first call on a device creates
+ * one hipBLASLt handle there (kept until the process ends); ws/ws_bytes is
+ * hipBLASLt's workspace (may be 0).  A combination of dtypes hipBLASLt does
+ * not serve returns PA_ERR_UNSUPPORTED. */
+pa_status pa_gemm(int transA, int transB, int64_t m, int64_t n, int64_t k, float alpha,
+                  const void* A, pa_dtype a_dtype, const void* B, pa_dtype b_dtype,
+                  float beta, const void* C, void* D, pa_dtype d_dtype, const float* bias,
+                  void* ws, size_t ws_bytes, void* stream);
+
+/* LayerNorm over the C channels of each of N rows (biased variance):
+ * s = x (+ r when r is given, rounded to dtype and written to xs when xs is
+ * given: the residual add that precedes a block's LayerNorm), y = (s -
+ * mean) / sqrt(var + eps) * g + b (g, b [C] nullable: 1, 0); mean, rstd [N]
+ * are saved for the backward.  C a power of two, 16 <= C <= 256 (fp32) or
+ * 512 (bf16). */
+pa_status pa_layernorm(int64_t N, int C, float eps, pa_dtype dtype, const void* x,
+                       const void* r, void* xs, const float* g, const float* b, void* y,
+                       float* mean, float* rstd, void* stream);
+
+/* Chain rule of pa_layernorm (x = the normalised input s): dx = the
+ * LayerNorm backward of dy, plus dres when given (the residual branch's
+ * gradient); dg, db [C] (nullable) need 256 * 2C floats of workspace. */
+pa_status pa_layernorm_backward(int64_t N, int C, pa_dtype dtype, const void* x,
+                                const float* g, const float* mean, const float* rstd,
+                                const void* dy, const void* dres, void* dx, float* dg,
+                                float* db, void* ws, size_t ws_bytes, void* stream);
+
+/* Exact GELU y = x Phi(x) over n elements (n a multiple of 16 bytes'
+ * worth), and its chain rule dx = dy (Phi(x) + x phi(x)). */
+pa_status pa_gelu(int64_t n, pa_dtype dtype, const void* x, void* y, void* stream);
+pa_status pa_gelu_backward(int64_t n, pa_dtype dtype, const void* x, const void* dy, void* dx,
+                           void* stream);
+
+/* out[c] = sum over the N rows of x [N,C] (the bias gradient of a linear
+ * layer); workspace min(N, 256) * C floats. */
+pa_status pa_colsum(int64_t N, int C, pa_dtype dtype, const void* x, float* out, void* ws,
+                    size_t ws_bytes, void* stream);
+
+/* Algorithm 1's Project step x_proj = h Wp + bp (Wp [C,C], bp [C]) folded
+ * into the slice parameters (A [C,M], b [M] nullable, a [C] nullable, all
+ * fp32): A_out = Wp A (dtype), b_out = b + bp A, a_out = Wp a (dtype),
+ * b_t_out[0] = bp.a (fp32 device scalar, for pa_slice_params.b_t_dev).  The
+ * logits and temperature of x_proj are then those of h under the folded
+ * parameters, so the layer's streaming calls run on h. */
+pa_status pa_project_fold(const pa_dims* dims, const float* Wp, const float* bp,
+                          const float* A, const float* b, const float* a, void* A_out,
+                          float* b_out, void* a_out, float* b_t_out, void* stream);
+
+/* The states of x_proj from those of h: S_proj [M,C] = S Wp + bp (each
+ * point's weights sum to 1; exact for every slice with den >= eps). */
+pa_status pa_project_states(const pa_dims* dims, const float* S, const float* Wp,
+                            const float* bp, float* S_proj, void* stream);
+
+/* Chain rule of pa_project_fold and pa_project_states: from the gradients
+ * of the folded parameters (*folded: dA, db, da, db_t, as
+ * pa_slice_aggregate_backward returns them for the folded call) and of the
+ * projected states dS_proj [M,C]: dWp [C,C], dbp [C], dS [M,C] (nullable;
+ * dS_proj Wp^T, the states gradient that pa_slice_aggregate_backward
+ * takes, which a caller forms before that call, e.g. with pa_gemm) and the
+ * gradients of the unfolded parameters in *gr (dA required; db, da, db_t
+ * nullable). */
+pa_status pa_project_backward(const pa_dims* dims, const float* Wp, const float* bp,
+                              const float* A, const float* a, const float* S,
+                              const float* dS_proj, const pa_slice_grads* folded, float* dWp,
+                              float* dbp, float* dS, const pa_slice_grads* gr, void* stream);
 
 #ifdef __cplusplus
 }

@@ -29,7 +29,9 @@ SYMBOLS = (
     "pa_slice_aggregate", "pa_token_attention", "pa_deslice", "pa_deslice_backward",
     "pa_token_attention_backward", "pa_slice_aggregate_backward",
     "pa_slice_weights_backward", "pa_time_kernel", "pa_slice_aggregate_w", "pa_deslice_w",
-    "pa_deslice_backward_w",
+    "pa_deslice_backward_w", "pa_gemm", "pa_layernorm", "pa_layernorm_backward", "pa_gelu",
+    "pa_gelu_backward", "pa_colsum", "pa_project_fold", "pa_project_states",
+    "pa_project_backward",
 )
 
 
@@ -47,7 +49,7 @@ class pa_dims(ctypes.Structure):
 
 class pa_slice_params(ctypes.Structure):
     _fields_ = [("A", ctypes.c_void_p), ("b", ctypes.c_void_p), ("a", ctypes.c_void_p),
-                ("b_t", ctypes.c_float)]
+                ("b_t", ctypes.c_float), ("b_t_dev", ctypes.c_void_p)]
 
 
 class pa_attn_params(ctypes.Structure):
@@ -73,6 +75,9 @@ def load(path: str = LIB_PATH):
         return _lib
     if not os.path.exists(path):
         raise RuntimeError(f"HIP library {path} is not built; run __graft_entry__.build()")
+    # torch's HIP runtime and hipBLASLt are loaded first, so libpa.so binds to
+    # the same copies (one HIP runtime per process)
+    import torch  # noqa: F401
     lib = ctypes.CDLL(path)
     P, S = ctypes.c_void_p, ctypes.c_size_t
     D = ctypes.POINTER(pa_dims)
@@ -95,6 +100,16 @@ def load(path: str = LIB_PATH):
     lib.pa_slice_aggregate_w.argtypes = [D, P, P, SPp, P, P, P, P, P, S, P]
     lib.pa_deslice_w.argtypes = [D, P, P, P, P, S, P]
     lib.pa_deslice_backward_w.argtypes = [D, P, P, P, P, S, P]
+    I64, I32, F = ctypes.c_int64, ctypes.c_int, ctypes.c_float
+    lib.pa_gemm.argtypes = [I32, I32, I64, I64, I64, F, P, I32, P, I32, F, P, P, I32, P, P, S, P]
+    lib.pa_layernorm.argtypes = [I64, I32, F, I32, P, P, P, P, P, P, P, P, P]
+    lib.pa_layernorm_backward.argtypes = [I64, I32, I32, P, P, P, P, P, P, P, P, P, P, S, P]
+    lib.pa_gelu.argtypes = [I64, I32, P, P, P]
+    lib.pa_gelu_backward.argtypes = [I64, I32, P, P, P, P]
+    lib.pa_colsum.argtypes = [I64, I32, I32, P, P, P, S, P]
+    lib.pa_project_fold.argtypes = [D, P, P, P, P, P, P, P, P, P, P]
+    lib.pa_project_states.argtypes = [D, P, P, P, P, P]
+    lib.pa_project_backward.argtypes = [D, P, P, P, P, P, P, SGp, P, P, P, SGp, P]
     for name in SYMBOLS:
         if name not in ("pa_version", "pa_last_error"):
             getattr(lib, name).restype = ctypes.c_int
@@ -130,8 +145,8 @@ def make_dims(N: int, C: int, H: int, M: int, tau0: float, tau_min: float, eps: 
                    int(dtype))
 
 
-def make_slice_params(A, b=None, a=None, b_t: float = 0.0) -> pa_slice_params:
-    return pa_slice_params(_ptr(A), _ptr(b), _ptr(a), float(b_t))
+def make_slice_params(A, b=None, a=None, b_t: float = 0.0, b_t_dev=None) -> pa_slice_params:
+    return pa_slice_params(_ptr(A), _ptr(b), _ptr(a), float(b_t), _ptr(b_t_dev))
 
 
 def make_attn_params(Wq, Wk, Wv, bq=None, bk=None, bv=None, Wo=None, bo=None) -> pa_attn_params:
@@ -288,3 +303,75 @@ class HipEvent:
         if self.handle and _hip is not None:
             _hip.hipEventDestroy(self.handle)
             self.handle = ctypes.c_void_p()
+
+
+# ---- block-stack primitives (include/pa.h) ----
+def _nbytes(t) -> int:
+    return 0 if t is None else t.numel() * t.element_size()
+
+
+def _dt(t) -> int:
+    import torch
+    if t.dtype == torch.bfloat16:
+        return PA_BF16
+    if t.dtype == torch.float32:
+        return PA_F32
+    raise ValueError(f"unsupported dtype {t.dtype}")
+
+
+def pa_gemm(A, B, D, transA=False, transB=False, alpha=1.0, beta=0.0, bias=None, ws=None,
+            C=None, stream=None):
+    """Row-major D = alpha op(A) op(B) + beta C (+ bias); C defaults to D."""
+    m = A.shape[1] if transA else A.shape[0]
+    k = A.shape[0] if transA else A.shape[1]
+    n = B.shape[0] if transB else B.shape[1]
+    _check(load().pa_gemm(int(transA), int(transB), m, n, k, float(alpha), _ptr(A), _dt(A),
+                          _ptr(B), _dt(B), float(beta), _ptr(C), _ptr(D), _dt(D), _ptr(bias),
+                          _ptr(ws), _nbytes(ws), _stream(stream)))
+
+
+def pa_layernorm(x, y, mean, rstd, g=None, b=None, r=None, xs=None, eps=1e-5, stream=None):
+    N, C = x.shape
+    _check(load().pa_layernorm(N, C, float(eps), _dt(x), _ptr(x), _ptr(r), _ptr(xs), _ptr(g),
+                               _ptr(b), _ptr(y), _ptr(mean), _ptr(rstd), _stream(stream)))
+
+
+def pa_layernorm_backward(x, mean, rstd, dy, dx, g=None, dres=None, dg=None, db=None, ws=None,
+                          stream=None):
+    N, C = x.shape
+    _check(load().pa_layernorm_backward(N, C, _dt(x), _ptr(x), _ptr(g), _ptr(mean), _ptr(rstd),
+                                        _ptr(dy), _ptr(dres), _ptr(dx), _ptr(dg), _ptr(db),
+                                        _ptr(ws), _nbytes(ws), _stream(stream)))
+
+
+def pa_gelu(x, y, stream=None):
+    _check(load().pa_gelu(x.numel(), _dt(x), _ptr(x), _ptr(y), _stream(stream)))
+
+
+def pa_gelu_backward(x, dy, dx, stream=None):
+    _check(load().pa_gelu_backward(x.numel(), _dt(x), _ptr(x), _ptr(dy), _ptr(dx),
+                                   _stream(stream)))
+
+
+def pa_colsum(x, out, ws, stream=None):
+    N, C = x.shape
+    _check(load().pa_colsum(N, C, _dt(x), _ptr(x), _ptr(out), _ptr(ws), _nbytes(ws),
+                            _stream(stream)))
+
+
+def pa_project_fold(dims, Wp, bp, A, b, a, A_out, b_out, a_out, b_t_out, stream=None):
+    _check(load().pa_project_fold(ctypes.byref(dims), _ptr(Wp), _ptr(bp), _ptr(A), _ptr(b),
+                                  _ptr(a), _ptr(A_out), _ptr(b_out), _ptr(a_out), _ptr(b_t_out),
+                                  _stream(stream)))
+
+
+def pa_project_states(dims, S, Wp, bp, S_proj, stream=None):
+    _check(load().pa_project_states(ctypes.byref(dims), _ptr(S), _ptr(Wp), _ptr(bp),
+                                    _ptr(S_proj), _stream(stream)))
+
+
+def pa_project_backward(dims, Wp, bp, A, a, S, dS_proj, folded, dWp, dbp, dS, gr, stream=None):
+    _check(load().pa_project_backward(ctypes.byref(dims), _ptr(Wp), _ptr(bp), _ptr(A), _ptr(a),
+                                      _ptr(S), _ptr(dS_proj), ctypes.byref(folded), _ptr(dWp),
+                                      _ptr(dbp), _ptr(dS), ctypes.byref(gr), _stream(stream)))
+

@@ -158,6 +158,7 @@ pa::StreamLaunch stream_of(const pa_dims& d, int pass, const void* x, const void
   L.rec = (int)pa::record_floats(pass, d.C, d.M);
   L.P = chunks(d, pass);
   L.tb = (double)d.tau0 + (sp ? (double)sp->b_t : 0.0);
+  L.tb_dev = sp ? sp->b_t_dev : nullptr;
   L.tau_min = d.tau_min;
   return L;
 }
@@ -176,6 +177,12 @@ pa_status check_slice(const pa_dims* dims, const void* x, const void* G,
 }
 
 hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+}  // namespace
+
+void pa::set_last_error(const char* msg) { g_err = msg; }
+
+namespace {
 
 // pa_time_kernel's hook: the pass whose streaming kernel is bracketed by the
 // caller's events on this thread (-1: disarmed).

@@ -23,6 +23,7 @@ struct StreamLaunch {
   int rec = 0;
   int P = 1;
   double tb = 0.0;  // tau0 + b_t
+  const float* tb_dev = nullptr;  // nullable device scalar added to tb
   float tau_min = 0.f;
   bool states = false;
   bool deslice = false;
@@ -131,5 +132,75 @@ hipError_t launch_attn_core(const float* Q, const float* K, const float* V, floa
 hipError_t launch_attn_core_bwd(const float* Q, const float* K, const float* V,
                                 const float* P, const float* dO, float* dQ, float* dK,
                                 float* dV, int M, int C, int H, hipStream_t st);
+
+// Sets the thread-local message of pa_last_error() (pa_api.cpp).
+void set_last_error(const char* msg);
+
+// ---- Block stack (pa_block.hip, pa_gemm.cpp) ----
+// LayerNorm over C channels: forward (s = x + r, optional; y = LN(s);
+// mean/rstd saved) or backward (dx = LN'(dy) + dres; dg/db partial records
+// of 2C floats per block, `blocks` blocks of `rows_per_block` rows).
+struct LayerNormArgs {
+  int64_t N = 0;
+  int C = 0;
+  float eps = 1e-5f;
+  const void* x = nullptr;
+  const void* r = nullptr;
+  void* xs = nullptr;
+  const float* g = nullptr;
+  const float* b = nullptr;
+  void* y = nullptr;
+  float* mean = nullptr;
+  float* rstd = nullptr;
+  const void* dy = nullptr;
+  const void* dres = nullptr;
+  void* dx = nullptr;
+  float* partials = nullptr;
+  int64_t rows_per_block = 0;
+  int blocks = 0;
+};
+hipError_t launch_layernorm(const LayerNormArgs& a, int dtype, bool bwd, hipStream_t st);
+// out = GELU(x), or out = dy GELU'(x) when dy is given (n a multiple of 16 B).
+hipError_t launch_gelu(int64_t n, int dtype, const void* x, const void* dy, void* out,
+                       hipStream_t st);
+// Per-block column sums of x [N,C] (P records of C floats).
+hipError_t launch_colsum(int64_t N, int C, int dtype, const void* x, float* partials, int P,
+                         hipStream_t st);
+// Project folding (fp32 parameters; A_out, a_out in dtype).
+struct FoldArgs {
+  int C = 0, M = 0;
+  const float *Wp = nullptr, *bp = nullptr, *A = nullptr, *b = nullptr, *a = nullptr;
+  void* A_out = nullptr;
+  void* a_out = nullptr;
+  float* b_out = nullptr;
+  float* bt_out = nullptr;
+};
+hipError_t launch_fold(const FoldArgs& f, int dtype, hipStream_t st);
+hipError_t launch_project_states(int M, int C, const float* S, const float* Wp, const float* bp,
+                                 float* Sp, hipStream_t st);
+struct FoldGradArgs {
+  int C = 0, M = 0;
+  const float *Wp = nullptr, *bp = nullptr, *A = nullptr, *a = nullptr, *S = nullptr;
+  const float *dSp = nullptr, *dAf = nullptr, *dbf = nullptr, *daf = nullptr, *dbtf = nullptr;
+  float *dWp = nullptr, *dbp = nullptr, *dA = nullptr, *db = nullptr, *da = nullptr;
+  float *dbt = nullptr, *dS = nullptr;
+};
+hipError_t launch_fold_grads(const FoldGradArgs& f, hipStream_t st);
+// Row-major D[m,n] = alpha op(A) op(B) + beta D (+ bias[n]) on hipBLASLt;
+// dtypes 0 fp32, 1 bf16.  Returns 0 or a hipblasStatus_t.
+struct Gemm {
+  bool transA = false, transB = false;
+  int64_t m = 0, n = 0, k = 0;
+  float alpha = 1.f, beta = 0.f;
+  const void* A = nullptr;
+  const void* B = nullptr;
+  const void* Cin = nullptr;  // beta's input (nullable: D itself), D's dtype and shape
+  void* D = nullptr;
+  int ta = 0, tb = 0, td = 0;
+  const float* bias = nullptr;
+  void* ws = nullptr;
+  size_t ws_bytes = 0;
+};
+int gemm(const Gemm& g, hipStream_t st);
 
 }  // namespace pa

@@ -39,7 +39,7 @@ hipError_t launch_stream(int pass, int dtype, int C, int MB, const StreamLaunch&
   StreamArgs a;
   a.x = L.x; a.G = L.G; a.dY = L.dY; a.img = L.img; a.out = L.out; a.tau_out = L.tau_out;
   a.dW = L.dW; a.dtau = L.dtau; a.partials = L.partials; a.N = L.N; a.M = L.M; a.rec = L.rec;
-  a.tb = L.tb; a.tau_min = L.tau_min;
+  a.tb = L.tb; a.tb_dev = L.tb_dev; a.tau_min = L.tau_min;
   a.flags = (L.G ? kHasG : 0) | (L.states ? kStatesTerm : 0) | (L.deslice ? kDesliceTerm : 0);
   switch (pass) {
     case kAggregate: return launch_aggregate_pass(dtype, C, MB, a, L.P, st);

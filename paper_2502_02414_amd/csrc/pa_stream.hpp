@@ -50,6 +50,7 @@ struct StreamArgs {
   int M;
   int rec;               // floats per record
   double tb;             // tau0 + b_t (exact sum of the two fp32 values)
+  const float* tb_dev;   // nullable: a device scalar added to tb
   float tau_min;
   int flags;
 };
@@ -72,6 +73,12 @@ template <typename T, int MB> constexpr int bwd_depth() { return 1; }
 // than their successors gained).
 constexpr bool kRevDeslice = true, kRevSliceBwd = false;
 template <int PASS> constexpr bool keep_loads() { return PASS == kAggregate; }
+
+// The temperature constant: tau0 + b_t, plus the device scalar when one is
+// given (a folded Project step's bias term, computed on the GPU).
+__device__ __forceinline__ void add_tb_dev(StreamArgs& a) {
+  if (a.tb_dev) a.tb += (double)a.tb_dev[0];
+}
 
 // Point-side tensors are streamed once per pass: their 16-byte stores are
 // non-temporal (no dirty data is left in the caches, so a pass does not pay
@@ -768,6 +775,7 @@ k_aggregate(StreamArgs a) {
   constexpr int SZ = (int)sizeof(T);
   using V = typename LAcc<T, true>::v;
   extern __shared__ __attribute__((aligned(16))) char smem[];
+  add_tb_dev(a);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r = lane_id() & 15, g = lane_id() >> 4;
   const bool hasG = WIN || (a.flags & kHasG);  // WIN: the Gumbel rows' buffer holds W
@@ -967,6 +975,7 @@ k_deslice(StreamArgs a) {
   constexpr int WAVES = G_::waves(PASS);
   constexpr int SZ = (int)sizeof(T);
   extern __shared__ __attribute__((aligned(16))) char smem[];
+  add_tb_dev(a);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r = lane_id() & 15, g = lane_id() >> 4;
   const bool hasG = WIN || (a.flags & kHasG);
@@ -1083,6 +1092,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kWeights)))
   using G_ = Geo<sizeof(T), C, MB>;
   constexpr int WAVES = G_::waves(kWeights);
   extern __shared__ __attribute__((aligned(16))) char smem[];
+  add_tb_dev(a);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r = lane_id() & 15, g = lane_id() >> 4;
   const bool hasG = a.flags & kHasG;
@@ -1162,6 +1172,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
   constexpr int SZ = (int)sizeof(T);
   constexpr int SROWF = M16 + 1;  // dl transpose row stride (floats)
   extern __shared__ __attribute__((aligned(16))) char smem[];
+  add_tb_dev(a);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r = lane_id() & 15, g = lane_id() >> 4;
   const bool hasG = a.flags & kHasG;

@@ -390,6 +390,47 @@ def make_params(w: Workload, biases: bool = False, out_proj: bool = False) -> di
     return p
 
 
+def layer_workload(w: Workload, layer: int) -> Workload:
+    """The workload of block `layer` of a stack: the same shapes, its own
+    seed (its own parameters and Gumbel noise)."""
+    return dataclasses.replace(w, seed=w.seed + 100003 * (layer + 1))
+
+
+def make_block_params(w: Workload, layer: int) -> dict:
+    """Parameters of block `layer` of a Transolver++ block stack: the layer's
+    (make_params of the layer's workload, with small nonzero biases and an
+    output projection Wo, bo) plus Algorithm 1's Project Wp [C,C], bp [C],
+    the two LayerNorms' gains (1 + small) and biases (small), and the MLP
+    W1 [C,4C], b1, W2 [4C,C], b2 (Xavier-uniform; W1, W2 rounded to bf16 for
+    bf16 workloads, as they feed bf16 GEMMs).  All float32."""
+    wl = layer_workload(w, layer)
+    C = w.C
+    p = make_params(wl, biases=True, out_proj=True)
+    off = 1 << 44                     # past make_params' draws in the weights stream
+    p["Wp"] = xavier_uniform(wl.seed, off, C, C, (C, C)).astype(np.float32); off += C * C
+    p["W1"] = xavier_uniform(wl.seed, off, C, 4 * C, (C, 4 * C)).astype(np.float32)
+    off += 4 * C * C
+    p["W2"] = xavier_uniform(wl.seed, off, 4 * C, C, (4 * C, C)).astype(np.float32)
+    off += 4 * C * C
+    if w.dtype == "bf16":
+        p["W1"], p["W2"] = round_bf16(p["W1"]), round_bf16(p["W2"])
+    small_u = lambda n, k: (0.2 * (2 * uniform(wl.seed, STREAM_WEIGHTS, off + k * 8192, n) - 1)
+                            ).astype(np.float32)
+    p["bp"] = small_u(C, 0)
+    p["ln1_g"] = 1.0 + small_u(C, 1)
+    p["ln1_b"] = small_u(C, 2)
+    p["ln2_g"] = 1.0 + small_u(C, 3)
+    p["ln2_b"] = small_u(C, 4)
+    p["b1"] = small_u(4 * C, 5)
+    p["b2"] = small_u(C, 6)
+    return p
+
+
+def make_layer_gumbel(w: Workload, layer: int, N: Optional[int] = None) -> np.ndarray:
+    """The Gumbel noise of block `layer` [N,M] (storage dtype values)."""
+    return make_gumbel(layer_workload(w, layer), N)
+
+
 def small(name: str, N: int, C: int, H: int, M: int, dtype: str = "f32",
           geometry: str = "normal", seed: int = 7, **kw) -> Workload:
     """An ad-hoc workload (tests, sweeps)."""
