@@ -105,11 +105,15 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration)")
+    ap.add_argument("--stack", action="store_true",
+                    help="time the 8-block Transolver++ stack at N = 2.5M instead (its own line)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); this build runs the "
               "hot path on a single MI355X and has no multi-GPU path.", file=sys.stderr)
         sys.exit(2)
+    if args.stack:
+        return stack_bench(args)
 
     import numpy as np
     import torch
@@ -223,6 +227,69 @@ def main():
 
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(x_np, G_np, dY_np, p, w)
+    print(json.dumps(out), flush=True)
+
+
+def stack_bench(args):
+    """The 8-block Transolver++ stack (LN -> Physics-Attention with the folded
+    Project step -> MLP 256-1024-256 with GELU, residual adds) at N = 2.5M
+    points, C = 256, H = 8, M = 64, bf16, forward + backward on one GPU: one
+    step is the stack's forward and backward (no optimizer step).  Prints its
+    own JSON line; the headline line is the layer's."""
+    import torch
+    from paper_2502_02414_amd import binding as B
+    from paper_2502_02414_amd import inputs as I
+    from paper_2502_02414_amd.stack import BlockStack
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    w = I.WORKLOADS["aircraft_2p5m_bf16"]
+    N, C, H, M, L = w.N, w.C, w.H, w.M, 8
+    t0 = time.time()
+    bf = torch.bfloat16
+    to = lambda a, dt=torch.float32: torch.from_numpy(a).cuda().to(dt)
+    x, dY = to(I.make_x(w), bf), to(I.make_grad(w), bf)
+    Gs = [to(I.make_layer_gumbel(w, l), bf) for l in range(L)]
+    params = []
+    for l in range(L):
+        p = I.make_block_params(w, l)
+        params.append({k: (float(v) if k == "b_t" else to(v, bf if k in ("W1", "W2") else
+                                                         torch.float32)) for k, v in p.items()})
+    print(f"[bench] stack inputs generated in {time.time() - t0:.1f}s", file=sys.stderr,
+          flush=True)
+    st = BlockStack(N, C, H, M, params, bf, w.tau0, w.tau_min, w.eps)
+    steps, warmup = max(1, min(args.steps, 5)), max(1, min(args.warmup, 2))
+    ev = [[B.HipEvent() for _ in range(3)] for _ in range(steps)]
+    for _ in range(warmup):
+        st.forward(x, Gs)
+        st.backward(dY)
+    torch.cuda.synchronize()
+    start, end = B.HipEvent(), B.HipEvent()
+    start.record()
+    for s in range(steps):
+        ev[s][0].record()
+        st.forward(x, Gs)
+        ev[s][1].record()
+        st.backward(dY)
+        ev[s][2].record()
+    end.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_ms(end) / steps
+    fwd = sum(e[0].elapsed_ms(e[1]) for e in ev) / steps
+    bwd = sum(e[1].elapsed_ms(e[2]) for e in ev) / steps
+    # MLP GEMM flops per step: forward 2 GEMMs, backward 4, each 2 N C 4C
+    mlp_flop = 6 * 2 * N * C * 4 * C * L
+    out = {
+        "metric": "mesh points/sec, 8-block Transolver++ stack fwd+bwd at N=2.5M, C=256, M=64",
+        "value": round(N / (ms * 1e-3), 1), "unit": "points/s", "n_gpus": 1, "steps": steps,
+        "warmup": warmup, "ms_per_step": round(ms, 2), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "aircraft_2p5m_bf16_8blocks", "N": N, "C": C, "H": H, "M": M,
+                   "blocks": L, "mlp_hidden": 4 * C, "pass": "forward+backward"},
+        "forward_ms": round(fwd, 2), "backward_ms": round(bwd, 2),
+        "mlp_gemm_tflops": round(mlp_flop / (ms * 1e-3) / 1e12, 1),
+        "peak_mem_gib": round(torch.cuda.max_memory_allocated() / 2**30, 1),
+    }
     print(json.dumps(out), flush=True)
 
 
