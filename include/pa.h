@@ -277,7 +277,8 @@ pa_status pa_layernorm(int64_t N, int C, float eps, pa_dtype dtype, const void* 
 
 /* Chain rule of pa_layernorm (x = the normalised input s): dx = the
  * LayerNorm backward of dy, plus dres when given (the residual branch's
- * gradient); dg, db [C] (nullable) need 256 * 2C floats of workspace. */
+ * gradient); dg, db [C] (nullable) need at most 1024 * 2C floats of
+ * workspace (one partial record per block). */
 pa_status pa_layernorm_backward(int64_t N, int C, pa_dtype dtype, const void* x,
                                 const float* g, const float* mean, const float* rstd,
                                 const void* dy, const void* dres, void* dx, float* dg,
@@ -290,7 +291,8 @@ pa_status pa_gelu_backward(int64_t n, pa_dtype dtype, const void* x, const void*
                            void* stream);
 
 /* out[c] = sum over the N rows of x [N,C] (the bias gradient of a linear
- * layer); workspace min(N, 256) * C floats. */
+ * layer; C a multiple of 16 bytes' worth, at most 256 x 16 bytes);
+ * workspace min(N, 1024) * C floats. */
 pa_status pa_colsum(int64_t N, int C, pa_dtype dtype, const void* x, float* out, void* ws,
                     size_t ws_bytes, void* stream);
 

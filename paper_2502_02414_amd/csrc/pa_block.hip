@@ -62,88 +62,128 @@ __device__ __forceinline__ float group_sum(float v, int L) {
 // LayerNorm: s = x (+ r, rounded to the storage dtype; written to xs when
 // given); y = (s - mean) rstd g + b with rstd = 1 / sqrt(var + eps), var the
 // biased variance; mean and rstd [N] saved for the backward.
+// A wave takes kLnRows row groups (rpw rows each) per iteration of a
+// grid-stride loop and issues all their loads before any arithmetic; rows
+// past N re-read row N - 1 and are not stored.  The loop bounds and every
+// shuffle are uniform within a row group.
 // ---------------------------------------------------------------------------
+constexpr int kLnRows = 4;
+
 template <typename T>
 __global__ void __launch_bounds__(256) k_ln_fwd(LayerNormArgs a) {
-  constexpr int E = Vec<T>::E;
+  constexpr int E = Vec<T>::E, R = kLnRows;
   const int L = a.C / E, rpw = 64 / L;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int64_t row = ((int64_t)blockIdx.x * 4 + wave) * rpw + lane / L;
-  const int c0 = (lane % L) * E;
-  if (row >= a.N) return;  // whole row groups leave together (their shuffles stay within the group)
-  const T* x = reinterpret_cast<const T*>(a.x) + row * a.C + c0;
-  float v[E];
-  load16<T>(x, v);
-  if (a.r) {
-    float rv[E];
-    load16<T>(reinterpret_cast<const T*>(a.r) + row * a.C + c0, rv);
+  const int lane = threadIdx.x & 63, sub = lane / L, c0 = (lane % L) * E;
+  const int64_t gw = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int64_t step = (int64_t)gridDim.x * 4 * R * rpw;
+  const T* X = reinterpret_cast<const T*>(a.x);
+  const T* Rr = reinterpret_cast<const T*>(a.r);
+  for (int64_t base = gw * R * rpw; base < a.N; base += step) {
+    float v[R][E];
+    int64_t row[R];
 #pragma unroll
-    for (int e = 0; e < E; ++e) v[e] = to_f<T>(from_f<T>(v[e] + rv[e]));
-    if (a.xs) store16<T>(reinterpret_cast<T*>(a.xs) + row * a.C + c0, v);
-  }
-  float s = 0.f;
+    for (int k = 0; k < R; ++k) {
+      row[k] = base + k * rpw + sub;
+      load16<T>(X + (row[k] < a.N ? row[k] : a.N - 1) * a.C + c0, v[k]);
+    }
+    if (Rr) {
+      float rv[R][E];
 #pragma unroll
-  for (int e = 0; e < E; ++e) s += v[e];
-  const float mean = group_sum(s, L) / (float)a.C;
-  float q = 0.f;
+      for (int k = 0; k < R; ++k)
+        load16<T>(Rr + (row[k] < a.N ? row[k] : a.N - 1) * a.C + c0, rv[k]);
 #pragma unroll
-  for (int e = 0; e < E; ++e) q += (v[e] - mean) * (v[e] - mean);
-  const float rstd = 1.0f / sqrtf(group_sum(q, L) / (float)a.C + a.eps);
-  float y[E];
+      for (int k = 0; k < R; ++k) {
 #pragma unroll
-  for (int e = 0; e < E; ++e)
-    y[e] = (v[e] - mean) * rstd * (a.g ? a.g[c0 + e] : 1.f) + (a.b ? a.b[c0 + e] : 0.f);
-  store16<T>(reinterpret_cast<T*>(a.y) + row * a.C + c0, y);
-  if (lane % L == 0) {
-    a.mean[row] = mean;
-    a.rstd[row] = rstd;
+        for (int e = 0; e < E; ++e) v[k][e] = to_f<T>(from_f<T>(v[k][e] + rv[k][e]));
+        if (a.xs && row[k] < a.N) store16<T>(reinterpret_cast<T*>(a.xs) + row[k] * a.C + c0, v[k]);
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+      float s = 0.f;
+#pragma unroll
+      for (int e = 0; e < E; ++e) s += v[k][e];
+      const float mean = group_sum(s, L) / (float)a.C;
+      float q = 0.f;
+#pragma unroll
+      for (int e = 0; e < E; ++e) q += (v[k][e] - mean) * (v[k][e] - mean);
+      const float rstd = 1.0f / sqrtf(group_sum(q, L) / (float)a.C + a.eps);
+      float y[E];
+#pragma unroll
+      for (int e = 0; e < E; ++e)
+        y[e] = (v[k][e] - mean) * rstd * (a.g ? a.g[c0 + e] : 1.f) + (a.b ? a.b[c0 + e] : 0.f);
+      if (row[k] < a.N) {
+        store16<T>(reinterpret_cast<T*>(a.y) + row[k] * a.C + c0, y);
+        if (lane % L == 0) {
+          a.mean[row[k]] = mean;
+          a.rstd[row[k]] = rstd;
+        }
+      }
+    }
   }
 }
 
 // Backward: with xhat = (s - mean) rstd and gh = dy g,
 //   dx = rstd (gh - mean_c(gh) - xhat mean_c(gh xhat)) (+ dres),
-// and per-block partial sums of dg = dy xhat, db = dy over the block's rows
-// (rows [blockIdx.x * R, +R), each lane's rows in order, then the block's
-// row slots in order), written as record [dg | db] of 2C floats.
+// and per-block partial sums of dg = dy xhat, db = dy: each lane adds its
+// rows in loop order, then the block's row slots are added in slot order,
+// giving the block's record [dg | db] of 2C floats.  The rows a block
+// handles are fixed by (N, C, grid), so the sums are deterministic.
 template <typename T>
 __global__ void __launch_bounds__(256) k_ln_bwd(LayerNormArgs a) {
-  constexpr int E = Vec<T>::E;
+  constexpr int E = Vec<T>::E, R = kLnRows;
   const int L = a.C / E, rpw = 64 / L, slots = 4 * rpw;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int slot = wave * rpw + lane / L;
-  const int c0 = (lane % L) * E;
-  const int64_t r0 = (int64_t)blockIdx.x * a.rows_per_block;
-  const int64_t r1 = r0 + a.rows_per_block < a.N ? r0 + a.rows_per_block : a.N;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, sub = lane / L;
+  const int slot = wave * rpw + sub, c0 = (lane % L) * E;
+  const int64_t gw = (int64_t)blockIdx.x * 4 + wave;
+  const int64_t step = (int64_t)gridDim.x * 4 * R * rpw;
+  const T* X = reinterpret_cast<const T*>(a.x);
+  const T* DY = reinterpret_cast<const T*>(a.dy);
+  const T* DR = reinterpret_cast<const T*>(a.dres);
   float ag[E], ab[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) ag[e] = ab[e] = 0.f;
-  // every lane of a row group runs the same number of iterations
-  for (int64_t row = r0 + slot; row < r1; row += slots) {
-    float v[E], dy[E];
-    load16<T>(reinterpret_cast<const T*>(a.x) + row * a.C + c0, v);
-    load16<T>(reinterpret_cast<const T*>(a.dy) + row * a.C + c0, dy);
-    const float mean = a.mean[row], rstd = a.rstd[row];
-    float xh[E], gh[E], sg = 0.f, sgx = 0.f;
+  for (int64_t base = gw * R * rpw; base < a.N; base += step) {
+    float v[R][E], dy[R][E], mean[R], rstd[R];
+    int64_t row[R];
 #pragma unroll
-    for (int e = 0; e < E; ++e) {
-      xh[e] = (v[e] - mean) * rstd;
-      gh[e] = dy[e] * (a.g ? a.g[c0 + e] : 1.f);
-      sg += gh[e];
-      sgx += gh[e] * xh[e];
-      ag[e] += dy[e] * xh[e];
-      ab[e] += dy[e];
+    for (int k = 0; k < R; ++k) {
+      row[k] = base + k * rpw + sub;
+      const int64_t rr = row[k] < a.N ? row[k] : a.N - 1;
+      load16<T>(X + rr * a.C + c0, v[k]);
+      load16<T>(DY + rr * a.C + c0, dy[k]);
+      mean[k] = a.mean[rr];
+      rstd[k] = a.rstd[rr];
     }
-    const float mg = group_sum(sg, L) / (float)a.C, mgx = group_sum(sgx, L) / (float)a.C;
-    float dx[E];
 #pragma unroll
-    for (int e = 0; e < E; ++e) dx[e] = rstd * (gh[e] - mg - xh[e] * mgx);
-    if (a.dres) {
-      float d2[E];
-      load16<T>(reinterpret_cast<const T*>(a.dres) + row * a.C + c0, d2);
+    for (int k = 0; k < R; ++k) {
+      const bool ok = row[k] < a.N;
+      float xh[E], gh[E], sg = 0.f, sgx = 0.f;
 #pragma unroll
-      for (int e = 0; e < E; ++e) dx[e] += d2[e];
+      for (int e = 0; e < E; ++e) {
+        xh[e] = (v[k][e] - mean[k]) * rstd[k];
+        gh[e] = dy[k][e] * (a.g ? a.g[c0 + e] : 1.f);
+        sg += gh[e];
+        sgx += gh[e] * xh[e];
+        if (ok) {
+          ag[e] += dy[k][e] * xh[e];
+          ab[e] += dy[k][e];
+        }
+      }
+      const float mg = group_sum(sg, L) / (float)a.C, mgx = group_sum(sgx, L) / (float)a.C;
+      float dx[E];
+#pragma unroll
+      for (int e = 0; e < E; ++e) dx[e] = rstd[k] * (gh[e] - mg - xh[e] * mgx);
+      if (ok) {
+        if (DR) {
+          float d2[E];
+          load16<T>(DR + row[k] * a.C + c0, d2);
+#pragma unroll
+          for (int e = 0; e < E; ++e) dx[e] += d2[e];
+        }
+        store16<T>(reinterpret_cast<T*>(a.dx) + row[k] * a.C + c0, dx);
+      }
     }
-    store16<T>(reinterpret_cast<T*>(a.dx) + row * a.C + c0, dx);
   }
   if (!a.partials) return;
   extern __shared__ float red[];  // [slots][2C]
@@ -192,17 +232,45 @@ __global__ void __launch_bounds__(256) k_gelu(int64_t n, const T* x, const T* dy
 }
 
 // ---------------------------------------------------------------------------
-// Column sums of x [N, C]: block b sums rows [b R, (b + 1) R) in order into
-// its record of C floats (threads over columns).
+// Column sums of x [N, C] (C / E <= 256 column groups of 16 bytes): block b
+// sums rows [b R0, (b + 1) R0); thread t owns column group t % CG of every
+// RL-th row (RL = 256 / CG row lanes), kLnRows rows' loads in flight; the
+// row lanes are then added in order through LDS into the block's record of
+// C floats.
 // ---------------------------------------------------------------------------
 template <typename T>
-__global__ void __launch_bounds__(256) k_colsum(int64_t N, int C, int64_t R, const T* x,
+__global__ void __launch_bounds__(256) k_colsum(int64_t N, int C, int64_t R0, const T* x,
                                                 float* partials) {
-  const int64_t r0 = (int64_t)blockIdx.x * R, r1 = r0 + R < N ? r0 + R : N;
-  for (int c = threadIdx.x; c < C; c += blockDim.x) {
+  constexpr int E = Vec<T>::E, U = kLnRows;
+  const int CG = C / E, RL = 256 / CG;
+  const int t = threadIdx.x, rl = t / CG, cg = t % CG;
+  const int64_t r0 = (int64_t)blockIdx.x * R0, r1 = r0 + R0 < N ? r0 + R0 : N;
+  float acc[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) acc[e] = 0.f;
+  if (rl < RL) {
+    for (int64_t r = r0 + rl; r < r1; r += (int64_t)RL * U) {
+      float v[U][E];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int64_t rr = r + (int64_t)u * RL;
+        load16<T>(x + (rr < r1 ? rr : r1 - 1) * C + cg * E, v[u]);
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (r + (int64_t)u * RL < r1)
+#pragma unroll
+          for (int e = 0; e < E; ++e) acc[e] += v[u][e];
+    }
+  }
+  extern __shared__ float red[];  // [RL][C]
+  if (rl < RL)
+#pragma unroll
+    for (int e = 0; e < E; ++e) red[rl * C + cg * E + e] = acc[e];
+  __syncthreads();
+  for (int c = t; c < C; c += blockDim.x) {
     float s = 0.f;
-#pragma unroll 8
-    for (int64_t r = r0; r < r1; ++r) s += to_f<T>(x[r * C + c]);
+    for (int k = 0; k < RL; ++k) s += red[k * C + c];
     partials[(int64_t)blockIdx.x * C + c] = s;
   }
 }
@@ -315,23 +383,31 @@ __global__ void __launch_bounds__(256) k_fold_grads(FoldGradArgs f) {
 
 }  // namespace
 
+int layernorm_blocks(int64_t N, int C, int dtype, bool bwd) {
+  const int E = dtype == 1 ? 8 : 4;
+  const int rpw = 64 / (C / E);
+  const int64_t per_block = (int64_t)4 * kLnRows * rpw;  // rows per block iteration
+  const int64_t need = (N + per_block - 1) / per_block;
+  const int64_t cap = bwd ? kLnPartials : 2048;
+  return (int)(need < cap ? need : cap);
+}
+
 hipError_t launch_layernorm(const LayerNormArgs& a, int dtype, bool bwd, hipStream_t st) {
   const int E = dtype == 1 ? 8 : 4;
   if (a.C % E || (a.C / E) > 64 || ((a.C / E) & (a.C / E - 1)) || a.N < 1) return hipErrorInvalidValue;
-  const int rpb = 4 * (64 / (a.C / E));  // rows per block-iteration
+  const int blocks = layernorm_blocks(a.N, a.C, dtype, bwd);
+  if (bwd && a.partials && a.blocks != blocks) return hipErrorInvalidValue;
   if (!bwd) {
-    const int64_t blocks = (a.N + rpb - 1) / rpb;
     if (dtype == 1)
-      hipLaunchKernelGGL(k_ln_fwd<bf16>, dim3((unsigned)blocks), dim3(256), 0, st, a);
+      hipLaunchKernelGGL(k_ln_fwd<bf16>, dim3(blocks), dim3(256), 0, st, a);
     else
-      hipLaunchKernelGGL(k_ln_fwd<float>, dim3((unsigned)blocks), dim3(256), 0, st, a);
+      hipLaunchKernelGGL(k_ln_fwd<float>, dim3(blocks), dim3(256), 0, st, a);
   } else {
-    const size_t lds = (size_t)rpb * 2 * a.C * sizeof(float);
-    const int P = a.blocks;
+    const size_t lds = (size_t)4 * (64 / (a.C / E)) * 2 * a.C * sizeof(float);
     if (dtype == 1)
-      hipLaunchKernelGGL(k_ln_bwd<bf16>, dim3(P), dim3(256), lds, st, a);
+      hipLaunchKernelGGL(k_ln_bwd<bf16>, dim3(blocks), dim3(256), lds, st, a);
     else
-      hipLaunchKernelGGL(k_ln_bwd<float>, dim3(P), dim3(256), lds, st, a);
+      hipLaunchKernelGGL(k_ln_bwd<float>, dim3(blocks), dim3(256), lds, st, a);
   }
   return hipGetLastError();
 }
@@ -351,15 +427,19 @@ hipError_t launch_gelu(int64_t n, int dtype, const void* x, const void* dy, void
   return hipGetLastError();
 }
 
+int colsum_blocks(int64_t N) { return (int)(N < kLnPartials ? N : kLnPartials); }
+
 hipError_t launch_colsum(int64_t N, int C, int dtype, const void* x, float* partials, int P,
                          hipStream_t st) {
-  if (N < 1 || C < 1 || P < 1) return hipErrorInvalidValue;
-  const int64_t R = (N + P - 1) / P;
+  const int E = dtype == 1 ? 8 : 4;
+  if (N < 1 || C < E || C % E || C / E > 256 || P != colsum_blocks(N)) return hipErrorInvalidValue;
+  const int64_t R0 = (N + P - 1) / P;
+  const size_t lds = (size_t)(256 / (C / E)) * C * sizeof(float);
   if (dtype == 1)
-    hipLaunchKernelGGL(k_colsum<bf16>, dim3(P), dim3(256), 0, st, N, C, R, (const bf16*)x,
+    hipLaunchKernelGGL(k_colsum<bf16>, dim3(P), dim3(256), lds, st, N, C, R0, (const bf16*)x,
                        partials);
   else
-    hipLaunchKernelGGL(k_colsum<float>, dim3(P), dim3(256), 0, st, N, C, R, (const float*)x,
+    hipLaunchKernelGGL(k_colsum<float>, dim3(P), dim3(256), lds, st, N, C, R0, (const float*)x,
                        partials);
   return hipGetLastError();
 }

@@ -49,7 +49,6 @@ pa_status dtype_ok(int dt) {
 
 hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 
-constexpr int kBlockPartials = 256;  // records of the block stack's sums over rows
 
 // Partial records -> dst segments, added in block order.
 pa_status reduce_to(const float* parts, int P, int64_t rec, float* d0, int64_t l0, float* d1,
@@ -142,7 +141,8 @@ pa_status pa_layernorm_backward(int64_t N, int C, pa_dtype dtype, const void* x,
   PB_TRY(opt(dres, "dres"));
   PB_TRY(need(dx, "dx"));
   const bool sums = dg || db;
-  const size_t need_ws = sums ? (size_t)kBlockPartials * 2 * C * sizeof(float) : 0;
+  const int P = pa::layernorm_blocks(N, C, dtype, true);
+  const size_t need_ws = sums ? (size_t)P * 2 * C * sizeof(float) : 0;
   if (sums && (!ws || ws_bytes < need_ws))
     return err(PA_ERR_WORKSPACE, "pa_layernorm_backward: workspace needs %zu bytes", need_ws);
   pa::LayerNormArgs a;
@@ -150,9 +150,7 @@ pa_status pa_layernorm_backward(int64_t N, int C, pa_dtype dtype, const void* x,
   a.x = x; a.g = g; a.mean = const_cast<float*>(mean); a.rstd = const_cast<float*>(rstd);
   a.dy = dy; a.dres = dres; a.dx = dx;
   a.partials = sums ? reinterpret_cast<float*>(ws) : nullptr;
-  const int64_t P = N < kBlockPartials ? N : kBlockPartials;
-  a.blocks = (int)P;
-  a.rows_per_block = (N + P - 1) / P;
+  a.blocks = P;
   hipStream_t st = as_stream(stream);
   PB_HIP(pa::launch_layernorm(a, dtype, true, st), "layernorm backward");
   if (sums) {
@@ -192,10 +190,12 @@ pa_status pa_gelu_backward(int64_t n, pa_dtype dtype, const void* x, const void*
 pa_status pa_colsum(int64_t N, int C, pa_dtype dtype, const void* x, float* out, void* ws,
                     size_t ws_bytes, void* stream) {
   PB_TRY(dtype_ok(dtype));
-  if (N < 1 || C < 1) return err(PA_ERR_INVALID, "pa_colsum: N, C must be >= 1");
+  const int E = dtype == PA_BF16 ? 8 : 4;
+  if (N < 1 || C < E || C % E || C / E > 256)
+    return err(PA_ERR_INVALID, "pa_colsum: C must be a multiple of %d, at most %d", E, 256 * E);
   PB_TRY(need(x, "x"));
   PB_TRY(need(out, "out"));
-  const int P = (int)(N < kBlockPartials ? N : kBlockPartials);
+  const int P = pa::colsum_blocks(N);
   const size_t need_ws = (size_t)P * C * sizeof(float);
   if (!ws || ws_bytes < need_ws)
     return err(PA_ERR_WORKSPACE, "pa_colsum: workspace needs %zu bytes", need_ws);

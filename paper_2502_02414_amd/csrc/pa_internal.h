@@ -139,7 +139,7 @@ void set_last_error(const char* msg);
 // ---- Block stack (pa_block.hip, pa_gemm.cpp) ----
 // LayerNorm over C channels: forward (s = x + r, optional; y = LN(s);
 // mean/rstd saved) or backward (dx = LN'(dy) + dres; dg/db partial records
-// of 2C floats per block, `blocks` blocks of `rows_per_block` rows).
+// of 2C floats per block, `blocks` = layernorm_blocks(...) of them).
 struct LayerNormArgs {
   int64_t N = 0;
   int C = 0;
@@ -156,10 +156,14 @@ struct LayerNormArgs {
   const void* dres = nullptr;
   void* dx = nullptr;
   float* partials = nullptr;
-  int64_t rows_per_block = 0;
   int blocks = 0;
 };
 hipError_t launch_layernorm(const LayerNormArgs& a, int dtype, bool bwd, hipStream_t st);
+// Blocks (= partial records of the backward) of the LayerNorm launches, and
+// of the column sums; at most kLnPartials records.
+constexpr int kLnPartials = 1024;
+int layernorm_blocks(int64_t N, int C, int dtype, bool bwd);
+int colsum_blocks(int64_t N);
 // out = GELU(x), or out = dy GELU'(x) when dy is given (n a multiple of 16 B).
 hipError_t launch_gelu(int64_t n, int dtype, const void* x, const void* dy, void* out,
                        hipStream_t st);

@@ -17,7 +17,9 @@ Every step is a call of libpa.so (the layer's calls, LayerNorm with the
 residual add fused, GELU, the Project folding, and hipBLASLt GEMMs for the
 MLP, whose second GEMM adds the residual).  torch only allocates the device
 buffers.  Per layer the forward keeps x, LN1(x), x1, LN2(x1), the MLP's
-pre-activation u and the small per-layer state for the backward.
+pre-activation u and GELU(u) (the backward's weight gradient of W2 reads it;
+keeping it costs 2 N 4C bytes per layer and saves recomputing it), and the
+small per-layer state for the backward.
 
 Parameters per layer (dict of device tensors): fp32 ln1_g, ln1_b, Wp [C,C],
 bp [C], A [C,M], b [M], a [C], Wq, bq, Wk, bk, Wv, bv (optional Wo, bo),
@@ -44,7 +46,7 @@ class BlockStack:
         self.dims = B.make_dims(N, C, H, M, tau0, tau_min, eps, self.pdt)
         self.ws = B.workspace(self.dims, device)
         # scratch of the sums over rows (LayerNorm gains, bias gradients) and of hipBLASLt
-        self.ws_rows = torch.empty(256 * 4 * C, dtype=torch.float32, device=device)
+        self.ws_rows = torch.empty(1024 * 4 * C, dtype=torch.float32, device=device)
         self.ws_gemm = torch.empty(64 << 20, dtype=torch.uint8, device=device)
         self.dev = device
 
@@ -98,10 +100,9 @@ class BlockStack:
             x2 = self._e(N, C)
             # x2 = x1 + GELU(u) W2 + b2 (the second residual add in the GEMM)
             self._gemm(gu, p["W2"], x2, bias=p["b2"], beta=1.0, C=x1)
-            del gu
             c.update({"h": h, "m1": m1, "r1": r1, "fold": fo, "num": num, "den": den, "S": S,
                       "S_proj": S_proj, "Sp": Sp, "apr": apr, "x1": x1, "h2": h2, "m2": m2,
-                      "r2": r2, "u": u})
+                      "r2": r2, "u": u, "gu": gu})
             self.caches.append(c)
             x = x2
         return x
@@ -116,8 +117,7 @@ class BlockStack:
             p, c = self.params[l], self.caches[l]
             g = {}
             # MLP: x2 = x1 + GELU(u) W2 + b2
-            gu = self._e(N, 4 * C)
-            B.pa_gelu(c["u"], gu)
+            gu = c.pop("gu")                                       # GELU(u), kept by the forward
             g["dW2"] = self._f(4 * C, C)
             self._gemm(gu, dy, g["dW2"], transA=True)
             g["db2"] = self._f(C)

@@ -85,7 +85,7 @@ def test_layernorm_backward(dt, C):
     B.pa_layernorm(xd, y, mean, rstd, g=dev(g), b=dev(b))
     dx = dev(np.zeros((N, C), np.float32), dt)
     dg, db = torch.empty(C, device="cuda"), torch.empty(C, device="cuda")
-    ws = torch.empty(256 * 2 * C, device="cuda")
+    ws = torch.empty(1024 * 2 * C, device="cuda")
     B.pa_layernorm_backward(xd, mean, rstd, dev(dy, dt), dx, g=dev(g), dres=dev(dres, dt), dg=dg,
                             db=db, ws=ws)
     rdx, rdg, rdb = oracle.layernorm_backward(x, g, dy)
@@ -144,7 +144,7 @@ def test_colsum():
     for dt, (N, C) in (("f32", (5003, 96)), ("bf16", (3001, 1024))):
         x = _rnd(dt, N, C, seed=16)
         out = torch.empty(C, device="cuda")
-        ws = torch.empty(256 * C, device="cuda")
+        ws = torch.empty(1024 * C, device="cuda")
         B.pa_colsum(dev(x, dt), out, ws)
         check(f"colsum {dt}", host(out), x.astype(np.float64).sum(axis=0), 1e-5)
 
