@@ -258,7 +258,14 @@ pa_status pa_time_kernel(const char* call, void* start, void* stop);
  * a residual add when it is another tensor and beta = 1).  The plain GEMMs of the MLP and the linear layers,
  * on hipBLASLt (fp32 accumulation).  The first call on a device creates
  * one hipBLASLt handle there (kept until the process ends); ws/ws_bytes is
- * hipBLASLt's workspace (may be 0).  A combination of dtypes hipBLASLt does
+ * hipBLASLt's workspace (may be 0).  The first call of each problem (shape,
+ * dtypes, transposes, bias) times up to 8 of hipBLASLt's candidate
+ * algorithms on `stream` (it synchronises that stream once) and keeps the
+ * fastest, unless D is also the accumulated input (beta != 0, C = D).
+ * A long reduction into a small fp32 output (transA, K >= 2^17, D at most
+ * 8 MB, beta = 0, no bias: the weight gradients) is split over K into up to
+ * 64 partial products kept at the end of ws (at most half of it) and added
+ * in order, deterministically.  A combination of dtypes hipBLASLt does
  * not serve returns PA_ERR_UNSUPPORTED. */
 pa_status pa_gemm(int transA, int transB, int64_t m, int64_t n, int64_t k, float alpha,
                   const void* A, pa_dtype a_dtype, const void* B, pa_dtype b_dtype,

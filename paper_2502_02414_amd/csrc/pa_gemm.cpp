@@ -11,6 +11,7 @@
 #include <map>
 #include <mutex>
 #include <tuple>
+#include <utility>
 
 #include "pa_internal.h"
 
@@ -36,7 +37,13 @@ hipblasStatus_t handle_for_current_device(hipblasLtHandle_t* h) {
 
 hipDataType hip_type(int dtype) { return dtype == 1 ? HIP_R_16BF : HIP_R_32F; }
 
-// Heuristic choice cached per problem (shape, types, transposes, bias).
+// Algorithm choice cached per problem (shape, types, transposes, bias).
+constexpr int kTune = 8;  // heuristic candidates timed on a problem's first call
+// split-K of long reductions: K >= kSplitMinK, output <= kSplitMaxOut bytes,
+// up to kSplitMax partials of about kSplitRows rows each
+constexpr int64_t kSplitMinK = 1 << 17, kSplitRows = 1 << 14;
+constexpr size_t kSplitMaxOut = 8u << 20;
+constexpr int kSplitMax = 64;
 using Key = std::tuple<int, int, int64_t, int64_t, int64_t, int, int, int, int, bool, int>;
 std::map<Key, hipblasLtMatmulAlgo_t> g_algo;
 
@@ -55,7 +62,10 @@ struct Descs {
 
 }  // namespace
 
-int gemm(const Gemm& g, hipStream_t st) {
+// One hipBLASLt product; batch > 1 runs `batch` products whose operands and
+// outputs are strided by sa, sb, sd elements.
+static int gemm_once(const Gemm& g, int batch, int64_t sa, int64_t sb, int64_t sd,
+                     hipStream_t st) {
   hipblasLtHandle_t h;
   hipblasStatus_t s = handle_for_current_device(&h);
   if (s != HIPBLAS_STATUS_SUCCESS) return (int)s;
@@ -91,11 +101,20 @@ int gemm(const Gemm& g, hipStream_t st) {
   else
     PA_LT(hipblasLtMatrixLayoutCreate(&d.b, hip_type(g.ta), g.k, g.m, g.k));
   PA_LT(hipblasLtMatrixLayoutCreate(&d.d, hip_type(g.td), g.n, g.m, g.n));
+  if (batch > 1) {
+    const int32_t bc = batch;
+    for (auto [lay, stride] : {std::pair{d.a, sb}, std::pair{d.b, sa}, std::pair{d.d, sd}}) {
+      PA_LT(hipblasLtMatrixLayoutSetAttribute(lay, HIPBLASLT_MATRIX_LAYOUT_BATCH_COUNT, &bc,
+                                              sizeof bc));
+      PA_LT(hipblasLtMatrixLayoutSetAttribute(lay, HIPBLASLT_MATRIX_LAYOUT_STRIDED_BATCH_OFFSET,
+                                              &stride, sizeof stride));
+    }
+  }
 
   int dev = 0;
   (void)hipGetDevice(&dev);
   const Key key{dev, (int)g.transA * 2 + (int)g.transB, g.m, g.n, g.k, g.ta, g.tb, g.td,
-                g.beta != 0.f ? 1 : 0, g.bias != nullptr, (int)(g.ws_bytes >> 20)};
+                (g.beta != 0.f ? 1 : 0) + 2 * batch, g.bias != nullptr, (int)(g.ws_bytes >> 20)};
   hipblasLtMatmulAlgo_t algo;
   bool have = false;
   {
@@ -111,11 +130,41 @@ int gemm(const Gemm& g, hipStream_t st) {
     uint64_t wmax = g.ws_bytes;
     PA_LT(hipblasLtMatmulPreferenceSetAttribute(d.pref, HIPBLASLT_MATMUL_PREF_MAX_WORKSPACE_BYTES,
                                                 &wmax, sizeof wmax));
-    hipblasLtMatmulHeuristicResult_t res[1];
+    hipblasLtMatmulHeuristicResult_t res[kTune];
     int n = 0;
-    PA_LT(hipblasLtMatmulAlgoGetHeuristic(h, d.op, d.a, d.b, d.d, d.d, d.pref, 1, res, &n));
-    if (n < 1 || res[0].state != HIPBLAS_STATUS_SUCCESS) return (int)HIPBLAS_STATUS_NOT_SUPPORTED;
-    algo = res[0].algo;
+    PA_LT(hipblasLtMatmulAlgoGetHeuristic(h, d.op, d.a, d.b, d.d, d.d, d.pref, kTune, res, &n));
+    int best = -1;
+    for (int i = 0; i < n && best < 0; ++i)
+      if (res[i].state == HIPBLAS_STATUS_SUCCESS) best = i;
+    if (best < 0) return (int)HIPBLAS_STATUS_NOT_SUPPORTED;
+    // The first call of a problem times the candidates once (synchronising
+    // the stream) and keeps the fastest -- only when rerunning the product
+    // is harmless, i.e. D is not also its accumulated input.
+    const bool rerun_safe = g.beta == 0.f || (g.Cin && g.Cin != g.D);
+    if (rerun_safe && n > 1) {
+      hipEvent_t e0, e1;
+      if (hipEventCreate(&e0) == hipSuccess && hipEventCreate(&e1) == hipSuccess) {
+        const float al = g.alpha, be = g.beta;
+        float best_ms = 1e30f;
+        for (int i = 0; i < n; ++i) {
+          if (res[i].state != HIPBLAS_STATUS_SUCCESS) continue;
+          (void)hipEventRecord(e0, st);
+          const hipblasStatus_t r = hipblasLtMatmul(h, d.op, &al, g.B, d.a, g.A, d.b, &be,
+                                                    g.Cin ? g.Cin : g.D, d.d, g.D, d.d,
+                                                    &res[i].algo, g.ws, g.ws_bytes, st);
+          (void)hipEventRecord(e1, st);
+          float ms = 0.f;
+          if (r == HIPBLAS_STATUS_SUCCESS && hipEventSynchronize(e1) == hipSuccess &&
+              hipEventElapsedTime(&ms, e0, e1) == hipSuccess && ms < best_ms) {
+            best_ms = ms;
+            best = i;
+          }
+        }
+        (void)hipEventDestroy(e0);
+        (void)hipEventDestroy(e1);
+      }
+    }
+    algo = res[best].algo;
     std::lock_guard<std::mutex> lk(g_mu);
     g_algo[key] = algo;
   }
@@ -124,6 +173,51 @@ int gemm(const Gemm& g, hipStream_t st) {
                         g.D, d.d, &algo, g.ws, g.ws_bytes, st));
 #undef PA_LT
   return 0;
+}
+
+int gemm(const Gemm& g, hipStream_t st) {
+  // A long reduction into a small fp32 output -- the weight gradients, op(A)
+  // = X^T with K the points -- is split over K: S strided-batched products
+  // of kc rows each (plus one for the rest) write S fp32 partials at the end
+  // of the workspace, added in order into D by the ordered reduction
+  // (deterministic; the whole GPU works on S times as many output tiles).
+  const size_t part = (size_t)g.m * g.n * sizeof(float);
+  if (g.transA && !g.transB && g.td == 0 && g.beta == 0.f && !g.bias && !g.Cin &&
+      g.k >= kSplitMinK && part <= kSplitMaxOut && g.ws) {
+    int S = (int)(g.k / kSplitRows);
+    S = S < kSplitMax ? S : kSplitMax;
+    while (S >= 2 && (size_t)(S + 1) * part > g.ws_bytes / 2) --S;
+    if (S >= 2) {
+      const int64_t kc = g.k / S / 8 * 8, rest = g.k - kc * S;
+      const int P = S + (rest > 0 ? 1 : 0);
+      const size_t pbytes = ((size_t)P * part + 255) / 256 * 256;
+      char* wsb = reinterpret_cast<char*>(g.ws);
+      float* parts = reinterpret_cast<float*>(wsb + (g.ws_bytes - pbytes) / 256 * 256);
+      Gemm b = g;
+      b.k = kc;
+      b.D = parts;
+      b.ws_bytes = (g.ws_bytes - pbytes) / 256 * 256;
+      const int esa = g.ta == 1 ? 2 : 4, esb = g.tb == 1 ? 2 : 4;
+      int r = gemm_once(b, S, kc * g.m, kc * g.n, g.m * g.n, st);
+      if (r) return r;
+      if (rest > 0) {
+        Gemm t = b;
+        t.k = rest;
+        t.A = reinterpret_cast<const char*>(g.A) + (size_t)S * kc * g.m * esa;
+        t.B = reinterpret_cast<const char*>(g.B) + (size_t)S * kc * g.n * esb;
+        t.D = parts + (size_t)S * g.m * g.n;
+        r = gemm_once(t, 1, 0, 0, 0, st);
+        if (r) return r;
+      }
+      Segments seg{};
+      seg.dst[0] = reinterpret_cast<float*>(g.D);
+      seg.len[0] = g.m * g.n;
+      seg.n = 1;
+      return launch_reduce(parts, P, g.m * g.n, seg, st) == hipSuccess
+                 ? 0 : (int)HIPBLAS_STATUS_EXECUTION_FAILED;
+    }
+  }
+  return gemm_once(g, 1, 0, 0, 0, st);
 }
 
 }  // namespace pa

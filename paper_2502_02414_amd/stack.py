@@ -47,7 +47,7 @@ class BlockStack:
         self.ws = B.workspace(self.dims, device)
         # scratch of the sums over rows (LayerNorm gains, bias gradients) and of hipBLASLt
         self.ws_rows = torch.empty(1024 * 4 * C, dtype=torch.float32, device=device)
-        self.ws_gemm = torch.empty(64 << 20, dtype=torch.uint8, device=device)
+        self.ws_gemm = torch.empty(256 << 20, dtype=torch.uint8, device=device)
         self.dev = device
 
     # -- helpers ------------------------------------------------------------

@@ -115,6 +115,8 @@ GEMMS = [  # m, n, k, transA, transB, in dtype, out dtype, bias, residual
     (1003, 256, 64, False, False, "bf16", "bf16", True, True),
     (256, 64, 3001, True, False, "bf16", "f32", False, False),
     (3001, 64, 256, False, True, "bf16", "bf16", False, False),
+    # a weight-gradient shape long enough for the split over K (18 chunks + a rest)
+    (256, 64, 300001, True, False, "bf16", "f32", False, False),
 ]
 
 
