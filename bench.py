@@ -67,10 +67,16 @@ STREAM_KERNEL = {
 }
 
 
+# The sources the streaming kernels are compiled from (the traffic summary
+# is valid while these are unchanged).
+STREAM_SOURCES = ("pa_device.hpp", "pa_internal.h", "pa_layout.h", "pa_stream.hpp",
+                  "pa_stream_slbwd.hip")
+
+
 def kernel_sources_sha() -> str:
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2502_02414_amd", "csrc")
-    for name in sorted(os.listdir(csrc)):
+    for name in STREAM_SOURCES:
         with open(os.path.join(csrc, name), "rb") as f:
             h.update(name.encode())
             h.update(f.read())
