@@ -326,3 +326,86 @@ def stack_backward(dy, Gs, ps, tau0, tau_min, eps, H, caches, ln_eps=LN_EPS):
         dy, grads[l] = block_backward(dy, Gs[l], ps[l], tau0, tau_min, eps, H, caches[l], ln_eps)
     return dy, grads
 
+
+
+# ---------------------------------------------------------------------------
+# Per-head slicing: the heads of Eq. 2 carried into the slicing of Eq. 1.
+# The C channels split into H contiguous blocks of D = C/H channels.  Head h
+# slices its own block x_h = x[:, hD:(h+1)D] with its own projection A_h
+# [D,M], b_h, Ada-Temp a_h, b_t,h and Gumbel noise G_h [N,M] (Eq. 3, Eq. 4),
+# forms its own M states S_h [M,D] (Eq. 1), runs one-head attention of width
+# D among them with the token projections shared by every head (Eq. 2's
+# Linear acting on the last axis of the [H,M,D] states), and its deslice
+# W_h S'_h fills the channels hD..(h+1)D of y.  Slice parameters may also be
+# shared by every head (A given as [D,M]): then their gradients are the sums
+# over the heads.  G is [H,N,M] or None (the Transolver mode has no noise;
+# with a None as well the temperature is the constant tau0 + b_t).
+# ---------------------------------------------------------------------------
+_SLICE_KEYS = ("A", "b", "a", "b_t")
+_ATTN_KEYS = ("Wq", "bq", "Wk", "bk", "Wv", "bv", "Wo", "bo")
+
+
+def _head_params(p, h, shared):
+    """The layer parameters of head h: its slice parameters (or the shared
+    ones) and the shared token projections."""
+    q = {k: p.get(k) for k in _ATTN_KEYS if p.get(k) is not None}
+    for k in _SLICE_KEYS:
+        v = p.get(k)
+        if v is None:
+            continue
+        if k == "b_t":
+            q[k] = float(v) if shared else float(np.asarray(v, dtype=np.float64)[h])
+        else:
+            q[k] = v if shared else np.asarray(v)[h]
+    return q
+
+
+def heads_shared(p):
+    """True when the slice parameters are one set for every head."""
+    return np.asarray(p["A"]).ndim == 2
+
+
+def heads_layer_forward(x, G, p, tau0, tau_min, eps, H):
+    """Per-head sliced layer forward on x [N,C].  Returns a dict with y [N,C]
+    and "heads", the per-head ``layer_forward`` results (on x_h)."""
+    x = _in(x)
+    N, C = x.shape
+    D = C // H
+    assert D * H == C
+    shared = heads_shared(p)
+    y = np.empty((N, C))
+    heads = []
+    for h in range(H):
+        xh = x[:, h * D:(h + 1) * D]
+        f = layer_forward(xh, None if G is None else G[h], _head_params(p, h, shared), tau0,
+                          tau_min, eps, 1)
+        y[:, h * D:(h + 1) * D] = f["y"]
+        heads.append(f)
+    return {"y": y, "heads": heads}
+
+
+def heads_layer_backward(x, G, p, tau0, tau_min, eps, H, fwd, dY):
+    """Chain rule of ``heads_layer_forward`` for dY [N,C].  Returns dx [N,C],
+    the slice-parameter gradients (per head, stacked on a leading axis of H,
+    or summed when the parameters are shared) and the token-projection
+    gradients summed over the heads."""
+    x, dY = _in(x), _in(dY)
+    N, C = x.shape
+    D = C // H
+    shared = heads_shared(p)
+    dx = np.empty((N, C))
+    per = []
+    for h in range(H):
+        sl = slice(h * D, (h + 1) * D)
+        g = layer_backward(x[:, sl], None if G is None else G[h], _head_params(p, h, shared),
+                           tau0, tau_min, eps, 1, fwd["heads"][h], dY[:, sl])
+        dx[:, sl] = g["dx"]
+        per.append(g)
+    out = {"dx": dx}
+    for k in ("dWq", "dbq", "dWk", "dbk", "dWv", "dbv", "dWo", "dbo", "dtau0"):
+        if k in per[0]:
+            out[k] = sum(g[k] for g in per)
+    for k in ("dA", "db", "da", "db_t"):
+        stacked = np.array([g[k] for g in per])
+        out[k] = stacked.sum(axis=0) if shared else stacked
+    return out
