@@ -113,6 +113,8 @@ def main():
                     help="also run a plain 1 GiB device copy (counter calibration)")
     ap.add_argument("--stack", action="store_true",
                     help="time the 8-block Transolver++ stack at N = 2.5M instead (its own line)")
+    ap.add_argument("--heads", action="store_true",
+                    help="time the per-head sliced layer at N = 1M instead (its own line)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); this build runs the "
@@ -120,6 +122,8 @@ def main():
         sys.exit(2)
     if args.stack:
         return stack_bench(args)
+    if args.heads:
+        return heads_bench(args)
 
     import numpy as np
     import torch
@@ -295,6 +299,95 @@ def stack_bench(args):
         "forward_ms": round(fwd, 2), "backward_ms": round(bwd, 2),
         "mlp_gemm_tflops": round(mlp_flop / (ms * 1e-3) / 1e12, 1),
         "peak_mem_gib": round(torch.cuda.max_memory_allocated() / 2**30, 1),
+    }
+    print(json.dumps(out), flush=True)
+
+
+def heads_bench(args):
+    """Per-head slicing at the million-point car workload's shape: N = 1M,
+    C = 256 as H = 8 heads of D = 32 channels, M = 32 slices per head (each
+    head its own slice parameters and noise), bf16, forward + backward on the
+    head-major tensors [H,N,D] (inputs resident).  The relayout of one [N,C]
+    tensor to or from the head-major layout is timed on its own.  Prints its
+    own JSON line; the headline line is the layer's."""
+    import numpy as np
+    import torch
+    from paper_2502_02414_amd import binding as B
+    from paper_2502_02414_amd import inputs as I
+    from paper_2502_02414_amd.heads import HeadSlicedLayer
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    w = I.WORKLOADS[WORKLOAD]
+    N, C, H, M = w.N, w.C, w.H, w.M
+    D = C // H
+    t0 = time.time()
+    bf = torch.bfloat16
+    to = lambda a, dt=torch.float32: torch.from_numpy(np.ascontiguousarray(a)).cuda().to(dt)
+    x, dY = to(I.make_x(w), bf), to(I.make_grad(w), bf)
+    G = to(I.make_head_gumbel(w), bf)
+    p = I.make_head_params(w)
+    pd = {k: ([float(t) for t in v] if k == "b_t" else to(v, bf if k in ("A", "a") else
+                                                          torch.float32)) for k, v in p.items()}
+    print(f"[bench] per-head inputs generated in {time.time() - t0:.1f}s", file=sys.stderr,
+          flush=True)
+    L = HeadSlicedLayer(N, H, D, M, pd, bf, w.tau0, w.tau_min, w.eps)
+    xh, dYh = L.to_heads(x), L.to_heads(dY)
+    del x, dY
+    steps, warmup = args.steps, args.warmup
+    for _ in range(warmup):
+        L.forward(xh, G)
+        L.backward(dYh)
+    torch.cuda.synchronize()
+    # forward / backward split in a pass of its own (events stay out of the
+    # timed region)
+    ev = [[B.HipEvent() for _ in range(3)] for _ in range(steps)]
+    for s in range(steps):
+        ev[s][0].record()
+        L.forward(xh, G)
+        ev[s][1].record()
+        L.backward(dYh)
+        ev[s][2].record()
+    torch.cuda.synchronize()
+    fwd = sum(e[0].elapsed_ms(e[1]) for e in ev) / steps
+    bwd = sum(e[1].elapsed_ms(e[2]) for e in ev) / steps
+    start, end = B.HipEvent(), B.HipEvent()
+    start.record()
+    for s in range(steps):
+        L.forward(xh, G)
+        L.backward(dYh)
+    end.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_ms(end) / steps
+    # one [N,C] tensor to the head-major layout and back
+    tmp = torch.empty(N, C, dtype=bf, device="cuda")
+    r0, r1 = B.HipEvent(), B.HipEvent()
+    r0.record()
+    for _ in range(steps):
+        B.pa_heads_relayout(xh, tmp, H, to_heads=False)
+        B.pa_heads_relayout(tmp, xh, H, to_heads=True)
+    r1.record()
+    torch.cuda.synchronize()
+    relayout_ms = r0.elapsed_ms(r1) / (2 * steps)
+    bpp = algo_bytes_per_point(D, M, 2, 2)
+    step_bytes = H * N * sum(bpp[n] for n in ("pa_slice_aggregate", "pa_deslice",
+                                              "pa_deslice_backward",
+                                              "pa_slice_aggregate_backward"))
+    gbs = step_bytes / (ms * 1e-3) / 1e9
+    out = {
+        "metric": "mesh points/sec, per-head sliced Physics-Attention layer fwd+bwd at N=1M, "
+                  "C=256 (H=8 heads of D=32), M=32 per head",
+        "value": round(N / (ms * 1e-3), 1), "unit": "points/s", "n_gpus": 1, "steps": steps,
+        "warmup": warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": WORKLOAD + "_per_head", "N": N, "C": C, "H": H, "D": D, "M": M,
+                   "slicing": "per-head", "layout": "head-major [H,N,D]",
+                   "pass": "forward+backward"},
+        "forward_ms": round(fwd, 4), "backward_ms": round(bwd, 4),
+        "step_hbm": {"algo_bytes": step_bytes, "achieved_GBs": round(gbs, 1),
+                     "frac": round(gbs / HBM_PEAK_GBS, 4)},
+        "relayout_ms_per_tensor": round(relayout_ms, 4),
+        "relayout_GBs": round(2 * N * C * 2 / (relayout_ms * 1e-3) / 1e9, 1),
     }
     print(json.dumps(out), flush=True)
 

@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define PA_VERSION 2
+#define PA_VERSION 3
 
 typedef enum { PA_F32 = 0, PA_BF16 = 1 } pa_dtype;
 
@@ -330,6 +330,48 @@ pa_status pa_project_backward(const pa_dims* dims, const float* Wp, const float*
                               const float* A, const float* a, const float* S,
                               const float* dS_proj, const pa_slice_grads* folded, float* dWp,
                               float* dbp, float* dS, const pa_slice_grads* gr, void* stream);
+
+/* ---------------------------------------------------------------------
+ * Per-head slicing: the heads of Eq. 2 carried into the slicing of Eq. 1.
+ * The C channels split into H contiguous blocks of D = C/H.  Head h slices
+ * its own block x_h [N,D] with its own slice parameters and Gumbel noise
+ * [N,M] (Eq. 3, Eq. 4), forms its own M states [M,D] (Eq. 1) and deslices
+ * them into the channels of its block; the token attention is one head of
+ * width D with projections shared by the heads (Eq. 2's Linear acting on
+ * the last axis of the [H,M,D] states).  On the GPU each head runs the
+ * layer's streaming calls above on x_h stored head-major ([H,N,D], dims
+ * with C = D, H = 1), and the token attention of all heads is one
+ * pa_token_attention call (dims with C = H D and H heads) on the heads'
+ * states side by side, [M, H D], with the shared D x D projections on the
+ * block diagonal.  The runner (paper_2502_02414_amd/heads.py) composes
+ * these calls.  Same conventions as above.
+ * --------------------------------------------------------------------- */
+
+/* Moves R rows of H blocks of D elements between the point-major layout
+ * [R,H,D] (= [R, H D]) and the head-major layout [H,R,D]: to_heads = 1
+ * reads src as [R,H,D] and writes dst as [H,R,D], 0 the reverse.  D a
+ * multiple of 16 bytes' worth; src and dst 16-byte aligned and disjoint
+ * (PA_ERR_INVALID otherwise).  A plain copy, bit-exact. */
+pa_status pa_heads_relayout(int64_t R, int H, int D, pa_dtype dtype, int to_heads,
+                            const void* src, void* dst, void* stream);
+
+/* One fp32 parameter shared by the heads, laid out for all H of them:
+ * blockdiag = 1 takes a D x D matrix (L = D) and writes the [H D, H D]
+ * matrix with it in every diagonal block and zeros elsewhere (the token
+ * projection of the H-head call); blockdiag = 0 takes L floats and writes
+ * them H times, [H,L] (a bias).  H L at most 4096 for a matrix; src, dst
+ * 4-byte aligned. */
+pa_status pa_heads_expand(int H, int64_t L, int blockdiag, const float* src, float* dst,
+                          void* stream);
+
+/* The gradient of a parameter shared by the heads, from the H-head
+ * gradient: blockdiag = 1 sums the H diagonal D x D blocks of an [H D, H D]
+ * matrix (L = D; the off-diagonal blocks belong to no parameter);
+ * blockdiag = 0 sums src [H,L] over its first axis (per-head gradients of
+ * a vector or, with L = 1, a scalar).  Added in head order in double
+ * precision, rounded once to fp32. */
+pa_status pa_heads_sum(int H, int64_t L, int blockdiag, const float* src, float* dst,
+                       void* stream);
 
 #ifdef __cplusplus
 }

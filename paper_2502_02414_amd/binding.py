@@ -31,7 +31,7 @@ SYMBOLS = (
     "pa_slice_weights_backward", "pa_time_kernel", "pa_slice_aggregate_w", "pa_deslice_w",
     "pa_deslice_backward_w", "pa_gemm", "pa_layernorm", "pa_layernorm_backward", "pa_gelu",
     "pa_gelu_backward", "pa_colsum", "pa_project_fold", "pa_project_states",
-    "pa_project_backward",
+    "pa_project_backward", "pa_heads_relayout", "pa_heads_expand", "pa_heads_sum",
 )
 
 
@@ -110,6 +110,9 @@ def load(path: str = LIB_PATH):
     lib.pa_project_fold.argtypes = [D, P, P, P, P, P, P, P, P, P, P]
     lib.pa_project_states.argtypes = [D, P, P, P, P, P]
     lib.pa_project_backward.argtypes = [D, P, P, P, P, P, P, SGp, P, P, P, SGp, P]
+    lib.pa_heads_relayout.argtypes = [I64, I32, I32, I32, I32, P, P, P]
+    lib.pa_heads_expand.argtypes = [I32, I64, I32, P, P, P]
+    lib.pa_heads_sum.argtypes = [I32, I64, I32, P, P, P]
     for name in SYMBOLS:
         if name not in ("pa_version", "pa_last_error"):
             getattr(lib, name).restype = ctypes.c_int
@@ -375,3 +378,29 @@ def pa_project_backward(dims, Wp, bp, A, a, S, dS_proj, folded, dWp, dbp, dS, gr
                                       _ptr(S), _ptr(dS_proj), ctypes.byref(folded), _ptr(dWp),
                                       _ptr(dbp), _ptr(dS), ctypes.byref(gr), _stream(stream)))
 
+
+
+# ---- per-head slicing layout (include/pa.h) ----
+def pa_heads_relayout(src, dst, H, to_heads, stream=None):
+    """[R,H,D] -> [H,R,D] (to_heads) or back; src/dst shapes (R, H*D) and
+    (H, R, D), either way round."""
+    if to_heads:
+        R, C = src.shape
+        assert dst.numel() == src.numel()
+    else:
+        R, C = dst.shape
+        assert src.numel() == dst.numel()
+    _check(load().pa_heads_relayout(R, H, C // H, _dt(src), int(bool(to_heads)), _ptr(src),
+                                    _ptr(dst), _stream(stream)))
+
+
+def pa_heads_expand(src, dst, H, blockdiag, stream=None):
+    L = src.shape[0] if blockdiag else src.numel()
+    _check(load().pa_heads_expand(H, L, int(bool(blockdiag)), _ptr(src), _ptr(dst),
+                                  _stream(stream)))
+
+
+def pa_heads_sum(src, dst, H, blockdiag, stream=None):
+    L = dst.shape[0] if blockdiag else dst.numel()
+    _check(load().pa_heads_sum(H, L, int(bool(blockdiag)), _ptr(src), _ptr(dst),
+                               _stream(stream)))

@@ -273,4 +273,47 @@ pa_status pa_project_backward(const pa_dims* dims, const float* Wp, const float*
   return PA_OK;
 }
 
+pa_status pa_heads_relayout(int64_t R, int H, int D, pa_dtype dtype, int to_heads,
+                            const void* src, void* dst, void* stream) {
+  PB_TRY(dtype_ok(dtype));
+  const int E = dtype == PA_BF16 ? 8 : 4;
+  if (R < 1 || H < 1 || D < E || D % E)
+    return err(PA_ERR_INVALID, "pa_heads_relayout: R, H >= 1 and D a positive multiple of %d", E);
+  PB_TRY(need(src, "src"));
+  PB_TRY(need(dst, "dst"));
+  const int64_t bytes = R * H * D * (dtype == PA_BF16 ? 2 : 4);
+  const uintptr_t s0 = (uintptr_t)src, d0 = (uintptr_t)dst;
+  if (s0 < d0 + (uintptr_t)bytes && d0 < s0 + (uintptr_t)bytes)
+    return err(PA_ERR_INVALID, "pa_heads_relayout: src and dst overlap");
+  PB_HIP(pa::launch_heads_relayout(R, H, D, dtype, to_heads ? 1 : 0, src, dst,
+                                   as_stream(stream)), "heads relayout");
+  return PA_OK;
+}
+
+static pa_status heads_small(const char* what, int H, int64_t L, int blockdiag,
+                             const float* src, float* dst) {
+  if (H < 1 || L < 1 || (blockdiag && (int64_t)H * L > 4096))
+    return err(PA_ERR_INVALID, "%s: H, L >= 1 (H L <= 4096 for a block-diagonal matrix)", what);
+  if (!src || !dst) return err(PA_ERR_INVALID, "%s: src and dst are required", what);
+  if (((uintptr_t)src & 3u) || ((uintptr_t)dst & 3u))
+    return err(PA_ERR_INVALID, "%s: src and dst must be 4-byte aligned", what);
+  return PA_OK;
+}
+
+pa_status pa_heads_expand(int H, int64_t L, int blockdiag, const float* src, float* dst,
+                          void* stream) {
+  PB_TRY(heads_small("pa_heads_expand", H, L, blockdiag, src, dst));
+  PB_HIP(pa::launch_heads_expand(H, L, blockdiag ? 1 : 0, src, dst, as_stream(stream)),
+         "heads expand");
+  return PA_OK;
+}
+
+pa_status pa_heads_sum(int H, int64_t L, int blockdiag, const float* src, float* dst,
+                       void* stream) {
+  PB_TRY(heads_small("pa_heads_sum", H, L, blockdiag, src, dst));
+  PB_HIP(pa::launch_heads_sum(H, L, blockdiag ? 1 : 0, src, dst, as_stream(stream)),
+         "heads sum");
+  return PA_OK;
+}
+
 }  // extern "C"

@@ -190,6 +190,15 @@ struct FoldGradArgs {
   float *dbt = nullptr, *dS = nullptr;
 };
 hipError_t launch_fold_grads(const FoldGradArgs& f, hipStream_t st);
+// Per-head slicing layout: [R,H,D] <-> [H,R,D] (D elements a multiple of
+// 16 bytes), a shared fp32 parameter expanded to every head (block-diagonal
+// or tiled) and the sum over the heads.
+hipError_t launch_heads_relayout(int64_t R, int H, int D, int dtype, int to_heads,
+                                 const void* src, void* dst, hipStream_t st);
+hipError_t launch_heads_expand(int H, int64_t L, int blockdiag, const float* src, float* dst,
+                               hipStream_t st);
+hipError_t launch_heads_sum(int H, int64_t L, int blockdiag, const float* src, float* dst,
+                            hipStream_t st);
 // Row-major D[m,n] = alpha op(A) op(B) + beta D (+ bias[n]) on hipBLASLt;
 // dtypes 0 fp32, 1 bf16.  Returns 0 or a hipblasStatus_t.
 struct Gemm {

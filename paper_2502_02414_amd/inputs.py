@@ -435,3 +435,36 @@ def small(name: str, N: int, C: int, H: int, M: int, dtype: str = "f32",
           geometry: str = "normal", seed: int = 7, **kw) -> Workload:
     """An ad-hoc workload (tests, sweeps)."""
     return Workload(name, N, C, H, M, dtype, True, geometry, seed, **kw)
+
+
+def head_workload(w: Workload, head: int) -> Workload:
+    """The workload of head `head` of a per-head sliced layer: D = C/H
+    channels, one head, its own seed (its own slice parameters and noise)."""
+    return dataclasses.replace(w, C=w.C // w.H, H=1, seed=w.seed + 7919 * (head + 1))
+
+
+def make_head_params(w: Workload, shared: bool = False, biases: bool = True,
+                     out_proj: bool = False) -> dict:
+    """Parameters of a per-head sliced layer: the slice parameters of every
+    head stacked on a leading axis of H (A [H,D,M], b [H,M], a [H,D], b_t
+    [H]; each head's from make_params of its head workload), or one set for
+    all heads with ``shared`` (head 0's: A [D,M], b [M], a [D], b_t float),
+    and the token projections Wq, Wk, Wv (Wo) [D,D] with biases [D], shared
+    by the heads (head 0's).  float32, A and a rounded to bf16 for bf16
+    workloads."""
+    hp = [make_params(head_workload(w, h), biases=biases, out_proj=out_proj)
+          for h in range(1 if shared else w.H)]
+    p = {k: v for k, v in hp[0].items() if k not in ("A", "b", "a", "b_t")}
+    if shared:
+        p.update({k: hp[0][k] for k in ("A", "b", "a", "b_t")})
+    else:
+        for k in ("A", "b", "a"):
+            p[k] = np.ascontiguousarray(np.stack([q[k] for q in hp]))
+        p["b_t"] = np.array([q["b_t"] for q in hp], dtype=np.float32)
+    return p
+
+
+def make_head_gumbel(w: Workload, N: Optional[int] = None) -> np.ndarray:
+    """Gumbel noise of every head [H,N,M] (storage dtype values)."""
+    return np.ascontiguousarray(np.stack([make_gumbel(head_workload(w, h), N)
+                                          for h in range(w.H)]))

@@ -32,14 +32,14 @@ def _declared_symbols():
 
 def test_every_declared_symbol_is_exported(lib):
     declared = _declared_symbols()
-    assert len(declared) == 24
+    assert len(declared) == 27
     assert sorted(B.SYMBOLS) == declared
     for name in declared:
         assert hasattr(lib, name), name
 
 
 def test_version(lib):
-    assert lib.pa_version() == 2
+    assert lib.pa_version() == 3
 
 
 def _dims(**kw):
@@ -163,3 +163,32 @@ def test_stored_weights_argument_checks(lib):
                                   FAKE, None, FAKE, n, None)
     assert st == B.PA_ERR_INVALID and "W" in lib.pa_last_error().decode()
 
+
+
+def test_heads_argument_checks(lib):
+    far = FAKE + (1 << 32)
+    # D not a multiple of 16 bytes' worth
+    st = lib.pa_heads_relayout(100, 4, 6, B.PA_F32, 1, FAKE, far, None)
+    assert st == B.PA_ERR_INVALID and "D" in lib.pa_last_error().decode()
+    st = lib.pa_heads_relayout(100, 4, 4, B.PA_BF16, 1, FAKE, far, None)
+    assert st == B.PA_ERR_INVALID
+    # overlapping buffers, misaligned or missing pointers, empty shapes
+    st = lib.pa_heads_relayout(100, 4, 8, B.PA_F32, 0, FAKE, FAKE + 64, None)
+    assert st == B.PA_ERR_INVALID and "overlap" in lib.pa_last_error().decode()
+    st = lib.pa_heads_relayout(100, 4, 8, B.PA_F32, 1, FAKE + 4, far, None)
+    assert st == B.PA_ERR_INVALID and "aligned" in lib.pa_last_error().decode()
+    st = lib.pa_heads_relayout(100, 4, 8, B.PA_F32, 1, None, far, None)
+    assert st == B.PA_ERR_INVALID
+    st = lib.pa_heads_relayout(0, 4, 8, B.PA_F32, 1, FAKE, far, None)
+    assert st == B.PA_ERR_INVALID
+    st = lib.pa_heads_relayout(100, 4, 8, 5, 1, FAKE, far, None)
+    assert st == B.PA_ERR_INVALID
+    # a block-diagonal matrix of more than 4096 rows; empty and misaligned
+    st = lib.pa_heads_expand(64, 128, 1, FAKE, far, None)
+    assert st == B.PA_ERR_INVALID
+    st = lib.pa_heads_sum(0, 4, 0, FAKE, far, None)
+    assert st == B.PA_ERR_INVALID
+    st = lib.pa_heads_sum(2, 4, 0, FAKE + 2, far, None)
+    assert st == B.PA_ERR_INVALID and "aligned" in lib.pa_last_error().decode()
+    st = lib.pa_heads_expand(2, 4, 0, FAKE, None, None)
+    assert st == B.PA_ERR_INVALID
