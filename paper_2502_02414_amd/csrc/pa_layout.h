@@ -92,9 +92,14 @@ struct Geo {
   }
   // the light passes run 8 waves per block with bf16 storage (two waves per
   // SIMD hide each other's latency); the accumulating passes, and fp32
-  // storage (whose tiles take twice the registers), run 4
+  // storage (whose tiles take twice the registers), run 4; rows of 64 bytes
+  // (a head's block of 32 bf16 channels) run 8 in every pass: their tiles
+  // are small in registers and in bytes, so more waves keep more loads in
+  // flight (measured at 8 heads x 1M points: the per-head step -24 %; 16
+  // waves spill the backward's registers)
   static constexpr int max_waves(int pass) {
-    return (pass == kDeslice || pass == kDesliceW || pass == kWeights) && SZ == 2 ? 8 : 4;
+    return C * SZ <= 64 ? 8
+         : (pass == kDeslice || pass == kDesliceW || pass == kWeights) && SZ == 2 ? 8 : 4;
   }
   static constexpr int waves(int pass) {
     return (max_waves(pass) >= 8 && img_bytes(pass) + 8 * wave_bytes(pass) <= kLdsBytes) ? 8

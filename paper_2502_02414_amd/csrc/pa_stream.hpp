@@ -60,10 +60,20 @@ enum Flags { kHasG = 1, kStatesTerm = 2, kDesliceTerm = 4 };
 // Tiles of loads in flight per wave (register stages) in each streaming pass:
 // two for the bf16 deslice with up to 32 slices, whose registers allow it;
 // the aggregating passes stream 32-point tiles there (one stage holds as
-// many points as two).
-template <typename T, int MB, bool BWD> constexpr int agg_depth() { return 1; }
-template <typename T, int MB> constexpr int des_depth() { return sizeof(T) == 2 && MB <= 2 ? 2 : 1; }
-template <typename T, int MB> constexpr int bwd_depth() { return 1; }
+// many points as two).  Rows of 64 bytes (a head's channel block of the
+// per-head slicing, 32 bf16 channels) carry so few bytes per tile that every
+// pass keeps two stages (measured at 8 heads x 1M points: the per-head step
+// -2 %, on top of the 8 waves of narrow rows, Geo::max_waves).
+template <typename T, int C> constexpr bool narrow_rows() { return C * (int)sizeof(T) <= 64; }
+template <typename T, int C, int MB, bool BWD> constexpr int agg_depth() {
+  return narrow_rows<T, C>() ? 2 : 1;
+}
+template <typename T, int C, int MB> constexpr int des_depth() {
+  return narrow_rows<T, C>() || (sizeof(T) == 2 && MB <= 2) ? 2 : 1;
+}
+template <typename T, int C, int MB> constexpr int bwd_depth() {
+  return narrow_rows<T, C>() ? 2 : 1;
+}
 // Cache reuse between the passes of a layer step: the aggregate's loads of
 // x keep their lines in the last-level cache, and the deslice (which reads
 // the same x next) walks its tile ranges backwards, so it starts on the lines
@@ -931,7 +941,7 @@ k_aggregate(StreamArgs a) {
     wave_sync();
     tile_body(t);
   };
-  stream_tiles<agg_depth<T, MB, BWD>(), Stage>(t0, t1, a.N / ROWS, load, store, tile_body, tail,
+  stream_tiles<agg_depth<T, C, MB, BWD>(), Stage>(t0, t1, a.N / ROWS, load, store, tile_body, tail,
                                              init);
 
   // block total in wave 0, written as this block's record: num [M][C]
@@ -1080,7 +1090,7 @@ k_deslice(StreamArgs a) {
     wave_sync();
     body(t);
   };
-  stream_tiles<des_depth<T, MB>(), Stage, kRevDeslice>(t0, t1, a.N / 16, load, store, body, tail,
+  stream_tiles<des_depth<T, C, MB>(), Stage, kRevDeslice>(t0, t1, a.N / 16, load, store, body, tail,
                                                      init);
 }
 
@@ -1426,7 +1436,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
     wave_sync();
     body(t);
   };
-  stream_tiles<bwd_depth<T, MB>(), Stage, kRevSliceBwd>(t0, t1, a.N / 16, load, store, body, tail,
+  stream_tiles<bwd_depth<T, C, MB>(), Stage, kRevSliceBwd>(t0, t1, a.N / 16, load, store, body, tail,
                                                        init);
 
   // lane partials -> wave totals
