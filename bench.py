@@ -115,6 +115,8 @@ def main():
                     help="time the 8-block Transolver++ stack at N = 2.5M instead (its own line)")
     ap.add_argument("--heads", action="store_true",
                     help="time the per-head sliced layer at N = 1M instead (its own line)")
+    ap.add_argument("--head-streams", type=int, default=2,
+                    help="streams the per-head layer spreads its heads over")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); this build runs the "
@@ -331,7 +333,7 @@ def heads_bench(args):
                                                           torch.float32)) for k, v in p.items()}
     print(f"[bench] per-head inputs generated in {time.time() - t0:.1f}s", file=sys.stderr,
           flush=True)
-    L = HeadSlicedLayer(N, H, D, M, pd, bf, w.tau0, w.tau_min, w.eps)
+    L = HeadSlicedLayer(N, H, D, M, pd, bf, w.tau0, w.tau_min, w.eps, streams=args.head_streams)
     xh, dYh = L.to_heads(x), L.to_heads(dY)
     del x, dY
     steps, warmup = args.steps, args.warmup
@@ -382,6 +384,7 @@ def heads_bench(args):
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": WORKLOAD + "_per_head", "N": N, "C": C, "H": H, "D": D, "M": M,
                    "slicing": "per-head", "layout": "head-major [H,N,D]",
+                   "streams": L.ns,
                    "pass": "forward+backward"},
         "forward_ms": round(fwd, 4), "backward_ms": round(bwd, 4),
         "step_hbm": {"algo_bytes": step_bytes, "achieved_GBs": round(gbs, 1),

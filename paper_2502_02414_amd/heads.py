@@ -22,6 +22,13 @@ attention runs over its own M tokens only.  The token gradients are the
 sums of the diagonal blocks (pa_heads_sum).  Every step is a call of
 libpa.so; torch only allocates the device buffers.
 
+Concurrency: the heads of one phase are independent, so they are spread
+over `streams` streams (default priority, forked from and joined back into
+the caller's current stream by events), each with its own workspace: one
+head's small table and reduction kernels then overlap another head's
+streaming pass.  Every head's arithmetic, and the order of its sums, is the
+same on any number of streams.
+
 Parameters (dict of device tensors): A [H,D,M] or [D,M] and a [H,D] or [D]
 in the storage dtype (a nullable), b [H,M] or [M] fp32 (nullable), b_t a
 list of H floats or one float; Wq, Wk, Wv [D,D], bq, bk, bv [D] fp32
@@ -37,7 +44,7 @@ ATTN_B = ("bq", "bk", "bv", "bo")
 
 class HeadSlicedLayer:
     def __init__(self, N, H, D, M, params, dtype, tau0=0.5, tau_min=0.01, eps=1e-5,
-                 device="cuda"):
+                 device="cuda", streams=2):
         import torch
         self.torch = torch
         self.N, self.H, self.D, self.M, self.C = N, H, D, M, H * D
@@ -49,7 +56,9 @@ class HeadSlicedLayer:
             raise ValueError("per-head biases b [H,M] need M to be a multiple of 4")
         self.dims_h = B.make_dims(N, D, 1, M, tau0, tau_min, eps, pdt)
         self.dims_t = B.make_dims(N, H * D, H, M, tau0, tau_min, eps, pdt)
-        self.ws_h = B.workspace(self.dims_h, device)
+        self.ns = max(1, min(int(streams), H))
+        self.ws_h = [B.workspace(self.dims_h, device) for _ in range(self.ns)]
+        self.side = [torch.cuda.Stream(device=device) for _ in range(self.ns - 1)]
         self.ws_t = B.workspace(self.dims_t, device)
         self.set_params(params)
 
@@ -79,6 +88,26 @@ class HeadSlicedLayer:
                 B.pa_heads_expand(p[k], self.att[k], H, blockdiag=False)
         self.ap = B.make_attn_params(**self.att)
 
+    def _heads(self, fn):
+        """fn(h, ws, stream) for every head, head h on stream h mod ns (the
+        current stream and the side streams), joined back into the current
+        stream."""
+        torch = self.torch
+        main = torch.cuda.current_stream()
+        if self.ns > 1:
+            fork = torch.cuda.Event()
+            fork.record(main)
+            for st in self.side:
+                st.wait_event(fork)
+        for h in range(self.H):
+            k = h % self.ns
+            fn(h, self.ws_h[k], main if k == 0 else self.side[k - 1])
+        if self.ns > 1:
+            for st in self.side:
+                done = torch.cuda.Event()
+                done.record(st)
+                main.wait_event(done)
+
     # -- layout helpers -----------------------------------------------------
     def to_heads(self, x):
         """[N,C] -> head-major [H,N,D]."""
@@ -98,9 +127,8 @@ class HeadSlicedLayer:
         H, N, D, M, C = self.H, self.N, self.D, self.M, self.C
         g = (lambda h: None) if G is None else (lambda h: G[h])
         num, den, S_h = self._f(H, M, D), self._f(H, M), self._f(H, M, D)
-        for h in range(H):
-            B.pa_slice_aggregate(self.dims_h, xh[h], g(h), self.sp[h], num[h], den[h], S_h[h],
-                                 self.ws_h)
+        self._heads(lambda h, ws, st: B.pa_slice_aggregate(
+            self.dims_h, xh[h], g(h), self.sp[h], num[h], den[h], S_h[h], ws, stream=st))
         S = self._f(M, C)
         B.pa_heads_relayout(S_h, S, H, to_heads=False)
         Sp = self._f(M, C)
@@ -108,8 +136,8 @@ class HeadSlicedLayer:
         Sp_h = self._f(H, M, D)
         B.pa_heads_relayout(Sp, Sp_h, H, to_heads=True)
         yh = self.torch.empty(H, N, D, dtype=xh.dtype, device=self.dev)
-        for h in range(H):
-            B.pa_deslice(self.dims_h, xh[h], g(h), self.sp[h], Sp_h[h], yh[h], self.ws_h)
+        self._heads(lambda h, ws, st: B.pa_deslice(
+            self.dims_h, xh[h], g(h), self.sp[h], Sp_h[h], yh[h], ws, stream=st))
         self.cache = {"x": xh, "G": G, "num": num, "den": den, "S": S, "Sp_h": Sp_h}
         return yh
 
@@ -124,9 +152,8 @@ class HeadSlicedLayer:
         xh, G = c["x"], c["G"]
         g = (lambda h: None) if G is None else (lambda h: G[h])
         dSp_h = self._f(H, M, D)
-        for h in range(H):
-            B.pa_deslice_backward(self.dims_h, xh[h], g(h), self.sp[h], dYh[h], dSp_h[h],
-                                  self.ws_h)
+        self._heads(lambda h, ws, st: B.pa_deslice_backward(
+            self.dims_h, xh[h], g(h), self.sp[h], dYh[h], dSp_h[h], ws, stream=st))
         dSp = self._f(M, C)
         B.pa_heads_relayout(dSp_h, dSp, H, to_heads=False)
         ag = {"d" + k: self._f(C, C) for k in ATTN_W if k in self.att}
@@ -139,11 +166,10 @@ class HeadSlicedLayer:
         per = {"dA": self._f(H, D, M), "db": self._f(H, M), "da": self._f(H, D),
                "db_t": self._f(H), "dtau0": self._f(H)}
         dxh = self.torch.empty(H, N, D, dtype=xh.dtype, device=self.dev)
-        for h in range(H):
-            gr = B.make_slice_grads(**{k: v[h] for k, v in per.items()})
-            B.pa_slice_aggregate_backward(self.dims_h, xh[h], g(h), self.sp[h], c["num"][h],
-                                          c["den"][h], dS_h[h], c["Sp_h"][h], dYh[h], dxh[h],
-                                          gr, self.ws_h)
+        grs = [B.make_slice_grads(**{k: v[h] for k, v in per.items()}) for h in range(H)]
+        self._heads(lambda h, ws, st: B.pa_slice_aggregate_backward(
+            self.dims_h, xh[h], g(h), self.sp[h], c["num"][h], c["den"][h], dS_h[h],
+            c["Sp_h"][h], dYh[h], dxh[h], grs[h], ws, stream=st))
         grads = {}
         for k in ATTN_W:
             if "d" + k in ag:

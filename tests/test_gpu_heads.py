@@ -83,7 +83,7 @@ def head_case(N, H, D, M, dt, shared, noise, out_proj, geometry="normal", seed=3
     return w, x, G, p, dY
 
 
-def run_gpu(w, N, x, G, p, dY, dt):
+def run_gpu(w, N, x, G, p, dY, dt, streams=2):
     import torch
     from paper_2502_02414_amd.heads import HeadSlicedLayer
     H, D, M = w.H, w.C // w.H, w.M
@@ -98,7 +98,7 @@ def run_gpu(w, N, x, G, p, dY, dt):
         else:
             pd[k] = dev(v)
     L = HeadSlicedLayer(N, H, D, M, pd, torch.bfloat16 if dt == "bf16" else torch.float32,
-                        w.tau0, w.tau_min, w.eps)
+                        w.tau0, w.tau_min, w.eps, streams=streams)
     xh = L.to_heads(dev(x, dt))
     Gd = dev(G, dt) if G is not None else None
     y = L.from_heads(L.forward(xh, Gd))
@@ -156,6 +156,18 @@ def test_heads_layer_parity(dt, N, H, D, M, shared, noise, out_proj):
     w, x, G, p, dY = head_case(N, H, D, M, dt, shared, noise, out_proj)
     out = run_gpu(w, N, x, G, p, dY, dt)
     compare(w, x, G, p, dY, out, dt)
+
+
+def test_heads_streams_bitwise_identical():
+    """The heads of a phase run on several streams; every head's arithmetic
+    and summation order is fixed, so any number of streams gives the same
+    bits."""
+    say("heads layer on 1, 2 and 3 streams: bf16 N=20000 H=8 D=32 M=32")
+    w, x, G, p, dY = head_case(20000, 8, 32, 32, "bf16", False, True, True)
+    outs = [run_gpu(w, 20000, x, G, p, dY, "bf16", streams=k) for k in (1, 2, 3)]
+    for o in outs[1:]:
+        for k, v in outs[0].items():
+            np.testing.assert_array_equal(o[k], v, err_msg=k)
 
 
 def test_heads_layer_full_size_car():
