@@ -55,6 +55,22 @@ def algo_bytes_per_point(C, M, b, g):
     }
 
 
+# Algorithmic MFMA flops per point of each streaming call: the logits
+# contraction (2 C M) plus the call's own contraction over C and M (2 C M);
+# the slice backward has the logits, dw from the deslice term dY S'^T and
+# from the states term x dnum^T, dx = dl A^T + W dnum and dA = x^T dl
+# (12 C M in all); the stored-weights deslice and its backward only their
+# own contraction.
+def algo_flops_per_point(C, M):
+    return {"pa_slice_aggregate": 4 * C * M, "pa_deslice": 4 * C * M,
+            "pa_deslice_backward": 4 * C * M, "pa_slice_aggregate_backward": 12 * C * M,
+            "pa_slice_aggregate_w": 4 * C * M, "pa_deslice_w": 2 * C * M,
+            "pa_deslice_backward_w": 2 * C * M}
+
+
+MFMA_PEAK_TFLOPS = 2500.0   # dense bf16
+
+
 # The streaming kernel each call launches (one per call).
 STREAM_KERNEL = {
     "pa_slice_aggregate": "aggregate",          # k_aggregate, forward
@@ -212,6 +228,11 @@ def main():
                 "traffic": read_traffic(STREAM_KERNEL[dom]), "call": dom,
                 "kernel": STREAM_KERNEL[dom], "algo_bytes_per_launch": dom_bytes,
                 "kernel_ms": round(kernel_ms, 4), "call_ms": round(per_call[dom], 4)}
+    # the same kernel against the dense bf16 MFMA peak (it is HBM-bound)
+    dom_flops = algo_flops_per_point(C, M)[dom] * N
+    tflops = dom_flops / (kernel_ms * 1e-3) / 1e12
+    mfma = {"achieved": round(tflops, 1), "peak": MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(tflops / MFMA_PEAK_TFLOPS, 4), "algo_flops_per_launch": dom_flops}
 
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "points/s", "n_gpus": 1,
@@ -222,6 +243,7 @@ def main():
                    "tau_min": w.tau_min, "storage": "bf16", "accumulate": "fp32",
                    "pass": "forward+backward"},
         "roofline": roofline,
+        "mfma": mfma,
         "step_hbm": {"algo_bytes": step_bytes,
                      "achieved_GBs": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
                      "frac": round(step_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
