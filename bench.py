@@ -132,7 +132,9 @@ def main():
     ap.add_argument("--heads", action="store_true",
                     help="time the per-head sliced layer at N = 1M instead (its own line)")
     ap.add_argument("--head-streams", type=int, default=2,
-                    help="streams the per-head layer spreads its heads over")
+                    help="streams the per-head layer spreads its heads over (one call per head)")
+    ap.add_argument("--head-calls", choices=("batched", "per-head"), default=None,
+                    help="per-head layer: all heads in one launch per kernel, or one call per head")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); this build runs the "
@@ -355,7 +357,8 @@ def heads_bench(args):
                                                           torch.float32)) for k, v in p.items()}
     print(f"[bench] per-head inputs generated in {time.time() - t0:.1f}s", file=sys.stderr,
           flush=True)
-    L = HeadSlicedLayer(N, H, D, M, pd, bf, w.tau0, w.tau_min, w.eps, streams=args.head_streams)
+    L = HeadSlicedLayer(N, H, D, M, pd, bf, w.tau0, w.tau_min, w.eps, streams=args.head_streams,
+                        batched=None if args.head_calls is None else args.head_calls == "batched")
     xh, dYh = L.to_heads(x), L.to_heads(dY)
     del x, dY
     steps, warmup = args.steps, args.warmup
@@ -406,7 +409,7 @@ def heads_bench(args):
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": WORKLOAD + "_per_head", "N": N, "C": C, "H": H, "D": D, "M": M,
                    "slicing": "per-head", "layout": "head-major [H,N,D]",
-                   "streams": L.ns,
+                   "calls": "batched" if L.batched else "per-head", "streams": L.ns,
                    "pass": "forward+backward"},
         "forward_ms": round(fwd, 4), "backward_ms": round(bwd, 4),
         "step_hbm": {"algo_bytes": step_bytes, "achieved_GBs": round(gbs, 1),

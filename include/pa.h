@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define PA_VERSION 3
+#define PA_VERSION 4
 
 typedef enum { PA_F32 = 0, PA_BF16 = 1 } pa_dtype;
 
@@ -372,6 +372,58 @@ pa_status pa_heads_expand(int H, int64_t L, int blockdiag, const float* src, flo
  * precision, rounded once to fp32. */
 pa_status pa_heads_sum(int H, int64_t L, int blockdiag, const float* src, float* dst,
                        void* stream);
+
+/* ---------------------------------------------------------------------
+ * Per-head slicing in one launch per kernel.  The calls below run the
+ * layer's aggregate, deslice, deslice backward and slice backward for all
+ * `heads` heads of a per-head sliced layer together (1 <= heads <= 16):
+ * `dims` describes ONE head (C = D channels, H = 1, M slices per head; M a
+ * multiple of 8), and every per-head tensor is stacked head after head:
+ * x, y, dY, dx [heads][N][D] (dtype), G [heads][N][M] (dtype, nullable),
+ * num, S, Sp, dSp, dS [heads][M][D] and den [heads][M] (fp32), the slice
+ * gradients dA [heads][D][M], db [heads][M], da [heads][D], db_t and
+ * dtau0 [heads] (fp32, *gr pointing at head 0's).  Each head's results are
+ * bit for bit those of the one-head call on its own tensors (same kernels,
+ * same ordered sums).  The workspace holds one one-head workspace per head
+ * (pa_heads_workspace_size).  Errors as in the one-head calls.
+ * --------------------------------------------------------------------- */
+
+/* The heads' slice parameters, stacked: A [heads][D][M] and a [heads][D]
+ * (dtype; a nullable), b [heads][M] and b_t [heads] (fp32 device arrays,
+ * nullable: 0; b_t is added to tau0 in double on the GPU, as
+ * pa_slice_params.b_t_dev, and not validated on the host).  With shared = 1
+ * one set serves every head: A [D][M], a [D], b [M], b_t [1]. */
+typedef struct {
+  const void* A;
+  const float* b;
+  const void* a;
+  const float* b_t;
+  int shared;
+} pa_heads_params;
+
+pa_status pa_heads_workspace_size(const pa_dims* dims, int heads, size_t* bytes);
+
+/* Eq. 1 per head (as pa_slice_aggregate). */
+pa_status pa_heads_slice_aggregate(const pa_dims* dims, int heads, const void* x, const void* G,
+                                   const pa_heads_params* hp, float* num, float* den, float* S,
+                                   void* ws, size_t ws_bytes, void* stream);
+/* The deslice per head (as pa_deslice). */
+pa_status pa_heads_deslice(const pa_dims* dims, int heads, const void* x, const void* G,
+                           const pa_heads_params* hp, const float* Sp, void* y, void* ws,
+                           size_t ws_bytes, void* stream);
+/* Chain rule of the deslice per head (as pa_deslice_backward). */
+pa_status pa_heads_deslice_backward(const pa_dims* dims, int heads, const void* x, const void* G,
+                                    const pa_heads_params* hp, const void* dY, float* dSp,
+                                    void* ws, size_t ws_bytes, void* stream);
+/* Chain rule of Eq. 1, 3 and 4 per head (as pa_slice_aggregate_backward;
+ * the gradients per head, a shared parameter's to be summed over the heads
+ * with pa_heads_sum). */
+pa_status pa_heads_slice_aggregate_backward(const pa_dims* dims, int heads, const void* x,
+                                            const void* G, const pa_heads_params* hp,
+                                            const float* num, const float* den, const float* dS,
+                                            const float* Sp, const void* dY, void* dx,
+                                            const pa_slice_grads* gr, void* ws, size_t ws_bytes,
+                                            void* stream);
 
 #ifdef __cplusplus
 }

@@ -32,6 +32,8 @@ SYMBOLS = (
     "pa_deslice_backward_w", "pa_gemm", "pa_layernorm", "pa_layernorm_backward", "pa_gelu",
     "pa_gelu_backward", "pa_colsum", "pa_project_fold", "pa_project_states",
     "pa_project_backward", "pa_heads_relayout", "pa_heads_expand", "pa_heads_sum",
+    "pa_heads_workspace_size", "pa_heads_slice_aggregate", "pa_heads_deslice",
+    "pa_heads_deslice_backward", "pa_heads_slice_aggregate_backward",
 )
 
 
@@ -58,6 +60,11 @@ class pa_attn_params(ctypes.Structure):
 
 class pa_slice_grads(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in ("dA", "db", "da", "db_t", "dtau0")]
+
+
+class pa_heads_params(ctypes.Structure):
+    _fields_ = [("A", ctypes.c_void_p), ("b", ctypes.c_void_p), ("a", ctypes.c_void_p),
+                ("b_t", ctypes.c_void_p), ("shared", ctypes.c_int)]
 
 
 class pa_attn_grads(ctypes.Structure):
@@ -113,6 +120,13 @@ def load(path: str = LIB_PATH):
     lib.pa_heads_relayout.argtypes = [I64, I32, I32, I32, I32, P, P, P]
     lib.pa_heads_expand.argtypes = [I32, I64, I32, P, P, P]
     lib.pa_heads_sum.argtypes = [I32, I64, I32, P, P, P]
+    HPp = ctypes.POINTER(pa_heads_params)
+    lib.pa_heads_workspace_size.argtypes = [D, I32, ctypes.POINTER(ctypes.c_size_t)]
+    lib.pa_heads_slice_aggregate.argtypes = [D, I32, P, P, HPp, P, P, P, P, S, P]
+    lib.pa_heads_deslice.argtypes = [D, I32, P, P, HPp, P, P, P, S, P]
+    lib.pa_heads_deslice_backward.argtypes = [D, I32, P, P, HPp, P, P, P, S, P]
+    lib.pa_heads_slice_aggregate_backward.argtypes = [D, I32, P, P, HPp, P, P, P, P, P, P, SGp,
+                                                      P, S, P]
     for name in SYMBOLS:
         if name not in ("pa_version", "pa_last_error"):
             getattr(lib, name).restype = ctypes.c_int
@@ -404,3 +418,46 @@ def pa_heads_sum(src, dst, H, blockdiag, stream=None):
     L = dst.shape[0] if blockdiag else dst.numel()
     _check(load().pa_heads_sum(H, L, int(bool(blockdiag)), _ptr(src), _ptr(dst),
                                _stream(stream)))
+
+
+# ---- per-head slicing in one launch per kernel (include/pa.h) ----
+def make_heads_params(A, b=None, a=None, b_t=None, shared=False) -> pa_heads_params:
+    """A [heads,D,M] (or [D,M] with shared) etc.; b_t a device fp32 tensor
+    [heads] (or [1] with shared)."""
+    return pa_heads_params(_ptr(A), _ptr(b), _ptr(a), _ptr(b_t), int(bool(shared)))
+
+
+def pa_heads_workspace_size(dims, heads: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(load().pa_heads_workspace_size(ctypes.byref(dims), heads, ctypes.byref(n)))
+    return n.value
+
+
+def heads_workspace(dims, heads: int, device="cuda"):
+    import torch
+    return torch.empty(pa_heads_workspace_size(dims, heads), dtype=torch.uint8, device=device)
+
+
+def pa_heads_slice_aggregate(dims, heads, x, G, hp, num, den, S, ws, stream=None):
+    _check(load().pa_heads_slice_aggregate(ctypes.byref(dims), heads, _ptr(x), _ptr(G),
+                                           ctypes.byref(hp), _ptr(num), _ptr(den), _ptr(S),
+                                           _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def pa_heads_deslice(dims, heads, x, G, hp, Sp, y, ws, stream=None):
+    _check(load().pa_heads_deslice(ctypes.byref(dims), heads, _ptr(x), _ptr(G), ctypes.byref(hp),
+                                   _ptr(Sp), _ptr(y), _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def pa_heads_deslice_backward(dims, heads, x, G, hp, dY, dSp, ws, stream=None):
+    _check(load().pa_heads_deslice_backward(ctypes.byref(dims), heads, _ptr(x), _ptr(G),
+                                            ctypes.byref(hp), _ptr(dY), _ptr(dSp), _ptr(ws),
+                                            ws.numel(), _stream(stream)))
+
+
+def pa_heads_slice_aggregate_backward(dims, heads, x, G, hp, num, den, dS, Sp, dY, dx, gr, ws,
+                                      stream=None):
+    _check(load().pa_heads_slice_aggregate_backward(
+        ctypes.byref(dims), heads, _ptr(x), _ptr(G), ctypes.byref(hp), _ptr(num), _ptr(den),
+        _ptr(dS), _ptr(Sp), _ptr(dY), _ptr(dx), ctypes.byref(gr), _ptr(ws), ws.numel(),
+        _stream(stream)))

@@ -592,6 +592,218 @@ pa_status pa_slice_aggregate_backward(const pa_dims* dims, const void* x, const 
   return reduce_slice_grads(*dims, L, gr, st);
 }
 
+// ---------------------------------------------------------------------------
+// Per-head batches: `heads` independent layers of one head each (dims: one
+// head), x, G, y, dY, dx, the states and the gradients stacked head after
+// head; head h's table image and partial records in its own copy of the
+// one-head workspace.  Every launch covers all heads (blockIdx.y = head).
+// ---------------------------------------------------------------------------
+namespace {
+struct HeadsCall {
+  int heads = 1;
+  int64_t sx = 0, sg = 0, sMD = 0, sM = 0, sA = 0, sb = 0, sa = 0;  // byte strides
+  int64_t wtot = 0;                                                // workspace per head
+};
+
+pa_status check_heads(const pa_dims* dims, int heads, const void* x, const void* G,
+                      const pa_heads_params* hp, HeadsCall& hc) {
+  PA_TRY(check_dims(dims));
+  const pa_dims& d = *dims;
+  if (heads < 1 || heads > pa::kMaxHeads)
+    return fail(PA_ERR_INVALID, "heads must be in [1, %d] (got %d)", pa::kMaxHeads, heads);
+  if (d.M % 8) return fail(PA_ERR_INVALID, "per-head calls need M a multiple of 8 (got %d)", d.M);
+  if (!hp) return fail(PA_ERR_INVALID, "per-head slice params are NULL");
+  PA_TRY(check_ptr(x, "x", true));
+  PA_TRY(check_ptr(G, "G", false));
+  PA_TRY(check_ptr(hp->A, "A", true));
+  PA_TRY(check_ptr(hp->b, "b", false));
+  PA_TRY(check_ptr(hp->a, "a", false));
+  if (hp->b_t && ((uintptr_t)hp->b_t & 3u)) return fail(PA_ERR_INVALID, "b_t misaligned");
+  const int64_t sz = d.dtype == PA_BF16 ? 2 : 4;
+  hc.heads = heads;
+  hc.sx = d.N * d.C * sz;
+  hc.sg = d.N * d.M * sz;
+  hc.sMD = (int64_t)d.M * d.C * 4;
+  hc.sM = (int64_t)d.M * 4;
+  hc.sA = hp->shared ? 0 : (int64_t)d.C * d.M * sz;
+  hc.sb = hp->shared ? 0 : (int64_t)d.M * 4;
+  hc.sa = hp->shared ? 0 : (int64_t)d.C * sz;
+  hc.wtot = (int64_t)layout_of(d).total;
+  return PA_OK;
+}
+
+pa_status check_heads_ws(const pa_dims& d, int heads, const void* ws, size_t ws_bytes) {
+  const size_t need = layout_of(d).total * (size_t)heads;
+  if (!ws) return fail(PA_ERR_WORKSPACE, "workspace is NULL (need %zu bytes)", need);
+  if (ws_bytes < need)
+    return fail(PA_ERR_WORKSPACE, "workspace too small: %zu < %zu bytes", ws_bytes, need);
+  if (((uintptr_t)ws & (kAlign - 1)) != 0)
+    return fail(PA_ERR_INVALID, "workspace is not %zu-byte aligned", kAlign);
+  return PA_OK;
+}
+
+pa::PrepArgs heads_prep(const pa_dims& d, int pass, const pa_heads_params* hp,
+                        const HeadsCall& hc, void* ws) {
+  pa::PrepArgs p = prep_of(d, pass, nullptr, ws);
+  p.A = hp->A;
+  p.b = hp->b;
+  p.a = hp->a;
+  p.heads = hc.heads;
+  p.hs_A = hc.sA; p.hs_b = hc.sb; p.hs_a = hc.sa;
+  p.hs_Sp = p.hs_num = p.hs_dS = hc.sMD;
+  p.hs_den = hc.sM;
+  p.hs_img = hc.wtot;
+  return p;
+}
+
+pa::StreamLaunch heads_stream(const pa_dims& d, int pass, const void* x, const void* G,
+                              const pa_heads_params* hp, const HeadsCall& hc, void* ws) {
+  pa::StreamLaunch L = stream_of(d, pass, x, G, nullptr, ws);
+  L.heads = hc.heads;
+  L.hs_x = L.hs_dy = L.hs_out = hc.sx;
+  L.hs_g = hc.sg;
+  L.hs_img = L.hs_part = hc.wtot;
+  // tau0 + b_t in double, b_t the head's device scalar (as b_t_dev adds it)
+  L.tb = (double)d.tau0;
+  L.tb_dev = hp->b_t;
+  L.hs_tb = hp->shared ? 0 : 4;
+  return L;
+}
+
+pa::Segments heads_segments(const HeadsCall& hc) {
+  pa::Segments seg{};
+  seg.heads = hc.heads;
+  seg.hs_parts = hc.wtot;
+  return seg;
+}
+}  // namespace
+
+pa_status pa_heads_workspace_size(const pa_dims* dims, int heads, size_t* bytes) {
+  PA_TRY(check_dims(dims));
+  if (heads < 1 || heads > pa::kMaxHeads)
+    return fail(PA_ERR_INVALID, "heads must be in [1, %d] (got %d)", pa::kMaxHeads, heads);
+  if (!bytes) return fail(PA_ERR_INVALID, "bytes is NULL");
+  *bytes = layout_of(*dims).total * (size_t)heads;
+  return PA_OK;
+}
+
+pa_status pa_heads_slice_aggregate(const pa_dims* dims, int heads, const void* x, const void* G,
+                                   const pa_heads_params* hp, float* num, float* den, float* S,
+                                   void* ws, size_t ws_bytes, void* stream) {
+  HeadsCall hc;
+  PA_TRY(check_heads(dims, heads, x, G, hp, hc));
+  PA_TRY(check_ptr(num, "num", true));
+  PA_TRY(check_ptr(den, "den", true));
+  PA_TRY(check_ptr(S, "S", true));
+  PA_TRY(check_pass(*dims, pa::kAggregate));
+  PA_TRY(check_heads_ws(*dims, heads, ws, ws_bytes));
+  hipStream_t st = as_stream(stream);
+  const pa_dims& d = *dims;
+  PA_HIP(pa::launch_prep(heads_prep(d, pa::kAggregate, hp, hc, ws), st), "prep");
+  pa::StreamLaunch L = heads_stream(d, pa::kAggregate, x, G, hp, hc, ws);
+  PA_HIP(run_stream(pa::kAggregate, d, L, st), "per-head slice aggregate");
+  pa::Segments seg = heads_segments(hc);
+  seg.dst[0] = num; seg.len[0] = (int64_t)d.M * d.C; seg.hs_dst[0] = hc.sMD;
+  seg.dst[1] = den; seg.len[1] = d.M; seg.hs_dst[1] = hc.sM;
+  seg.n = 2;
+  seg.S = S; seg.hs_S = hc.sMD;
+  seg.nS = (int64_t)d.M * d.C;
+  seg.den_col = seg.nS;
+  seg.C = d.C;
+  seg.eps = d.eps;
+  PA_HIP(pa::launch_reduce(L.partials, L.P, L.rec, seg, st), "reduce");
+  return PA_OK;
+}
+
+pa_status pa_heads_deslice(const pa_dims* dims, int heads, const void* x, const void* G,
+                           const pa_heads_params* hp, const float* Sp, void* y, void* ws,
+                           size_t ws_bytes, void* stream) {
+  HeadsCall hc;
+  PA_TRY(check_heads(dims, heads, x, G, hp, hc));
+  PA_TRY(check_ptr(Sp, "Sp", true));
+  PA_TRY(check_ptr(y, "y", true));
+  PA_TRY(check_pass(*dims, pa::kDeslice));
+  PA_TRY(check_heads_ws(*dims, heads, ws, ws_bytes));
+  hipStream_t st = as_stream(stream);
+  const pa_dims& d = *dims;
+  pa::PrepArgs p = heads_prep(d, pa::kDeslice, hp, hc, ws);
+  p.Sp = Sp;
+  PA_HIP(pa::launch_prep(p, st), "prep");
+  pa::StreamLaunch L = heads_stream(d, pa::kDeslice, x, G, hp, hc, ws);
+  L.out = y;
+  PA_HIP(run_stream(pa::kDeslice, d, L, st), "per-head deslice");
+  return PA_OK;
+}
+
+pa_status pa_heads_deslice_backward(const pa_dims* dims, int heads, const void* x, const void* G,
+                                    const pa_heads_params* hp, const void* dY, float* dSp,
+                                    void* ws, size_t ws_bytes, void* stream) {
+  HeadsCall hc;
+  PA_TRY(check_heads(dims, heads, x, G, hp, hc));
+  PA_TRY(check_ptr(dY, "dY", true));
+  PA_TRY(check_ptr(dSp, "dSp", true));
+  PA_TRY(check_pass(*dims, pa::kDesliceBwd));
+  PA_TRY(check_heads_ws(*dims, heads, ws, ws_bytes));
+  hipStream_t st = as_stream(stream);
+  const pa_dims& d = *dims;
+  PA_HIP(pa::launch_prep(heads_prep(d, pa::kDesliceBwd, hp, hc, ws), st), "prep");
+  pa::StreamLaunch L = heads_stream(d, pa::kDesliceBwd, x, G, hp, hc, ws);
+  L.dY = dY;
+  PA_HIP(run_stream(pa::kDesliceBwd, d, L, st), "per-head deslice backward");
+  pa::Segments seg = heads_segments(hc);
+  seg.dst[0] = dSp; seg.len[0] = (int64_t)d.M * d.C; seg.hs_dst[0] = hc.sMD;
+  seg.n = 1;
+  PA_HIP(pa::launch_reduce(L.partials, L.P, L.rec, seg, st), "reduce");
+  return PA_OK;
+}
+
+pa_status pa_heads_slice_aggregate_backward(const pa_dims* dims, int heads, const void* x,
+                                            const void* G, const pa_heads_params* hp,
+                                            const float* num, const float* den, const float* dS,
+                                            const float* Sp, const void* dY, void* dx,
+                                            const pa_slice_grads* gr, void* ws, size_t ws_bytes,
+                                            void* stream) {
+  HeadsCall hc;
+  PA_TRY(check_heads(dims, heads, x, G, hp, hc));
+  PA_TRY(check_ptr(dS, "dS", false));
+  PA_TRY(check_ptr(Sp, "Sp", false));
+  PA_TRY(check_ptr(dY, "dY", false));
+  PA_TRY(check_ptr(dx, "dx", true));
+  if ((Sp == nullptr) != (dY == nullptr))
+    return fail(PA_ERR_INVALID, "Sp and dY must both be given or both be NULL");
+  if (dS) {
+    PA_TRY(check_ptr(num, "num", true));
+    PA_TRY(check_ptr(den, "den", true));
+  }
+  PA_TRY(check_grads(gr));
+  PA_TRY(check_pass(*dims, pa::kSliceBwd));
+  PA_TRY(check_heads_ws(*dims, heads, ws, ws_bytes));
+  hipStream_t st = as_stream(stream);
+  const pa_dims& d = *dims;
+  pa::PrepArgs p = heads_prep(d, pa::kSliceBwd, hp, hc, ws);
+  p.num = num;
+  p.den = den;
+  p.dS = dS;
+  p.Sp = Sp;
+  PA_HIP(pa::launch_prep(p, st), "prep");
+  pa::StreamLaunch L = heads_stream(d, pa::kSliceBwd, x, G, hp, hc, ws);
+  L.dY = dY;
+  L.out = dx;
+  L.states = dS != nullptr;
+  L.deslice = Sp != nullptr;
+  PA_HIP(run_stream(pa::kSliceBwd, d, L, st), "per-head slice backward");
+  if (!gr) return PA_OK;
+  pa::Segments seg = heads_segments(hc);
+  seg.dst[0] = gr->dA; seg.len[0] = (int64_t)d.C * d.M; seg.hs_dst[0] = (int64_t)d.C * d.M * 4;
+  seg.dst[1] = gr->db; seg.len[1] = d.M; seg.hs_dst[1] = (int64_t)d.M * 4;
+  seg.dst[2] = gr->da; seg.len[2] = d.C; seg.hs_dst[2] = (int64_t)d.C * 4;
+  seg.dst[3] = gr->db_t; seg.dst2[3] = gr->dtau0; seg.len[3] = 1;  // d tau0 = d b_t
+  seg.hs_dst[3] = seg.hs_dst2[3] = 4;
+  seg.n = 4;
+  PA_HIP(pa::launch_reduce(L.partials, L.P, L.rec, seg, st), "reduce");
+  return PA_OK;
+}
+
 pa_status pa_slice_weights_backward(const pa_dims* dims, const void* x, const void* G,
                                     const pa_slice_params* sp, const float* dW,
                                     const float* dtau, void* dx, const pa_slice_grads* gr,

@@ -8,6 +8,10 @@
 
 namespace pa {
 
+// Heads of one batched per-head call (pa_heads_*): head h = blockIdx.y of
+// every launch, its tensors at fixed byte strides from head 0's.
+constexpr int kMaxHeads = 16;
+
 struct StreamLaunch {
   const void* x = nullptr;
   const void* G = nullptr;
@@ -27,6 +31,10 @@ struct StreamLaunch {
   float tau_min = 0.f;
   bool states = false;
   bool deslice = false;
+  // per-head batch: heads (gridDim.y), byte strides of x, G, dY, out, the
+  // table image, the partial records and tb_dev (each head's b_t)
+  int heads = 1;
+  int64_t hs_x = 0, hs_g = 0, hs_dy = 0, hs_out = 0, hs_img = 0, hs_part = 0, hs_tb = 0;
 };
 
 // Streaming passes (pass = pa::Pass).  dtype: 0 fp32, 1 bf16.
@@ -49,6 +57,9 @@ struct PrepArgs {
   const float* den = nullptr; // [M]
   const float* dS = nullptr;  // [M,C]
   void* img = nullptr;
+  // per-head batch: heads (gridDim.y) and byte strides (0: shared by heads)
+  int heads = 1;
+  int64_t hs_A = 0, hs_b = 0, hs_a = 0, hs_Sp = 0, hs_num = 0, hs_den = 0, hs_dS = 0, hs_img = 0;
 };
 hipError_t launch_prep(const PrepArgs& p, hipStream_t st);
 // Bytes of the table image of a pass.
@@ -68,6 +79,10 @@ struct Segments {
   int64_t nS, den_col;
   int C;
   float eps;
+  // per-head batch (heads < 2: one): byte strides of the partial records,
+  // the destinations and S
+  int heads;
+  int64_t hs_parts, hs_dst[6], hs_dst2[6], hs_S;
 };
 hipError_t launch_reduce(const float* partials, int P, int64_t rec, const Segments& seg,
                          hipStream_t st);

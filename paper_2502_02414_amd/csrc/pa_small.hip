@@ -7,6 +7,8 @@
 //     sums of Section 4.2, here over point chunks of one GPU);
 //     with the states s_j = num_j / max(den_j, eps) (Eq. 1) formed there;
 // (token attention lives in pa_tokens.hip).
+#include <type_traits>
+
 #include "pa_device.hpp"
 #include "pa_internal.h"
 #include "pa_layout.h"
@@ -152,9 +154,27 @@ __device__ __forceinline__ void prep_deslice_table(const PrepGeo& g, const PrepA
   }
 }
 
+// A per-head batch builds head blockIdx.y's image from its parameters and
+// states at the batch's byte strides (a stride of 0: shared by the heads).
+template <typename Q>
+__device__ __forceinline__ Q* head_at(Q* q, int64_t stride) {
+  using B = typename std::conditional<std::is_const<Q>::value, const char*, char*>::type;
+  return q ? reinterpret_cast<Q*>(reinterpret_cast<B>(q) + (int64_t)blockIdx.y * stride) : q;
+}
+
 template <typename T>
 __global__ void __launch_bounds__(256) k_prep(PrepGeo g, PrepArgs p) {
   __shared__ float red[256];
+  if (gridDim.y > 1) {
+    p.A = head_at(p.A, p.hs_A);
+    p.b = head_at(p.b, p.hs_b);
+    p.a = head_at(p.a, p.hs_a);
+    p.Sp = head_at(p.Sp, p.hs_Sp);
+    p.num = head_at(p.num, p.hs_num);
+    p.den = head_at(p.den, p.hs_den);
+    p.dS = head_at(p.dS, p.hs_dS);
+    p.img = head_at(p.img, p.hs_img);
+  }
   const bool back = p.pass == kSliceBwd || p.pass == kWeightsBwd;
   const int nback = back ? g.M + (2 * g.C + 255) / 256 : 0;
   if ((int)blockIdx.x < nback) {
@@ -199,11 +219,12 @@ hipError_t launch_prep(const PrepArgs& p, hipStream_t st) {
   if (p.pass == kSliceBwd && p.dS && (!p.num || !p.den)) return hipErrorInvalidValue;
   PrepGeo g = prep_geo(p.dtype, p.C, p.M, p.MB);
   const bool back = p.pass == kSliceBwd || p.pass == kWeightsBwd;
+  if (p.heads < 1 || p.heads > kMaxHeads) return hipErrorInvalidValue;
   const int blocks = 64 + (back ? p.M + (2 * p.C + 255) / 256 : 0);
   if (p.dtype == 1)
-    hipLaunchKernelGGL(k_prep<bf16>, dim3(blocks), dim3(256), 0, st, g, p);
+    hipLaunchKernelGGL(k_prep<bf16>, dim3(blocks, p.heads), dim3(256), 0, st, g, p);
   else
-    hipLaunchKernelGGL(k_prep<float>, dim3(blocks), dim3(256), 0, st, g, p);
+    hipLaunchKernelGGL(k_prep<float>, dim3(blocks, p.heads), dim3(256), 0, st, g, p);
   return hipGetLastError();
 }
 
@@ -227,9 +248,14 @@ __global__ void k_reduce(const float* __restrict__ parts, int P, int64_t rec, Se
   // (16 columns of one slice j, as 16 divides C) also forms den_j, in the
   // same order as den_j's own block, for the states.
   __shared__ double sh[17][16];
+  // head blockIdx.y of a per-head batch (0 otherwise): its records and
+  // destinations at the batch's strides, applied where they are used (the
+  // argument struct is only read: writing its arrays would copy it to scratch)
+  parts = head_at(parts, seg.hs_parts);
+  float* const S = head_at(seg.S, seg.hs_S);
   const int kk = threadIdx.x & 15, pg = threadIdx.x >> 4;
   const int64_t k0 = (int64_t)blockIdx.x * 16, k = k0 + kk;
-  const bool states = seg.S != nullptr && k0 < seg.nS;
+  const bool states = S != nullptr && k0 < seg.nS;
   double acc = 0.0;
   if (k < rec) {
 #pragma unroll 8
@@ -249,15 +275,15 @@ __global__ void k_reduce(const float* __restrict__ parts, int P, int64_t rec, Se
     int64_t off = k;
     for (int i = 0; i < seg.n; ++i) {
       if (off < seg.len[i]) {
-        if (seg.dst[i]) seg.dst[i][off] = tot;
-        if (seg.dst2[i]) seg.dst2[i][off] = tot;
+        if (seg.dst[i]) head_at(seg.dst[i], seg.hs_dst[i])[off] = tot;
+        if (seg.dst2[i]) head_at(seg.dst2[i], seg.hs_dst2[i])[off] = tot;
         break;
       }
       off -= seg.len[i];
     }
     if (states && k < seg.nS) {
       const float den = group_total(sh[16]);
-      seg.S[k] = tot / (den >= seg.eps ? den : seg.eps);
+      S[k] = tot / (den >= seg.eps ? den : seg.eps);
     }
   }
 }
@@ -268,8 +294,10 @@ hipError_t launch_reduce(const float* partials, int P, int64_t rec, const Segmen
   if (seg.S && (seg.C < 16 || seg.C % 16 || seg.nS > rec || seg.den_col < 0 ||
                 seg.den_col + seg.nS / seg.C > rec))
     return hipErrorInvalidValue;
+  const int heads = seg.heads > 1 ? seg.heads : 1;
+  if (heads > kMaxHeads) return hipErrorInvalidValue;
   const int blocks = (int)((rec + 15) / 16);
-  hipLaunchKernelGGL(k_reduce, dim3(blocks), dim3(256), 0, st, partials, P, rec, seg);
+  hipLaunchKernelGGL(k_reduce, dim3(blocks, heads), dim3(256), 0, st, partials, P, rec, seg);
   return hipGetLastError();
 }
 

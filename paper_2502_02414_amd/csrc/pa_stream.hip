@@ -41,6 +41,10 @@ hipError_t launch_stream(int pass, int dtype, int C, int MB, const StreamLaunch&
   a.dW = L.dW; a.dtau = L.dtau; a.partials = L.partials; a.N = L.N; a.M = L.M; a.rec = L.rec;
   a.tb = L.tb; a.tb_dev = L.tb_dev; a.tau_min = L.tau_min;
   a.flags = (L.G ? kHasG : 0) | (L.states ? kStatesTerm : 0) | (L.deslice ? kDesliceTerm : 0);
+  if (L.heads < 1 || L.heads > kMaxHeads) return hipErrorInvalidValue;
+  a.heads = L.heads;
+  a.hs_x = L.hs_x; a.hs_g = L.hs_g; a.hs_dy = L.hs_dy; a.hs_out = L.hs_out;
+  a.hs_img = L.hs_img; a.hs_part = L.hs_part; a.hs_tb = L.hs_tb;
   switch (pass) {
     case kAggregate: return launch_aggregate_pass(dtype, C, MB, a, L.P, st);
     case kDeslice: return launch_deslice_pass(dtype, C, MB, a, L.P, st);

@@ -30,6 +30,8 @@
 // P records in block order.
 #pragma once
 
+#include <type_traits>
+
 #include "pa_device.hpp"
 #include "pa_internal.h"
 #include "pa_layout.h"
@@ -53,6 +55,9 @@ struct StreamArgs {
   const float* tb_dev;   // nullable: a device scalar added to tb
   float tau_min;
   int flags;
+  // per-head batch (see StreamLaunch)
+  int heads;
+  int64_t hs_x, hs_g, hs_dy, hs_out, hs_img, hs_part, hs_tb;
 };
 
 enum Flags { kHasG = 1, kStatesTerm = 2, kDesliceTerm = 4 };
@@ -83,6 +88,27 @@ template <typename T, int C, int MB> constexpr int bwd_depth() {
 // than their successors gained).
 constexpr bool kRevDeslice = true, kRevSliceBwd = false;
 template <int PASS> constexpr bool keep_loads() { return PASS == kAggregate; }
+
+// A per-head batch runs head blockIdx.y: its tensors at the batch's byte
+// strides, its b_t the device scalar at tb_dev's stride (one head: nothing
+// changes).  Only pointers move: an array among the by-value arguments would
+// send them all to scratch.
+template <typename P>
+__device__ __forceinline__ P head_ptr(P p, int64_t stride) {
+  using B = typename std::conditional<std::is_const<typename std::remove_pointer<P>::type>::value,
+                                      const char*, char*>::type;
+  return p ? reinterpret_cast<P>(reinterpret_cast<B>(p) + (int64_t)blockIdx.y * stride) : p;
+}
+__device__ __forceinline__ void head_offsets(StreamArgs& a) {
+  if (gridDim.y == 1) return;
+  a.x = head_ptr(a.x, a.hs_x);
+  a.G = head_ptr(a.G, a.hs_g);
+  a.dY = head_ptr(a.dY, a.hs_dy);
+  a.out = head_ptr(a.out, a.hs_out);
+  a.img = head_ptr(a.img, a.hs_img);
+  a.partials = head_ptr(a.partials, a.hs_part);
+  a.tb_dev = head_ptr(a.tb_dev, a.hs_tb);
+}
 
 // The temperature constant: tau0 + b_t, plus the device scalar when one is
 // given (a folded Project step's bias term, computed on the GPU).
@@ -785,6 +811,7 @@ k_aggregate(StreamArgs a) {
   constexpr int SZ = (int)sizeof(T);
   using V = typename LAcc<T, true>::v;
   extern __shared__ __attribute__((aligned(16))) char smem[];
+  head_offsets(a);
   add_tb_dev(a);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r = lane_id() & 15, g = lane_id() >> 4;
@@ -985,6 +1012,7 @@ k_deslice(StreamArgs a) {
   constexpr int WAVES = G_::waves(PASS);
   constexpr int SZ = (int)sizeof(T);
   extern __shared__ __attribute__((aligned(16))) char smem[];
+  head_offsets(a);
   add_tb_dev(a);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r = lane_id() & 15, g = lane_id() >> 4;
@@ -1102,6 +1130,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kWeights)))
   using G_ = Geo<sizeof(T), C, MB>;
   constexpr int WAVES = G_::waves(kWeights);
   extern __shared__ __attribute__((aligned(16))) char smem[];
+  head_offsets(a);
   add_tb_dev(a);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r = lane_id() & 15, g = lane_id() >> 4;
@@ -1182,6 +1211,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
   constexpr int SZ = (int)sizeof(T);
   constexpr int SROWF = M16 + 1;  // dl transpose row stride (floats)
   extern __shared__ __attribute__((aligned(16))) char smem[];
+  head_offsets(a);
   add_tb_dev(a);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r = lane_id() & 15, g = lane_id() >> 4;
@@ -1498,22 +1528,23 @@ static hipError_t launch_t(const StreamArgs& a, int P, hipStream_t st) {
   } else {
     const int threads = 64 * G_::waves(PASS);
     const size_t lds = (size_t)G_::lds_bytes(PASS);
+    const dim3 grid(P, a.heads);
     if constexpr (PASS == kAggregate)
-      hipLaunchKernelGGL((k_aggregate<T, C, MB, false>), dim3(P), dim3(threads), lds, st, a);
+      hipLaunchKernelGGL((k_aggregate<T, C, MB, false>), grid, dim3(threads), lds, st, a);
     else if constexpr (PASS == kAggregateW)
-      hipLaunchKernelGGL((k_aggregate<T, C, MB, false, true>), dim3(P), dim3(threads), lds, st, a);
+      hipLaunchKernelGGL((k_aggregate<T, C, MB, false, true>), grid, dim3(threads), lds, st, a);
     else if constexpr (PASS == kDesliceBwd)
-      hipLaunchKernelGGL((k_aggregate<T, C, MB, true>), dim3(P), dim3(threads), lds, st, a);
+      hipLaunchKernelGGL((k_aggregate<T, C, MB, true>), grid, dim3(threads), lds, st, a);
     else if constexpr (PASS == kDesliceBwdW)
-      hipLaunchKernelGGL((k_aggregate<T, C, MB, true, true>), dim3(P), dim3(threads), lds, st, a);
+      hipLaunchKernelGGL((k_aggregate<T, C, MB, true, true>), grid, dim3(threads), lds, st, a);
     else if constexpr (PASS == kDeslice)
-      hipLaunchKernelGGL((k_deslice<T, C, MB>), dim3(P), dim3(threads), lds, st, a);
+      hipLaunchKernelGGL((k_deslice<T, C, MB>), grid, dim3(threads), lds, st, a);
     else if constexpr (PASS == kDesliceW)
-      hipLaunchKernelGGL((k_deslice<T, C, MB, true>), dim3(P), dim3(threads), lds, st, a);
+      hipLaunchKernelGGL((k_deslice<T, C, MB, true>), grid, dim3(threads), lds, st, a);
     else if constexpr (PASS == kWeights)
-      hipLaunchKernelGGL((k_weights<T, C, MB>), dim3(P), dim3(threads), lds, st, a);
+      hipLaunchKernelGGL((k_weights<T, C, MB>), grid, dim3(threads), lds, st, a);
     else
-      hipLaunchKernelGGL((k_slice_bwd<T, C, MB, PASS>), dim3(P), dim3(threads), lds, st, a);
+      hipLaunchKernelGGL((k_slice_bwd<T, C, MB, PASS>), grid, dim3(threads), lds, st, a);
     return hipGetLastError();
   }
 }

@@ -22,12 +22,15 @@ attention runs over its own M tokens only.  The token gradients are the
 sums of the diagonal blocks (pa_heads_sum).  Every step is a call of
 libpa.so; torch only allocates the device buffers.
 
-Concurrency: the heads of one phase are independent, so they are spread
-over `streams` streams (default priority, forked from and joined back into
-the caller's current stream by events), each with its own workspace: one
-head's small table and reduction kernels then overlap another head's
+Launches: by default (M a multiple of 8, at most 16 heads) each phase is
+ONE pa_heads_* call, whose table, streaming and reduction kernels each cover
+all heads in one launch (the head is the grid's second index).  Otherwise
+(or with batched=False) each head makes its own one-head call, and the heads
+of a phase are spread over `streams` streams (default priority, forked from
+and joined back into the caller's current stream by events), each with its
+own workspace, so that one head's small kernels overlap another head's
 streaming pass.  Every head's arithmetic, and the order of its sums, is the
-same on any number of streams.
+same either way: the results are the same bits.
 
 Parameters (dict of device tensors): A [H,D,M] or [D,M] and a [H,D] or [D]
 in the storage dtype (a nullable), b [H,M] or [M] fp32 (nullable), b_t a
@@ -44,7 +47,7 @@ ATTN_B = ("bq", "bk", "bv", "bo")
 
 class HeadSlicedLayer:
     def __init__(self, N, H, D, M, params, dtype, tau0=0.5, tau_min=0.01, eps=1e-5,
-                 device="cuda", streams=2):
+                 device="cuda", streams=2, batched=None):
         import torch
         self.torch = torch
         self.N, self.H, self.D, self.M, self.C = N, H, D, M, H * D
@@ -56,8 +59,13 @@ class HeadSlicedLayer:
             raise ValueError("per-head biases b [H,M] need M to be a multiple of 4")
         self.dims_h = B.make_dims(N, D, 1, M, tau0, tau_min, eps, pdt)
         self.dims_t = B.make_dims(N, H * D, H, M, tau0, tau_min, eps, pdt)
-        self.ns = max(1, min(int(streams), H))
-        self.ws_h = [B.workspace(self.dims_h, device) for _ in range(self.ns)]
+        self.batched = (M % 8 == 0 and H <= 16) if batched is None else bool(batched)
+        if self.batched and (M % 8 or H > 16):
+            raise ValueError("batched per-head calls need M a multiple of 8 and H <= 16")
+        self.ws_b = B.heads_workspace(self.dims_h, H, device) if self.batched else None
+        self.ns = 1 if self.batched else max(1, min(int(streams), H))
+        self.ws_h = [] if self.batched else [B.workspace(self.dims_h, device)
+                                             for _ in range(self.ns)]
         self.side = [torch.cuda.Stream(device=device) for _ in range(self.ns - 1)]
         self.ws_t = B.workspace(self.dims_t, device)
         self.set_params(params)
@@ -77,6 +85,12 @@ class HeadSlicedLayer:
                 (lambda k: None if p.get(k) is None else p[k][h])
             b_t = float(bt) if self.shared or isinstance(bt, (int, float)) else float(bt[h])
             self.sp.append(B.make_slice_params(pick("A"), pick("b"), pick("a"), b_t))
+        bts = [float(bt)] if self.shared or isinstance(bt, (int, float)) else [float(v) for v in bt]
+        if not self.shared and len(bts) == 1:
+            bts = bts * H
+        self.bt_dev = self.torch.tensor(bts, dtype=self.torch.float32, device=self.dev)
+        self.hp = B.make_heads_params(p["A"], p.get("b"), p.get("a"), self.bt_dev,
+                                      shared=self.shared)
         self.att = {}
         for k in ATTN_W:
             if p.get(k) is not None:
@@ -127,8 +141,11 @@ class HeadSlicedLayer:
         H, N, D, M, C = self.H, self.N, self.D, self.M, self.C
         g = (lambda h: None) if G is None else (lambda h: G[h])
         num, den, S_h = self._f(H, M, D), self._f(H, M), self._f(H, M, D)
-        self._heads(lambda h, ws, st: B.pa_slice_aggregate(
-            self.dims_h, xh[h], g(h), self.sp[h], num[h], den[h], S_h[h], ws, stream=st))
+        if self.batched:
+            B.pa_heads_slice_aggregate(self.dims_h, H, xh, G, self.hp, num, den, S_h, self.ws_b)
+        else:
+            self._heads(lambda h, ws, st: B.pa_slice_aggregate(
+                self.dims_h, xh[h], g(h), self.sp[h], num[h], den[h], S_h[h], ws, stream=st))
         S = self._f(M, C)
         B.pa_heads_relayout(S_h, S, H, to_heads=False)
         Sp = self._f(M, C)
@@ -136,8 +153,11 @@ class HeadSlicedLayer:
         Sp_h = self._f(H, M, D)
         B.pa_heads_relayout(Sp, Sp_h, H, to_heads=True)
         yh = self.torch.empty(H, N, D, dtype=xh.dtype, device=self.dev)
-        self._heads(lambda h, ws, st: B.pa_deslice(
-            self.dims_h, xh[h], g(h), self.sp[h], Sp_h[h], yh[h], ws, stream=st))
+        if self.batched:
+            B.pa_heads_deslice(self.dims_h, H, xh, G, self.hp, Sp_h, yh, self.ws_b)
+        else:
+            self._heads(lambda h, ws, st: B.pa_deslice(
+                self.dims_h, xh[h], g(h), self.sp[h], Sp_h[h], yh[h], ws, stream=st))
         self.cache = {"x": xh, "G": G, "num": num, "den": den, "S": S, "Sp_h": Sp_h}
         return yh
 
@@ -152,8 +172,11 @@ class HeadSlicedLayer:
         xh, G = c["x"], c["G"]
         g = (lambda h: None) if G is None else (lambda h: G[h])
         dSp_h = self._f(H, M, D)
-        self._heads(lambda h, ws, st: B.pa_deslice_backward(
-            self.dims_h, xh[h], g(h), self.sp[h], dYh[h], dSp_h[h], ws, stream=st))
+        if self.batched:
+            B.pa_heads_deslice_backward(self.dims_h, H, xh, G, self.hp, dYh, dSp_h, self.ws_b)
+        else:
+            self._heads(lambda h, ws, st: B.pa_deslice_backward(
+                self.dims_h, xh[h], g(h), self.sp[h], dYh[h], dSp_h[h], ws, stream=st))
         dSp = self._f(M, C)
         B.pa_heads_relayout(dSp_h, dSp, H, to_heads=False)
         ag = {"d" + k: self._f(C, C) for k in ATTN_W if k in self.att}
@@ -166,10 +189,15 @@ class HeadSlicedLayer:
         per = {"dA": self._f(H, D, M), "db": self._f(H, M), "da": self._f(H, D),
                "db_t": self._f(H), "dtau0": self._f(H)}
         dxh = self.torch.empty(H, N, D, dtype=xh.dtype, device=self.dev)
-        grs = [B.make_slice_grads(**{k: v[h] for k, v in per.items()}) for h in range(H)]
-        self._heads(lambda h, ws, st: B.pa_slice_aggregate_backward(
-            self.dims_h, xh[h], g(h), self.sp[h], c["num"][h], c["den"][h], dS_h[h],
-            c["Sp_h"][h], dYh[h], dxh[h], grs[h], ws, stream=st))
+        if self.batched:
+            B.pa_heads_slice_aggregate_backward(self.dims_h, H, xh, G, self.hp, c["num"], c["den"],
+                                                dS_h, c["Sp_h"], dYh, dxh,
+                                                B.make_slice_grads(**per), self.ws_b)
+        else:
+            grs = [B.make_slice_grads(**{k: v[h] for k, v in per.items()}) for h in range(H)]
+            self._heads(lambda h, ws, st: B.pa_slice_aggregate_backward(
+                self.dims_h, xh[h], g(h), self.sp[h], c["num"][h], c["den"][h], dS_h[h],
+                c["Sp_h"][h], dYh[h], dxh[h], grs[h], ws, stream=st))
         grads = {}
         for k in ATTN_W:
             if "d" + k in ag:

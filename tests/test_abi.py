@@ -32,14 +32,14 @@ def _declared_symbols():
 
 def test_every_declared_symbol_is_exported(lib):
     declared = _declared_symbols()
-    assert len(declared) == 27
+    assert len(declared) == 32
     assert sorted(B.SYMBOLS) == declared
     for name in declared:
         assert hasattr(lib, name), name
 
 
 def test_version(lib):
-    assert lib.pa_version() == 3
+    assert lib.pa_version() == 4
 
 
 def _dims(**kw):
@@ -192,3 +192,34 @@ def test_heads_argument_checks(lib):
     assert st == B.PA_ERR_INVALID and "aligned" in lib.pa_last_error().decode()
     st = lib.pa_heads_expand(2, 4, 0, FAKE, None, None)
     assert st == B.PA_ERR_INVALID
+
+
+def test_heads_batched_argument_checks(lib):
+    d = _dims(N=1000, C=32, H=1, M=16, dtype=B.PA_BF16)
+    far = FAKE + (1 << 32)
+    hp = B.pa_heads_params(FAKE, None, None, None, 0)
+    n = ctypes.c_size_t(0)
+    assert lib.pa_heads_workspace_size(ctypes.byref(d), 4, ctypes.byref(n)) == B.PA_OK
+    _, one = _ws_size(lib, d)
+    assert n.value == 4 * one
+    assert lib.pa_heads_workspace_size(ctypes.byref(d), 17, ctypes.byref(n)) == B.PA_ERR_INVALID
+    # heads out of range, M not a multiple of 8, no params, workspace too small
+    st = lib.pa_heads_slice_aggregate(ctypes.byref(d), 0, FAKE, None, ctypes.byref(hp), FAKE,
+                                      FAKE, FAKE, far, n.value, None)
+    assert st == B.PA_ERR_INVALID and "heads" in lib.pa_last_error().decode()
+    d12 = _dims(N=1000, C=32, H=1, M=12, dtype=B.PA_BF16)
+    st = lib.pa_heads_deslice(ctypes.byref(d12), 4, FAKE, None, ctypes.byref(hp), FAKE, FAKE,
+                              far, n.value, None)
+    assert st == B.PA_ERR_INVALID and "multiple of 8" in lib.pa_last_error().decode()
+    st = lib.pa_heads_deslice_backward(ctypes.byref(d), 4, FAKE, None, None, FAKE, FAKE, far,
+                                       n.value, None)
+    assert st == B.PA_ERR_INVALID
+    st = lib.pa_heads_slice_aggregate_backward(ctypes.byref(d), 4, FAKE, None, ctypes.byref(hp),
+                                               None, None, None, None, None, FAKE, None, far,
+                                               n.value - 256, None)
+    assert st == B.PA_ERR_WORKSPACE
+    # a misaligned b_t array
+    hpn = B.pa_heads_params(FAKE, None, None, FAKE + 2, 0)
+    st = lib.pa_heads_slice_aggregate(ctypes.byref(d), 4, FAKE, None, ctypes.byref(hpn), FAKE,
+                                      FAKE, FAKE, far, n.value, None)
+    assert st == B.PA_ERR_INVALID and "b_t" in lib.pa_last_error().decode()

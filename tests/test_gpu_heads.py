@@ -83,7 +83,7 @@ def head_case(N, H, D, M, dt, shared, noise, out_proj, geometry="normal", seed=3
     return w, x, G, p, dY
 
 
-def run_gpu(w, N, x, G, p, dY, dt, streams=2):
+def run_gpu(w, N, x, G, p, dY, dt, streams=2, batched=None):
     import torch
     from paper_2502_02414_amd.heads import HeadSlicedLayer
     H, D, M = w.H, w.C // w.H, w.M
@@ -98,7 +98,7 @@ def run_gpu(w, N, x, G, p, dY, dt, streams=2):
         else:
             pd[k] = dev(v)
     L = HeadSlicedLayer(N, H, D, M, pd, torch.bfloat16 if dt == "bf16" else torch.float32,
-                        w.tau0, w.tau_min, w.eps, streams=streams)
+                        w.tau0, w.tau_min, w.eps, streams=streams, batched=batched)
     xh = L.to_heads(dev(x, dt))
     Gd = dev(G, dt) if G is not None else None
     y = L.from_heads(L.forward(xh, Gd))
@@ -146,6 +146,7 @@ CASES = [
     ("bf16", 20000, 8, 32, 32, False, True, True),
     ("bf16", 9001, 4, 64, 64, False, True, False),
     ("bf16", 5000, 2, 128, 16, True, False, False),
+    ("f32", 1000, 2, 32, 12, False, True, False),   # M not a multiple of 8: one call per head
 ]
 
 
@@ -158,13 +159,15 @@ def test_heads_layer_parity(dt, N, H, D, M, shared, noise, out_proj):
     compare(w, x, G, p, dY, out, dt)
 
 
-def test_heads_streams_bitwise_identical():
-    """The heads of a phase run on several streams; every head's arithmetic
-    and summation order is fixed, so any number of streams gives the same
-    bits."""
-    say("heads layer on 1, 2 and 3 streams: bf16 N=20000 H=8 D=32 M=32")
-    w, x, G, p, dY = head_case(20000, 8, 32, 32, "bf16", False, True, True)
-    outs = [run_gpu(w, 20000, x, G, p, dY, "bf16", streams=k) for k in (1, 2, 3)]
+@pytest.mark.parametrize("shared", [False, True])
+def test_heads_launch_modes_bitwise_identical(shared):
+    """All heads in one launch per kernel (pa_heads_*), and one call per head
+    on 1, 2 or 3 streams: every head's arithmetic and summation order is the
+    same, so every mode gives the same bits."""
+    say(f"heads layer batched vs per-head calls: bf16 N=20000 H=8 D=32 M=32 shared={shared}")
+    w, x, G, p, dY = head_case(20000, 8, 32, 32, "bf16", shared, True, True)
+    outs = [run_gpu(w, 20000, x, G, p, dY, "bf16", batched=True)]
+    outs += [run_gpu(w, 20000, x, G, p, dY, "bf16", streams=k, batched=False) for k in (1, 2, 3)]
     for o in outs[1:]:
         for k, v in outs[0].items():
             np.testing.assert_array_equal(o[k], v, err_msg=k)
