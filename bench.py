@@ -133,6 +133,11 @@ def main():
                     help="time the per-head sliced layer at N = 1M instead (its own line)")
     ap.add_argument("--head-streams", type=int, default=2,
                     help="streams the per-head layer spreads its heads over (one call per head)")
+    ap.add_argument("--workload", default=None,
+                    help="time the layer on another workload instead (its own line): "
+                         "ns2d_fwd_f32, grid2d_16k_f32, ellipsoid_32k_bf16, aircraft_2p5m_bf16")
+    ap.add_argument("--flush", action="store_true",
+                    help="with --workload: overwrite 1 GiB between steps (cold last-level cache)")
     ap.add_argument("--head-calls", choices=("batched", "per-head"), default=None,
                     help="per-head layer: all heads in one launch per kernel, or one call per head")
     args = ap.parse_args()
@@ -144,6 +149,8 @@ def main():
         return stack_bench(args)
     if args.heads:
         return heads_bench(args)
+    if args.workload:
+        return workload_bench(args)
 
     import numpy as np
     import torch
@@ -325,6 +332,82 @@ def stack_bench(args):
         "forward_ms": round(fwd, 2), "backward_ms": round(bwd, 2),
         "mlp_gemm_tflops": round(mlp_flop / (ms * 1e-3) / 1e12, 1),
         "peak_mem_gib": round(torch.cuda.max_memory_allocated() / 2**30, 1),
+    }
+    print(json.dumps(out), flush=True)
+
+
+def workload_bench(args):
+    """The layer's call sequence on another workload (forward only when the
+    workload is), each step bracketed by its own events; with --flush a
+    1 GiB buffer is overwritten before every step (outside the events), so
+    that no input is left in the 256 MB last-level cache.  Prints its own
+    JSON line (the headline line is the million-point one)."""
+    import numpy as np
+    import torch
+    from paper_2502_02414_amd import binding as B
+    from paper_2502_02414_amd import inputs as I
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    w = I.WORKLOADS[args.workload]
+    N, C, H, M = w.N, w.C, w.H, w.M
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    pdt = B.PA_BF16 if w.dtype == "bf16" else B.PA_F32
+    to = lambda a, t=torch.float32: torch.from_numpy(np.ascontiguousarray(a)).cuda().to(t)
+    p = I.make_params(w)
+    x, G, dY = to(I.make_x(w), dt), to(I.make_gumbel(w), dt), to(I.make_grad(w), dt)
+    A, a, b = to(p["A"], dt), to(p["a"], dt), to(p["b"])
+    att = {k: to(p[k]) for k in ("Wq", "bq", "Wk", "bk", "Wv", "bv")}
+    dims = B.make_dims(N, C, H, M, w.tau0, w.tau_min, w.eps, pdt)
+    sp, apr, ws = B.make_slice_params(A, b, a, p["b_t"]), B.make_attn_params(**att), B.workspace(dims)
+    f32 = lambda *s: torch.empty(*s, dtype=torch.float32, device="cuda")
+    num, den, S, Sp, dSp, dS = f32(M, C), f32(M), f32(M, C), f32(M, C), f32(M, C), f32(M, C)
+    y, dx = torch.empty(N, C, dtype=dt, device="cuda"), torch.empty(N, C, dtype=dt, device="cuda")
+    ag = {k: f32(C, C) for k in ("dWq", "dWk", "dWv")}
+    ag.update({k: f32(C) for k in ("dbq", "dbk", "dbv")})
+    agr = B.make_attn_grads(**ag)
+    sgr = B.make_slice_grads(dA=f32(C, M), db=f32(M), da=f32(C), db_t=f32(1), dtau0=f32(1))
+
+    def step():
+        B.pa_slice_aggregate(dims, x, G, sp, num, den, S, ws)
+        B.pa_token_attention(dims, S, apr, Sp, ws)
+        B.pa_deslice(dims, x, G, sp, Sp, y, ws)
+        if w.backward:
+            B.pa_deslice_backward(dims, x, G, sp, dY, dSp, ws)
+            B.pa_token_attention_backward(dims, S, apr, dSp, dS, agr, ws)
+            B.pa_slice_aggregate_backward(dims, x, G, sp, num, den, dS, Sp, dY, dx, sgr, ws)
+
+    junk = torch.empty(1 << 28, dtype=torch.float32, device="cuda") if args.flush else None
+    for _ in range(args.warmup):
+        step()
+    ev = [(B.HipEvent(), B.HipEvent()) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    for e0, e1 in ev:
+        if junk is not None:
+            junk.fill_(1.0)
+        e0.record()
+        step()
+        e1.record()
+    torch.cuda.synchronize()
+    times = sorted(e0.elapsed_ms(e1) for e0, e1 in ev)
+    ms = times[len(times) // 2]
+    bpp = algo_bytes_per_point(C, M, 2 if w.dtype == "bf16" else 4, 2 if w.dtype == "bf16" else 4)
+    calls = ["pa_slice_aggregate", "pa_deslice"] + (
+        ["pa_deslice_backward", "pa_slice_aggregate_backward"] if w.backward else [])
+    nbytes = N * sum(bpp[c] for c in calls)
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    out = {
+        "metric": f"mesh points/sec per Physics-Attention layer "
+                  f"{'fwd+bwd' if w.backward else 'fwd'} at N={N}, C={C}, M={M}",
+        "value": round(N / (ms * 1e-3), 1), "unit": "points/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "ms_per_step_min": round(times[0], 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": w.name, "N": N, "C": C, "H": H, "M": M,
+                   "pass": "forward+backward" if w.backward else "forward",
+                   "cache": "flushed before every step" if args.flush else "warm"},
+        "step_hbm": {"algo_bytes": nbytes, "achieved_GBs": round(gbs, 1),
+                     "frac": round(gbs / HBM_PEAK_GBS, 4)},
     }
     print(json.dumps(out), flush=True)
 
