@@ -214,7 +214,7 @@ def layer_backward(x, G, p, tau0, tau_min, eps, H, fwd, dY):
 # Transformer block with Physics-Attention in place of attention; block
 # diagram of Figure 2a), read as pre-norm with residual adds:
 #     x1 = x + PA(LN1(x)),   x2 = x1 + MLP(LN2(x1)),
-#     MLP(h) = GELU(h W1 + b1) W2 + b2 (exact GELU),
+#     MLP(h) = GELU(h W1 + b1) W2 + b2 (GELU in its tanh form),
 # and PA with Algorithm 1's Project step applied explicitly:
 #     x_proj = LN1(x) Wp + bp, then the layer on x_proj (to_out = Wo, bo).
 # ---------------------------------------------------------------------------
@@ -241,7 +241,7 @@ def layernorm_backward(x, g, dy, eps=LN_EPS):
 
 
 def gelu(x):
-    """Exact GELU x Phi(x)."""
+    """GELU in its tanh form x (1 + tanh(sqrt(2/pi) (x + 0.044715 x^3))) / 2."""
     x = _in(x)
     y = np.empty_like(x)
     _load().pao_gelu(x.size, _p(x), _p(y))

@@ -125,7 +125,8 @@ void pao_layernorm(int64_t N, int C, double eps, const double* x, const double* 
 /* Its chain rule: dx [N,C], dg [C], db [C] (each nullable). */
 void pao_layernorm_backward(int64_t N, int C, double eps, const double* x, const double* g,
                             const double* dy, double* dx, double* dg, double* db);
-/* Exact GELU x Phi(x) and its chain rule. */
+/* GELU in its tanh form x (1 + tanh(sqrt(2/pi) (x + 0.044715 x^3))) / 2
+ * and its chain rule. */
 void pao_gelu(int64_t n, const double* x, double* y);
 void pao_gelu_backward(int64_t n, const double* x, const double* dy, double* dx);
 /* y = x W + b and its chain rule (dx, dW, db nullable). */

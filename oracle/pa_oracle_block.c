@@ -95,20 +95,29 @@ void pao_layernorm_backward(int64_t N, int C, double eps, const double* x, const
   free(pb);
 }
 
-/* GELU in its exact form: y = x Phi(x) = x (1 + erf(x / sqrt 2)) / 2. */
+/* GELU in its tanh form (the feedforward layer's activation is not
+ * specified; this is the form of Hendrycks & Gimpel's approximation):
+ *   y = x (1 + tanh(u)) / 2,  u = sqrt(2/pi) (x + 0.044715 x^3). */
+#define GELU_S 0.7978845608028654   /* sqrt(2 / pi) */
+#define GELU_K 0.044715
 void pao_gelu(int64_t n, const double* x, double* y) {
 #pragma omp parallel for schedule(static)
-  for (int64_t k = 0; k < n; ++k) y[k] = 0.5 * x[k] * (1.0 + erf(x[k] / sqrt(2.0)));
+  for (int64_t k = 0; k < n; ++k) {
+    const double u = GELU_S * (x[k] + GELU_K * x[k] * x[k] * x[k]);
+    y[k] = 0.5 * x[k] * (1.0 + tanh(u));
+  }
 }
 
-/* dx = dy (Phi(x) + x phi(x)), phi the standard normal density. */
+/* dx = dy d/dx [x (1 + tanh u) / 2]
+ *    = dy [(1 + tanh u) / 2 + x (1 - tanh^2 u) u'(x) / 2],
+ *   u'(x) = sqrt(2/pi) (1 + 3 * 0.044715 x^2). */
 void pao_gelu_backward(int64_t n, const double* x, const double* dy, double* dx) {
-  const double inv_sqrt_2pi = 0.3989422804014327;  /* 1 / sqrt(2 pi) */
 #pragma omp parallel for schedule(static)
   for (int64_t k = 0; k < n; ++k) {
-    const double cdf = 0.5 * (1.0 + erf(x[k] / sqrt(2.0)));
-    const double pdf = inv_sqrt_2pi * exp(-0.5 * x[k] * x[k]);
-    dx[k] = dy[k] * (cdf + x[k] * pdf);
+    const double u = GELU_S * (x[k] + GELU_K * x[k] * x[k] * x[k]);
+    const double t = tanh(u);
+    const double du = GELU_S * (1.0 + 3.0 * GELU_K * x[k] * x[k]);
+    dx[k] = dy[k] * (0.5 * (1.0 + t) + 0.5 * x[k] * (1.0 - t * t) * du);
   }
 }
 
