@@ -6,8 +6,8 @@
 //     precedes it fused (the sum is written once, in the storage dtype), and
 //     its backward with the residual gradient added; the gain and bias
 //     gradients are per-block partial sums added in block order;
-//   - GELU in its exact form (x Phi(x); Phi from a published erfc
-//     approximation accurate to 1.5e-7) and its derivative, elementwise;
+//   - GELU in its tanh form (x sigmoid(2u), u = sqrt(2/pi)(x + 0.044715 x^3))
+//     and its derivative, elementwise;
 //   - column sums of a [N, C] matrix (the bias gradients of the linear
 //     layers), deterministic;
 //   - Algorithm 1's Project step x_proj = h Wp + bp folded into the slice
@@ -212,30 +212,25 @@ __global__ void __launch_bounds__(256) k_ln_bwd(LayerNormArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// GELU in its exact form x Phi(x) and its derivative Phi(x) + x phi(x),
-// elementwise (n a multiple of E).  Phi is evaluated through erfc with
-// Abramowitz & Stegun's rational approximation 7.1.26,
-//   erfc(z) ~ t (a1 + t (a2 + t (a3 + t (a4 + t a5)))) exp(-z^2),
-//   t = 1 / (1 + p z),  z >= 0,  |error| <= 1.5e-7,
-// which shares exp(-z^2) (z = |x| / sqrt 2) with the normal density phi(x):
-// about 15 operations per element instead of a library erf and exp.
+// GELU in its tanh form, y = x (1 + tanh u) / 2 with u = sqrt(2/pi) (x +
+// 0.044715 x^3), evaluated as y = x s, s = 1 / (1 + exp(-2u)) (the same
+// value: (1 + tanh u) / 2 is the logistic function of 2u, which has no
+// cancellation near u = 0 and saturates to 0 and 1 without overflow), and
+// its derivative dy/dx = s + 2 x s (1 - s) u'(x), u'(x) = sqrt(2/pi)
+// (1 + 3 * 0.044715 x^2); elementwise (n a multiple of E).
 // ---------------------------------------------------------------------------
-struct PhiPhi { float cdf, pdf; };
-__device__ __forceinline__ PhiPhi phi_both(float x) {
-  const float z = fabsf(x) * 0.70710678118654752f;
-  const float t = __frcp_rn(fmaf(0.3275911f, z, 1.f));
-  const float e = __builtin_amdgcn_exp2f(-z * z * 1.4426950408889634f);  // exp(-z^2)
-  float poly = fmaf(t, 1.061405429f, -1.453152027f);
-  poly = fmaf(t, poly, 1.421413741f);
-  poly = fmaf(t, poly, -0.284496736f);
-  poly = fmaf(t, poly, 0.254829592f);
-  const float half_erfc = 0.5f * t * poly * e;  // Phi(-|x|)
-  return {x >= 0.f ? 1.f - half_erfc : half_erfc, 0.39894228040143268f * e};
+struct GeluS { float s, du; };
+__device__ __forceinline__ GeluS gelu_s(float x) {
+  constexpr float kS = 0.7978845608028654f, kK = 0.044715f;
+  const float x2 = x * x;
+  const float u = kS * fmaf(kK * x2, x, x);
+  const float e = __builtin_amdgcn_exp2f(-2.f * 1.4426950408889634f * u);  // exp(-2u)
+  return {__frcp_rn(1.f + e), kS * fmaf(3.f * kK, x2, 1.f)};
 }
-__device__ __forceinline__ float gelu_f(float x) { return x * phi_both(x).cdf; }
+__device__ __forceinline__ float gelu_f(float x) { return x * gelu_s(x).s; }
 __device__ __forceinline__ float dgelu_f(float x) {
-  const PhiPhi p = phi_both(x);
-  return fmaf(x, p.pdf, p.cdf);
+  const GeluS g = gelu_s(x);
+  return fmaf(2.f * x * g.s * (1.f - g.s), g.du, g.s);
 }
 
 template <typename T>

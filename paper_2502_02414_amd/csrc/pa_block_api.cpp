@@ -96,7 +96,7 @@ pa_status pa_gemm(int transA, int transB, int64_t m, int64_t n, int64_t k, float
   g.ws = ws; g.ws_bytes = ws_bytes;
   const int s = pa::gemm(g, as_stream(stream));
   if (s != 0)
-    return err(s == 6 /* HIPBLAS_STATUS_NOT_SUPPORTED */ ? PA_ERR_UNSUPPORTED : PA_ERR_HIP,
+    return err(s == 7 /* HIPBLAS_STATUS_NOT_SUPPORTED */ ? PA_ERR_UNSUPPORTED : PA_ERR_HIP,
                "pa_gemm: hipBLASLt status %d (m=%lld n=%lld k=%lld types %d,%d->%d)", s,
                (long long)m, (long long)n, (long long)k, a_dtype, b_dtype, d_dtype);
   return PA_OK;

@@ -14,8 +14,8 @@ run on h = LN1(x), and the states are projected, S_proj = S Wp + bp
 the layer's output projection).  x_proj is never formed.
 
 Every step is a call of libpa.so (the layer's calls, LayerNorm with the
-residual add fused, GELU, the Project folding, and hipBLASLt GEMMs for the
-MLP, whose second GEMM adds the residual).  torch only allocates the device
+residual add fused, GELU (tanh form), the Project folding, and hipBLASLt
+GEMMs for the MLP, whose second GEMM adds the residual).  torch only allocates the device
 buffers.  Per layer the forward keeps x, LN1(x), x1, LN2(x1), the MLP's
 pre-activation u and GELU(u) (the backward's weight gradient of W2 reads it;
 keeping it costs 2 N 4C bytes per layer and saves recomputing it), and the
