@@ -66,12 +66,14 @@ enum Flags { kHasG = 1, kStatesTerm = 2, kDesliceTerm = 4 };
 // two for the bf16 deslice with up to 32 slices, whose registers allow it;
 // the aggregating passes stream 32-point tiles there (one stage holds as
 // many points as two).  Rows of 64 bytes (a head's channel block of the
-// per-head slicing, 32 bf16 channels) carry so few bytes per tile that every
-// pass keeps two stages (measured at 8 heads x 1M points: the per-head step
-// -2 %, on top of the 8 waves of narrow rows, Geo::max_waves).
+// per-head slicing, 32 bf16 channels) carry so few bytes per tile that the
+// passes on 16-point tiles keep two stages (measured at 8 heads x 1M points,
+// on top of the 8 waves of narrow rows, Geo::max_waves); the forward
+// aggregate's 32-point stage already holds as many points (a second stage
+// cost it 40 us per step there).
 template <typename T, int C> constexpr bool narrow_rows() { return C * (int)sizeof(T) <= 64; }
 template <typename T, int C, int MB, bool BWD> constexpr int agg_depth() {
-  return narrow_rows<T, C>() ? 2 : 1;
+  return narrow_rows<T, C>() && BWD ? 2 : 1;
 }
 template <typename T, int C, int MB> constexpr int des_depth() {
   return narrow_rows<T, C>() || (sizeof(T) == 2 && MB <= 2) ? 2 : 1;
