@@ -223,3 +223,33 @@ def test_heads_batched_argument_checks(lib):
     st = lib.pa_heads_slice_aggregate(ctypes.byref(d), 4, FAKE, None, ctypes.byref(hpn), FAKE,
                                       FAKE, FAKE, far, n.value, None)
     assert st == B.PA_ERR_INVALID and "b_t" in lib.pa_last_error().decode()
+
+
+def test_struct_layouts_match_header(tmp_path):
+    """The ctypes structs of the binding have the sizes and field offsets the
+    C compiler gives the header's structs."""
+    import subprocess
+    structs = {"pa_dims": B.pa_dims, "pa_slice_params": B.pa_slice_params,
+               "pa_attn_params": B.pa_attn_params, "pa_slice_grads": B.pa_slice_grads,
+               "pa_attn_grads": B.pa_attn_grads, "pa_heads_params": B.pa_heads_params}
+    lines = ['#include <stdio.h>', '#include "pa.h"', "int main(void) {"]
+    for name, cls in structs.items():
+        lines.append(f'  printf("{name} sizeof %zu\\n", sizeof({name}));')
+        for f in cls._fields_:
+            lines.append(f'  printf("{name} {f[0]} %zu\\n", offsetof({name}, {f[0]}));')
+    lines += ["  return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    subprocess.run(["gcc", "-std=c11", "-I", os.path.join(root, "include"), str(src), "-o",
+                    str(exe)], check=True)
+    got = {}
+    for line in subprocess.run([str(exe)], check=True, capture_output=True,
+                               text=True).stdout.splitlines():
+        name, field, val = line.split()
+        got[(name, field)] = int(val)
+    for name, cls in structs.items():
+        assert got[(name, "sizeof")] == ctypes.sizeof(cls), name
+        for f in cls._fields_:
+            assert got[(name, f[0])] == getattr(cls, f[0]).offset, (name, f[0])
