@@ -142,7 +142,7 @@ def main():
                     help="per-head layer: all heads in one launch per kernel, or one call per head")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); this build runs the "
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the library runs the "
               "hot path on a single MI355X and has no multi-GPU path.", file=sys.stderr)
         sys.exit(2)
     if args.stack:

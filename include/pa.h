@@ -62,7 +62,7 @@ typedef enum { PA_F32 = 0, PA_BF16 = 1 } pa_dtype;
 typedef enum {
   PA_OK = 0,
   PA_ERR_INVALID = -1,     /* bad argument value or NULL pointer           */
-  PA_ERR_UNSUPPORTED = -2, /* valid, but a shape this build does not serve */
+  PA_ERR_UNSUPPORTED = -2, /* valid, but a shape the library does not serve */
   PA_ERR_WORKSPACE = -3,   /* workspace smaller than pa_workspace_size     */
   PA_ERR_HIP = -4          /* a HIP runtime call or launch failed          */
 } pa_status;
