@@ -138,6 +138,8 @@ def main():
                          "ns2d_fwd_f32, grid2d_16k_f32, ellipsoid_32k_bf16, aircraft_2p5m_bf16")
     ap.add_argument("--flush", action="store_true",
                     help="with --workload: overwrite 1 GiB between steps (cold last-level cache)")
+    ap.add_argument("--graph", action="store_true",
+                    help="with --workload: replay the step from a captured HIP graph")
     ap.add_argument("--head-calls", choices=("batched", "per-head"), default=None,
                     help="per-head layer: all heads in one launch per kernel, or one call per head")
     args = ap.parse_args()
@@ -380,6 +382,19 @@ def workload_bench(args):
     junk = torch.empty(1 << 28, dtype=torch.float32, device="cuda") if args.flush else None
     for _ in range(args.warmup):
         step()
+    if args.graph:
+        # capture the step once on a side stream, then time its replays (the
+        # library's calls only launch kernels: capturable as they are)
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step()
+        torch.cuda.current_stream().wait_stream(side)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        step = graph.replay
+        step()
     ev = [(B.HipEvent(), B.HipEvent()) for _ in range(args.steps)]
     torch.cuda.synchronize()
     for e0, e1 in ev:
@@ -405,7 +420,8 @@ def workload_bench(args):
         "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
         "config": {"workload": w.name, "N": N, "C": C, "H": H, "M": M,
                    "pass": "forward+backward" if w.backward else "forward",
-                   "cache": "flushed before every step" if args.flush else "warm"},
+                   "cache": "flushed before every step" if args.flush else "warm",
+                   "launch": "HIP graph replay" if args.graph else "eager"},
         "step_hbm": {"algo_bytes": nbytes, "achieved_GBs": round(gbs, 1),
                      "frac": round(gbs / HBM_PEAK_GBS, 4)},
     }
