@@ -477,14 +477,22 @@ def heads_bench(args):
     torch.cuda.synchronize()
     fwd = sum(e[0].elapsed_ms(e[1]) for e in ev) / steps
     bwd = sum(e[1].elapsed_ms(e[2]) for e in ev) / steps
+    # the timed region; the library brackets the streaming kernel of the
+    # slice backward (all heads in one launch) with an event pair per step
     start, end = B.HipEvent(), B.HipEvent()
+    kev = [(B.HipEvent(), B.HipEvent()) for _ in range(steps)]
+    batched = L.batched
     start.record()
     for s in range(steps):
+        if batched:
+            B.pa_time_kernel("pa_slice_aggregate_backward", *kev[s])
         L.forward(xh, G)
         L.backward(dYh)
     end.record()
     torch.cuda.synchronize()
+    B.pa_time_kernel(None)
     ms = start.elapsed_ms(end) / steps
+    kernel_ms = sum(e0.elapsed_ms(e1) for e0, e1 in kev) / steps if batched else None
     # one [N,C] tensor to the head-major layout and back
     tmp = torch.empty(N, C, dtype=bf, device="cuda")
     r0, r1 = B.HipEvent(), B.HipEvent()
@@ -516,6 +524,13 @@ def heads_bench(args):
         "relayout_ms_per_tensor": round(relayout_ms, 4),
         "relayout_GBs": round(2 * N * C * 2 / (relayout_ms * 1e-3) / 1e9, 1),
     }
+    if kernel_ms:
+        kb = H * N * bpp["pa_slice_aggregate_backward"]
+        ach = kb / (kernel_ms * 1e-3) / 1e9
+        out["roofline"] = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
+                           "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None,
+                           "call": "pa_heads_slice_aggregate_backward", "kernel": "slice_bwd (C=32)",
+                           "algo_bytes_per_launch": kb, "kernel_ms": round(kernel_ms, 4)}
     print(json.dumps(out), flush=True)
 
 
