@@ -493,6 +493,13 @@ def heads_bench(args):
     B.pa_time_kernel(None)
     ms = start.elapsed_ms(end) / steps
     kernel_ms = sum(e0.elapsed_ms(e1) for e0, e1 in kev) / steps if batched else None
+    if args.copy_calibration:
+        src = torch.empty(1 << 28, dtype=torch.float32, device="cuda")  # 1 GiB
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     # one [N,C] tensor to the head-major layout and back
     tmp = torch.empty(N, C, dtype=bf, device="cuda")
     r0, r1 = B.HipEvent(), B.HipEvent()
@@ -528,7 +535,8 @@ def heads_bench(args):
         kb = H * N * bpp["pa_slice_aggregate_backward"]
         ach = kb / (kernel_ms * 1e-3) / 1e9
         out["roofline"] = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
-                           "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None,
+                           "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
+                           "traffic": read_traffic("slice_bwd_heads"),
                            "call": "pa_heads_slice_aggregate_backward", "kernel": "slice_bwd (C=32)",
                            "algo_bytes_per_launch": kb, "kernel_ms": round(kernel_ms, 4)}
     print(json.dumps(out), flush=True)
