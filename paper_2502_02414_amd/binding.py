@@ -150,6 +150,52 @@ def _ptr(t) -> Optional[int]:
     return t.data_ptr()
 
 
+# Element-count and dtype checks against the dims of a call: the library
+# only sees pointers, so a tensor smaller than the shape it stands for would
+# be read or written past its end.  A requirement is (elements, dtype), the
+# dtype a PA_* code, or None for "fp32 or the storage dtype" (not checked).
+def _need(t, n: int, dt: Optional[int], name: str):
+    if t is None:
+        return
+    if t.numel() < n:
+        raise ValueError(f"{name}: {t.numel()} elements, the call needs {n}")
+    if dt is not None and _dt(t) != dt:
+        raise ValueError(f"{name}: dtype {t.dtype} does not match the call's "
+                         f"{'bf16' if dt == PA_BF16 else 'fp32'}")
+
+
+def _arg(t, n: int, dt: Optional[int], name: str) -> Optional[int]:
+    """Pointer of t after checking it against (n elements, dtype dt)."""
+    _need(t, n, dt, name)
+    return _ptr(t)
+
+
+def _check_struct(st, dims, heads: int = 1, stacked: bool = False):
+    """Checks the tensors a parameter struct was made from against dims
+    (structs built by the make_* helpers below carry their tensors);
+    ``stacked``: every tensor holds one block per head."""
+    for name, (t, kind) in getattr(st, "_tensors", {}).items():
+        n = _struct_count(kind, dims, heads) * (heads if stacked else 1)
+        _need(t, n, _struct_dtype(kind, dims), name)
+
+
+def _struct_count(kind: str, d, heads: int) -> int:
+    C, M = d.C, d.M
+    return {"CM": C * M, "CM32": C * M, "M": M, "C": C, "C32": C, "1": 1, "CC": C * C,
+            "hCM": heads * C * M, "hCM32": heads * C * M, "hM": heads * M, "hC": heads * C,
+            "hC32": heads * C, "h": heads}[kind]
+
+
+def _struct_dtype(kind: str, d) -> Optional[int]:
+    # A and a are in the storage dtype; everything else in the structs is fp32
+    return {"CM": d.dtype, "C": d.dtype, "hCM": d.dtype, "hC": d.dtype}.get(kind, PA_F32)
+
+
+def _with(st, **tensors):
+    st._tensors = {k: v for k, v in tensors.items() if v[0] is not None}
+    return st
+
+
 def _stream(stream=None) -> Optional[int]:
     import torch
     s = torch.cuda.current_stream() if stream is None else stream
@@ -163,22 +209,38 @@ def make_dims(N: int, C: int, H: int, M: int, tau0: float, tau_min: float, eps: 
 
 
 def make_slice_params(A, b=None, a=None, b_t: float = 0.0, b_t_dev=None) -> pa_slice_params:
-    return pa_slice_params(_ptr(A), _ptr(b), _ptr(a), float(b_t), _ptr(b_t_dev))
+    return _with(pa_slice_params(_ptr(A), _ptr(b), _ptr(a), float(b_t), _ptr(b_t_dev)),
+                 A=(A, "CM"), b=(b, "M"), a=(a, "C"), b_t_dev=(b_t_dev, "1"))
 
 
 def make_attn_params(Wq, Wk, Wv, bq=None, bk=None, bv=None, Wo=None, bo=None) -> pa_attn_params:
-    return pa_attn_params(_ptr(Wq), _ptr(bq), _ptr(Wk), _ptr(bk), _ptr(Wv), _ptr(bv), _ptr(Wo),
-                          _ptr(bo))
+    return _with(pa_attn_params(_ptr(Wq), _ptr(bq), _ptr(Wk), _ptr(bk), _ptr(Wv), _ptr(bv),
+                                _ptr(Wo), _ptr(bo)),
+                 Wq=(Wq, "CC"), Wk=(Wk, "CC"), Wv=(Wv, "CC"), Wo=(Wo, "CC"), bq=(bq, "C32"),
+                 bk=(bk, "C32"), bv=(bv, "C32"), bo=(bo, "C32"))
 
 
 def make_slice_grads(dA=None, db=None, da=None, db_t=None, dtau0=None) -> pa_slice_grads:
-    return pa_slice_grads(_ptr(dA), _ptr(db), _ptr(da), _ptr(db_t), _ptr(dtau0))
+    return _with(pa_slice_grads(_ptr(dA), _ptr(db), _ptr(da), _ptr(db_t), _ptr(dtau0)),
+                 dA=(dA, "CM32"), db=(db, "M"), da=(da, "C32"), db_t=(db_t, "1"),
+                 dtau0=(dtau0, "1"))
 
 
 def make_attn_grads(dWq=None, dbq=None, dWk=None, dbk=None, dWv=None, dbv=None, dWo=None,
                     dbo=None) -> pa_attn_grads:
-    return pa_attn_grads(_ptr(dWq), _ptr(dbq), _ptr(dWk), _ptr(dbk), _ptr(dWv), _ptr(dbv),
-                         _ptr(dWo), _ptr(dbo))
+    return _with(pa_attn_grads(_ptr(dWq), _ptr(dbq), _ptr(dWk), _ptr(dbk), _ptr(dWv), _ptr(dbv),
+                               _ptr(dWo), _ptr(dbo)),
+                 dWq=(dWq, "CC"), dWk=(dWk, "CC"), dWv=(dWv, "CC"), dWo=(dWo, "CC"),
+                 dbq=(dbq, "C32"), dbk=(dbk, "C32"), dbv=(dbv, "C32"), dbo=(dbo, "C32"))
+
+
+def _shapes(dims, heads: int = 1) -> dict:
+    """(elements, dtype) of the tensors of a layer call at these dims; with
+    heads > 1 the point-side tensors and the states are stacked per head."""
+    N, C, M, dt = int(dims.N), int(dims.C), int(dims.M), int(dims.dtype)
+    h = int(heads)
+    return {"x": (h * N * C, dt), "G": (h * N * M, dt), "W32": (N * M, PA_F32),
+            "N32": (N, PA_F32), "MC": (h * M * C, PA_F32), "M": (h * M, PA_F32)}
 
 
 def pa_version() -> int:
@@ -202,65 +264,98 @@ def workspace(dims: pa_dims, device="cuda"):
 
 
 def pa_slice_weights(dims, x, G, sp, W, tau, ws, stream=None):
-    _check(load().pa_slice_weights(ctypes.byref(dims), _ptr(x), _ptr(G), ctypes.byref(sp),
-                                   _ptr(W), _ptr(tau), _ptr(ws), ws.numel(), _stream(stream)))
+    d = _shapes(dims)
+    _check_struct(sp, dims)
+    _check(load().pa_slice_weights(ctypes.byref(dims), _arg(x, *d["x"], "x"), _arg(G, *d["G"], "G"),
+                                   ctypes.byref(sp), _arg(W, *d["W32"], "W"), _arg(tau, *d["N32"], "tau"),
+                                   _ptr(ws), ws.numel(), _stream(stream)))
 
 
 def pa_slice_aggregate(dims, x, G, sp, num, den, S, ws, stream=None):
-    _check(load().pa_slice_aggregate(ctypes.byref(dims), _ptr(x), _ptr(G), ctypes.byref(sp),
-                                     _ptr(num), _ptr(den), _ptr(S), _ptr(ws), ws.numel(),
-                                     _stream(stream)))
+    d = _shapes(dims)
+    _check_struct(sp, dims)
+    _check(load().pa_slice_aggregate(ctypes.byref(dims), _arg(x, *d["x"], "x"), _arg(G, *d["G"], "G"),
+                                     ctypes.byref(sp), _arg(num, *d["MC"], "num"), _arg(den, *d["M"], "den"),
+                                     _arg(S, *d["MC"], "S"), _ptr(ws), ws.numel(), _stream(stream)))
 
 
 def pa_token_attention(dims, S, ap, Sp, ws, stream=None):
-    _check(load().pa_token_attention(ctypes.byref(dims), _ptr(S), ctypes.byref(ap), _ptr(Sp),
-                                     _ptr(ws), ws.numel(), _stream(stream)))
+    d = _shapes(dims)
+    _check_struct(ap, dims)
+    _check(load().pa_token_attention(ctypes.byref(dims), _arg(S, *d["MC"], "S"), ctypes.byref(ap),
+                                     _arg(Sp, *d["MC"], "Sp"), _ptr(ws), ws.numel(), _stream(stream)))
 
 
 def pa_deslice(dims, x, G, sp, Sp, y, ws, stream=None):
-    _check(load().pa_deslice(ctypes.byref(dims), _ptr(x), _ptr(G), ctypes.byref(sp), _ptr(Sp),
-                             _ptr(y), _ptr(ws), ws.numel(), _stream(stream)))
+    d = _shapes(dims)
+    _check_struct(sp, dims)
+    _check(load().pa_deslice(ctypes.byref(dims), _arg(x, *d["x"], "x"), _arg(G, *d["G"], "G"),
+                             ctypes.byref(sp), _arg(Sp, *d["MC"], "Sp"), _arg(y, *d["x"], "y"), _ptr(ws),
+                             ws.numel(), _stream(stream)))
 
 
 def pa_deslice_backward(dims, x, G, sp, dY, dSp, ws, stream=None):
-    _check(load().pa_deslice_backward(ctypes.byref(dims), _ptr(x), _ptr(G), ctypes.byref(sp),
-                                      _ptr(dY), _ptr(dSp), _ptr(ws), ws.numel(),
-                                      _stream(stream)))
+    d = _shapes(dims)
+    _check_struct(sp, dims)
+    _check(load().pa_deslice_backward(ctypes.byref(dims), _arg(x, *d["x"], "x"), _arg(G, *d["G"], "G"),
+                                      ctypes.byref(sp), _arg(dY, *d["x"], "dY"), _arg(dSp, *d["MC"], "dSp"),
+                                      _ptr(ws), ws.numel(), _stream(stream)))
 
 
 def pa_token_attention_backward(dims, S, ap, dSp, dS, ag, ws, stream=None):
+    d = _shapes(dims)
+    _check_struct(ap, dims)
+    if ag is not None:
+        _check_struct(ag, dims)
     _check(load().pa_token_attention_backward(
-        ctypes.byref(dims), _ptr(S), ctypes.byref(ap), _ptr(dSp), _ptr(dS),
+        ctypes.byref(dims), _arg(S, *d["MC"], "S"), ctypes.byref(ap), _arg(dSp, *d["MC"], "dSp"),
+        _arg(dS, *d["MC"], "dS"),
         ctypes.byref(ag) if ag is not None else None, _ptr(ws), ws.numel(), _stream(stream)))
 
 
 def pa_slice_aggregate_backward(dims, x, G, sp, num, den, dS, Sp, dY, dx, gr, ws, stream=None):
+    d = _shapes(dims)
+    _check_struct(sp, dims)
+    if gr is not None:
+        _check_struct(gr, dims)
     _check(load().pa_slice_aggregate_backward(
-        ctypes.byref(dims), _ptr(x), _ptr(G), ctypes.byref(sp), _ptr(num), _ptr(den), _ptr(dS),
-        _ptr(Sp), _ptr(dY), _ptr(dx), ctypes.byref(gr) if gr is not None else None, _ptr(ws),
-        ws.numel(), _stream(stream)))
+        ctypes.byref(dims), _arg(x, *d["x"], "x"), _arg(G, *d["G"], "G"), ctypes.byref(sp),
+        _arg(num, *d["MC"], "num"), _arg(den, *d["M"], "den"), _arg(dS, *d["MC"], "dS"), _arg(Sp, *d["MC"], "Sp"),
+        _arg(dY, *d["x"], "dY"), _arg(dx, *d["x"], "dx"), ctypes.byref(gr) if gr is not None else None,
+        _ptr(ws), ws.numel(), _stream(stream)))
 
 
 def pa_slice_weights_backward(dims, x, G, sp, dW, dtau, dx, gr, ws, stream=None):
+    d = _shapes(dims)
+    _check_struct(sp, dims)
+    if gr is not None:
+        _check_struct(gr, dims)
     _check(load().pa_slice_weights_backward(
-        ctypes.byref(dims), _ptr(x), _ptr(G), ctypes.byref(sp), _ptr(dW), _ptr(dtau), _ptr(dx),
+        ctypes.byref(dims), _arg(x, *d["x"], "x"), _arg(G, *d["G"], "G"), ctypes.byref(sp),
+        _arg(dW, *d["W32"], "dW"), _arg(dtau, *d["N32"], "dtau"), _arg(dx, *d["x"], "dx"),
         ctypes.byref(gr) if gr is not None else None, _ptr(ws), ws.numel(), _stream(stream)))
 
 
 def pa_slice_aggregate_w(dims, x, G, sp, num, den, S, W, ws, stream=None):
-    _check(load().pa_slice_aggregate_w(ctypes.byref(dims), _ptr(x), _ptr(G), ctypes.byref(sp),
-                                       _ptr(num), _ptr(den), _ptr(S), _ptr(W), _ptr(ws),
-                                       ws.numel(), _stream(stream)))
+    d = _shapes(dims)
+    _check_struct(sp, dims)
+    _check(load().pa_slice_aggregate_w(ctypes.byref(dims), _arg(x, *d["x"], "x"), _arg(G, *d["G"], "G"),
+                                       ctypes.byref(sp), _arg(num, *d["MC"], "num"),
+                                       _arg(den, *d["M"], "den"), _arg(S, *d["MC"], "S"), _arg(W, *d["G"], "W"),
+                                       _ptr(ws), ws.numel(), _stream(stream)))
 
 
 def pa_deslice_w(dims, W, Sp, y, ws, stream=None):
-    _check(load().pa_deslice_w(ctypes.byref(dims), _ptr(W), _ptr(Sp), _ptr(y), _ptr(ws),
-                               ws.numel(), _stream(stream)))
+    d = _shapes(dims)
+    _check(load().pa_deslice_w(ctypes.byref(dims), _arg(W, *d["G"], "W"), _arg(Sp, *d["MC"], "Sp"),
+                               _arg(y, *d["x"], "y"), _ptr(ws), ws.numel(), _stream(stream)))
 
 
 def pa_deslice_backward_w(dims, W, dY, dSp, ws, stream=None):
-    _check(load().pa_deslice_backward_w(ctypes.byref(dims), _ptr(W), _ptr(dY), _ptr(dSp),
-                                        _ptr(ws), ws.numel(), _stream(stream)))
+    d = _shapes(dims)
+    _check(load().pa_deslice_backward_w(ctypes.byref(dims), _arg(W, *d["G"], "W"), _arg(dY, *d["x"], "dY"),
+                                        _arg(dSp, *d["MC"], "dSp"), _ptr(ws), ws.numel(),
+                                        _stream(stream)))
 
 
 def pa_time_kernel(call: Optional[str], start=None, stop=None):
@@ -424,7 +519,10 @@ def pa_heads_sum(src, dst, H, blockdiag, stream=None):
 def make_heads_params(A, b=None, a=None, b_t=None, shared=False) -> pa_heads_params:
     """A [heads,D,M] (or [D,M] with shared) etc.; b_t a device fp32 tensor
     [heads] (or [1] with shared)."""
-    return pa_heads_params(_ptr(A), _ptr(b), _ptr(a), _ptr(b_t), int(bool(shared)))
+    sh = bool(shared)
+    return _with(pa_heads_params(_ptr(A), _ptr(b), _ptr(a), _ptr(b_t), int(sh)),
+                 A=(A, "CM" if sh else "hCM"), b=(b, "M" if sh else "hM"),
+                 a=(a, "C" if sh else "hC"), b_t=(b_t, "1" if sh else "h"))
 
 
 def pa_heads_workspace_size(dims, heads: int) -> int:
@@ -439,25 +537,39 @@ def heads_workspace(dims, heads: int, device="cuda"):
 
 
 def pa_heads_slice_aggregate(dims, heads, x, G, hp, num, den, S, ws, stream=None):
-    _check(load().pa_heads_slice_aggregate(ctypes.byref(dims), heads, _ptr(x), _ptr(G),
-                                           ctypes.byref(hp), _ptr(num), _ptr(den), _ptr(S),
-                                           _ptr(ws), ws.numel(), _stream(stream)))
+    d = _shapes(dims, heads)
+    _check_struct(hp, dims, heads)
+    _check(load().pa_heads_slice_aggregate(ctypes.byref(dims), heads, _arg(x, *d["x"], "x"),
+                                           _arg(G, *d["G"], "G"), ctypes.byref(hp),
+                                           _arg(num, *d["MC"], "num"), _arg(den, *d["M"], "den"),
+                                           _arg(S, *d["MC"], "S"), _ptr(ws), ws.numel(),
+                                           _stream(stream)))
 
 
 def pa_heads_deslice(dims, heads, x, G, hp, Sp, y, ws, stream=None):
-    _check(load().pa_heads_deslice(ctypes.byref(dims), heads, _ptr(x), _ptr(G), ctypes.byref(hp),
-                                   _ptr(Sp), _ptr(y), _ptr(ws), ws.numel(), _stream(stream)))
+    d = _shapes(dims, heads)
+    _check_struct(hp, dims, heads)
+    _check(load().pa_heads_deslice(ctypes.byref(dims), heads, _arg(x, *d["x"], "x"), _arg(G, *d["G"], "G"),
+                                   ctypes.byref(hp), _arg(Sp, *d["MC"], "Sp"), _arg(y, *d["x"], "y"),
+                                   _ptr(ws), ws.numel(), _stream(stream)))
 
 
 def pa_heads_deslice_backward(dims, heads, x, G, hp, dY, dSp, ws, stream=None):
-    _check(load().pa_heads_deslice_backward(ctypes.byref(dims), heads, _ptr(x), _ptr(G),
-                                            ctypes.byref(hp), _ptr(dY), _ptr(dSp), _ptr(ws),
+    d = _shapes(dims, heads)
+    _check_struct(hp, dims, heads)
+    _check(load().pa_heads_deslice_backward(ctypes.byref(dims), heads, _arg(x, *d["x"], "x"),
+                                            _arg(G, *d["G"], "G"), ctypes.byref(hp),
+                                            _arg(dY, *d["x"], "dY"), _arg(dSp, *d["MC"], "dSp"), _ptr(ws),
                                             ws.numel(), _stream(stream)))
 
 
 def pa_heads_slice_aggregate_backward(dims, heads, x, G, hp, num, den, dS, Sp, dY, dx, gr, ws,
                                       stream=None):
+    d = _shapes(dims, heads)
+    _check_struct(hp, dims, heads)
+    _check_struct(gr, dims, heads, stacked=True)
     _check(load().pa_heads_slice_aggregate_backward(
-        ctypes.byref(dims), heads, _ptr(x), _ptr(G), ctypes.byref(hp), _ptr(num), _ptr(den),
-        _ptr(dS), _ptr(Sp), _ptr(dY), _ptr(dx), ctypes.byref(gr), _ptr(ws), ws.numel(),
+        ctypes.byref(dims), heads, _arg(x, *d["x"], "x"), _arg(G, *d["G"], "G"), ctypes.byref(hp),
+        _arg(num, *d["MC"], "num"), _arg(den, *d["M"], "den"), _arg(dS, *d["MC"], "dS"), _arg(Sp, *d["MC"], "Sp"),
+        _arg(dY, *d["x"], "dY"), _arg(dx, *d["x"], "dx"), ctypes.byref(gr), _ptr(ws), ws.numel(),
         _stream(stream)))

@@ -64,7 +64,9 @@ Layout layout_of(const pa_dims& d) {
   const int64_t rec = (int64_t)d.C * d.M + d.M + d.C + 1;  // the largest record
   const int P = pa::kPartialsMax;
   const size_t mc = (size_t)d.M * d.C;
-  const size_t attn = (8 * mc + (size_t)d.H * d.M * d.M) * sizeof(float);
+  // token scratch: eight [M,C] matrices in double (fp32 storage) or float,
+  // and the attention matrices of the heads
+  const size_t attn = (16 * mc + (size_t)d.H * d.M * d.M) * sizeof(float);
   L.img = 0;
   L.parts = up(img);
   L.attn = L.parts + up((size_t)P * rec * sizeof(float));
@@ -397,6 +399,107 @@ pa_status attn_forward_general(const pa_dims& d, const float* S, const pa_attn_p
   return PA_OK;
 }
 
+// Double-precision token side (fp32 storage): the same eight matrices as
+// doubles over the same region.
+struct AttnWs64 {
+  double *Q, *K, *V, *O, *dO, *dQ, *dK, *dV;
+};
+AttnWs64 attn_ws64(const pa_dims& d, void* ws) {
+  const size_t mc = (size_t)d.M * d.C;
+  double* base = reinterpret_cast<double*>(wsb(ws) + layout_of(d).attn);
+  return {base, base + mc, base + 2 * mc, base + 3 * mc,
+          base + 4 * mc, base + 5 * mc, base + 6 * mc, base + 7 * mc};
+}
+
+// (this block has C linkage: no overloads)
+pa::Opnd64 opf(const float* p, int64_t rs, int64_t cs) { return {p, rs, cs, 0}; }
+pa::Opnd64 opd(const double* p, int64_t rs, int64_t cs) { return {p, rs, cs, 1}; }
+
+// out [rows, cols] = sum_t A_t B_t (+ bias): one product of a batch.
+pa::MM64& mm64_add(pa::MM64Batch& b, int rows, int cols, void* out, bool out_dbl,
+                   const float* bias = nullptr) {
+  pa::MM64& q = b.p[b.n++];
+  q = pa::MM64{};
+  q.rows = rows; q.cols = cols; q.ld = cols;
+  q.out = out; q.out_dbl = out_dbl ? 1 : 0; q.bias = bias;
+  return q;
+}
+void mm64_term(pa::MM64& q, pa::Opnd64 A, pa::Opnd64 B, int K) {
+  q.A[q.nt] = A; q.B[q.nt] = B; q.K[q.nt] = K;
+  ++q.nt;
+}
+
+// Q, K, V = S W + b in double.
+pa_status attn64_project(const pa_dims& d, const float* S, const pa_attn_params* ap,
+                         const AttnWs64& w, hipStream_t st) {
+  const int M = d.M, C = d.C;
+  const float* W[3] = {ap->Wq, ap->Wk, ap->Wv};
+  const float* bias[3] = {ap->bq, ap->bk, ap->bv};
+  double* out[3] = {w.Q, w.K, w.V};
+  pa::MM64Batch b{};
+  for (int p = 0; p < 3; ++p)
+    mm64_term(mm64_add(b, M, C, out[p], true, bias[p]), opf(S, C, 1), opf(W[p], C, 1), C);
+  PA_HIP(pa::launch_mm64(b, st), "QKV projection (double)");
+  return PA_OK;
+}
+
+pa_status attn64_forward(const pa_dims& d, const float* S, const pa_attn_params* ap, float* Sp,
+                         void* ws, hipStream_t st) {
+  const int M = d.M, C = d.C;
+  const AttnWs64 w = attn_ws64(d, ws);
+  PA_TRY(attn64_project(d, S, ap, w, st));
+  if (!ap->Wo) {
+    PA_HIP(pa::launch_core64(w.Q, w.K, w.V, Sp, false, M, C, d.H, st), "attention core (double)");
+    return PA_OK;
+  }
+  PA_HIP(pa::launch_core64(w.Q, w.K, w.V, w.O, true, M, C, d.H, st), "attention core (double)");
+  pa::MM64Batch b{};
+  mm64_term(mm64_add(b, M, C, Sp, false, ap->bo), opd(w.O, C, 1), opf(ap->Wo, C, 1), C);
+  PA_HIP(pa::launch_mm64(b, st), "output projection (double)");
+  return PA_OK;
+}
+
+pa_status attn64_backward(const pa_dims& d, const float* S, const pa_attn_params* ap,
+                          const float* dSp, float* dS, const pa_attn_grads* ag, void* ws,
+                          hipStream_t st) {
+  const int M = d.M, C = d.C;
+  const AttnWs64 w = attn_ws64(d, ws);
+  const bool wantWo = ag && ap->Wo && (ag->dWo || ag->dbo);
+  if (ap->Wo) {  // dO = dSp Wo^T
+    pa::MM64Batch b{};
+    mm64_term(mm64_add(b, M, C, w.dO, true), opf(dSp, C, 1), opf(ap->Wo, 1, C), C);
+    PA_HIP(pa::launch_mm64(b, st), "dO (double)");
+  }
+  PA_TRY(attn64_project(d, S, ap, w, st));
+  const void* dO = ap->Wo ? static_cast<const void*>(w.dO) : static_cast<const void*>(dSp);
+  PA_HIP(pa::launch_core64_bwd(w.Q, w.K, w.V, dO, ap->Wo != nullptr, w.dQ, w.dK, w.dV,
+                               wantWo ? w.O : nullptr, M, C, d.H, st),
+         "attention core backward (double)");
+  // dS = sum_p dX_p W_p^T; dW_p = S^T dX_p, db_p = 1^T dX_p; dWo = O^T dSp
+  pa::MM64Batch b{};
+  const double* dX[3] = {w.dQ, w.dK, w.dV};
+  const float* W[3] = {ap->Wq, ap->Wk, ap->Wv};
+  pa::MM64& qs = mm64_add(b, M, C, dS, false);
+  for (int p = 0; p < 3; ++p) mm64_term(qs, opd(dX[p], C, 1), opf(W[p], 1, C), C);
+  if (ag) {
+    float* dW[3] = {ag->dWq, ag->dWk, ag->dWv};
+    float* db[3] = {ag->dbq, ag->dbk, ag->dbv};
+    for (int p = 0; p < 3; ++p) {
+      if (dW[p]) mm64_term(mm64_add(b, C, C, dW[p], false), opf(S, 1, C), opd(dX[p], C, 1), M);
+      if (db[p])
+        mm64_term(mm64_add(b, 1, C, db[p], false), opf(nullptr, 0, 0),
+                  opd(dX[p], C, 1), M);
+    }
+    if (wantWo && ag->dWo)
+      mm64_term(mm64_add(b, C, C, ag->dWo, false), opd(w.O, 1, C), opf(dSp, C, 1), M);
+    if (wantWo && ag->dbo)
+      mm64_term(mm64_add(b, 1, C, ag->dbo, false), opf(nullptr, 0, 0),
+                opf(dSp, C, 1), M);
+  }
+  PA_HIP(pa::launch_mm64(b, st), "token gradients (double)");
+  return PA_OK;
+}
+
 pa::HeadArgs head_args(const pa_dims& d, const float* S, const pa_attn_params* ap) {
   pa::HeadArgs h{};
   h.S = S;
@@ -414,6 +517,7 @@ pa_status pa_token_attention(const pa_dims* dims, const float* S, const pa_attn_
   PA_TRY(check_ws(*dims, ws, ws_bytes));
   hipStream_t st = as_stream(stream);
   const pa_dims& d = *dims;
+  if (d.dtype == PA_F32) return attn64_forward(d, S, ap, Sp, ws, st);
   const AttnWs w = attn_ws(d, ws);
   // the heads' output: straight to Sp without an output projection
   float* O = ap->Wo ? w.O : Sp;
@@ -447,6 +551,7 @@ pa_status pa_token_attention_backward(const pa_dims* dims, const float* S,
   PA_TRY(check_ws(*dims, ws, ws_bytes));
   hipStream_t st = as_stream(stream);
   const pa_dims& d = *dims;
+  if (d.dtype == PA_F32) return attn64_backward(d, S, ap, dSp, dS, ag, ws, st);
   const int M = d.M, C = d.C;
   const AttnWs w = attn_ws(d, ws);
   const float* dO = dSp;

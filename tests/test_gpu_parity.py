@@ -30,6 +30,9 @@ SHAPES = [
     (66013, 256, 8, 32, "bf16"),
     (50003, 256, 8, 64, "bf16"),
     (40007, 128, 8, 32, "f32"),
+    # the 128 x 128 grid workload's shape (fp32, M = 64: two waves per CU in
+    # the backward, several tiles each)
+    (16384, 128, 8, 64, "f32"),
 ]
 IDS = [f"N{n}-C{c}-H{h}-M{m}-{d}" for n, c, h, m, d in SHAPES]
 
@@ -240,11 +243,10 @@ def test_slice_weights_backward(cases, shape):
 
 
 # The chain feeds every call the previous calls' outputs instead of the
-# oracle's: each call meets TOL on oracle inputs (the per-call tests above),
-# and the backward of the slice projection (dx, dA through dnum = dS / den and
-# the softmax backward) amplifies the relative error of its inputs by a
-# small factor.  With fp32 storage the chain is held to 5x the per-call bar.
-CHAIN_TOL = {"f32": 5 * TOL["f32"], "bf16": TOL["bf16"]}
+# oracle's, through the ABI's fp32 token tensors.  Those roundings alone use
+# under half of the fp32 bar (tests/test_oracle_rounding.py, on the oracle),
+# so the chained layer is held to the per-call bars.
+CHAIN_TOL = TOL
 
 
 @pytest.mark.parametrize("shape", SHAPES, ids=IDS)
@@ -369,3 +371,22 @@ def test_edge_cases(variant):
             check(k, out[k], f[k], c.dt)
         for k in ("dSp", "dS", "dx", "dA", "db", "da"):
             check(k, out[k], gr[k], c.dt)
+
+
+@pytest.mark.parametrize("name", ["grid2d_16k_f32", "ellipsoid_32k_bf16"])
+def test_workload_inputs(name):
+    """The benchmark workloads' own inputs (their geometry, seeds and zero
+    biases), the whole layer chained, recomputed and with stored weights."""
+    from paper_2502_02414_amd import inputs as I
+    w = I.WORKLOADS[name]
+    say(f"workload {name}")
+    c = make_case(w.N, w.C, w.H, w.M, w.dtype, workload=w, biases=False)
+    g = Gpu(c)
+    f, gr = oracle_layer(c)
+    for out in (g.layer(), g.layer_w()):
+        for k in ("num", "den", "S", "Sp", "y"):
+            check(k, out[k], f[k], c.dt)
+        for k in ("dSp", "dS", "dWq", "dbq", "dWk", "dWv", "dbv", "dx", "dA", "db", "da"):
+            check(k, out[k], gr[k], c.dt)
+        check_ada_temp(out, gr, c.dt)
+        check_key_bias(out["dbk"], out["dbq"], c.dt)
