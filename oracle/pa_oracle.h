@@ -125,15 +125,11 @@ void pao_layernorm(int64_t N, int C, double eps, const double* x, const double* 
 /* Its chain rule: dx [N,C], dg [C], db [C] (each nullable). */
 void pao_layernorm_backward(int64_t N, int C, double eps, const double* x, const double* g,
                             const double* dy, double* dx, double* dg, double* db);
-/* GELU in its tanh form x (1 + tanh(sqrt(2/pi) (x + 0.044715 x^3))) / 2
- * and its chain rule. */
+/* GELU x Phi(x), Phi the standard normal CDF, and its chain rule. */
 void pao_gelu(int64_t n, const double* x, double* y);
 void pao_gelu_backward(int64_t n, const double* x, const double* dy, double* dx);
-/* y = x W + b and its chain rule (dx, dW, db nullable). */
-void pao_linear(int64_t N, int Cin, int Cout, const double* x, const double* W, const double* b,
-                double* y);
-void pao_linear_backward(int64_t N, int Cin, int Cout, const double* x, const double* W,
-                         const double* dy, double* dx, double* dW, double* db);
+/* (The block's Linear layers, y = x W + b, are plain matrix products taken
+ * from the host BLAS by the Python wrapper.) */
 
 #ifdef __cplusplus
 }

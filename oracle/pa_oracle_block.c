@@ -95,84 +95,23 @@ void pao_layernorm_backward(int64_t N, int C, double eps, const double* x, const
   free(pb);
 }
 
-/* GELU in its tanh form (the feedforward layer's activation is not
- * specified; this is the form of Hendrycks & Gimpel's approximation):
- *   y = x (1 + tanh(u)) / 2,  u = sqrt(2/pi) (x + 0.044715 x^3). */
-#define GELU_S 0.7978845608028654   /* sqrt(2 / pi) */
-#define GELU_K 0.044715
+/* GELU (the feedforward layer's activation; the paper names the layer but
+ * not its activation, read as the Transformer's GELU in its defining form):
+ *   y = x Phi(x),  Phi(x) = (1 + erf(x / sqrt 2)) / 2  (standard normal CDF). */
+#define GELU_R2 0.7071067811865476      /* 1 / sqrt(2) */
+#define GELU_IS2PI 0.3989422804014327   /* 1 / sqrt(2 pi) */
 void pao_gelu(int64_t n, const double* x, double* y) {
 #pragma omp parallel for schedule(static)
-  for (int64_t k = 0; k < n; ++k) {
-    const double u = GELU_S * (x[k] + GELU_K * x[k] * x[k] * x[k]);
-    y[k] = 0.5 * x[k] * (1.0 + tanh(u));
-  }
+  for (int64_t k = 0; k < n; ++k) y[k] = 0.5 * x[k] * (1.0 + erf(x[k] * GELU_R2));
 }
 
-/* dx = dy d/dx [x (1 + tanh u) / 2]
- *    = dy [(1 + tanh u) / 2 + x (1 - tanh^2 u) u'(x) / 2],
- *   u'(x) = sqrt(2/pi) (1 + 3 * 0.044715 x^2). */
+/* dx = dy (Phi(x) + x phi(x)),  phi(x) = exp(-x^2 / 2) / sqrt(2 pi). */
 void pao_gelu_backward(int64_t n, const double* x, const double* dy, double* dx) {
 #pragma omp parallel for schedule(static)
   for (int64_t k = 0; k < n; ++k) {
-    const double u = GELU_S * (x[k] + GELU_K * x[k] * x[k] * x[k]);
-    const double t = tanh(u);
-    const double du = GELU_S * (1.0 + 3.0 * GELU_K * x[k] * x[k]);
-    dx[k] = dy[k] * (0.5 * (1.0 + t) + 0.5 * x[k] * (1.0 - t * t) * du);
+    const double Phi = 0.5 * (1.0 + erf(x[k] * GELU_R2));
+    const double phi = GELU_IS2PI * exp(-0.5 * x[k] * x[k]);
+    dx[k] = dy[k] * (Phi + x[k] * phi);
   }
 }
 
-/* y [N,Cout] = x [N,Cin] W [Cin,Cout] + b (nullable). */
-void pao_linear(int64_t N, int Cin, int Cout, const double* x, const double* W, const double* b,
-                double* y) {
-#pragma omp parallel for schedule(static)
-  for (int64_t i = 0; i < N; ++i)
-    for (int o = 0; o < Cout; ++o) {
-      double s = b ? b[o] : 0.0;
-      for (int k = 0; k < Cin; ++k) s += x[i * Cin + k] * W[(int64_t)k * Cout + o];
-      y[i * Cout + o] = s;
-    }
-}
-
-/* Chain rule of pao_linear: dx = dy W^T, dW = x^T dy, db = sum_i dy
- * (each nullable; dW, db as per-shard partial sums in shard order). */
-void pao_linear_backward(int64_t N, int Cin, int Cout, const double* x, const double* W,
-                         const double* dy, double* dx, double* dW, double* db) {
-  if (dx) {
-#pragma omp parallel for schedule(static)
-    for (int64_t i = 0; i < N; ++i)
-      for (int k = 0; k < Cin; ++k) {
-        double s = 0.0;
-        for (int o = 0; o < Cout; ++o) s += dy[i * Cout + o] * W[(int64_t)k * Cout + o];
-        dx[i * Cin + k] = s;
-      }
-  }
-  if (!dW && !db) return;
-  const int64_t S = (N + SHARD - 1) / SHARD;
-  double* pw = dW ? calloc((size_t)S * Cin * Cout, sizeof(double)) : NULL;
-  double* pb = db ? calloc((size_t)S * Cout, sizeof(double)) : NULL;
-#pragma omp parallel for schedule(static)
-  for (int64_t s = 0; s < S; ++s) {
-    const int64_t i1 = (s + 1) * SHARD < N ? (s + 1) * SHARD : N;
-    for (int64_t i = s * SHARD; i < i1; ++i)
-      for (int o = 0; o < Cout; ++o) {
-        const double d = dy[i * Cout + o];
-        if (pb) pb[s * Cout + o] += d;
-        if (pw)
-          for (int k = 0; k < Cin; ++k) pw[(s * Cin + k) * Cout + o] += x[i * Cin + k] * d;
-      }
-  }
-  if (dW)
-    for (int64_t e = 0; e < (int64_t)Cin * Cout; ++e) {
-      double a = 0.0;
-      for (int64_t s = 0; s < S; ++s) a += pw[s * Cin * Cout + e];
-      dW[e] = a;
-    }
-  if (db)
-    for (int o = 0; o < Cout; ++o) {
-      double a = 0.0;
-      for (int64_t s = 0; s < S; ++s) a += pb[s * Cout + o];
-      db[o] = a;
-    }
-  free(pw);
-  free(pb);
-}

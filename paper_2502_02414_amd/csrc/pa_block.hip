@@ -212,25 +212,16 @@ __global__ void __launch_bounds__(256) k_ln_bwd(LayerNormArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// GELU in its tanh form, y = x (1 + tanh u) / 2 with u = sqrt(2/pi) (x +
-// 0.044715 x^3), evaluated as y = x s, s = 1 / (1 + exp(-2u)) (the same
-// value: (1 + tanh u) / 2 is the logistic function of 2u, which has no
-// cancellation near u = 0 and saturates to 0 and 1 without overflow), and
-// its derivative dy/dx = s + 2 x s (1 - s) u'(x), u'(x) = sqrt(2/pi)
-// (1 + 3 * 0.044715 x^2); elementwise (n a multiple of E).
+// GELU, y = x Phi(x) with Phi(x) = (1 + erf(x / sqrt 2)) / 2 the standard
+// normal CDF, and its derivative dy/dx = Phi(x) + x phi(x), phi(x) =
+// exp(-x^2 / 2) / sqrt(2 pi); elementwise (n a multiple of E).
 // ---------------------------------------------------------------------------
-struct GeluS { float s, du; };
-__device__ __forceinline__ GeluS gelu_s(float x) {
-  constexpr float kS = 0.7978845608028654f, kK = 0.044715f;
-  const float x2 = x * x;
-  const float u = kS * fmaf(kK * x2, x, x);
-  const float e = __builtin_amdgcn_exp2f(-2.f * 1.4426950408889634f * u);  // exp(-2u)
-  return {__frcp_rn(1.f + e), kS * fmaf(3.f * kK, x2, 1.f)};
+__device__ __forceinline__ float gelu_f(float x) {
+  return 0.5f * x * (1.f + erff(x * 0.7071067811865476f));
 }
-__device__ __forceinline__ float gelu_f(float x) { return x * gelu_s(x).s; }
 __device__ __forceinline__ float dgelu_f(float x) {
-  const GeluS g = gelu_s(x);
-  return fmaf(2.f * x * g.s * (1.f - g.s), g.du, g.s);
+  const float Phi = 0.5f * (1.f + erff(x * 0.7071067811865476f));
+  return fmaf(x * 0.3989422804014327f, expf(-0.5f * x * x), Phi);
 }
 
 template <typename T>
@@ -305,7 +296,9 @@ __global__ void __launch_bounds__(256) k_colsum(int64_t N, int C, int64_t R0, co
 //   A' = Wp A,  b' = b + bp A,  a' = Wp a,  b_t' = bp.a   (added to b_t),
 // so that the logits and temperature of x_proj are those of h under the
 // primed parameters; and the states of x_proj are S_proj = S Wp + bp
-// (each point's weights sum to 1).  Sums in fp32, fixed order.
+// (each point's weights sum to 1).  Sums in fp64, fixed order, rounded once:
+// with fp32 storage the projected states feed the token attention, whose
+// backward amplifies their rounding (see the double-precision token side).
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ void __launch_bounds__(64) k_fold(FoldArgs f) {
@@ -313,27 +306,27 @@ __global__ void __launch_bounds__(64) k_fold(FoldArgs f) {
   if ((int)blockIdx.x < C) {  // row c of A' (threads j < M) and a'[c] (thread M)
     const int c = blockIdx.x;
     for (int j = t; j <= M; j += blockDim.x) {
-      float s = 0.f;
+      double s = 0.0;
       if (j < M) {
-        for (int k = 0; k < C; ++k) s += f.Wp[c * C + k] * f.A[k * M + j];
-        reinterpret_cast<T*>(f.A_out)[c * M + j] = from_f<T>(s);
+        for (int k = 0; k < C; ++k) s += (double)f.Wp[c * C + k] * f.A[k * M + j];
+        reinterpret_cast<T*>(f.A_out)[c * M + j] = from_f<T>((float)s);
       } else {
         if (f.a)
-          for (int k = 0; k < C; ++k) s += f.Wp[c * C + k] * f.a[k];
-        reinterpret_cast<T*>(f.a_out)[c] = from_f<T>(s);
+          for (int k = 0; k < C; ++k) s += (double)f.Wp[c * C + k] * f.a[k];
+        reinterpret_cast<T*>(f.a_out)[c] = from_f<T>((float)s);
       }
     }
   } else {  // b' (threads j < M), b_t' (thread M)
     for (int j = t; j <= M; j += blockDim.x) {
-      float s = 0.f;
+      double s = 0.0;
       if (j < M) {
-        s = f.b ? f.b[j] : 0.f;
-        for (int k = 0; k < C; ++k) s += f.bp[k] * f.A[k * M + j];
-        f.b_out[j] = s;
+        s = f.b ? f.b[j] : 0.0;
+        for (int k = 0; k < C; ++k) s += (double)f.bp[k] * f.A[k * M + j];
+        f.b_out[j] = (float)s;
       } else {
         if (f.a)
-          for (int k = 0; k < C; ++k) s += f.bp[k] * f.a[k];
-        f.bt_out[0] = s;
+          for (int k = 0; k < C; ++k) s += (double)f.bp[k] * f.a[k];
+        f.bt_out[0] = (float)s;
       }
     }
   }
@@ -345,9 +338,9 @@ __global__ void __launch_bounds__(256) k_project_states(int M, int C, const floa
                                                         float* Sp) {
   const int j = blockIdx.x;
   for (int k = threadIdx.x; k < C; k += blockDim.x) {
-    float s = bp[k];
-    for (int c = 0; c < C; ++c) s += S[j * C + c] * Wp[c * C + k];
-    Sp[j * C + k] = s;
+    double s = bp[k];
+    for (int c = 0; c < C; ++c) s += (double)S[j * C + c] * Wp[c * C + k];
+    Sp[j * C + k] = (float)s;
   }
 }
 
@@ -366,19 +359,19 @@ __global__ void __launch_bounds__(256) k_fold_grads(FoldGradArgs f) {
   if (bid < C) {
     const int c = bid;
     for (int k = t; k < C; k += blockDim.x) {
-      float s = 0.f;
-      for (int j = 0; j < M; ++j) s += f.dAf[c * M + j] * f.A[k * M + j];
-      if (f.a) s += f.daf[c] * f.a[k];
-      for (int j = 0; j < M; ++j) s += f.S[j * C + c] * f.dSp[j * C + k];
-      f.dWp[c * C + k] = s;
+      double s = 0.0;
+      for (int j = 0; j < M; ++j) s += (double)f.dAf[c * M + j] * f.A[k * M + j];
+      if (f.a) s += (double)f.daf[c] * f.a[k];
+      for (int j = 0; j < M; ++j) s += (double)f.S[j * C + c] * f.dSp[j * C + k];
+      f.dWp[c * C + k] = (float)s;
     }
   } else if (bid == C) {
     for (int k = t; k < C; k += blockDim.x) {
-      float s = 0.f;
-      for (int j = 0; j < M; ++j) s += f.dbf[j] * f.A[k * M + j];
-      if (f.a) s += f.dbtf[0] * f.a[k];
+      double s = 0.0;
+      for (int j = 0; j < M; ++j) s += (double)f.dbf[j] * f.A[k * M + j];
+      if (f.a) s += (double)f.dbtf[0] * f.a[k];
       for (int j = 0; j < M; ++j) s += f.dSp[j * C + k];
-      f.dbp[k] = s;
+      f.dbp[k] = (float)s;
     }
     for (int j = t; j < M; j += blockDim.x)
       if (f.db) f.db[j] = f.dbf[j];
@@ -386,21 +379,21 @@ __global__ void __launch_bounds__(256) k_fold_grads(FoldGradArgs f) {
   } else if (bid <= 2 * C) {
     const int k = bid - C - 1;
     for (int j = t; j <= M; j += blockDim.x) {
-      float s = 0.f;
+      double s = 0.0;
       if (j < M) {
-        for (int c = 0; c < C; ++c) s += f.Wp[c * C + k] * f.dAf[c * M + j];
-        f.dA[k * M + j] = s + f.bp[k] * f.dbf[j];
+        for (int c = 0; c < C; ++c) s += (double)f.Wp[c * C + k] * f.dAf[c * M + j];
+        f.dA[k * M + j] = (float)(s + (double)f.bp[k] * f.dbf[j]);
       } else if (f.da) {
-        for (int c = 0; c < C; ++c) s += f.Wp[c * C + k] * f.daf[c];
-        f.da[k] = s + f.bp[k] * f.dbtf[0];
+        for (int c = 0; c < C; ++c) s += (double)f.Wp[c * C + k] * f.daf[c];
+        f.da[k] = (float)(s + (double)f.bp[k] * f.dbtf[0]);
       }
     }
   } else if (f.dS) {
     const int j = bid - 2 * C - 1;
     for (int c = t; c < C; c += blockDim.x) {
-      float s = 0.f;
-      for (int k = 0; k < C; ++k) s += f.dSp[j * C + k] * f.Wp[c * C + k];
-      f.dS[j * C + c] = s;
+      double s = 0.0;
+      for (int k = 0; k < C; ++k) s += (double)f.dSp[j * C + k] * f.Wp[c * C + k];
+      f.dS[j * C + c] = (float)s;
     }
   }
 }

@@ -4,21 +4,27 @@ C ABI.
 Each primitive is compared with the oracle's function on the same stored
 values (LayerNorm with the fused residual add, its backward, GELU), or with
 its plain definition in float64 numpy (the GEMM, the column sums, the
-Project folding algebra).  The stack runner (LN -> Physics-Attention with
-the folded Project step -> MLP, residual adds, several blocks) is compared
-with oracle.stack_forward / stack_backward, which applies the Project step
-explicitly.  Bars: relative L2 1e-5 per primitive in fp32 and 2e-2 in bf16.
-The stack chains two blocks; its backward stores about ten intermediate
-gradients per block in the storage dtype (dGELU, du, dLN2, dx1, dh, dx),
-each adding up to 2^-9 of relative rounding error in bf16, so the stack's
-bars are 1e-4 in fp32 (measured <= 1.5e-5) and 4e-2 in bf16 (measured
-1e-2 to 2.5e-2).  With the generator's Xavier Ada-Temp projection about a
-third of a block's points sit at the temperature floor tau_min, where the
-softmax is 1/tau_min = 100 times sharper: there an exact evaluation moves
-dA by 10-14 % when only its forward inputs (LN1(x), the folded A') are
-rounded to bf16, so no bf16 path can meet a fixed bar on it.  The bf16
-stack cases scale that projection by 0.05 (no point at the floor, asserted);
-the fp32 case keeps the floor and checks every gradient at 1e-4.
+Project folding algebra), at relative L2 1e-5 in fp32 and 2e-2 in bf16.
+
+The stack runner (LN -> Physics-Attention with the folded Project step ->
+MLP, residual adds, several blocks) is compared with oracle.stack_forward /
+stack_backward, which applies the Project step explicitly.  The stack
+stores its point-side intermediates in the storage dtype, and those
+roundings alone move the exact result.  tests/stack_rounding.py evaluates
+the oracle's own stack with exactly those roundings: its distance from the
+exact stack (the envelope) and the distance between two such evaluations
+whose values differ in the last bits before each rounding (the flip spread)
+are measured per output tensor on the CPU, on the same inputs.  An output
+is held to max(plain bar, 2 x envelope) (plain bars: 1e-5 fp32, 2e-2
+bf16); with bf16 storage only when its flip spread is below 2e-2, for
+otherwise no evaluation with bf16 storage can pin it, and it is checked for
+finiteness.  That happens in bf16 where a block's Ada-Temp leaves points at
+the temperature floor tau_min: the softmax is 1/tau_min = 100 times
+sharper, the slice-parameter gradients (dA, db, da, b_t) move by tens of
+percent when only the block's input LN1(x) or the folded A' is rounded to
+bf16, and in a deep stack the backward carries that into every gradient
+below the block.  Without clamped points (the Ada-Temp projection scaled by
+0.05) and in fp32 every output is pinned.
 """
 import numpy as np
 import pytest
@@ -30,7 +36,6 @@ from pa_cases import TOL, dev, host, rel_l2, say
 
 pytestmark = pytest.mark.gpu
 
-STACK_TOL = {"f32": 1e-4, "bf16": 4e-2}
 
 
 def check(name, got, ref, bar):
@@ -219,42 +224,91 @@ def device_params(ps, dt):
     return out
 
 
-STACKS = [(2000, 64, 4, 16, 2, "f32"), (2000, 64, 4, 16, 2, "bf16"),
-          (3001, 256, 8, 32, 2, "bf16")]
+STACKS = [
+    # N, C, H, M, blocks, dtype, Ada-Temp scale
+    (2000, 64, 4, 16, 2, "f32", 1.0),
+    (2000, 64, 4, 16, 2, "bf16", 0.05),
+    (3001, 256, 8, 32, 2, "bf16", 0.05),
+    # the generator's Ada-Temp: about a third of the points at tau_min
+    (2000, 64, 4, 16, 2, "bf16", 1.0),
+    (3001, 256, 8, 32, 2, "bf16", 1.0),
+]
 
 
-@pytest.mark.parametrize("shape", STACKS, ids=[f"N{s[0]}-C{s[1]}-M{s[3]}-L{s[4]}-{s[5]}"
-                                               for s in STACKS])
-def test_block_stack(shape):
-    """GPU stack (folded Project) vs the oracle stack (explicit Project)."""
+def _compare_stack(N, C, H, M, L, dt, a_scale, geometry="normal"):
     from paper_2502_02414_amd.stack import BlockStack
+    import stack_rounding as SR
     import torch
-    N, C, H, M, L, dt = shape
-    say(f"stack {shape}")
-    w, x, dY, ps, Gs = stack_case(N, C, H, M, L, dt, a_scale=0.05 if dt == "bf16" else 1.0)
+    w, x, dY, ps, Gs = stack_case(N, C, H, M, L, dt, geometry=geometry, a_scale=a_scale)
     tdt = torch.bfloat16 if dt == "bf16" else torch.float32
     st = BlockStack(N, C, H, M, device_params(ps, dt), tdt, w.tau0, w.tau_min, w.eps)
     out = st.forward(dev(x, dt), [dev(G, dt) for G in Gs])
     dx, grads = st.backward(dev(dY, dt))
     torch.cuda.synchronize()
+    say("  GPU stack done; oracle stack and its rounded evaluation on the CPU")
     ref, caches = oracle.stack_forward(x, Gs, ps, w.tau0, w.tau_min, w.eps, H)
     for c in caches:  # the folded states are exact for den >= eps
         assert np.all(c["pa"]["den"] >= w.eps)
-        if dt == "bf16":
-            assert np.all(c["pa"]["t"] > w.tau_min)
+    clamped = [float(np.mean(c["pa"]["t"] <= w.tau_min)) for c in caches]
+    say(f"  points at tau_min per block: {np.round(clamped, 2).tolist()}")
     rdx, rgr = oracle.stack_backward(dY, Gs, ps, w.tau0, w.tau_min, w.eps, H, caches)
-    bar = STACK_TOL[dt]
-    check("out", host(out), ref, bar)
-    check("dx", host(dx), rdx, bar)
+    say("  oracle stack done")
+    env = SR.envelope(x, dY, Gs, ps, w.tau0, w.tau_min, w.eps, H, dt, ref, rdx, rgr)
+    say("  rounded evaluation done")
+    # (fp32 storage: the roundings are at the level of the evaluation's own
+    # last bits, and every output is pinned)
+    spread = SR.flip_spread(x, dY, Gs, ps, w.tau0, w.tau_min, w.eps, H, dt, log=say) \
+        if dt == "bf16" else None
+    unpinned = []
+
+    def cmp(key, name, got, want):
+        if spread is not None and spread[key] > TOL[dt]:
+            say(f"  {name:10s} not pinned (flip spread {spread[key]:.2e}, envelope "
+                f"{env[key]:.2e}); finite")
+            assert np.all(np.isfinite(got)), name
+            unpinned.append((key, name))
+            return
+        check(name, got, want, max(TOL[dt], 2.0 * env[key]))
+
+    cmp("out", "out", host(out), ref)
+    cmp("dx", "dx", host(dx), rdx)
     for l in range(L):
         say(f" layer {l}")
-        for k in ("dW2", "db2", "dW1", "db1", "dln2_g", "dln2_b", "dWq", "dbq", "dWk", "dWv",
-                  "dbv", "dWo", "dbo", "dWp", "dbp", "dA", "db", "dln1_g", "dln1_b"):
-            check(k, host(grads[l][k]), rgr[l][k], bar)
+        for k in SR.GRADS:
+            cmp((l, k), k, host(grads[l][k]), rgr[l][k])
         ga = np.concatenate([host(grads[l]["da"]).ravel(), host(grads[l]["db_t"]).ravel()])
-        check("d(a,b_t)", ga, np.concatenate([rgr[l]["da"].ravel(), [rgr[l]["db_t"]]]), bar)
+        cmp((l, "d(a,b_t)"), "d(a,b_t)", ga,
+            np.concatenate([rgr[l]["da"].ravel(), [rgr[l]["db_t"]]]))
         # the key bias shifts a whole score row: its gradient is 0 up to rounding
-        assert np.linalg.norm(host(grads[l]["dbk"])) <= bar * np.linalg.norm(host(grads[l]["dbq"]))
+        assert np.linalg.norm(host(grads[l]["dbk"])) <= \
+            TOL[dt] * np.linalg.norm(host(grads[l]["dbq"]))
+    say(f"  {len(unpinned)} outputs not pinned")
+    # the forward output and the input gradient are always pinned
+    assert "out" not in [k for k, _ in unpinned] and "dx" not in [k for k, _ in unpinned]
+    if a_scale < 1.0 or dt == "f32":
+        assert not unpinned
+    return clamped
+
+
+@pytest.mark.parametrize("shape", STACKS, ids=[f"N{s[0]}-C{s[1]}-M{s[3]}-L{s[4]}-{s[5]}-a{s[6]}"
+                                               for s in STACKS])
+def test_block_stack(shape):
+    """GPU stack (folded Project) vs the oracle stack (explicit Project)."""
+    say(f"stack {shape}")
+    clamped = _compare_stack(*shape)
+    if shape[6] < 1.0:
+        assert max(clamped) == 0.0
+    else:
+        assert max(clamped) > 0.2
+
+
+def test_block_stack_eight_blocks():
+    """The configuration of the full-size stack (8 blocks, C = 256, H = 8,
+    M = 64, bf16, the aircraft-surface inputs and the generator's weights)
+    at N = 50,000 points (several 16-point tiles per wave in every streaming
+    pass), every output and gradient against the oracle."""
+    say("stack 8 blocks, N=50000 C=256 H=8 M=64 bf16 (aircraft surface)")
+    _compare_stack(50000, 256, 8, 64, 8, "bf16", 1.0, geometry="aircraft")
 
 
 def test_block_stack_full_size():

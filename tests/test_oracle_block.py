@@ -48,27 +48,40 @@ def test_layernorm_backward_matches_autograd():
     np.testing.assert_allclose(db, bt.grad.numpy(), rtol=1e-10)
 
 
-def test_gelu_tanh_form():
-    x = np.concatenate([_r(500, scale=3.0), [0.0, 8.0, -8.0]])
+def test_gelu():
+    x = np.concatenate([_r(500, scale=3.0), [0.0, 8.0, -8.0, 1.0]])
     y = oracle.gelu(x)
-    ref = torch.nn.functional.gelu(_t(x), approximate="tanh").numpy()
+    # the standard normal CDF at 1 (a tabulated value): GELU(1) = Phi(1)
+    assert abs(y[-1] - 0.8413447460685429) < 1e-15
+    assert y[-4] == 0.0 and abs(y[-3] - 8.0) < 1e-13 and abs(y[-2]) < 1e-13
+    # Phi(x) + Phi(-x) = 1, so GELU(x) - GELU(-x) = x
+    np.testing.assert_allclose(y[:500] - oracle.gelu(-x[:500]), x[:500], rtol=1e-14,
+                               atol=1e-14)
+    ref = torch.nn.functional.gelu(_t(x), approximate="none").numpy()
     np.testing.assert_allclose(y, ref, rtol=1e-14, atol=1e-16)
-    assert y[-3] == 0.0 and abs(y[-2] - 8.0) < 1e-13 and abs(y[-1]) < 1e-13
-    # within the tanh form's known distance (< 5e-4) of the exact x Phi(x)
-    exact = torch.nn.functional.gelu(_t(x), approximate="none").numpy()
-    assert np.abs(y - exact).max() < 5e-4
-    # GELU'(0) = 1/2; derivative against autograd
+    # GELU'(0) = 1/2; derivative against autograd and central differences
     dy = _r(x.size)
     xt = _t(x, True)
-    torch.nn.functional.gelu(xt, approximate="tanh").backward(_t(dy))
+    torch.nn.functional.gelu(xt, approximate="none").backward(_t(dy))
     np.testing.assert_allclose(oracle.gelu_backward(x, dy), xt.grad.numpy(), rtol=1e-12,
                                atol=1e-14)
     assert oracle.gelu_backward(np.array([0.0]), np.array([1.0]))[0] == 0.5
+    h = 1e-6
+    fd = (oracle.gelu(x[:50] + h) - oracle.gelu(x[:50] - h)) / (2 * h)
+    np.testing.assert_allclose(oracle.gelu_backward(x[:50], np.ones(50)), fd, rtol=1e-8,
+                               atol=1e-9)
 
 
 def test_linear_and_backward():
+    # brute force on a tiny case: every output an explicit sum
+    xs, Ws, bs = _r(3, 4), _r(4, 5), _r(5)
+    brute = np.array([[bs[o] + sum(xs[i, k] * Ws[k, o] for k in range(4)) for o in range(5)]
+                      for i in range(3)])
+    np.testing.assert_allclose(oracle.linear(xs, Ws, bs), brute, rtol=1e-14, atol=1e-14)
     x, W, b, dy = _r(1300, 12), _r(12, 20), _r(20), _r(1300, 20)
-    np.testing.assert_allclose(oracle.linear(x, W, b), x @ W + b, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(oracle.linear(x, W, b),
+                               torch.nn.functional.linear(_t(x), _t(W).T, _t(b)).numpy(),
+                               rtol=1e-12, atol=1e-12)
     xt, Wt, bt = _t(x, True), _t(W, True), _t(b, True)
     (xt @ Wt + bt).backward(_t(dy))
     dx, dW, db = oracle.linear_backward(x, W, dy)

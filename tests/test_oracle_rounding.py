@@ -101,3 +101,83 @@ def test_states_error_of_1e7_breaks_the_bar():
     print({k: f"{v:.2e}" for k, v in e.items()})
     assert e["Sp"] < 2e-7
     assert e["dA"] > TOL["f32"]
+
+
+# ---------------------------------------------------------------------------
+# The block stack: the oracle's stack with the GPU path's storage roundings
+# (tests/stack_rounding.py), against the exact oracle stack.
+# ---------------------------------------------------------------------------
+
+def _stack(N, C, H, M, L, dt, a_scale):
+    w = I.small("stack", N, C, H, M, dt)
+    x, dY = I.make_x(w, N), I.make_grad(w, N)
+    ps = [I.make_block_params(w, l) for l in range(L)]
+    for p in ps:
+        a = (p["a"] * np.float32(a_scale)).astype(np.float32)
+        p["a"] = I.round_bf16(a) if dt == "bf16" else a
+    Gs = [I.make_layer_gumbel(w, l, N) for l in range(L)]
+    ref, caches = oracle.stack_forward(x, Gs, ps, w.tau0, w.tau_min, w.eps, H)
+    rdx, rgr = oracle.stack_backward(dY, Gs, ps, w.tau0, w.tau_min, w.eps, H, caches)
+    return w, x, dY, ps, Gs, (ref, rdx, rgr), caches
+
+
+STACK_CASES = [(1000, 64, 4, 16, 2, "f32", 1.0), (1000, 64, 4, 16, 2, "bf16", 0.05),
+               (1000, 64, 4, 16, 2, "bf16", 1.0)]
+
+
+@pytest.mark.parametrize("case", STACK_CASES, ids=lambda c: f"{c[5]}-a{c[6]}")
+def test_stack_model_unrounded_is_the_oracle_stack(case):
+    """The folded evaluation without roundings equals the oracle's stack with
+    its explicit Project step (the folding is exact while den >= eps)."""
+    import stack_rounding as SR
+    N, C, H, M, L, dt, sc = case
+    w, x, dY, ps, Gs, (ref, rdx, rgr), caches = _stack(*case)
+    assert all(np.all(c["pa"]["den"] >= w.eps) for c in caches)
+    out, dx, grads = SR.stack_model(x, dY, Gs, ps, w.tau0, w.tau_min, w.eps, H, dt, rnd=False)
+    assert rel_l2(out, ref) < 1e-11 and rel_l2(dx, rdx) < 1e-11
+    for l in range(L):
+        for k in SR.GRADS:
+            assert rel_l2(grads[l][k], rgr[l][k]) < 1e-9, (l, k)
+        assert abs(grads[l]["db_t"] - rgr[l]["db_t"]) <= 1e-9 * abs(rgr[l]["db_t"]) + 1e-12
+
+
+def test_stack_rounding_envelopes():
+    """fp32 storage: every output within 1.5e-5 (the clamped-temperature
+    slice gradients use more than half of 1e-5); bf16 without clamped
+    points: within half of 2e-2; bf16 with the generator's Ada-Temp: the
+    slice-parameter gradients move by more than 10 %, while the stack's
+    output and its input gradient stay within 2e-2."""
+    import stack_rounding as SR
+    env = {}
+    for case in STACK_CASES:
+        w, x, dY, ps, Gs, (ref, rdx, rgr), caches = _stack(*case)
+        e = SR.envelope(x, dY, Gs, ps, w.tau0, w.tau_min, w.eps, case[2], case[5], ref, rdx,
+                        rgr)
+        env[case[5:]] = e
+        print(case, [(k, f"{v:.2e}") for k, v in sorted(e.items(), key=lambda t: t[1])[-4:]])
+    f32, bf_plain, bf_clamped = env[("f32", 1.0)], env[("bf16", 0.05)], env[("bf16", 1.0)]
+    assert max(f32.values()) < 1.5e-5
+    assert max(bf_plain.values()) < 0.5 * TOL["bf16"]
+    slice_keys = [k for k in bf_clamped if isinstance(k, tuple) and k[1] in ("dA", "db")]
+    assert max(bf_clamped[k] for k in slice_keys) > 0.1
+    # the stack's output and input gradient stay within the plain bar
+    assert bf_clamped["out"] < TOL["bf16"] and bf_clamped["dx"] < TOL["bf16"]
+
+
+def test_stack_flip_spread():
+    """Two rounded evaluations whose values differ by a relative JITTER
+    before each bf16 rounding: without clamped points they agree within
+    half of 2e-2 everywhere; at the temperature floor the slice gradients
+    are more than 2e-2 apart (no bf16 evaluation of that regime pins them),
+    while the stack's output and input gradient still agree."""
+    import stack_rounding as SR
+    plain = _stack(1000, 64, 4, 16, 2, "bf16", 0.05)
+    w, x, dY, ps, Gs = plain[:5]
+    sp = SR.flip_spread(x, dY, Gs, ps, w.tau0, w.tau_min, w.eps, 4, "bf16")
+    assert max(sp.values()) < 0.5 * TOL["bf16"]
+    clamped = _stack(1000, 64, 4, 16, 2, "bf16", 1.0)
+    w, x, dY, ps, Gs = clamped[:5]
+    sp = SR.flip_spread(x, dY, Gs, ps, w.tau0, w.tau_min, w.eps, 4, "bf16")
+    print({k: f"{v:.2e}" for k, v in sp.items() if v > 1e-2})
+    assert max(sp[(l, "dA")] for l in range(2)) > TOL["bf16"]
+    assert sp["out"] < TOL["bf16"] and sp["dx"] < TOL["bf16"]
