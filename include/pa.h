@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define PA_VERSION 4
+#define PA_VERSION 5
 
 typedef enum { PA_F32 = 0, PA_BF16 = 1 } pa_dtype;
 
@@ -211,6 +211,24 @@ pa_status pa_slice_aggregate_w(const pa_dims* dims, const void* x, const void* G
                                const pa_slice_params* sp, float* num, float* den,
                                float* S, void* W, void* ws, size_t ws_bytes,
                                void* stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * computation as pa_slice_aggregate, bit for bit, with no workspace
+ * argument.  Its table image and per-block partial records live in a
+ * static device array of the library (17 MiB on each device it runs on,
+ * held until the process ends); the call allocates and frees nothing.
+ * Shapes whose scratch would exceed the array return PA_ERR_UNSUPPORTED
+ * (every shape the layer calls serve fits).  The first call on a device
+ * looks up the array's address there (hipGetSymbolAddress, with that device
+ * current; the stream must belong to the current device) and keeps it.
+ * Every call on one device uses that device's one array: calls that overlap
+ * on a device (other streams, other threads) race and must be ordered by
+ * the caller.  Nothing in the array has to start at zero: every call
+ * rewrites what it reads. */
+pa_status pa_slice_aggregate_noalloc(const pa_dims* dims, const void* x, const void* G,
+                                     const pa_slice_params* sp, float* num, float* den,
+                                     float* S, void* stream);
 
 /* pa_deslice_w: y = W Sp (the deslice of Section 3) from a stored W [N,M]
  * dtype; y [N,C] dtype.  dims->tau0, tau_min and eps are not used. */

@@ -34,6 +34,7 @@ SYMBOLS = (
     "pa_project_backward", "pa_heads_relayout", "pa_heads_expand", "pa_heads_sum",
     "pa_heads_workspace_size", "pa_heads_slice_aggregate", "pa_heads_deslice",
     "pa_heads_deslice_backward", "pa_heads_slice_aggregate_backward",
+    "pa_slice_aggregate_noalloc",
 )
 
 
@@ -105,6 +106,7 @@ def load(path: str = LIB_PATH):
     lib.pa_slice_weights_backward.argtypes = [D, P, P, SPp, P, P, P, SGp, P, S, P]
     lib.pa_time_kernel.argtypes = [ctypes.c_char_p, P, P]
     lib.pa_slice_aggregate_w.argtypes = [D, P, P, SPp, P, P, P, P, P, S, P]
+    lib.pa_slice_aggregate_noalloc.argtypes = [D, P, P, SPp, P, P, P, P]
     lib.pa_deslice_w.argtypes = [D, P, P, P, P, S, P]
     lib.pa_deslice_backward_w.argtypes = [D, P, P, P, P, S, P]
     I64, I32, F = ctypes.c_int64, ctypes.c_int, ctypes.c_float
@@ -343,6 +345,16 @@ def pa_slice_aggregate_w(dims, x, G, sp, num, den, S, W, ws, stream=None):
                                        ctypes.byref(sp), _arg(num, *d["MC"], "num"),
                                        _arg(den, *d["M"], "den"), _arg(S, *d["MC"], "S"), _arg(W, *d["G"], "W"),
                                        _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def pa_slice_aggregate_noalloc(dims, x, G, sp, num, den, S, stream=None):
+    """pa_slice_aggregate with the library's static scratch (no workspace)."""
+    d = _shapes(dims)
+    _check_struct(sp, dims)
+    _check(load().pa_slice_aggregate_noalloc(ctypes.byref(dims), _arg(x, *d["x"], "x"),
+                                             _arg(G, *d["G"], "G"), ctypes.byref(sp),
+                                             _arg(num, *d["MC"], "num"), _arg(den, *d["M"], "den"),
+                                             _arg(S, *d["MC"], "S"), _stream(stream)))
 
 
 def pa_deslice_w(dims, W, Sp, y, ws, stream=None):

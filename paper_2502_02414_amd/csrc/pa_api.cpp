@@ -9,6 +9,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 
 #include "pa_internal.h"
@@ -270,18 +271,22 @@ pa_status pa_slice_weights(const pa_dims* dims, const void* x, const void* G,
 }  // extern "C"
 
 namespace {
-// pa_slice_aggregate and pa_slice_aggregate_w (which also writes W).
-pa_status slice_aggregate(int pass, const pa_dims* dims, const void* x, const void* G,
-                          const pa_slice_params* sp, float* num, float* den, float* S, void* W,
-                          void* ws, size_t ws_bytes, void* stream) {
+pa_status check_aggregate(int pass, const pa_dims* dims, const void* x, const void* G,
+                          const pa_slice_params* sp, float* num, float* den, float* S,
+                          void* W) {
   PA_TRY(check_slice(dims, x, G, sp));
   PA_TRY(check_ptr(num, "num", true));
   PA_TRY(check_ptr(den, "den", true));
   PA_TRY(check_ptr(S, "S", true));
   PA_TRY(check_ptr(W, "W", pass == pa::kAggregateW));
-  PA_TRY(check_pass(*dims, pass));
-  PA_TRY(check_ws(*dims, ws, ws_bytes));
-  hipStream_t st = as_stream(stream);
+  return check_pass(*dims, pass);
+}
+
+// The launches of pa_slice_aggregate(_w) on a validated workspace: the
+// table image at its start, the block records at the layout's offset.
+pa_status slice_aggregate_launch(int pass, const pa_dims* dims, const void* x, const void* G,
+                                 const pa_slice_params* sp, float* num, float* den, float* S,
+                                 void* W, void* ws, hipStream_t st) {
   PA_HIP(pa::launch_prep(prep_of(*dims, pass, sp, ws), st), "prep");
   pa::StreamLaunch L = stream_of(*dims, pass, x, G, sp, ws);
   L.out = W;
@@ -298,6 +303,15 @@ pa_status slice_aggregate(int pass, const pa_dims* dims, const void* x, const vo
   PA_HIP(pa::launch_reduce(L.partials, L.P, L.rec, seg, st), "reduce");
   return PA_OK;
 }
+
+// pa_slice_aggregate and pa_slice_aggregate_w (which also writes W).
+pa_status slice_aggregate(int pass, const pa_dims* dims, const void* x, const void* G,
+                          const pa_slice_params* sp, float* num, float* den, float* S, void* W,
+                          void* ws, size_t ws_bytes, void* stream) {
+  PA_TRY(check_aggregate(pass, dims, x, G, sp, num, den, S, W));
+  PA_TRY(check_ws(*dims, ws, ws_bytes));
+  return slice_aggregate_launch(pass, dims, x, G, sp, num, den, S, W, ws, as_stream(stream));
+}
 }  // namespace
 
 extern "C" {
@@ -313,6 +327,73 @@ pa_status pa_slice_aggregate_w(const pa_dims* dims, const void* x, const void* G
                                const pa_slice_params* sp, float* num, float* den, float* S,
                                void* W, void* ws, size_t ws_bytes, void* stream) {
   return slice_aggregate(pa::kAggregateW, dims, x, G, sp, num, den, S, W, ws, ws_bytes, stream);
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// pa_slice_aggregate_noalloc: the aggregate's table image and block records
+// in a static device array instead of a caller's workspace.  Each device
+// holds its own copy of the array for the life of the process; host code
+// uses only the address hipGetSymbolAddress returns for it on that device
+// (the array's name is a host-side stand-in, not a device address).
+// ---------------------------------------------------------------------------
+namespace {
+constexpr size_t kNoallocScratchBytes = (size_t)17 << 20;  // 17 MiB
+constexpr int kNoallocMaxDevices = 64;
+std::mutex g_noalloc_mu;
+void* g_noalloc_scratch[kNoallocMaxDevices] = {};
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[kNoallocScratchBytes];
+
+namespace {
+// Device address of `scratch` on the current device, looked up on the first
+// call on that device (with it current) and kept.
+pa_status noalloc_scratch(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kNoallocMaxDevices)
+    return fail(PA_ERR_UNSUPPORTED, "pa_slice_aggregate_noalloc: device %d beyond %d", dev,
+                kNoallocMaxDevices);
+  std::lock_guard<std::mutex> lock(g_noalloc_mu);
+  if (!g_noalloc_scratch[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(PA_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_noalloc_scratch[dev] = p;
+  }
+  *out = g_noalloc_scratch[dev];
+  return PA_OK;
+}
+
+// Scratch bytes the aggregate needs: the workspace layout up to the end of
+// the aggregate's own block records (its table image sits at offset 0).
+size_t noalloc_bytes(const pa_dims& d) {
+  return layout_of(d).parts +
+         (size_t)chunks(d, pa::kAggregate) * pa::record_floats(pa::kAggregate, d.C, d.M) *
+             sizeof(float);
+}
+}  // namespace
+
+extern "C" {
+
+pa_status pa_slice_aggregate_noalloc(const pa_dims* dims, const void* x, const void* G,
+                                     const pa_slice_params* sp, float* num, float* den,
+                                     float* S, void* stream) {
+  PA_TRY(check_aggregate(pa::kAggregate, dims, x, G, sp, num, den, S, nullptr));
+  const size_t need = noalloc_bytes(*dims);
+  if (need > kNoallocScratchBytes)
+    return fail(PA_ERR_UNSUPPORTED,
+                "pa_slice_aggregate_noalloc: this shape needs %zu bytes of scratch, more than "
+                "the %zu the library holds",
+                need, kNoallocScratchBytes);
+  void* base = nullptr;
+  PA_TRY(noalloc_scratch(&base));
+  return slice_aggregate_launch(pa::kAggregate, dims, x, G, sp, num, den, S, nullptr, base,
+                                as_stream(stream));
 }
 
 pa_status pa_deslice_w(const pa_dims* dims, const void* W, const float* Sp, void* y, void* ws,

@@ -32,14 +32,14 @@ def _declared_symbols():
 
 def test_every_declared_symbol_is_exported(lib):
     declared = _declared_symbols()
-    assert len(declared) == 32
+    assert len(declared) == 33
     assert sorted(B.SYMBOLS) == declared
     for name in declared:
         assert hasattr(lib, name), name
 
 
 def test_version(lib):
-    assert lib.pa_version() == 4
+    assert lib.pa_version() == 5
 
 
 def _dims(**kw):

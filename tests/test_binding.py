@@ -66,13 +66,15 @@ def test_layer_calls_accept_their_shapes(fake, dt):
     B.pa_slice_aggregate_w(d, x, G, sp, mc, m, mc, _t(N, M, dt=tdt), ws)
     B.pa_deslice_w(d, _t(N, M, dt=tdt), mc, y, ws)
     B.pa_deslice_backward_w(d, _t(N, M, dt=tdt), y, mc, ws)
+    B.pa_slice_aggregate_noalloc(d, x, G, sp, mc, m, mc)
     # one argument per parameter of each C declaration
     nargs = {name: len(args) for name, args in fake.calls}
     assert nargs == {"pa_slice_weights": 9, "pa_slice_aggregate": 10, "pa_token_attention": 7,
                      "pa_deslice": 9, "pa_deslice_backward": 9,
                      "pa_token_attention_backward": 9, "pa_slice_aggregate_backward": 14,
                      "pa_slice_weights_backward": 11, "pa_slice_aggregate_w": 11,
-                     "pa_deslice_w": 7, "pa_deslice_backward_w": 7}
+                     "pa_deslice_w": 7, "pa_deslice_backward_w": 7,
+                     "pa_slice_aggregate_noalloc": 8}
 
 
 def test_heads_calls_accept_their_shapes(fake):
