@@ -271,7 +271,8 @@ def main():
     }
 
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(x_np, G_np, dY_np, p, w)
+        out["cpu_baseline"] = cpu_baseline(x_np, G_np, dY_np, p, w,
+                                           per_core=I.WORKLOADS["ellipsoid_32k_bf16"])
     print(json.dumps(out), flush=True)
 
 
@@ -425,6 +426,8 @@ def workload_bench(args):
         "step_hbm": {"algo_bytes": nbytes, "achieved_GBs": round(gbs, 1),
                      "frac": round(gbs / HBM_PEAK_GBS, 4)},
     }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(I.make_x(w), I.make_gumbel(w), I.make_grad(w), p, w)
     print(json.dumps(out), flush=True)
 
 
@@ -592,31 +595,57 @@ def time_steps(calls, bpp, args, B, torch):
             "wall_s": t_wall}
 
 
-def cpu_baseline(x_np, G_np, dY_np, p, w, target_s: float = 10.0):
-    """The oracle, as it stands, on the first n points of the same workload:
-    forward + backward of the layer in float64 on the host cores.  n is sized
-    from a short calibration run so that the timed run takes about
-    ``target_s`` seconds."""
-    import numpy as np
-    import oracle
+def _oracle_rate(oracle, w, x_np, G_np, dY_np, p, target_s):
+    """Points/s of the oracle's layer (forward, and backward if the workload
+    has one) on the first n points, n sized from a short calibration run so
+    that the timed run takes about target_s seconds.  Returns (rate, n, s)."""
     pp = {k: v for k, v in p.items() if v is not None}
 
     def run(n):
         xs, Gs, dYs = x_np[:n], G_np[:n], dY_np[:n]
         t = time.perf_counter()
         f = oracle.layer_forward(xs, Gs, pp, w.tau0, w.tau_min, w.eps, w.H)
-        oracle.layer_backward(xs, Gs, pp, w.tau0, w.tau_min, w.eps, w.H, f, dYs)
+        if w.backward:
+            oracle.layer_backward(xs, Gs, pp, w.tau0, w.tau_min, w.eps, w.H, f, dYs)
         return time.perf_counter() - t
 
-    n0 = 16384
+    n0 = min(len(x_np), 4096)
     rate0 = n0 / run(n0)
     n = int(min(len(x_np), max(n0, rate0 * target_s)))
     n = (n // 1024) * 1024 or n0
     dt = run(n)
-    return {"value": round(n / dt, 1), "unit": "points/s", "cores": oracle.num_threads(),
-            "kind": "oracle",
-            "sample": f"first {n} of the {len(x_np)} points of {WORKLOAD}, fwd+bwd in float64 "
-                      f"({dt:.1f} s)"}
+    return n / dt, n, dt
+
+
+def cpu_baseline(x_np, G_np, dY_np, p, w, target_s: float = 10.0, per_core=None):
+    """The oracle, as it stands, on the host cores: the layer in float64 on
+    the first n points of the same workload, built on this host with -O3
+    -march=native (oracle/build.py's native variant), OpenMP over all the
+    cores it may use.  With per_core (a workload), also a one-thread run on
+    that workload."""
+    import oracle
+    oracle.use_variant("native", rebuild=True)
+    rate, n, dt = _oracle_rate(oracle, w, x_np, G_np, dY_np, p, target_s)
+    passes = "fwd+bwd" if w.backward else "fwd"
+    out = {"value": round(rate, 1), "unit": "points/s", "cores": oracle.num_threads(),
+           "kind": "oracle",
+           "sample": f"first {n} of the {len(x_np)} points of {w.name}, {passes} in float64 "
+                     f"({dt:.1f} s; gcc -O3 -march=native, OpenMP)"}
+    if per_core is not None:
+        from paper_2502_02414_amd import inputs as I
+        w3 = per_core
+        x3, G3, dY3, p3 = I.make_x(w3), I.make_gumbel(w3), I.make_grad(w3), I.make_params(w3)
+        threads = oracle.num_threads()
+        oracle.set_num_threads(1)
+        try:
+            r1, n1, t1 = _oracle_rate(oracle, w3, x3, G3, dY3, p3, target_s / 2)
+        finally:
+            oracle.set_num_threads(threads)
+        out["per_core"] = {"value": round(r1, 1), "unit": "points/s", "cores": 1,
+                           "workload": w3.name,
+                           "sample": f"first {n1} of the {len(x3)} points of {w3.name}, "
+                                     f"fwd+bwd in float64 on one thread ({t1:.1f} s)"}
+    return out
 
 
 if __name__ == "__main__":

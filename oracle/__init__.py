@@ -16,17 +16,38 @@ import os
 
 import numpy as np
 
-from .build import LIB, build
+from .build import LIB, build, lib_path
 
 _lib = None
+# The library variant this process loads (oracle/build.py): PA_ORACLE_VARIANT
+# in the environment, else the portable build; use_variant() before the
+# first call chooses another.
+_variant = os.environ.get("PA_ORACLE_VARIANT", "portable")
+
+
+def use_variant(variant: str, rebuild: bool = False) -> str:
+    """Load the given library variant from now on (before any oracle call);
+    with rebuild, compile it first on this host."""
+    global _variant
+    if _lib is not None and variant != _variant:
+        raise RuntimeError(f"oracle library {_variant} already loaded")
+    _variant = variant
+    if rebuild or not os.path.exists(lib_path(variant)):
+        build(variant=variant)
+    return lib_path(variant)
+
+
+def variant() -> str:
+    return _variant
 
 
 def _load():
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB):
-            build()
-        lib = ctypes.CDLL(LIB)
+        path = lib_path(_variant)
+        if not os.path.exists(path):
+            build(variant=_variant)
+        lib = ctypes.CDLL(path)
         P = ctypes.c_void_p
         I64, I32, D = ctypes.c_int64, ctypes.c_int, ctypes.c_double
         lib.pao_slice_weights.argtypes = [I64, I32, I32, D, D, P, P, P, P, P, D, P, P, P]
