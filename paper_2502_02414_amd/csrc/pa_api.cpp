@@ -480,8 +480,12 @@ pa_status attn_forward_general(const pa_dims& d, const float* S, const pa_attn_p
   return PA_OK;
 }
 
-// Double-precision token side (fp32 storage): the same eight matrices as
-// doubles over the same region.
+// Double-precision token forward (fp32 storage): S' feeds the slice
+// backward through the differences of nearly equal tokens, where an fp32
+// evaluation error of ~1e-7 moves dA by ~1e-5; so Q, K, V, the attention
+// and S' are formed in double and S' is rounded once.  The backward's dS
+// is ten times less sensitive and keeps the fp32 kernels.  Its matrices
+// (as doubles) share the token scratch region.
 struct AttnWs64 {
   double *Q, *K, *V, *O, *dO, *dQ, *dK, *dV;
 };
@@ -540,47 +544,6 @@ pa_status attn64_forward(const pa_dims& d, const float* S, const pa_attn_params*
   return PA_OK;
 }
 
-pa_status attn64_backward(const pa_dims& d, const float* S, const pa_attn_params* ap,
-                          const float* dSp, float* dS, const pa_attn_grads* ag, void* ws,
-                          hipStream_t st) {
-  const int M = d.M, C = d.C;
-  const AttnWs64 w = attn_ws64(d, ws);
-  const bool wantWo = ag && ap->Wo && (ag->dWo || ag->dbo);
-  if (ap->Wo) {  // dO = dSp Wo^T
-    pa::MM64Batch b{};
-    mm64_term(mm64_add(b, M, C, w.dO, true), opf(dSp, C, 1), opf(ap->Wo, 1, C), C);
-    PA_HIP(pa::launch_mm64(b, st), "dO (double)");
-  }
-  PA_TRY(attn64_project(d, S, ap, w, st));
-  const void* dO = ap->Wo ? static_cast<const void*>(w.dO) : static_cast<const void*>(dSp);
-  PA_HIP(pa::launch_core64_bwd(w.Q, w.K, w.V, dO, ap->Wo != nullptr, w.dQ, w.dK, w.dV,
-                               wantWo ? w.O : nullptr, M, C, d.H, st),
-         "attention core backward (double)");
-  // dS = sum_p dX_p W_p^T; dW_p = S^T dX_p, db_p = 1^T dX_p; dWo = O^T dSp
-  pa::MM64Batch b{};
-  const double* dX[3] = {w.dQ, w.dK, w.dV};
-  const float* W[3] = {ap->Wq, ap->Wk, ap->Wv};
-  pa::MM64& qs = mm64_add(b, M, C, dS, false);
-  for (int p = 0; p < 3; ++p) mm64_term(qs, opd(dX[p], C, 1), opf(W[p], 1, C), C);
-  if (ag) {
-    float* dW[3] = {ag->dWq, ag->dWk, ag->dWv};
-    float* db[3] = {ag->dbq, ag->dbk, ag->dbv};
-    for (int p = 0; p < 3; ++p) {
-      if (dW[p]) mm64_term(mm64_add(b, C, C, dW[p], false), opf(S, 1, C), opd(dX[p], C, 1), M);
-      if (db[p])
-        mm64_term(mm64_add(b, 1, C, db[p], false), opf(nullptr, 0, 0),
-                  opd(dX[p], C, 1), M);
-    }
-    if (wantWo && ag->dWo)
-      mm64_term(mm64_add(b, C, C, ag->dWo, false), opd(w.O, 1, C), opf(dSp, C, 1), M);
-    if (wantWo && ag->dbo)
-      mm64_term(mm64_add(b, 1, C, ag->dbo, false), opf(nullptr, 0, 0),
-                opf(dSp, C, 1), M);
-  }
-  PA_HIP(pa::launch_mm64(b, st), "token gradients (double)");
-  return PA_OK;
-}
-
 pa::HeadArgs head_args(const pa_dims& d, const float* S, const pa_attn_params* ap) {
   pa::HeadArgs h{};
   h.S = S;
@@ -632,7 +595,6 @@ pa_status pa_token_attention_backward(const pa_dims* dims, const float* S,
   PA_TRY(check_ws(*dims, ws, ws_bytes));
   hipStream_t st = as_stream(stream);
   const pa_dims& d = *dims;
-  if (d.dtype == PA_F32) return attn64_backward(d, S, ap, dSp, dS, ag, ws, st);
   const int M = d.M, C = d.C;
   const AttnWs w = attn_ws(d, ws);
   const float* dO = dSp;

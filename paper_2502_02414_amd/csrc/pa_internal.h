@@ -148,7 +148,8 @@ hipError_t launch_attn_core_bwd(const float* Q, const float* K, const float* V,
                                 const float* P, const float* dO, float* dQ, float* dK,
                                 float* dV, int M, int C, int H, hipStream_t st);
 
-// Token side in double precision (pa_tokens64.hip; the fp32-storage path).
+// Token attention forward in double precision (pa_tokens64.hip; the
+// fp32-storage path).
 // Operand element (i, k) = p[i rs + k cs], fp32 or fp64; p == NULL: all ones.
 struct Opnd64 {
   const void* p;
@@ -167,20 +168,16 @@ struct MM64 {
   int rows, cols;
   int64_t ld;
 };
-constexpr int kMM64Max = 9;
+constexpr int kMM64Max = 3;
 struct MM64Batch {
   MM64 p[kMM64Max];
   int n;
 };
 hipError_t launch_mm64(const MM64Batch& b, hipStream_t st);
 // Per head h (channels [hD, hD + D)): O_h = softmax(Q_h K_h^T / sqrt(D)) V_h
-// (O fp32 or fp64), and the backward dQ_h, dK_h, dV_h from dO_h (fp32 or
-// fp64), with O_h too when O is given.  Q, K, V, dQ, dK, dV: [M,C] fp64.
+// (O fp32 or fp64); Q, K, V: [M,C] fp64.
 hipError_t launch_core64(const double* Q, const double* K, const double* V, void* O, bool O_dbl,
                          int M, int C, int H, hipStream_t st);
-hipError_t launch_core64_bwd(const double* Q, const double* K, const double* V, const void* dO,
-                             bool dO_dbl, double* dQ, double* dK, double* dV, double* O, int M,
-                             int C, int H, hipStream_t st);
 
 // Sets the thread-local message of pa_last_error() (pa_api.cpp).
 void set_last_error(const char* msg);

@@ -1,26 +1,29 @@
-// Token side of the layer in double precision (gfx950), used for fp32
-// storage.  Attention among the M <= 64 states (Eq. 2) and its backward are
-// tiny products whose results feed the slice backward through the
-// differences s'_j - s'_k of nearly equal tokens: an fp32 rounding error of
-// 1e-7 in S' moves dA by about 1e-5 at the synthetic workloads' shapes.  So
-// for fp32 storage every token-side value is formed in double and rounded
-// once, when it leaves as an fp32 output (S', dS, the parameter gradients).
+// Token attention forward in double precision (gfx950), used for fp32
+// storage.  Attention among the M <= 64 states (Eq. 2) is a tiny product,
+// but its result S' feeds the slice backward through the differences
+// s'_j - s'_k of nearly equal tokens: an fp32 rounding error of 1e-7 in S'
+// moves dA by about 1e-5 at the synthetic workloads' shapes.  So for fp32
+// storage Q, K, V, the attention and S' are formed in double and S' is
+// rounded once.
 //
-//   k_mm64        batches of small products out = sum_t op(A_t) op(B_t) + b
-//                 (operands fp32 or fp64 with arbitrary strides, "ones"
-//                 operands for column sums), 32 x 32 output tiles, K chunks
-//                 staged in LDS, fp64 FMAs
-//   k_core64      per head: P = softmax(Q_h K_h^T / sqrt(D)), O_h = P V_h
-//   k_core64_bwd  per head: P recomputed, dP = dO_h V_h^T,
-//                 dE = P o (dP - rowsum(dP o P)), dQ_h, dK_h, dV_h (and O_h)
+//   k_mm64    batches of up to three small products out = sum_t op(A_t)
+//             op(B_t) + b (operands fp32 or fp64 with arbitrary strides),
+//             32 x 32 output tiles, K chunks of
+//             64 staged in LDS (the next chunk's loads in flight while one
+//             is multiplied), fp64 FMAs
+//   k_core64  per head: P = softmax(Q_h K_h^T / sqrt(D)), O_h = P V_h, with
+//             the head's matrices staged in LDS when they fit and each
+//             softmax row reduced over a group of lanes
 #include "pa_internal.h"
 
 namespace pa {
 
 namespace {
 
-constexpr int kT = 32;          // output tile edge and K chunk
+constexpr int kT = 32;          // output tile edge
+constexpr int kKC = 64;         // K chunk staged in LDS
 constexpr int kMMThreads = 256; // 16 x 16 threads, 2 x 2 outputs each
+constexpr int kPer = kT * kKC / kMMThreads;  // operand elements per thread and chunk
 
 __device__ __forceinline__ double opnd_at(const Opnd64& o, int64_t i, int64_t k) {
   if (!o.p) return 1.0;
@@ -28,40 +31,63 @@ __device__ __forceinline__ double opnd_at(const Opnd64& o, int64_t i, int64_t k)
   return o.dbl ? static_cast<const double*>(o.p)[e] : (double)static_cast<const float*>(o.p)[e];
 }
 
-// One 32 x 32 tile (tile index blockIdx.x) of product q.
+// Element u of a thread's share of a chunk: (row or column, k) with
+// consecutive threads walking the operand's unit-stride dimension.
+struct ChunkIdx { int mn, k; };
+__device__ __forceinline__ ChunkIdx chunk_idx(int u, bool k_fast) {
+  const int e = threadIdx.x + kMMThreads * u;  // < kT * kKC
+  return k_fast ? ChunkIdx{e / kKC, e % kKC} : ChunkIdx{e % kT, e / kT};
+}
+
+// One 32 x 32 tile (tile index blockIdx.x) of product q.  The K chunks of
+// every term are visited in order; the next chunk of a term is loaded into
+// registers while the current one is multiplied from LDS.
 __device__ __forceinline__ void mm64_tile(const MM64& q) {
-  __shared__ double as[kT][kT + 1];  // [row][k]
-  __shared__ double bs[kT][kT + 1];  // [k][col]
+  __shared__ double as[kT][kKC + 1];  // [row][k]
+  __shared__ double bs[kKC][kT + 1];  // [k][col]
   const int tc = (q.cols + kT - 1) / kT;
   const int tiles = tc * ((q.rows + kT - 1) / kT);
   if ((int)blockIdx.x >= tiles) return;
   const int i0 = (blockIdx.x / tc) * kT, j0 = (blockIdx.x % tc) * kT;
   const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
   double acc[2][2] = {{0.0, 0.0}, {0.0, 0.0}};
-  for (int t = 0; t < q.nt; ++t) {
+  double ra[kPer], rb[kPer];
+  // chunk k0 of a term's operands into registers, with consecutive threads
+  // on each operand's unit-stride dimension; B element (k, column) is
+  // (ib.k, ib.mn)
+  auto load = [&](const Opnd64& A, const Opnd64& B, int K, int k0) {
+    const bool a_k_fast = A.cs == 1 || !A.p, b_j_fast = B.cs == 1 || !B.p;
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const ChunkIdx ia = chunk_idx(u, a_k_fast);
+      ra[u] = (i0 + ia.mn < q.rows && k0 + ia.k < K) ? opnd_at(A, i0 + ia.mn, k0 + ia.k) : 0.0;
+      const ChunkIdx ib = chunk_idx(u, !b_j_fast);
+      rb[u] = (k0 + ib.k < K && j0 + ib.mn < q.cols) ? opnd_at(B, k0 + ib.k, j0 + ib.mn) : 0.0;
+    }
+  };
+  auto store = [&](const Opnd64& A, const Opnd64& B) {
+    const bool a_k_fast = A.cs == 1 || !A.p, b_j_fast = B.cs == 1 || !B.p;
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const ChunkIdx ia = chunk_idx(u, a_k_fast);
+      as[ia.mn][ia.k] = ra[u];
+      const ChunkIdx ib = chunk_idx(u, !b_j_fast);
+      bs[ib.k][ib.mn] = rb[u];
+    }
+  };
+  // terms by constant index (no run-time indexing of the argument struct)
+#pragma unroll
+  for (int t = 0; t < 3; ++t) {
+    if (t >= q.nt) break;
     const Opnd64 A = q.A[t], B = q.B[t];
     const int K = q.K[t];
-    // consecutive threads walk the operand's unit-stride dimension
-    const bool a_k_fast = A.cs == 1 || !A.p, b_j_fast = B.cs == 1 || !B.p;
-    for (int k0 = 0; k0 < K; k0 += kT) {
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int e = threadIdx.x + kMMThreads * u;  // < 1024 = kT * kT
-        const int hi = e >> 5, lo = e & 31;
-        {
-          const int i = a_k_fast ? hi : lo, k = a_k_fast ? lo : hi;
-          const bool in = i0 + i < q.rows && k0 + k < K;
-          as[i][k] = in ? opnd_at(A, i0 + i, k0 + k) : 0.0;
-        }
-        {
-          const int k = b_j_fast ? hi : lo, j = b_j_fast ? lo : hi;
-          const bool in = k0 + k < K && j0 + j < q.cols;
-          bs[k][j] = in ? opnd_at(B, k0 + k, j0 + j) : 0.0;
-        }
-      }
+    load(A, B, K, 0);
+    for (int k0 = 0; k0 < K; k0 += kKC) {
+      store(A, B);
       __syncthreads();
+      if (k0 + kKC < K) load(A, B, K, k0 + kKC);
 #pragma unroll 8
-      for (int k = 0; k < kT; ++k) {
+      for (int k = 0; k < kKC; ++k) {
         const double a0 = as[2 * ty][k], a1 = as[2 * ty + 1][k];
         const double b0 = bs[k][2 * tx], b1 = bs[k][2 * tx + 1];
         acc[0][0] = fma(a0, b0, acc[0][0]);
@@ -95,8 +121,7 @@ __global__ void __launch_bounds__(kMMThreads) k_mm64(MM64Batch b) {
     case I:             \
       if (I < b.n) mm64_tile(b.p[I]); \
       break;
-    PA_MM64_CASE(0) PA_MM64_CASE(1) PA_MM64_CASE(2) PA_MM64_CASE(3) PA_MM64_CASE(4)
-    PA_MM64_CASE(5) PA_MM64_CASE(6) PA_MM64_CASE(7) PA_MM64_CASE(8)
+    PA_MM64_CASE(0) PA_MM64_CASE(1) PA_MM64_CASE(2)
 #undef PA_MM64_CASE
     default:
       break;
@@ -105,103 +130,129 @@ __global__ void __launch_bounds__(kMMThreads) k_mm64(MM64Batch b) {
 
 constexpr int kCoreThreads = 256;
 
-// P = softmax(Q_h K_h^T * scale) of head h into ps ([M][M + 1], LDS).
-__device__ __forceinline__ void core64_probs(const double* Q, const double* K, int M, int C,
-                                             int off, int D, double* ps) {
+// Lanes per softmax row: 256 / (M rounded up to a power of two), at most a
+// wave, so a row's lanes stay inside one wave.
+__device__ __forceinline__ int core_row_lanes(int M) {
+  int mp = 1;
+  while (mp < M) mp <<= 1;
+  const int g = kCoreThreads / mp;
+  return g < 64 ? g : 64;
+}
+
+template <typename Op>
+__device__ __forceinline__ double lanes_reduce64(double v, int G, Op op) {
+  for (int o = 1; o < G; o <<= 1) v = op(v, __shfl_xor(v, o));
+  return v;
+}
+
+// Head matrices [M][D] of head h: staged in LDS rows of stride D + 1 when
+// they fit (STAGE), else read from global memory.
+struct HeadMat {
+  const double* g;  // global [M][C] at the head's columns
+  double* s;        // LDS [M][D + 1]
+  int C, DS;
+};
+template <bool STAGE>
+__device__ __forceinline__ double at(const HeadMat& m, int r, int d) {
+  return STAGE ? m.s[r * m.DS + d] : m.g[(int64_t)r * m.C + d];
+}
+template <bool STAGE, typename TS>
+__device__ __forceinline__ void stage_mat(HeadMat& m, const TS* src, int M, int D, int C,
+                                          int off, double* lds) {
+  m.g = nullptr;
+  m.s = lds;
+  m.C = C;
+  m.DS = D + 1;
+  for (int e = threadIdx.x; e < M * D; e += kCoreThreads) {
+    const int r = e / D, d = e - r * D;
+    lds[r * (D + 1) + d] = (double)src[(int64_t)r * C + off + d];
+  }
+}
+
+// P = softmax(Q_h K_h^T * scale) into ps ([M][M + 1], LDS): scores from the
+// staged heads, then G lanes per row (max, exponentials, sum, normalise).
+template <bool STAGE>
+__device__ __forceinline__ void core64_probs(const HeadMat& q, const HeadMat& k, int M, int D,
+                                             double* ps) {
   const int MS = M + 1;
   const double scale = 1.0 / sqrt((double)D);
   for (int e = threadIdx.x; e < M * M; e += kCoreThreads) {
     const int r = e / M, c = e - r * M;
-    const double* q = Q + (int64_t)r * C + off;
-    const double* k = K + (int64_t)c * C + off;
     double s = 0.0;
-    for (int d = 0; d < D; ++d) s = fma(q[d], k[d], s);
+    for (int d = 0; d < D; ++d) s = fma(at<STAGE>(q, r, d), at<STAGE>(k, c, d), s);
     ps[r * MS + c] = s * scale;
   }
   __syncthreads();
-  // one thread per row: max, exponentials, sum, normalisation
-  for (int r = threadIdx.x; r < M; r += kCoreThreads) {
-    double* row = ps + r * MS;
-    double mx = row[0];
-    for (int c = 1; c < M; ++c) mx = fmax(mx, row[c]);
-    double sum = 0.0;
-    for (int c = 0; c < M; ++c) {
-      const double e = exp(row[c] - mx);
-      row[c] = e;
+  const int G = core_row_lanes(M), r = threadIdx.x / G, li = threadIdx.x - r * G;
+  double mx = -INFINITY;
+  if (r < M)
+    for (int c = li; c < M; c += G) mx = fmax(mx, ps[r * MS + c]);
+  mx = lanes_reduce64(mx, G, [](double a, double b) { return fmax(a, b); });
+  double sum = 0.0;
+  if (r < M)
+    for (int c = li; c < M; c += G) {
+      const double e = exp(ps[r * MS + c] - mx);
+      ps[r * MS + c] = e;
       sum += e;
     }
-    const double inv = 1.0 / sum;
-    for (int c = 0; c < M; ++c) row[c] *= inv;
-  }
+  sum = lanes_reduce64(sum, G, [](double a, double b) { return a + b; });
+  const double inv = 1.0 / sum;
+  if (r < M)
+    for (int c = li; c < M; c += G) ps[r * MS + c] *= inv;
   __syncthreads();
 }
 
-// O_h = P V_h (rows of O at stride C, columns off .. off + D).
-template <typename TO>
-__device__ __forceinline__ void core64_pv(const double* ps, const double* V, int M, int C, int off,
-                                          int D, TO* O) {
+// O_h = P V_h into global O (rows at stride C, the head's columns).
+template <bool STAGE, typename TO>
+__device__ __forceinline__ void core64_pv(const double* ps, const HeadMat& v, int M, int D, int C,
+                                          int off, TO* O) {
   const int MS = M + 1;
   for (int e = threadIdx.x; e < M * D; e += kCoreThreads) {
     const int r = e / D, d = e - r * D;
     double s = 0.0;
-    for (int c = 0; c < M; ++c) s = fma(ps[r * MS + c], V[(int64_t)c * C + off + d], s);
+    for (int c = 0; c < M; ++c) s = fma(ps[r * MS + c], at<STAGE>(v, c, d), s);
     O[(int64_t)r * C + off + d] = (TO)s;
   }
 }
 
-template <typename TO>
+template <bool STAGE>
+__device__ __forceinline__ HeadMat head_mat(const double* g, int M, int D, int C, int off,
+                                            double*& lds) {
+  HeadMat m;
+  if (STAGE) {
+    stage_mat<true>(m, g, M, D, C, off, lds);
+    lds += M * (D + 1);
+  } else {
+    m.g = g + off;
+    m.s = nullptr;
+    m.C = C;
+    m.DS = D + 1;
+  }
+  return m;
+}
+
+template <bool STAGE, typename TO>
 __global__ void __launch_bounds__(kCoreThreads) k_core64(const double* Q, const double* K,
                                                          const double* V, TO* O, int M, int C,
                                                          int H) {
   extern __shared__ __attribute__((aligned(16))) double dsm[];
   const int D = C / H, off = blockIdx.x * D;
-  core64_probs(Q, K, M, C, off, D, dsm);
-  core64_pv(dsm, V, M, C, off, D, O);
+  double* ps = dsm;  // [M][M+1]
+  double* lds = dsm + M * (M + 1);
+  const HeadMat q = head_mat<STAGE>(Q, M, D, C, off, lds);
+  const HeadMat k = head_mat<STAGE>(K, M, D, C, off, lds);
+  const HeadMat v = head_mat<STAGE>(V, M, D, C, off, lds);
+  if (STAGE) __syncthreads();
+  core64_probs<STAGE>(q, k, M, D, ps);
+  core64_pv<STAGE>(ps, v, M, D, C, off, O);
 }
 
-template <typename TD>
-__global__ void __launch_bounds__(kCoreThreads) k_core64_bwd(const double* Q, const double* K,
-                                                             const double* V, const TD* dO,
-                                                             double* dQ, double* dK, double* dV,
-                                                             double* O, int M, int C, int H) {
-  extern __shared__ __attribute__((aligned(16))) double dsm[];
-  const int D = C / H, off = blockIdx.x * D, MS = M + 1;
-  double* ps = dsm;           // P  [M][M+1]
-  double* es = dsm + M * MS;  // dP, then dE
-  core64_probs(Q, K, M, C, off, D, ps);
-  if (O) core64_pv(ps, V, M, C, off, D, O);
-  for (int e = threadIdx.x; e < M * M; e += kCoreThreads) {
-    const int r = e / M, c = e - r * M;
-    double s = 0.0;
-    for (int d = 0; d < D; ++d)
-      s = fma((double)dO[(int64_t)r * C + off + d], V[(int64_t)c * C + off + d], s);
-    es[r * MS + c] = s;
-  }
-  __syncthreads();
-  for (int r = threadIdx.x; r < M; r += kCoreThreads) {
-    double rs = 0.0;
-    for (int c = 0; c < M; ++c) rs = fma(es[r * MS + c], ps[r * MS + c], rs);
-    for (int c = 0; c < M; ++c) es[r * MS + c] = ps[r * MS + c] * (es[r * MS + c] - rs);
-  }
-  __syncthreads();
-  const double scale = 1.0 / sqrt((double)D);
-  for (int e = threadIdx.x; e < M * D; e += kCoreThreads) {
-    const int r = e / D, d = e - r * D;
-    double sq = 0.0, sk = 0.0, sv = 0.0;
-    for (int c = 0; c < M; ++c) {
-      const int64_t cd = (int64_t)c * C + off + d;
-      sq = fma(es[r * MS + c], K[cd], sq);
-      sk = fma(es[c * MS + r], Q[cd], sk);
-      sv = fma(ps[c * MS + r], (double)dO[cd], sv);
-    }
-    const int64_t rd = (int64_t)r * C + off + d;
-    dQ[rd] = scale * sq;
-    dK[rd] = scale * sk;
-    dV[rd] = sv;
-  }
+// LDS of the core kernel: P, plus the staged head matrices.
+size_t core64_lds(int M, int D, bool stage) {
+  const size_t hm = stage ? (size_t)3 * M * (D + 1) : 0;
+  return ((size_t)M * (M + 1) + hm) * sizeof(double);
 }
-
-size_t core64_lds(int M, bool bwd) { return (size_t)(bwd ? 2 : 1) * M * (M + 1) * sizeof(double); }
+constexpr size_t kCoreLdsMax = 150 * 1024;
 
 bool core64_ok(int M, int C, int H) { return M >= 1 && M <= 64 && H >= 1 && C % H == 0; }
 
@@ -226,26 +277,18 @@ hipError_t launch_mm64(const MM64Batch& b, hipStream_t st) {
 hipError_t launch_core64(const double* Q, const double* K, const double* V, void* O, bool O_dbl,
                          int M, int C, int H, hipStream_t st) {
   if (!Q || !K || !V || !O || !core64_ok(M, C, H)) return hipErrorInvalidValue;
-  if (O_dbl)
-    hipLaunchKernelGGL(k_core64<double>, dim3(H), dim3(kCoreThreads), core64_lds(M, false), st,
-                       Q, K, V, static_cast<double*>(O), M, C, H);
-  else
-    hipLaunchKernelGGL(k_core64<float>, dim3(H), dim3(kCoreThreads), core64_lds(M, false), st,
-                       Q, K, V, static_cast<float*>(O), M, C, H);
-  return hipGetLastError();
-}
-
-hipError_t launch_core64_bwd(const double* Q, const double* K, const double* V, const void* dO,
-                             bool dO_dbl, double* dQ, double* dK, double* dV, double* O, int M,
-                             int C, int H, hipStream_t st) {
-  if (!Q || !K || !V || !dO || !dQ || !dK || !dV || !core64_ok(M, C, H))
-    return hipErrorInvalidValue;
-  if (dO_dbl)
-    hipLaunchKernelGGL(k_core64_bwd<double>, dim3(H), dim3(kCoreThreads), core64_lds(M, true), st,
-                       Q, K, V, static_cast<const double*>(dO), dQ, dK, dV, O, M, C, H);
-  else
-    hipLaunchKernelGGL(k_core64_bwd<float>, dim3(H), dim3(kCoreThreads), core64_lds(M, true), st,
-                       Q, K, V, static_cast<const float*>(dO), dQ, dK, dV, O, M, C, H);
+  const int D = C / H;
+  const bool stage = core64_lds(M, D, true) <= kCoreLdsMax;
+  const size_t lds = core64_lds(M, D, stage);
+#define PA_CORE64(S, TO) \
+  hipLaunchKernelGGL((k_core64<S, TO>), dim3(H), dim3(kCoreThreads), lds, st, Q, K, V, \
+                     static_cast<TO*>(O), M, C, H)
+  if (stage) {
+    if (O_dbl) PA_CORE64(true, double); else PA_CORE64(true, float);
+  } else {
+    if (O_dbl) PA_CORE64(false, double); else PA_CORE64(false, float);
+  }
+#undef PA_CORE64
   return hipGetLastError();
 }
 
