@@ -33,6 +33,10 @@ SHAPES = [
     # the 128 x 128 grid workload's shape (fp32, M = 64: two waves per CU in
     # the backward, several tiles each)
     (16384, 128, 8, 64, "f32"),
+    # the block-cooperative slice backward (bf16, C = 256, 33..64 slices):
+    # three slice blocks over several tiles; one block with a ragged tile
+    (20011, 256, 8, 48, "bf16"),
+    (33, 256, 8, 50, "bf16"),
 ]
 IDS = [f"N{n}-C{c}-H{h}-M{m}-{d}" for n, c, h, m, d in SHAPES]
 
