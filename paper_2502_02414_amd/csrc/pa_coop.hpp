@@ -501,8 +501,13 @@ __global__ void __launch_bounds__(256) k_slice_bwd_coop(StreamArgs a) {
               ld_tr<T>(f.xa[tt], tile_lds(tt) + CG::OFF_X, xtr, 16 * cb * SZ, G_::XT_ROW);
           },
           [&](int cb, FA& f) {
+            if constexpr (TT == 2) {
+              // the two tiles' K16 products as one K32 product (32 points)
+              dA[cb] = mma16x2(f.xa[0], lp[0], f.xa[1], lp[1], dA[cb]);
+            } else {
 #pragma unroll
-            for (int tt = 0; tt < TT; ++tt) dA[cb] = mma16(f.xa[tt], lp[tt], dA[cb]);
+              for (int tt = 0; tt < TT; ++tt) dA[cb] = mma16(f.xa[tt], lp[tt], dA[cb]);
+            }
           });
     }
   };
