@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define PA_VERSION 5
+#define PA_VERSION 6
 
 typedef enum { PA_F32 = 0, PA_BF16 = 1 } pa_dtype;
 
@@ -315,6 +315,25 @@ pa_status pa_layernorm_backward(int64_t N, int C, pa_dtype dtype, const void* x,
 pa_status pa_gelu(int64_t n, pa_dtype dtype, const void* x, void* y, void* stream);
 pa_status pa_gelu_backward(int64_t n, pa_dtype dtype, const void* x, const void* dy, void* dx,
                            void* stream);
+
+/* The first product of the block's feed-forward layer (Figure 2a) with
+ * its activation, as one kernel (bf16 storage, fp32 accumulation):
+ * G [N,F] = GELU(X W1 + b1), X [N,K] and W1 [K,F] bf16, b1 [F] fp32,
+ * K in {64, 128, 256}, F a positive multiple of 64, all pointers 16-byte
+ * aligned.  GELU(u) = u Phi(u) is applied to the fp32 accumulator (Phi
+ * from an erf approximation with absolute error below 1.5e-7) and rounded
+ * to bf16 once; the pre-activation u is not written.  ws: at least 2 F K
+ * bytes (W1 transposed), caller-owned, clobbered.  bf16 only: with fp32
+ * storage the stack uses pa_gemm and pa_gelu.  Unserved K or F return
+ * PA_ERR_UNSUPPORTED. */
+pa_status pa_mlp_up(int64_t N, int K, int F, const void* X, const void* W1, const float* b1,
+                    void* G, void* ws, size_t ws_bytes, void* stream);
+/* Its chain rule with the pre-activation recomputed from X:
+ * dU [N,F] = (dY W2^T) GELU'(X W1 + b1), dY [N,K] and W2 [F,K] bf16 (the
+ * second product's input gradient and weight), the rest as pa_mlp_up. */
+pa_status pa_mlp_up_backward(int64_t N, int K, int F, const void* X, const void* W1,
+                             const float* b1, const void* dY, const void* W2, void* dU,
+                             void* ws, size_t ws_bytes, void* stream);
 
 /* out[c] = sum over the N rows of x [N,C] (the bias gradient of a linear
  * layer; C a multiple of 16 bytes' worth, at most 256 x 16 bytes);

@@ -34,7 +34,7 @@ SYMBOLS = (
     "pa_project_backward", "pa_heads_relayout", "pa_heads_expand", "pa_heads_sum",
     "pa_heads_workspace_size", "pa_heads_slice_aggregate", "pa_heads_deslice",
     "pa_heads_deslice_backward", "pa_heads_slice_aggregate_backward",
-    "pa_slice_aggregate_noalloc",
+    "pa_slice_aggregate_noalloc", "pa_mlp_up", "pa_mlp_up_backward",
 )
 
 
@@ -116,6 +116,8 @@ def load(path: str = LIB_PATH):
     lib.pa_gelu.argtypes = [I64, I32, P, P, P]
     lib.pa_gelu_backward.argtypes = [I64, I32, P, P, P, P]
     lib.pa_colsum.argtypes = [I64, I32, I32, P, P, P, S, P]
+    lib.pa_mlp_up.argtypes = [I64, I32, I32, P, P, P, P, P, S, P]
+    lib.pa_mlp_up_backward.argtypes = [I64, I32, I32, P, P, P, P, P, P, P, S, P]
     lib.pa_project_fold.argtypes = [D, P, P, P, P, P, P, P, P, P, P]
     lib.pa_project_states.argtypes = [D, P, P, P, P, P]
     lib.pa_project_backward.argtypes = [D, P, P, P, P, P, P, SGp, P, P, P, SGp, P]
@@ -469,12 +471,37 @@ def pa_layernorm_backward(x, mean, rstd, dy, dx, g=None, dres=None, dg=None, db=
 
 
 def pa_gelu(x, y, stream=None):
-    _check(load().pa_gelu(x.numel(), _dt(x), _ptr(x), _ptr(y), _stream(stream)))
+    n, dt = x.numel(), _dt(x)
+    _check(load().pa_gelu(n, dt, _ptr(x), _arg(y, n, dt, "y"), _stream(stream)))
 
 
 def pa_gelu_backward(x, dy, dx, stream=None):
-    _check(load().pa_gelu_backward(x.numel(), _dt(x), _ptr(x), _ptr(dy), _ptr(dx),
+    n, dt = x.numel(), _dt(x)
+    _check(load().pa_gelu_backward(n, dt, _ptr(x), _arg(dy, n, dt, "dy"), _arg(dx, n, dt, "dx"),
                                    _stream(stream)))
+
+
+def pa_mlp_up(X, W1, b1, G, ws, stream=None):
+    """G [N,F] = GELU(X W1 + b1) in one kernel (bf16; X [N,K], W1 [K,F], b1
+    [F] fp32); ws: a device buffer of at least 2 F K bytes."""
+    N, K = X.shape
+    F = W1.shape[1]
+    _need(X, N * K, PA_BF16, "X")
+    _check(load().pa_mlp_up(N, K, F, _ptr(X), _arg(W1, K * F, PA_BF16, "W1"),
+                            _arg(b1, F, PA_F32, "b1"), _arg(G, N * F, PA_BF16, "G"), _ptr(ws),
+                            _nbytes(ws), _stream(stream)))
+
+
+def pa_mlp_up_backward(X, W1, b1, dY, W2, dU, ws, stream=None):
+    """dU [N,F] = (dY W2^T) GELU'(X W1 + b1), the pre-activation recomputed
+    (bf16; dY [N,K], W2 [F,K])."""
+    N, K = X.shape
+    F = W1.shape[1]
+    _need(X, N * K, PA_BF16, "X")
+    _check(load().pa_mlp_up_backward(N, K, F, _ptr(X), _arg(W1, K * F, PA_BF16, "W1"),
+                                     _arg(b1, F, PA_F32, "b1"), _arg(dY, N * K, PA_BF16, "dY"),
+                                     _arg(W2, F * K, PA_BF16, "W2"), _arg(dU, N * F, PA_BF16, "dU"),
+                                     _ptr(ws), _nbytes(ws), _stream(stream)))
 
 
 def pa_colsum(x, out, ws, stream=None):

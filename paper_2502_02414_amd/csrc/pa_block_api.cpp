@@ -187,6 +187,40 @@ pa_status pa_gelu_backward(int64_t n, pa_dtype dtype, const void* x, const void*
   return PA_OK;
 }
 
+static pa_status mlp_up(const char* who, int64_t N, int K, int F, const void* X,
+                        const void* W1, const float* b1, const void* dY, const void* W2,
+                        void* out, void* ws, size_t ws_bytes, void* stream) {
+  if (N < 1) return err(PA_ERR_INVALID, "%s: N must be >= 1", who);
+  if (!pa::mlp_up_served(K, F))
+    return err(PA_ERR_UNSUPPORTED, "%s: K must be 64, 128 or 256 and F a multiple of 64", who);
+  const void* ps[] = {X, W1, b1, out, ws};
+  const char* names[] = {"X", "W1", "b1", "out", "ws"};
+  for (int i = 0; i < 5; ++i) {
+    PB_TRY(need(ps[i], names[i]));
+    if (!a16(ps[i])) return err(PA_ERR_INVALID, "%s: %s must be 16-byte aligned", who, names[i]);
+  }
+  if (dY) {
+    PB_TRY(need(W2, "W2"));
+    if (!a16(dY) || !a16(W2)) return err(PA_ERR_INVALID, "%s: dY and W2 must be 16-byte aligned", who);
+  }
+  const size_t need_ws = (size_t)2 * F * K;
+  if (ws_bytes < need_ws) return err(PA_ERR_WORKSPACE, "%s: workspace needs %zu bytes", who, need_ws);
+  PB_HIP(pa::launch_mlp_up(N, K, F, X, W1, b1, dY, W2, out, ws, as_stream(stream)), who);
+  return PA_OK;
+}
+
+pa_status pa_mlp_up(int64_t N, int K, int F, const void* X, const void* W1, const float* b1,
+                    void* G, void* ws, size_t ws_bytes, void* stream) {
+  return mlp_up("pa_mlp_up", N, K, F, X, W1, b1, nullptr, nullptr, G, ws, ws_bytes, stream);
+}
+
+pa_status pa_mlp_up_backward(int64_t N, int K, int F, const void* X, const void* W1,
+                             const float* b1, const void* dY, const void* W2, void* dU,
+                             void* ws, size_t ws_bytes, void* stream) {
+  PB_TRY(need(dY, "dY"));
+  return mlp_up("pa_mlp_up_backward", N, K, F, X, W1, b1, dY, W2, dU, ws, ws_bytes, stream);
+}
+
 pa_status pa_colsum(int64_t N, int C, pa_dtype dtype, const void* x, float* out, void* ws,
                     size_t ws_bytes, void* stream) {
   PB_TRY(dtype_ok(dtype));

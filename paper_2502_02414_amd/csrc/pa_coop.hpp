@@ -81,14 +81,6 @@ struct CoopStage {
 #endif
 constexpr int kCoopDepth = PA_COOP_DEPTH;
 
-// Block-wide LDS barrier: this wave's LDS accesses have completed (lgkmcnt)
-// when it reaches the barrier, and no memory access moves across it.  Not
-// __syncthreads(): its workgroup fence would also wait for every
-// outstanding global load, i.e. for the tiles being prefetched.
-__device__ __forceinline__ void block_sync() {
-  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-}
-
 template <typename T, int C, int MB, int TT>
 __global__ void __launch_bounds__(256) k_slice_bwd_coop(StreamArgs a) {
   using G_ = Geo<sizeof(T), C, MB>;

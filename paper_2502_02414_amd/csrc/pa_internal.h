@@ -216,6 +216,13 @@ hipError_t launch_gelu(int64_t n, int dtype, const void* x, const void* dy, void
 // Per-block column sums of x [N,C] (P records of C floats).
 hipError_t launch_colsum(int64_t N, int C, int dtype, const void* x, float* partials, int P,
                          hipStream_t st);
+// The MLP's first product with its activation (pa_mlp.hip, bf16): forward
+// (DY == NULL) out = GELU(X W1 + b1); backward out = (DY W2^T) GELU'(X W1 +
+// b1).  X, DY [N, K]; W1 [K, F]; W2 [F, K]; b1 [F]; out [N, F]; W1T: F K
+// bf16 of scratch for W1 transposed.
+bool mlp_up_served(int K, int F);
+hipError_t launch_mlp_up(int64_t N, int K, int F, const void* X, const void* W1, const float* b1,
+                         const void* DY, const void* W2, void* out, void* W1T, hipStream_t st);
 // Project folding (fp32 parameters; A_out, a_out in dtype).
 struct FoldArgs {
   int C = 0, M = 0;

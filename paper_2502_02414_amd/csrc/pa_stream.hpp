@@ -145,6 +145,14 @@ __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_wave_barrier();
 }
 
+// Block-wide LDS barrier: this wave's LDS accesses have completed (lgkmcnt)
+// when it reaches the barrier, and no memory access moves across it.  Not
+// __syncthreads(): its workgroup fence would also wait for every
+// outstanding global load, i.e. for the tiles being prefetched.
+__device__ __forceinline__ void block_sync() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 // Software pipeline over N unrolled steps: the LDS reads of step i + D - 1
 // are issued before the MFMAs of step i (the scheduling barrier keeps the
 // compiler from sinking them back next to their use).

@@ -14,12 +14,14 @@ run on h = LN1(x), and the states are projected, S_proj = S Wp + bp
 the layer's output projection).  x_proj is never formed.
 
 Every step is a call of libpa.so (the layer's calls, LayerNorm with the
-residual add fused, GELU (tanh form), the Project folding, and hipBLASLt
-GEMMs for the MLP, whose second GEMM adds the residual).  torch only allocates the device
-buffers.  Per layer the forward keeps x, LN1(x), x1, LN2(x1), the MLP's
-pre-activation u and GELU(u) (the backward's weight gradient of W2 reads it;
-keeping it costs 2 N 4C bytes per layer and saves recomputing it), and the
-small per-layer state for the backward.
+residual add fused, the Project folding, the MLP's first product with its
+GELU as one kernel (bf16; fp32 storage: a hipBLASLt GEMM and the GELU
+kernel), and hipBLASLt GEMMs for the rest of the MLP, whose second GEMM
+adds the residual).  torch only allocates the device buffers.  Per layer the
+forward keeps x, LN1(x), x1, LN2(x1), GELU(u) (the backward's weight
+gradient of W2 reads it) and the small per-layer state for the backward;
+the pre-activation u is recomputed by the backward's fused kernel from
+LN2(x1) (bf16; fp32 storage keeps u).
 
 Parameters per layer (dict of device tensors): fp32 ln1_g, ln1_b, Wp [C,C],
 bp [C], A [C,M], b [M], a [C], Wq, bq, Wk, bk, Wv, bv (optional Wo, bo),
@@ -48,6 +50,8 @@ class BlockStack:
         # scratch of the sums over rows (LayerNorm gains, bias gradients) and of hipBLASLt
         self.ws_rows = torch.empty(1024 * 4 * C, dtype=torch.float32, device=device)
         self.ws_gemm = torch.empty(256 << 20, dtype=torch.uint8, device=device)
+        # bf16: the MLP's first product and GELU as one kernel (pa_mlp_up)
+        self.fused_mlp = self.pdt == B.PA_BF16 and C in (64, 128, 256)
         self.dev = device
 
     # -- helpers ------------------------------------------------------------
@@ -93,10 +97,15 @@ class BlockStack:
             x1, h2, m2, r2 = self._e(N, C), self._e(N, C), self._f(N), self._f(N)
             B.pa_layernorm(x, h2, m2, r2, g=p["ln2_g"], b=p["ln2_b"], r=y, xs=x1, eps=self.ln_eps)
             del y
-            u = self._e(N, 4 * C)
-            self._gemm(h2, p["W1"], u, bias=p["b1"])
             gu = self._e(N, 4 * C)
-            B.pa_gelu(u, gu)
+            if self.fused_mlp:
+                # GELU(h2 W1 + b1) in one kernel; u is recomputed in the backward
+                u = None
+                B.pa_mlp_up(h2, p["W1"], p["b1"], gu, self.ws_gemm)
+            else:
+                u = self._e(N, 4 * C)
+                self._gemm(h2, p["W1"], u, bias=p["b1"])
+                B.pa_gelu(u, gu)
             x2 = self._e(N, C)
             # x2 = x1 + GELU(u) W2 + b2 (the second residual add in the GEMM)
             self._gemm(gu, p["W2"], x2, bias=p["b2"], beta=1.0, C=x1)
@@ -122,8 +131,11 @@ class BlockStack:
             self._gemm(gu, dy, g["dW2"], transA=True)
             g["db2"] = self._f(C)
             B.pa_colsum(dy, g["db2"], self.ws_rows)
-            self._gemm(dy, p["W2"], gu, transB=True)              # dGELU(u), in place of gu
-            B.pa_gelu_backward(c["u"], gu, gu)                     # du
+            if self.fused_mlp:                                     # du, in place of gu
+                B.pa_mlp_up_backward(c["h2"], p["W1"], p["b1"], dy, p["W2"], gu, self.ws_gemm)
+            else:
+                self._gemm(dy, p["W2"], gu, transB=True)          # dGELU(u), in place of gu
+                B.pa_gelu_backward(c["u"], gu, gu)                 # du
             g["dW1"] = self._f(C, 4 * C)
             self._gemm(c["h2"], gu, g["dW1"], transA=True)
             g["db1"] = self._f(4 * C)

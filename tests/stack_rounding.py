@@ -3,8 +3,9 @@
 
 The GPU stack (paper_2502_02414_amd/stack.py) stores its point-side
 intermediates in the storage dtype (LN1(x), the deslice output, x1,
-LN2(x1), the MLP's pre-activation and its GELU, every block output, and in
-the backward dGELU, du, dLN2, dx1, dh, dx), keeps the token-side tensors in
+LN2(x1), GELU of the MLP's pre-activation, every block output, and in the
+backward du, dLN2, dx1, dh, dx; with fp32 storage also the pre-activation
+and dGELU, which bf16 storage keeps in registers), keeps the token-side tensors in
 fp32 (num, den, S, S_proj, S', dS', dS_proj, dS) and folds Algorithm 1's
 Project step into the slice parameters (A' = Wp A and a' = Wp a, in the
 storage dtype).  ``stack_model`` evaluates the oracle's own steps (its
@@ -49,6 +50,10 @@ def stack_model(x, dY, Gs, ps, tau0, tau_min, eps, H, dt, rnd=True, jitter=0.0, 
     """Forward + backward of the stack.  Returns (out, dx, [grads per layer])
     with the gradients named as in oracle.stack_backward."""
     R, F = _rounders(dt, rnd, jitter, seed)  # storage-dtype and fp32 rounding
+    # bf16: the MLP's first product and its activation are one kernel
+    # (pa_mlp_up): u and dY W2^T stay in fp32 registers, only GELU(u) and
+    # dU are stored; fp32 storage stores u and dY W2^T (pa_gemm, pa_gelu)
+    fused = dt == "bf16"
     x = np.asarray(x, dtype=np.float64)
     caches = []
     for G, p in zip(Gs, ps):
@@ -64,7 +69,9 @@ def stack_model(x, dY, Gs, ps, tau0, tau_min, eps, H, dt, rnd=True, jitter=0.0, 
         Sp = F(oracle.token_attention(S_proj, H, *att))
         x1 = R(x + R(oracle.deslice(W, Sp)))
         h2 = R(oracle.layernorm(x1, p["ln2_g"], p["ln2_b"])[0])
-        u = R(h2 @ np.asarray(p["W1"], dtype=np.float64) + p["b1"])
+        u = h2 @ np.asarray(p["W1"], dtype=np.float64) + p["b1"]
+        if not fused:
+            u = R(u)
         gu = R(oracle.gelu(u))
         x2 = R(x1 + gu @ np.asarray(p["W2"], dtype=np.float64) + p["b2"])
         caches.append(dict(x=x, h=h, Af=Af, bf=bf, af=af, bt=bt, W=W, num=num, den=den, S=S,
@@ -78,7 +85,8 @@ def stack_model(x, dY, Gs, ps, tau0, tau_min, eps, H, dt, rnd=True, jitter=0.0, 
         Wp, bp, A, a = (np.asarray(p[k], dtype=np.float64) for k in ("Wp", "bp", "A", "a"))
         W1, W2 = (np.asarray(p[k], dtype=np.float64) for k in ("W1", "W2"))
         g = {"dW2": c["gu"].T @ dy, "db2": dy.sum(axis=0)}
-        du = R(oracle.gelu_backward(c["u"], R(dy @ W2.T)))
+        dgu = dy @ W2.T
+        du = R(oracle.gelu_backward(c["u"], dgu if fused else R(dgu)))
         g["dW1"], g["db1"] = c["h2"].T @ du, du.sum(axis=0)
         dh2 = R(du @ W1.T)
         dx1_ln, g["dln2_g"], g["dln2_b"] = oracle.layernorm_backward(c["x1"], p["ln2_g"], dh2)

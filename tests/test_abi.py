@@ -32,14 +32,14 @@ def _declared_symbols():
 
 def test_every_declared_symbol_is_exported(lib):
     declared = _declared_symbols()
-    assert len(declared) == 33
+    assert len(declared) == 35
     assert sorted(B.SYMBOLS) == declared
     for name in declared:
         assert hasattr(lib, name), name
 
 
 def test_version(lib):
-    assert lib.pa_version() == 5
+    assert lib.pa_version() == 6
 
 
 def _dims(**kw):
@@ -99,7 +99,6 @@ fake_addresses = pytest.mark.skipif(_gpu_visible(),
 
 
 @fake_addresses
-@fake_addresses
 def test_null_and_misaligned_pointers_rejected(lib):
     d = _dims()
     sp = B.pa_slice_params(FAKE, None, None, 0.0)
@@ -124,7 +123,6 @@ def test_null_and_misaligned_pointers_rejected(lib):
 
 
 @fake_addresses
-@fake_addresses
 def test_small_workspace_rejected(lib):
     d = _dims()
     sp = B.pa_slice_params(FAKE, None, None, 0.0)
@@ -138,7 +136,6 @@ def test_small_workspace_rejected(lib):
 
 
 @fake_addresses
-@fake_addresses
 def test_attention_argument_checks(lib):
     d = _dims()
     _, n = _ws_size(lib, d)
@@ -150,7 +147,6 @@ def test_attention_argument_checks(lib):
     assert st == B.PA_ERR_INVALID
 
 
-@fake_addresses
 @fake_addresses
 def test_unserved_table_shape_is_unsupported(lib):
     # the backward tables of C=256, M=64 in fp32 exceed the 160 KB of LDS
@@ -280,3 +276,28 @@ def test_struct_layouts_match_header(tmp_path):
         assert got[(name, "sizeof")] == ctypes.sizeof(cls), name
         for f in cls._fields_:
             assert got[(name, f[0])] == getattr(cls, f[0]).offset, (name, f[0])
+
+
+@fake_addresses
+def test_mlp_up_argument_checks(lib):
+    F, K = 1024, 256
+    # unserved K or F
+    st = lib.pa_mlp_up(1000, 96, F, FAKE, FAKE, FAKE, FAKE, FAKE, 2 * F * K, None)
+    assert st == B.PA_ERR_UNSUPPORTED
+    st = lib.pa_mlp_up(1000, K, 1000, FAKE, FAKE, FAKE, FAKE, FAKE, 2 * F * K, None)
+    assert st == B.PA_ERR_UNSUPPORTED
+    # missing or misaligned pointers, small workspace, missing dY / W2
+    st = lib.pa_mlp_up(1000, K, F, None, FAKE, FAKE, FAKE, FAKE, 2 * F * K, None)
+    assert st == B.PA_ERR_INVALID and "X" in lib.pa_last_error().decode()
+    st = lib.pa_mlp_up(1000, K, F, FAKE, FAKE + 4, FAKE, FAKE, FAKE, 2 * F * K, None)
+    assert st == B.PA_ERR_INVALID and "W1" in lib.pa_last_error().decode()
+    st = lib.pa_mlp_up(1000, K, F, FAKE, FAKE, FAKE, FAKE, FAKE, 2 * F * K - 1, None)
+    assert st == B.PA_ERR_WORKSPACE
+    st = lib.pa_mlp_up(0, K, F, FAKE, FAKE, FAKE, FAKE, FAKE, 2 * F * K, None)
+    assert st == B.PA_ERR_INVALID
+    st = lib.pa_mlp_up_backward(1000, K, F, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, 2 * F * K,
+                                None)
+    assert st == B.PA_ERR_INVALID and "dY" in lib.pa_last_error().decode()
+    st = lib.pa_mlp_up_backward(1000, K, F, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, 2 * F * K,
+                                None)
+    assert st == B.PA_ERR_INVALID and "W2" in lib.pa_last_error().decode()

@@ -113,6 +113,41 @@ def test_gelu(dt):
     check("dgelu", host(dx), oracle.gelu_backward(x, dy), TOL[dt])
 
 
+MLP_UP = [  # N, K, F: ragged last block (128 points per block), every K served
+    (1000, 64, 256), (77, 128, 512), (4099, 256, 1024), (1, 256, 1024)]
+
+
+@pytest.mark.parametrize("case", MLP_UP, ids=[f"N{c[0]}-K{c[1]}-F{c[2]}" for c in MLP_UP])
+def test_mlp_up(case):
+    """The MLP's first product with GELU in one kernel, and its chain rule
+    with the pre-activation recomputed, against the oracle's GELU and its
+    derivative applied to the float64 products of the same bf16 values."""
+    import torch
+    N, K, F = case
+    say(f"mlp_up N={N} K={K} F={F}")
+    X, dY = _rnd("bf16", N, K, seed=20), _rnd("bf16", N, K, seed=21)
+    W1 = _rnd("bf16", K, F, scale=K ** -0.5, seed=22)
+    W2 = _rnd("bf16", F, K, scale=F ** -0.5, seed=23)
+    b1 = _rnd("f32", F, scale=0.1, seed=24)
+    ws = torch.empty(2 * F * K, dtype=torch.uint8, device="cuda")
+    Xd, W1d, b1d = dev(X, "bf16"), dev(W1, "bf16"), dev(b1)
+    G = dev(np.zeros((N, F), np.float32), "bf16")
+    dU = dev(np.zeros((N, F), np.float32), "bf16")
+    B.pa_mlp_up(Xd, W1d, b1d, G, ws)
+    B.pa_mlp_up_backward(Xd, W1d, b1d, dev(dY, "bf16"), dev(W2, "bf16"), dU, ws)
+    u = X.astype(np.float64) @ W1.astype(np.float64) + b1
+    dg = dY.astype(np.float64) @ W2.astype(np.float64).T
+    ref_g, ref_du = oracle.gelu(u), oracle.gelu_backward(u, dg)
+    check("G", host(G), ref_g, TOL["bf16"])
+    check("dU", host(dU), ref_du, TOL["bf16"])
+    # the kernels round a fp32 accumulation once: within a few bf16 steps of
+    # the exact values, element by element
+    for name, got, ref in (("G", host(G), ref_g), ("dU", host(dU), ref_du)):
+        err = np.abs(got - ref) / (np.abs(ref) + 1e-3 * np.abs(ref).max())
+        say(f"  {name:10s} max element error {err.max():.2e} (bf16 step 3.9e-3)")
+        assert err.max() < 2e-2, (name, err.max())
+
+
 GEMMS = [  # m, n, k, transA, transB, in dtype, out dtype, bias, residual
     (1000, 96, 64, False, False, "f32", "f32", True, False),
     (1000, 96, 64, False, True, "f32", "f32", False, True),
