@@ -33,10 +33,10 @@
 
 namespace pa {
 
-template <typename T, int C, int MB, int TT>
+template <typename T, int C, int MB, int TT, int NG = 1>
 struct CoopGeo {
   using G_ = Geo<sizeof(T), C, MB>;
-  static constexpr int WAVES = 4;
+  static constexpr int WAVES = 4 * NG;  // NG groups of four waves
   static constexpr int SZ = (int)sizeof(T);
   static constexpr int IMG = G_::img_bytes(kSliceBwd);
   static constexpr int SROW = G_::M16 * SZ + 16;  // published w / dl rows (per point)
@@ -48,19 +48,27 @@ struct CoopGeo {
   static constexpr int OFF_L = OFF_W + 16 * SROW;
   static constexpr int TILE = OFF_L + 16 * SROW;
   // per tile and wave: (max, sum), <w, dw>, (res, P1, P2, -) for 16 points
-  static constexpr int OFF_EX = IMG + TT * TILE;
+  static constexpr int OFF_EX = IMG + NG * TT * TILE;
   static constexpr int EX = 4 * 16 * (8 + 4 + 16);
-  static constexpr int LDS = OFF_EX + TT * EX;
+  static constexpr int LDS = OFF_EX + NG * TT * EX;
+  // the second group's per-lane partial sums at the end (over the tables
+  // and tiles, no longer read then)
+  static constexpr int PART = 80;  // floats per lane: dA 64, db 4, da 4, db_t 1
   // a quarter of a tile's rows per wave: 16-byte chunks per lane
   static constexpr int QCH = 4 * C * SZ / 16 / 64;
   static constexpr bool fits = LDS <= kLdsBytes && QCH >= 1 && 4 * C * SZ == QCH * 16 * 64;
 };
 
-// Tiles per round: two (every table fragment read once for 32 points) when
-// both tiles fit in LDS beside the tables.
+// Tiles per round and groups: two groups of four waves, each on its own
+// tile (two waves per SIMD, one per group: one group's compute overlaps the
+// other's waits), when both tiles fit in LDS beside the tables.
+template <typename T, int C, int MB>
+constexpr int coop_groups() {
+  return CoopGeo<T, C, MB, 1, 2>::fits ? 2 : 1;
+}
 template <typename T, int C, int MB>
 constexpr int coop_tiles() {
-  return CoopGeo<T, C, MB, 2>::fits ? 2 : 1;
+  return 1;
 }
 
 // Whether kSliceBwd runs the block-cooperative kernel at this shape.
@@ -75,24 +83,28 @@ struct CoopStage {
   uint4 g[TT];
 };
 
-// Register prefetch (rounds in flight) of the cooperative kernel.
-#ifndef PA_COOP_DEPTH
-#define PA_COOP_DEPTH 2
-#endif
-constexpr int kCoopDepth = PA_COOP_DEPTH;
+// Register prefetch (rounds in flight) of the cooperative kernel: two with
+// one group (one wave per SIMD), one with two groups (whose registers then
+// fit two waves per SIMD).
+template <int NG>
+constexpr int coop_depth() {
+  return NG == 1 ? 2 : 1;
+}
 
-template <typename T, int C, int MB, int TT>
-__global__ void __launch_bounds__(256) k_slice_bwd_coop(StreamArgs a) {
+template <typename T, int C, int MB, int TT, int NG>
+__global__ void __launch_bounds__(256 * NG) __attribute__((amdgpu_waves_per_eu(NG)))
+k_slice_bwd_coop(StreamArgs a) {
   using G_ = Geo<sizeof(T), C, MB>;
-  using CG = CoopGeo<T, C, MB, TT>;
+  using CG = CoopGeo<T, C, MB, TT, NG>;
   using Stage = CoopStage<T, C, MB, TT>;
   constexpr int M16 = G_::M16, SZ = CG::SZ, CB = G_::CB, XF = G_::XF;
   constexpr int RCH = C * SZ / 16;  // 16-byte chunks per row
-  constexpr int DEPTH = kCoopDepth;
+  constexpr int DEPTH = coop_depth<NG>();
   extern __shared__ __attribute__((aligned(16))) char smem[];
   head_offsets(a);
   add_tb_dev(a);
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) & 3;  // in its group
+  const int grp = __builtin_amdgcn_readfirstlane(threadIdx.x >> 8);
   const int lane = lane_id(), r = lane & 15, g = lane >> 4;
   const bool hasG = a.flags & kHasG;
   const bool deslice = a.flags & kDesliceTerm;
@@ -105,16 +117,12 @@ __global__ void __launch_bounds__(256) k_slice_bwd_coop(StreamArgs a) {
   const float* af = hdr + 3 * M16 + 2 * C;
   const char* tabL = smem + G_::OFF_L;
   const char* tabW = smem + G_::OFF_2;
-  auto tile_lds = [&](int tt) { return smem + CG::IMG + tt * CG::TILE; };
-  auto ex_ms = [&](int tt) {
-    return reinterpret_cast<float2*>(smem + CG::OFF_EX + tt * CG::EX);
-  };
-  auto ex_s1 = [&](int tt) {
-    return reinterpret_cast<float*>(smem + CG::OFF_EX + tt * CG::EX + 4 * 16 * 8);
-  };
-  auto ex_s3 = [&](int tt) {
-    return reinterpret_cast<f32x4*>(smem + CG::OFF_EX + tt * CG::EX + 4 * 16 * 12);
-  };
+  // the group's tiles and exchange slots
+  auto tile_lds = [&](int tt) { return smem + CG::IMG + (grp * TT + tt) * CG::TILE; };
+  auto ex_at = [&](int tt) { return smem + CG::OFF_EX + (grp * TT + tt) * CG::EX; };
+  auto ex_ms = [&](int tt) { return reinterpret_cast<float2*>(ex_at(tt)); };
+  auto ex_s1 = [&](int tt) { return reinterpret_cast<float*>(ex_at(tt) + 4 * 16 * 8); };
+  auto ex_s3 = [&](int tt) { return reinterpret_cast<f32x4*>(ex_at(tt) + 4 * 16 * 12); };
 
   const auto lb = logits_bases<T, C, MB, true>();
   const RowBase<T> yb = row_base<T>(r, G_::XT_ROW);
@@ -130,7 +138,7 @@ __global__ void __launch_bounds__(256) k_slice_bwd_coop(StreamArgs a) {
   copy_image(smem, a.img, CG::IMG);
 #pragma unroll
   for (int tt = 0; tt < TT; ++tt)
-    for (int q = threadIdx.x; q < G_::GT / 16; q += 256)
+    for (int q = threadIdx.x & 255; q < G_::GT / 16; q += 256)
       reinterpret_cast<uint4*>(tile_lds(tt) + CG::OFF_G)[q] = uint4{0, 0, 0, 0};
   __syncthreads();  // (before any prefetch: a full fence costs nothing here)
   float bias[4], dden[4];
@@ -157,13 +165,15 @@ __global__ void __launch_bounds__(256) k_slice_bwd_coop(StreamArgs a) {
   const T* Y = reinterpret_cast<const T*>(a.dY);
   const T* Gp = reinterpret_cast<const T*>(a.G);
   T* DX = reinterpret_cast<T*>(a.out);
-  // the block's tiles [t0, t1) in rounds of TT; a round's tile past t1 is
-  // the last tile again, with no contribution (live = false)
+  // the block's tiles [t0, t1) in rounds of NG TT (group grp: TT tiles from
+  // the round's grp-th); a round's tile past t1 is the last tile again, with
+  // no contribution (live = false)
   const int64_t T_ = (a.N + 15) / 16;
   const int64_t t0 = T_ * blockIdx.x / gridDim.x, t1 = T_ * (blockIdx.x + 1) / gridDim.x;
-  const int64_t nr = (t1 - t0 + TT - 1) / TT;  // rounds
+  const int64_t nr = (t1 - t0 + NG * TT - 1) / (NG * TT);  // rounds
+  auto tile_at = [&](int64_t rd, int tt) { return t0 + (NG * rd + grp) * TT + tt; };
   auto tile_of = [&](int64_t rd, int tt) {
-    const int64_t t = t0 + TT * rd + tt;
+    const int64_t t = tile_at(rd, tt);
     return t < t1 ? t : t1 - 1;
   };
   const int gchunks = 16 * a.M * SZ / 16;  // the Gumbel rows of a full tile
@@ -228,7 +238,7 @@ __global__ void __launch_bounds__(256) k_slice_bwd_coop(StreamArgs a) {
     bool live[TT], pv[TT];
 #pragma unroll
     for (int tt = 0; tt < TT; ++tt) {
-      live[tt] = t0 + TT * rd + tt < t1;  // uniform over the block
+      live[tt] = tile_at(rd, tt) < t1;  // uniform over the group
       p0[tt] = tile_of(rd, tt) * 16;
       nvalid[tt] = (int)(a.N - p0[tt] < 16 ? a.N - p0[tt] : 16);
       pv[tt] = live[tt] && r < nvalid[tt];
@@ -446,7 +456,7 @@ __global__ void __launch_bounds__(256) k_slice_bwd_coop(StreamArgs a) {
     wave_sync();
 #pragma unroll
     for (int tt = 0; tt < TT; ++tt) {
-      if (live[tt]) {  // uniform over the block
+      if (live[tt]) {  // uniform over the group
         // the wave's 64 channels of the tile's rows: 8 chunks per row (rows
         // past the tile's last point write that point's chunk again: the
         // same bytes, and every lane stores unconditionally)
@@ -531,7 +541,7 @@ __global__ void __launch_bounds__(256) k_slice_bwd_coop(StreamArgs a) {
   }
 #pragma unroll
   for (int d = 0; d < DEPTH - 1; ++d) {
-    if (rd + d < nr) {  // uniform over the block
+    if (rd + d < nr) {  // uniform over the block (every group runs nr rounds)
       block_sync();
       store(st[d], rd + d);
       block_sync();
@@ -539,6 +549,33 @@ __global__ void __launch_bounds__(256) k_slice_bwd_coop(StreamArgs a) {
     }
   }
 
+  // two groups: the second group's per-lane partials through LDS (over the
+  // tables and tiles, no longer read), added to the first's in that order
+  if constexpr (NG == 2) {
+    static_assert(4 * 64 * CG::PART * 4 <= CG::LDS, "group partials must fit in LDS");
+    float* part = reinterpret_cast<float*>(smem) + (wave * 64 + lane) * CG::PART;
+    block_sync();
+    if (grp == 1) {
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb) *reinterpret_cast<f32x4*>(part + 4 * cb) = dA[cb];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        part[4 * CB + i] = db[i];
+        part[4 * CB + 4 + i] = da[i];
+      }
+      part[4 * CB + 8] = dbt;
+    }
+    block_sync();
+    if (grp == 1) return;
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) dA[cb] += *reinterpret_cast<const f32x4*>(part + 4 * cb);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      db[i] += part[4 * CB + i];
+      da[i] += part[4 * CB + 4 + i];
+    }
+    dbt += part[4 * CB + 8];
+  }
   // lane partials -> wave totals, then the block's record: dA [C][M],
   // db [M], da [C], db_t, each part written by the wave that owns it
 #pragma unroll
