@@ -267,8 +267,11 @@ def test_layer_chain(cases, shape):
     check_key_bias(out["dbk"], out["dbq"], c.dt)
 
 
-def test_deterministic(cases):
-    shape = (3001, 256, 8, 32, "bf16")
+@pytest.mark.parametrize("shape", [(3001, 256, 8, 32, "bf16"), (50003, 256, 8, 64, "bf16")],
+                         ids=["per-wave", "cooperative"])
+def test_deterministic(cases, shape):
+    """Two runs of the layer are bitwise identical (every sum in a fixed
+    order; the second shape runs the cooperative slice backward)."""
     c, g, _ = get_case(cases, shape)
     a = g.layer()
     b = g.layer()
