@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define PA_VERSION 6
+#define PA_VERSION 7
 
 typedef enum { PA_F32 = 0, PA_BF16 = 1 } pa_dtype;
 
@@ -276,11 +276,9 @@ pa_status pa_time_kernel(const char* call, void* start, void* stop);
  * a residual add when it is another tensor and beta = 1).  The plain GEMMs of the MLP and the linear layers,
  * on hipBLASLt (fp32 accumulation).  The first call on a device creates
  * one hipBLASLt handle there (kept until the process ends); ws/ws_bytes is
- * hipBLASLt's workspace (may be 0).  The first call of each problem (shape,
- * dtypes, transposes, bias) times up to 8 of hipBLASLt's candidate
- * algorithms on `stream` (it synchronises that stream once) and keeps the
- * fastest, unless D is also the accumulated input (beta != 0, C = D).
- * A long reduction into a small fp32 output (transA, K >= 2^17, D at most
+ * hipBLASLt's workspace (may be 0).  pa_gemm itself never synchronises: a
+ * problem (shape, dtypes, transposes, bias) that pa_gemm_prepare has not
+ * tuned runs hipBLASLt's first heuristic candidate.  A long reduction into a small fp32 output (transA, K >= 2^17, D at most
  * 8 MB, beta = 0, no bias: the weight gradients) is split over K into up to
  * 64 partial products kept at the end of ws (at most half of it) and added
  * in order, deterministically.  A combination of dtypes hipBLASLt does
@@ -289,6 +287,18 @@ pa_status pa_gemm(int transA, int transB, int64_t m, int64_t n, int64_t k, float
                   const void* A, pa_dtype a_dtype, const void* B, pa_dtype b_dtype,
                   float beta, const void* C, void* D, pa_dtype d_dtype, const float* bias,
                   void* ws, size_t ws_bytes, void* stream);
+
+/* pa_gemm, and the tuning of its problem (same arguments, same result):
+ * up to 8 of hipBLASLt's candidate algorithms are timed on `stream` (the
+ * stream is synchronised) and the fastest is kept for every later pa_gemm
+ * of that problem on this device, unless D is also the accumulated input
+ * (beta != 0, C = D: the first candidate is kept).  It also creates the
+ * device's hipBLASLt handle: calling it once per problem before a timed or
+ * captured loop leaves pa_gemm with no allocation and no synchronisation. */
+pa_status pa_gemm_prepare(int transA, int transB, int64_t m, int64_t n, int64_t k, float alpha,
+                          const void* A, pa_dtype a_dtype, const void* B, pa_dtype b_dtype,
+                          float beta, const void* C, void* D, pa_dtype d_dtype,
+                          const float* bias, void* ws, size_t ws_bytes, void* stream);
 
 /* LayerNorm over the C channels of each of N rows (biased variance):
  * s = x (+ r when r is given, rounded to dtype and written to xs when xs is

@@ -34,7 +34,7 @@ SYMBOLS = (
     "pa_project_backward", "pa_heads_relayout", "pa_heads_expand", "pa_heads_sum",
     "pa_heads_workspace_size", "pa_heads_slice_aggregate", "pa_heads_deslice",
     "pa_heads_deslice_backward", "pa_heads_slice_aggregate_backward",
-    "pa_slice_aggregate_noalloc", "pa_mlp_up", "pa_mlp_up_backward",
+    "pa_slice_aggregate_noalloc", "pa_mlp_up", "pa_mlp_up_backward", "pa_gemm_prepare",
 )
 
 
@@ -111,6 +111,7 @@ def load(path: str = LIB_PATH):
     lib.pa_deslice_backward_w.argtypes = [D, P, P, P, P, S, P]
     I64, I32, F = ctypes.c_int64, ctypes.c_int, ctypes.c_float
     lib.pa_gemm.argtypes = [I32, I32, I64, I64, I64, F, P, I32, P, I32, F, P, P, I32, P, P, S, P]
+    lib.pa_gemm_prepare.argtypes = lib.pa_gemm.argtypes
     lib.pa_layernorm.argtypes = [I64, I32, F, I32, P, P, P, P, P, P, P, P, P]
     lib.pa_layernorm_backward.argtypes = [I64, I32, I32, P, P, P, P, P, P, P, P, P, P, S, P]
     lib.pa_gelu.argtypes = [I64, I32, P, P, P]
@@ -446,14 +447,19 @@ def _dt(t) -> int:
 
 
 def pa_gemm(A, B, D, transA=False, transB=False, alpha=1.0, beta=0.0, bias=None, ws=None,
-            C=None, stream=None):
-    """Row-major D = alpha op(A) op(B) + beta C (+ bias); C defaults to D."""
+            C=None, stream=None, prepare=False):
+    """Row-major D = alpha op(A) op(B) + beta C (+ bias); C defaults to D.
+    prepare: through pa_gemm_prepare (tunes the problem, synchronises)."""
     m = A.shape[1] if transA else A.shape[0]
     k = A.shape[0] if transA else A.shape[1]
     n = B.shape[0] if transB else B.shape[1]
-    _check(load().pa_gemm(int(transA), int(transB), m, n, k, float(alpha), _ptr(A), _dt(A),
-                          _ptr(B), _dt(B), float(beta), _ptr(C), _ptr(D), _dt(D), _ptr(bias),
-                          _ptr(ws), _nbytes(ws), _stream(stream)))
+    if (B.shape[1] if transB else B.shape[0]) != k:
+        raise ValueError(f"pa_gemm: inner dimensions {k} and {tuple(B.shape)} do not match")
+    dt = _dt(D)
+    fn = load().pa_gemm_prepare if prepare else load().pa_gemm
+    _check(fn(int(transA), int(transB), m, n, k, float(alpha), _ptr(A), _dt(A), _ptr(B), _dt(B),
+              float(beta), _arg(C, m * n, dt, "C"), _arg(D, m * n, dt, "D"), dt,
+              _arg(bias, n, PA_F32, "bias"), _ptr(ws), _nbytes(ws), _stream(stream)))
 
 
 def pa_layernorm(x, y, mean, rstd, g=None, b=None, r=None, xs=None, eps=1e-5, stream=None):

@@ -71,11 +71,12 @@ pa_status reduce_to(const float* parts, int P, int64_t rec, float* d0, int64_t l
 
 extern "C" {
 
-pa_status pa_gemm(int transA, int transB, int64_t m, int64_t n, int64_t k, float alpha,
-                  const void* A, pa_dtype a_dtype, const void* B, pa_dtype b_dtype, float beta,
-                  const void* C, void* D, pa_dtype d_dtype, const float* bias, void* ws,
-                  size_t ws_bytes, void* stream) {
-  if (m < 1 || n < 1 || k < 1) return err(PA_ERR_INVALID, "pa_gemm: m, n, k must be >= 1");
+static pa_status gemm_call(const char* who, bool tune, int transA, int transB, int64_t m,
+                           int64_t n, int64_t k, float alpha, const void* A, pa_dtype a_dtype,
+                           const void* B, pa_dtype b_dtype, float beta, const void* C, void* D,
+                           pa_dtype d_dtype, const float* bias, void* ws, size_t ws_bytes,
+                           void* stream) {
+  if (m < 1 || n < 1 || k < 1) return err(PA_ERR_INVALID, "%s: m, n, k must be >= 1", who);
   PB_TRY(dtype_ok(a_dtype));
   PB_TRY(dtype_ok(b_dtype));
   PB_TRY(dtype_ok(d_dtype));
@@ -84,7 +85,7 @@ pa_status pa_gemm(int transA, int transB, int64_t m, int64_t n, int64_t k, float
   PB_TRY(opt(C, "C"));
   PB_TRY(need(D, "D"));
   PB_TRY(opt(bias, "bias"));
-  if (ws_bytes && !ws) return err(PA_ERR_WORKSPACE, "pa_gemm: workspace is NULL");
+  if (ws_bytes && !ws) return err(PA_ERR_WORKSPACE, "%s: workspace is NULL", who);
   pa::Gemm g;
   g.transA = transA != 0;
   g.transB = transB != 0;
@@ -94,12 +95,28 @@ pa_status pa_gemm(int transA, int transB, int64_t m, int64_t n, int64_t k, float
   g.ta = a_dtype; g.tb = b_dtype; g.td = d_dtype;
   g.bias = bias;
   g.ws = ws; g.ws_bytes = ws_bytes;
-  const int s = pa::gemm(g, as_stream(stream));
+  const int s = pa::gemm(g, as_stream(stream), tune);
   if (s != 0)
     return err(s == 7 /* HIPBLAS_STATUS_NOT_SUPPORTED */ ? PA_ERR_UNSUPPORTED : PA_ERR_HIP,
-               "pa_gemm: hipBLASLt status %d (m=%lld n=%lld k=%lld types %d,%d->%d)", s,
+               "%s: hipBLASLt status %d (m=%lld n=%lld k=%lld types %d,%d->%d)", who, s,
                (long long)m, (long long)n, (long long)k, a_dtype, b_dtype, d_dtype);
   return PA_OK;
+}
+
+pa_status pa_gemm(int transA, int transB, int64_t m, int64_t n, int64_t k, float alpha,
+                  const void* A, pa_dtype a_dtype, const void* B, pa_dtype b_dtype, float beta,
+                  const void* C, void* D, pa_dtype d_dtype, const float* bias, void* ws,
+                  size_t ws_bytes, void* stream) {
+  return gemm_call("pa_gemm", false, transA, transB, m, n, k, alpha, A, a_dtype, B, b_dtype, beta,
+                   C, D, d_dtype, bias, ws, ws_bytes, stream);
+}
+
+pa_status pa_gemm_prepare(int transA, int transB, int64_t m, int64_t n, int64_t k, float alpha,
+                          const void* A, pa_dtype a_dtype, const void* B, pa_dtype b_dtype,
+                          float beta, const void* C, void* D, pa_dtype d_dtype,
+                          const float* bias, void* ws, size_t ws_bytes, void* stream) {
+  return gemm_call("pa_gemm_prepare", true, transA, transB, m, n, k, alpha, A, a_dtype, B, b_dtype,
+                   beta, C, D, d_dtype, bias, ws, ws_bytes, stream);
 }
 
 pa_status pa_layernorm(int64_t N, int C, float eps, pa_dtype dtype, const void* x, const void* r,

@@ -65,7 +65,7 @@ struct Descs {
 // One hipBLASLt product; batch > 1 runs `batch` products whose operands and
 // outputs are strided by sa, sb, sd elements.
 static int gemm_once(const Gemm& g, int batch, int64_t sa, int64_t sb, int64_t sd,
-                     hipStream_t st) {
+                     hipStream_t st, bool tune) {
   hipblasLtHandle_t h;
   hipblasStatus_t s = handle_for_current_device(&h);
   if (s != HIPBLAS_STATUS_SUCCESS) return (int)s;
@@ -125,7 +125,7 @@ static int gemm_once(const Gemm& g, int batch, int64_t sa, int64_t sb, int64_t s
       have = true;
     }
   }
-  if (!have) {
+  if (!have || tune) {
     PA_LT(hipblasLtMatmulPreferenceCreate(&d.pref));
     uint64_t wmax = g.ws_bytes;
     PA_LT(hipblasLtMatmulPreferenceSetAttribute(d.pref, HIPBLASLT_MATMUL_PREF_MAX_WORKSPACE_BYTES,
@@ -137,11 +137,11 @@ static int gemm_once(const Gemm& g, int batch, int64_t sa, int64_t sb, int64_t s
     for (int i = 0; i < n && best < 0; ++i)
       if (res[i].state == HIPBLAS_STATUS_SUCCESS) best = i;
     if (best < 0) return (int)HIPBLAS_STATUS_NOT_SUPPORTED;
-    // The first call of a problem times the candidates once (synchronising
-    // the stream) and keeps the fastest -- only when rerunning the product
-    // is harmless, i.e. D is not also its accumulated input.
+    // Tuning times the candidates once (synchronising the stream) and keeps
+    // the fastest -- only when rerunning the product is harmless, i.e. D is
+    // not also its accumulated input.  Untuned problems keep the first.
     const bool rerun_safe = g.beta == 0.f || (g.Cin && g.Cin != g.D);
-    if (rerun_safe && n > 1) {
+    if (tune && rerun_safe && n > 1) {
       hipEvent_t e0, e1;
       if (hipEventCreate(&e0) == hipSuccess && hipEventCreate(&e1) == hipSuccess) {
         const float al = g.alpha, be = g.beta;
@@ -175,7 +175,7 @@ static int gemm_once(const Gemm& g, int batch, int64_t sa, int64_t sb, int64_t s
   return 0;
 }
 
-int gemm(const Gemm& g, hipStream_t st) {
+int gemm(const Gemm& g, hipStream_t st, bool tune) {
   // A long reduction into a small fp32 output -- the weight gradients, op(A)
   // = X^T with K the points -- is split over K: S strided-batched products
   // of kc rows each (plus one for the rest) write S fp32 partials at the end
@@ -198,7 +198,7 @@ int gemm(const Gemm& g, hipStream_t st) {
       b.D = parts;
       b.ws_bytes = (g.ws_bytes - pbytes) / 256 * 256;
       const int esa = g.ta == 1 ? 2 : 4, esb = g.tb == 1 ? 2 : 4;
-      int r = gemm_once(b, S, kc * g.m, kc * g.n, g.m * g.n, st);
+      int r = gemm_once(b, S, kc * g.m, kc * g.n, g.m * g.n, st, tune);
       if (r) return r;
       if (rest > 0) {
         Gemm t = b;
@@ -206,7 +206,7 @@ int gemm(const Gemm& g, hipStream_t st) {
         t.A = reinterpret_cast<const char*>(g.A) + (size_t)S * kc * g.m * esa;
         t.B = reinterpret_cast<const char*>(g.B) + (size_t)S * kc * g.n * esb;
         t.D = parts + (size_t)S * g.m * g.n;
-        r = gemm_once(t, 1, 0, 0, 0, st);
+        r = gemm_once(t, 1, 0, 0, 0, st, tune);
         if (r) return r;
       }
       Segments seg{};
@@ -217,7 +217,7 @@ int gemm(const Gemm& g, hipStream_t st) {
                  ? 0 : (int)HIPBLAS_STATUS_EXECUTION_FAILED;
     }
   }
-  return gemm_once(g, 1, 0, 0, 0, st);
+  return gemm_once(g, 1, 0, 0, 0, st, tune);
 }
 
 }  // namespace pa

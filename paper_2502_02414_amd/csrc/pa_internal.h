@@ -267,6 +267,9 @@ struct Gemm {
   void* ws = nullptr;
   size_t ws_bytes = 0;
 };
-int gemm(const Gemm& g, hipStream_t st);
+// tune: time hipBLASLt's candidates for this problem (synchronising st) and
+// keep the fastest for later calls; otherwise a problem not tuned before
+// takes the heuristic's first candidate (no synchronisation).
+int gemm(const Gemm& g, hipStream_t st, bool tune = false);
 
 }  // namespace pa

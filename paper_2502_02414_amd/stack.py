@@ -50,6 +50,7 @@ class BlockStack:
         # scratch of the sums over rows (LayerNorm gains, bias gradients) and of hipBLASLt
         self.ws_rows = torch.empty(1024 * 4 * C, dtype=torch.float32, device=device)
         self.ws_gemm = torch.empty(256 << 20, dtype=torch.uint8, device=device)
+        self.tuned = set()  # GEMM problems already tuned (pa_gemm_prepare)
         # bf16: the MLP's first product and GELU as one kernel (pa_mlp_up)
         self.fused_mlp = self.pdt == B.PA_BF16 and C in (64, 128, 256)
         self.dev = device
@@ -62,7 +63,14 @@ class BlockStack:
         return self.torch.empty(*shape, dtype=self.torch.float32, device=self.dev)
 
     def _gemm(self, A, Bm, D, **kw):
-        B.pa_gemm(A, Bm, D, ws=self.ws_gemm, **kw)
+        # each GEMM problem is tuned once, on its first call (pa_gemm_prepare
+        # synchronises); later calls never synchronise
+        key = (tuple(A.shape), A.dtype, tuple(Bm.shape), Bm.dtype, D.dtype,
+               tuple(sorted((k, v if isinstance(v, (bool, float, int)) else v is not None)
+                            for k, v in kw.items())))
+        first = key not in self.tuned
+        self.tuned.add(key)
+        B.pa_gemm(A, Bm, D, ws=self.ws_gemm, prepare=first, **kw)
 
     def _folded(self, p):
         """The folded slice parameters of a layer (pa_project_fold)."""

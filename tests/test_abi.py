@@ -32,14 +32,14 @@ def _declared_symbols():
 
 def test_every_declared_symbol_is_exported(lib):
     declared = _declared_symbols()
-    assert len(declared) == 35
+    assert len(declared) == 36
     assert sorted(B.SYMBOLS) == declared
     for name in declared:
         assert hasattr(lib, name), name
 
 
 def test_version(lib):
-    assert lib.pa_version() == 6
+    assert lib.pa_version() == 7
 
 
 def _dims(**kw):

@@ -122,3 +122,30 @@ def test_small_or_mistyped_tensors_refused_before_the_call(fake):
         B.pa_slice_aggregate_backward(d, x, G, sp, mc, m, mc, None, None, x,
                                       B.make_slice_grads(dA=_t(C * M - 1)), ws)
     assert fake.calls == []
+
+
+def test_wrapper_calls_match_argtypes():
+    """Every load().pa_*(...) call in the binding passes exactly as many
+    arguments as the symbol's ctypes argtypes declare (read from the source,
+    no GPU needed)."""
+    import ast
+    import inspect
+    from paper_2502_02414_amd import binding as B
+    lib = B.load()
+    tree = ast.parse(inspect.getsource(B))
+    calls = 0
+    for node in ast.walk(tree):
+        if not (isinstance(node, ast.Call) and isinstance(node.func, ast.Attribute)):
+            continue
+        f = node.func
+        if isinstance(f.value, ast.Call) and getattr(f.value.func, "id", "") == "load" \
+                and f.attr.startswith("pa_"):
+            calls += 1
+            assert len(node.args) == len(getattr(lib, f.attr).argtypes or []), f.attr
+    assert calls > 30
+    # pa_gemm and pa_gemm_prepare are called through a chosen function
+    assert lib.pa_gemm.argtypes == lib.pa_gemm_prepare.argtypes
+    src = inspect.getsource(B.pa_gemm)
+    call = next(n for n in ast.walk(ast.parse(src.strip()))
+                if isinstance(n, ast.Call) and getattr(n.func, "id", "") == "fn")
+    assert len(call.args) == len(lib.pa_gemm.argtypes)

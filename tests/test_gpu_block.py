@@ -169,16 +169,21 @@ def test_gemm(case):
     Bm = _rnd(ti, *((n, k) if tB else (k, n)), seed=13)
     bv = _rnd("f32", n, seed=14) if bias else None
     Cr = _rnd(to, m, n, seed=15) if resid else None
-    D = dev(np.zeros((m, n), np.float32), to)
     ws = dev(np.zeros(16 << 18, np.float32))
-    B.pa_gemm(dev(A, ti), dev(Bm, ti), D, transA=tA, transB=tB, bias=dev(bv) if bias else None,
-              beta=1.0 if resid else 0.0, C=dev(Cr, to) if resid else None, ws=ws)
     ref = (A.T if tA else A).astype(np.float64) @ (Bm.T if tB else Bm).astype(np.float64)
     if bias:
         ref = ref + bv
     if resid:
         ref = ref + Cr
-    check("D", host(D), ref, TOL[to] if to == "bf16" else 1e-5)
+    # untuned (the heuristic's first algorithm), then tuned by
+    # pa_gemm_prepare, then the tuned algorithm through pa_gemm
+    for prepare in (False, True, False):
+        D = dev(np.zeros((m, n), np.float32), to)
+        B.pa_gemm(dev(A, ti), dev(Bm, ti), D, transA=tA, transB=tB,
+                  bias=dev(bv) if bias else None, beta=1.0 if resid else 0.0,
+                  C=dev(Cr, to) if resid else None, ws=ws, prepare=prepare)
+        check(f"D{' (prepare)' if prepare else ''}", host(D), ref,
+              TOL[to] if to == "bf16" else 1e-5)
 
 
 def test_colsum():
