@@ -12,7 +12,7 @@ import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 PINS = ["tests/test_oracle.py", "tests/test_oracle_heads.py", "tests/test_oracle_block.py",
-        "tests/test_oracle_rounding.py"]
+        "tests/test_oracle_rounding.py", "tests/test_oracle_explicit.py"]
 
 
 def _runtime(name):
