@@ -354,8 +354,13 @@ def test_kernel_timing_hook(cases):
             assert g.torch.equal(ref[k], b[k]), (call, k)
 
 
-@pytest.mark.parametrize("variant", ["no_noise", "no_adatemp", "single_point", "empty_slice"])
+@pytest.mark.parametrize("variant", ["no_noise", "no_adatemp", "single_point", "empty_slice",
+                                     "no_noise_coop", "no_adatemp_coop", "single_point_coop",
+                                     "empty_slice_coop"])
 def test_edge_cases(variant):
+    """No noise, no Ada-Temp (constant temperature), a single point and an
+    empty slice; the *_coop variants run them at bf16 rows of 256 channels
+    with 40 to 64 slices, the cooperative slice backward's shapes."""
     say(f"edge {variant}")
     if variant == "no_noise":
         c = make_case(300, 64, 4, 16, "f32", noise=False)
@@ -363,15 +368,22 @@ def test_edge_cases(variant):
         c = make_case(300, 64, 4, 16, "bf16", ada=False)
     elif variant == "single_point":
         c = make_case(1, 32, 1, 3, "f32")
+    elif variant == "no_noise_coop":
+        c = make_case(3001, 256, 8, 64, "bf16", noise=False)
+    elif variant == "no_adatemp_coop":
+        c = make_case(2003, 256, 8, 40, "bf16", ada=False)
+    elif variant == "single_point_coop":
+        c = make_case(1, 256, 8, 64, "bf16")
     else:
-        c = make_case(500, 64, 4, 8, "f32")
+        coop = variant == "empty_slice_coop"
+        c = make_case(2000, 256, 8, 64, "bf16") if coop else make_case(500, 64, 4, 8, "f32")
         c.p["b"] = c.p["b"].copy()
         c.p["b"][2] = -60.0            # slice 2 is (numerically) empty: den < eps
         c.p["A"] = c.p["A"].copy()
         c.p["A"][:, 2] = 0.0
     g = Gpu(c)
     f, gr = oracle_layer(c)
-    if variant == "empty_slice":
+    if variant.startswith("empty_slice"):
         assert f["den"][2] < c.eps
     for out in (g.layer(), g.layer_w()):  # recomputed, then stored weights
         for k in ("num", "den", "S", "Sp", "y"):
