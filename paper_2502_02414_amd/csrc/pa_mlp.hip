@@ -13,7 +13,8 @@
 // on v_mfma_f32_16x16x32_bf16 with fp32 accumulation; the activation is
 // applied to the fp32 accumulator and rounded to bf16 once.
 //
-// A block of four waves takes 128 points (32 per wave, two 16-point MFMA
+// A block of four waves (eight in the backward, whose two products double
+// the weights staged per chunk) takes 32 points per wave (two 16-point MFMA
 // tiles) and walks the F = 4C output columns in chunks of FC: each chunk of
 // the weights ([F, K] rows: W1 transposed, or W2 as it is) is staged in LDS
 // once for the block, with the next chunk's loads in flight in registers;
@@ -62,9 +63,9 @@ __device__ __forceinline__ float dgelu_ap(float x) {
 #define PA_MLP_WPAD 32
 #endif
 
-template <int K, int FC, int PT, bool BWD>
+template <int K, int FC, int PT, int NW, bool BWD>
 struct MlpGeo {
-  static constexpr int WAVES = 4;
+  static constexpr int WAVES = NW;
   static constexpr int PW = 16 * PT;           // points per wave (PT 16-point MFMA tiles)
   static constexpr int PTS = PW * WAVES;       // points per block
   static constexpr int NM = BWD ? 2 : 1;       // weight matrices per chunk
@@ -95,10 +96,10 @@ struct MlpArgs {
   bf16* out;        // [N, F]: GELU(u), or dU
 };
 
-template <int K, int FC, int PT, bool BWD>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
+template <int K, int FC, int PT, int NW, bool BWD>
+__global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2)))
 k_mlp_up(MlpArgs a) {
-  using Gm = MlpGeo<K, FC, PT, BWD>;
+  using Gm = MlpGeo<K, FC, PT, NW, BWD>;
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int wave = threadIdx.x >> 6, lane = lane_id(), r = lane & 15, g = lane >> 4;
   const int64_t n0 = (int64_t)blockIdx.x * Gm::PTS + Gm::PW * wave;  // the wave's first point
@@ -115,7 +116,7 @@ k_mlp_up(MlpArgs a) {
   auto wload = [&](int c) {
 #pragma unroll
     for (int j = 0; j < Gm::WCH; ++j) {
-      const int e = threadIdx.x + 256 * j;
+      const int e = threadIdx.x + 64 * NW * j;
       const auto mq = wsrc(e);
       const bf16* W = mq.first ? a.W2 : a.W1T;
       wpre[j] = ld_global16<false>(reinterpret_cast<const char*>(W + (int64_t)c * FC * K) +
@@ -125,7 +126,7 @@ k_mlp_up(MlpArgs a) {
   auto wstore = [&]() {
 #pragma unroll
     for (int j = 0; j < Gm::WCH; ++j) {
-      const int e = threadIdx.x + 256 * j;
+      const int e = threadIdx.x + 64 * NW * j;
       const auto mq = wsrc(e);
       const int row = mq.second / Gm::RCH, cc = mq.second - row * Gm::RCH;
       *reinterpret_cast<uint4*>(smem + mq.first * Gm::WMAT + row * Gm::WROW + 16 * cc) = wpre[j];
@@ -238,13 +239,13 @@ __global__ void __launch_bounds__(256) k_transpose_bf16(int K, int F, const bf16
   }
 }
 
-template <int K, int FC, int PT, bool BWD>
+template <int K, int FC, int PT, int NW, bool BWD>
 hipError_t launch_k(const MlpArgs& a, hipStream_t st) {
-  using Gm = MlpGeo<K, FC, PT, BWD>;
+  using Gm = MlpGeo<K, FC, PT, NW, BWD>;
   const int64_t blocks = (a.N + Gm::PTS - 1) / Gm::PTS;
   if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((k_mlp_up<K, FC, PT, BWD>), dim3((unsigned)blocks), dim3(256), Gm::LDS, st,
-                     a);
+  hipLaunchKernelGGL((k_mlp_up<K, FC, PT, NW, BWD>), dim3((unsigned)blocks), dim3(64 * NW),
+                     Gm::LDS, st, a);
   return hipGetLastError();
 }
 
@@ -264,9 +265,11 @@ hipError_t launch_mlp_up(int64_t N, int K, int F, const void* X, const void* W1,
             (bf16*)out};
   const bool bwd = DY != nullptr;
   switch (K) {
-    case 64: return bwd ? launch_k<64, 32, 2, true>(a, st) : launch_k<64, 64, 2, false>(a, st);
-    case 128: return bwd ? launch_k<128, 32, 2, true>(a, st) : launch_k<128, 64, 2, false>(a, st);
-    default: return bwd ? launch_k<256, 32, 2, true>(a, st) : launch_k<256, 64, 2, false>(a, st);
+    case 64: return bwd ? launch_k<64, 32, 2, 8, true>(a, st) : launch_k<64, 64, 2, 4, false>(a, st);
+    case 128:
+      return bwd ? launch_k<128, 32, 2, 8, true>(a, st) : launch_k<128, 64, 2, 4, false>(a, st);
+    default:
+      return bwd ? launch_k<256, 32, 2, 8, true>(a, st) : launch_k<256, 64, 2, 4, false>(a, st);
   }
 }
 
