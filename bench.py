@@ -407,6 +407,13 @@ def workload_bench(args):
     torch.cuda.synchronize()
     times = sorted(e0.elapsed_ms(e1) for e0, e1 in ev)
     ms = times[len(times) // 2]
+    if args.copy_calibration:  # a 1 GiB copy for the HBM counters' scale, after the timing
+        src = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     bpp = algo_bytes_per_point(C, M, 2 if w.dtype == "bf16" else 4, 2 if w.dtype == "bf16" else 4)
     calls = ["pa_slice_aggregate", "pa_deslice"] + (
         ["pa_deslice_backward", "pa_slice_aggregate_backward"] if w.backward else [])
