@@ -319,9 +319,9 @@ pa_status pa_layernorm_backward(int64_t N, int C, pa_dtype dtype, const void* x,
                                 const void* dy, const void* dres, void* dx, float* dg,
                                 float* db, void* ws, size_t ws_bytes, void* stream);
 
-/* GELU in its tanh form y = x (1 + tanh(sqrt(2/pi) (x + 0.044715 x^3))) / 2
- * over n elements (n a multiple of 16 bytes' worth), and its chain rule
- * dx = dy GELU'(x). */
+/* GELU in its exact form y = x Phi(x) = x (1 + erf(x / sqrt 2)) / 2 over n
+ * elements (n a multiple of 16 bytes' worth), and its chain rule
+ * dx = dy GELU'(x), GELU'(x) = Phi(x) + x phi(x). */
 pa_status pa_gelu(int64_t n, pa_dtype dtype, const void* x, void* y, void* stream);
 pa_status pa_gelu_backward(int64_t n, pa_dtype dtype, const void* x, const void* dy, void* dx,
                            void* stream);

@@ -6,8 +6,8 @@
 //     precedes it fused (the sum is written once, in the storage dtype), and
 //     its backward with the residual gradient added; the gain and bias
 //     gradients are per-block partial sums added in block order;
-//   - GELU in its tanh form (x sigmoid(2u), u = sqrt(2/pi)(x + 0.044715 x^3))
-//     and its derivative, elementwise;
+//   - GELU in its exact form, x Phi(x) with Phi the standard normal CDF
+//     (device erf), and its derivative Phi(x) + x phi(x), elementwise;
 //   - column sums of a [N, C] matrix (the bias gradients of the linear
 //     layers), deterministic;
 //   - Algorithm 1's Project step x_proj = h Wp + bp folded into the slice

@@ -1,19 +1,18 @@
-// kSliceBwd for many slices and wide rows (bf16, C = 256, M > 32): the four
-// waves of a block work on the same TT 16-point tiles at a time (gfx950).
+// kSliceBwd for many slices and wide rows (bf16, C = 256, M > 32): groups
+// of four waves work together on one 16-point tile at a time (gfx950).
 //
 // The per-wave kernel of pa_stream.hpp gives every wave its own tiles and
 // the whole chain rule of a point: at C = 256 with up to 64 slices its
 // tables (104 KB of LDS) leave room for two such waves per CU, and its dA
 // accumulator (C M floats per wave) does not fit in the register file.
-// Here a block streams TT tiles at a time, shared in LDS, and splits the
-// work over its four waves (one per SIMD): wave w owns slice block w
-// (slices 16w .. 16w + 15) for the logits, the softmax, dw and the dA
-// accumulator (C x 16 floats), and channel blocks 4w .. 4w + 3 for dx and
-// da.  Each table fragment read from LDS serves all TT tiles, whose
-// contractions are independent MFMA chains issued side by side.  Per round
-// of TT tiles:
+// Here the work of a tile is split over a group of four waves: wave w owns
+// slice block w (slices 16w .. 16w + 15) for the logits, the softmax, dw
+// and the dA accumulator (C x 16 floats), and channel blocks 4w .. 4w + 3
+// for dx and da.  A block holds NG groups (two: one wave of each per SIMD)
+// that share the tables and each take their own tiles (TT per round).  Per
+// round, in each group:
 //   1. the tiles' x, dY and Gumbel rows (each wave loads a quarter, a round
-//      or more ahead in registers) are stored into the shared tiles;
+//      or more ahead in registers) are stored into the group's tiles;
 //   2. logits of the wave's slices and the temperature (MFMA over C); a
 //      softmax over all slices from per-wave partial (max, sum) pairs
 //      exchanged in LDS;
@@ -24,9 +23,10 @@
 //      blocks (MFMA over [dl | w] against [A^T | dnum - cN]) staged and
 //      written back;
 //   5. dA (its slice block) += x^T dl and da (its channel blocks) += x^T dt.
-// Every cross-wave sum is formed in the same fixed order in every wave, so
-// the result is deterministic; each block's record is written by the waves
-// that own its parts (no reduction across waves).
+// Every cross-wave sum is formed in the same fixed order in every wave, and
+// the groups' partial sums are added in group order at the end, so the
+// result is deterministic; each block's record is written by the waves of
+// the first group that own its parts.
 #pragma once
 
 #include "pa_stream.hpp"
