@@ -86,7 +86,7 @@ STREAM_KERNEL = {
 # The sources the streaming kernels are compiled from (the traffic summary
 # is valid while these are unchanged).
 STREAM_SOURCES = ("pa_device.hpp", "pa_internal.h", "pa_layout.h", "pa_stream.hpp",
-                  "pa_stream_slbwd.hip")
+                  "pa_stream_slbwd.hip", "pa_coop.hpp")
 
 
 def kernel_sources_sha() -> str:

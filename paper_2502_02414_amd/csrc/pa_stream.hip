@@ -8,9 +8,9 @@ template <int SZ>
 static int waves_of(int pass, int C, int MB) {
   // the block-cooperative slice backward (groups of four waves per block)
   if (pass == kSliceBwd && SZ == 2 && C == 256 && MB == 4 && coop_slice_bwd<bf16, 256, 4>())
-    return CoopGeo<bf16, 256, 4, 1, coop_groups<bf16, 256, 4>()>::WAVES;
+    return CoopGeo<bf16, 256, 4, coop_groups<bf16, 256, 4>()>::WAVES;
   if (pass == kSliceBwd && SZ == 2 && C == 256 && MB == 3 && coop_slice_bwd<bf16, 256, 3>())
-    return CoopGeo<bf16, 256, 3, 1, coop_groups<bf16, 256, 3>()>::WAVES;
+    return CoopGeo<bf16, 256, 3, coop_groups<bf16, 256, 3>()>::WAVES;
 #define PA_W(CC, BB) \
   if (C == CC && MB == BB) return Geo<SZ, CC, BB>::fits(pass) ? Geo<SZ, CC, BB>::waves(pass) : 0;
   PA_W(32, 1) PA_W(32, 2) PA_W(32, 3) PA_W(32, 4)

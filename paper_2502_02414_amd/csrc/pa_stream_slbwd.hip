@@ -7,9 +7,9 @@ namespace pa {
 
 template <int MB>
 static hipError_t launch_coop(const StreamArgs& a, int P, hipStream_t st) {
-  constexpr int TT = coop_tiles<bf16, 256, MB>(), NG = coop_groups<bf16, 256, MB>();
-  using CG = CoopGeo<bf16, 256, MB, TT, NG>;
-  hipLaunchKernelGGL((k_slice_bwd_coop<bf16, 256, MB, TT, NG>), dim3(P, a.heads),
+  constexpr int NG = coop_groups<bf16, 256, MB>();
+  using CG = CoopGeo<bf16, 256, MB, NG>;
+  hipLaunchKernelGGL((k_slice_bwd_coop<bf16, 256, MB, NG>), dim3(P, a.heads),
                      dim3(64 * CG::WAVES), CG::LDS, st, a);
   return hipGetLastError();
 }
