@@ -38,9 +38,12 @@
  *   outputs (fixed point partition that depends on N only, fixed-order
  *   reductions, no floating-point atomics).
  * - Arguments are validated on the host before anything is launched:
- *   N >= 1; 1 <= M <= 64; C in {32, 64, 128, 256}; H >= 1 and C % H == 0;
- *   tau_min > 0; eps > 0; required pointers non-NULL; workspace large
- *   enough.  Failures return PA_ERR_INVALID, PA_ERR_UNSUPPORTED or
+ *   N >= 1; 1 <= M <= 64; H >= 1 and C % H == 0; tau_min > 0; eps > 0;
+ *   required pointers non-NULL; workspace large enough.  Served channel
+ *   counts: C a multiple of 16 in [16, 256] (other C >= 1 return
+ *   PA_ERR_UNSUPPORTED; C = 256 with M > 48 in fp32 does not fit the slice
+ *   backward's on-chip tables either).  Failures return PA_ERR_INVALID,
+ *   PA_ERR_UNSUPPORTED or
  *   PA_ERR_WORKSPACE and set the thread-local message of pa_last_error().
  *   A failed HIP launch returns PA_ERR_HIP with HIP's message.  Non-finite
  *   input values propagate; there are no device-side checks.
@@ -55,7 +58,7 @@
 extern "C" {
 #endif
 
-#define PA_VERSION 7
+#define PA_VERSION 8
 
 typedef enum { PA_F32 = 0, PA_BF16 = 1 } pa_dtype;
 

@@ -45,6 +45,11 @@ size_t up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
 int mblocks(int M) { return (M + 15) / 16; }
 
+// The width the streaming kernels are built for that holds C channels: rows
+// of C channels run on the kernels of the next width up, with the tables'
+// extra channels zero.
+int cpad(int C) { return C <= 32 ? 32 : C <= 64 ? 64 : C <= 128 ? 128 : 256; }
+
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 // Workspace carve-up (offsets in bytes).
@@ -58,7 +63,7 @@ Layout layout_of(const pa_dims& d) {
   const int MB = mblocks(d.M);
   size_t img = 0;
   for (int pass = 0; pass < pa::kNumPasses; ++pass) {
-    size_t b = pa::image_bytes(pass, d.dtype, d.C, MB);
+    size_t b = pa::image_bytes(pass, d.dtype, cpad(d.C), MB);
     if (b > img) img = b;
   }
   // chunks: every pass uses at most kPartialsMax blocks
@@ -90,13 +95,13 @@ pa_status check_dims(const pa_dims* d) {
   if (!std::isfinite(d->tau0)) return fail(PA_ERR_INVALID, "tau0 must be finite");
   if (d->dtype != PA_F32 && d->dtype != PA_BF16)
     return fail(PA_ERR_INVALID, "dtype must be PA_F32 or PA_BF16 (got %d)", d->dtype);
-  if (d->C != 32 && d->C != 64 && d->C != 128 && d->C != 256)
-    return fail(PA_ERR_UNSUPPORTED, "C must be one of 32, 64, 128, 256 (got %d)", d->C);
+  if (d->C % 16 != 0 || d->C > 256)
+    return fail(PA_ERR_UNSUPPORTED, "C must be a multiple of 16 in [16, 256] (got %d)", d->C);
   return PA_OK;
 }
 
 pa_status check_pass(const pa_dims& d, int pass) {
-  if (pa::stream_waves(pass, d.dtype, d.C, mblocks(d.M)) <= 0)
+  if (pa::stream_waves(pass, d.dtype, cpad(d.C), mblocks(d.M), d.C) <= 0)
     return fail(PA_ERR_UNSUPPORTED,
                 "shape C=%d M=%d dtype=%d does not fit the on-chip tables of this pass", d.C,
                 d.M, d.dtype);
@@ -128,14 +133,15 @@ pa_status check_ws(const pa_dims& d, const void* ws, size_t ws_bytes) {
 char* wsb(void* ws) { return reinterpret_cast<char*>(ws); }
 
 int chunks(const pa_dims& d, int pass) {
-  return pa::num_chunks(d.N, pa::stream_waves(pass, d.dtype, d.C, mblocks(d.M)));
+  return pa::num_chunks(d.N, pa::stream_waves(pass, d.dtype, cpad(d.C), mblocks(d.M), d.C));
 }
 
 pa::PrepArgs prep_of(const pa_dims& d, int pass, const pa_slice_params* sp, void* ws) {
   pa::PrepArgs p;
   p.pass = pass;
   p.dtype = d.dtype;
-  p.C = d.C;
+  p.C = cpad(d.C);
+  p.cr = d.C;
   p.M = d.M;
   p.MB = mblocks(d.M);
   p.eps = d.eps;
@@ -158,6 +164,7 @@ pa::StreamLaunch stream_of(const pa_dims& d, int pass, const void* x, const void
   L.partials = reinterpret_cast<float*>(wsb(ws) + lay.parts);
   L.N = d.N;
   L.M = d.M;
+  L.cr = d.C;
   L.rec = (int)pa::record_floats(pass, d.C, d.M);
   L.P = chunks(d, pass);
   L.tb = (double)d.tau0 + (sp ? (double)sp->b_t : 0.0);
@@ -203,7 +210,7 @@ hipError_t run_stream(int pass, const pa_dims& d, const pa::StreamLaunch& L, hip
     hipError_t e = hipEventRecord(g_timer.start, st);
     if (e != hipSuccess) return e;
   }
-  hipError_t e = pa::launch_stream(pass, d.dtype, d.C, mblocks(d.M), L, st);
+  hipError_t e = pa::launch_stream(pass, d.dtype, cpad(d.C), mblocks(d.M), L, st);
   if (e == hipSuccess && timed) e = hipEventRecord(g_timer.stop, st);
   return e;
 }

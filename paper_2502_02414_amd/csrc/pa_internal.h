@@ -24,6 +24,7 @@ struct StreamLaunch {
   float* partials = nullptr;
   int64_t N = 0;
   int M = 0;
+  int cr = 0;   // channels of the point rows (<= the kernels' C, a multiple of 16)
   int rec = 0;
   int P = 1;
   double tb = 0.0;  // tau0 + b_t
@@ -38,24 +39,29 @@ struct StreamLaunch {
 };
 
 // Streaming passes (pass = pa::Pass).  dtype: 0 fp32, 1 bf16.
+// C is the width the kernels are built for (32, 64, 128 or 256); rows of
+// L.cr <= C channels are laid out in LDS as C channels, the others zero in
+// the tables.
 hipError_t launch_stream(int pass, int dtype, int C, int MB, const StreamLaunch& L,
                          hipStream_t st);
-// Waves per block of a pass at this shape (0 = shape not served).
-int stream_waves(int pass, int dtype, int C, int MB);
+// Waves per block of a pass at this shape (0 = shape not served); cr the
+// channels of the point rows.
+int stream_waves(int pass, int dtype, int C, int MB, int cr);
 
 // Table image for a pass, written into `img` (device).
 struct PrepArgs {
   int pass = 0;
   int dtype = 0;
-  int C = 0, M = 0, MB = 0;
+  int C = 0, M = 0, MB = 0;  // C: the tables' (padded) width
+  int cr = 0;                // channels of the parameters and states (<= C)
   float eps = 0.f;
-  const void* A = nullptr;    // [C,M] dtype
+  const void* A = nullptr;    // [cr,M] dtype
   const float* b = nullptr;   // [M]
-  const void* a = nullptr;    // [C] dtype
-  const float* Sp = nullptr;  // [M,C]  (kDeslice, kSliceBwd deslice term)
-  const float* num = nullptr; // [M,C]  (kSliceBwd states term)
+  const void* a = nullptr;    // [cr] dtype
+  const float* Sp = nullptr;  // [M,cr]  (kDeslice, kSliceBwd deslice term)
+  const float* num = nullptr; // [M,cr]  (kSliceBwd states term)
   const float* den = nullptr; // [M]
-  const float* dS = nullptr;  // [M,C]
+  const float* dS = nullptr;  // [M,cr]
   void* img = nullptr;
   // per-head batch: heads (gridDim.y) and byte strides (0: shared by heads)
   int heads = 1;

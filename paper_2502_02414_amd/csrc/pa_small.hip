@@ -19,7 +19,7 @@ namespace pa {
 // Table image
 // ---------------------------------------------------------------------------
 struct PrepGeo {
-  int C, M, MB, M16, SZ;
+  int C, M, MB, M16, SZ;  // C: the tables' width (the parameters' cr <= C channels, zeros beyond)
   int TROW, SROW, WROW, OFF_L, OFF_2;
 };
 
@@ -60,7 +60,7 @@ __device__ __forceinline__ void prep_back(const PrepGeo& g, const PrepArgs& p, i
                                           float* red) {
   char* img = reinterpret_cast<char*>(p.img);
   float* hdr = reinterpret_cast<float*>(img);
-  const int C = g.C, M = g.M, M16 = g.M16;
+  const int C = g.C, M = g.M, M16 = g.M16, cr = p.cr;
   const bool states = p.dS != nullptr && p.pass == kSliceBwd;
   const bool desl = p.Sp != nullptr && p.pass == kSliceBwd;
   if (bid < M) {
@@ -69,8 +69,8 @@ __device__ __forceinline__ void prep_back(const PrepGeo& g, const PrepArgs& p, i
     // C <= 256), and in wave 0 the weights w_k (one slice per lane)
     const float dj = states ? p.den[j] : 1.f;
     float s = 0.f;
-    for (int c = threadIdx.x; c < C; c += 256) {
-      const float dv = states ? p.dS[j * C + c] : 0.f, nv = states ? p.num[j * C + c] : 0.f;
+    for (int c = threadIdx.x; c < cr; c += 256) {
+      const float dv = states ? p.dS[j * cr + c] : 0.f, nv = states ? p.num[j * cr + c] : 0.f;
       s += dv * (nv / dj);
     }
     const int k = threadIdx.x < 64 ? (int)threadIdx.x : 0;
@@ -110,13 +110,15 @@ __device__ __forceinline__ void prep_back(const PrepGeo& g, const PrepArgs& p, i
   if (cc >= 2 * C) return;
   const bool first = cc < C;
   const int c = first ? cc : cc - C;
-  const bool on = first ? states : desl;
+  // (columns c >= cr are padding: zero rows, centre 0)
+  const bool on = (first ? states : desl) && c < cr;
+  const int cl = c < cr ? c : 0;
   // the column's values, all loads issued at once (M <= 64)
   float v[64];
 #pragma unroll
   for (int j = 0; j < 64; ++j) {
     const int jj = j < M ? j : M - 1;
-    v[j] = on ? (first ? p.dS[jj * C + c] : p.Sp[jj * C + c]) : 0.f;
+    v[j] = on ? (first ? p.dS[jj * cr + cl] : p.Sp[jj * cr + cl]) : 0.f;
   }
   float wsum = 0.f, sum = 0.f;
 #pragma unroll
@@ -144,12 +146,12 @@ __device__ __forceinline__ void prep_back(const PrepGeo& g, const PrepArgs& p, i
 template <typename T>
 __device__ __forceinline__ void prep_deslice_table(const PrepGeo& g, const PrepArgs& p, char* img,
                                                    int64_t tid, int64_t nth) {
-  const int C = g.C, M = g.M, M16 = g.M16;
+  const int C = g.C, M = g.M, M16 = g.M16, cr = p.cr;
   const int64_t nS = (int64_t)C * M16;
 #pragma unroll 4
   for (int64_t k = tid; k < nS; k += nth) {
     const int c = (int)(k / M16), j = (int)(k - (int64_t)c * M16);
-    const float v = (j < M) ? p.Sp[j * C + c] : 0.f;
+    const float v = (j < M && c < cr) ? p.Sp[j * cr + c] : 0.f;
     *reinterpret_cast<T*>(img + g.OFF_2 + c * g.SROW + j * g.SZ) = from_f<T>(v);
   }
 }
@@ -184,7 +186,7 @@ __global__ void __launch_bounds__(256) k_prep(PrepGeo g, PrepArgs p) {
   char* img = reinterpret_cast<char*>(p.img);
   const T* A = reinterpret_cast<const T*>(p.A);
   const T* av = reinterpret_cast<const T*>(p.a);
-  const int C = g.C, M = g.M, M16 = g.M16;
+  const int C = g.C, M = g.M, M16 = g.M16, cr = p.cr;
   const int64_t tid = (int64_t)(blockIdx.x - nback) * blockDim.x + threadIdx.x;
   const int64_t nth = (int64_t)(gridDim.x - nback) * blockDim.x;
 
@@ -197,14 +199,18 @@ __global__ void __launch_bounds__(256) k_prep(PrepGeo g, PrepArgs p) {
   for (int64_t j = tid; j < M16; j += nth) hdr[j] = j < M ? (p.b ? p.b[j] : 0.f) : -INFINITY;
   if (!back)
     for (int64_t k = tid; k < 2 * M16 + 2 * C; k += nth) hdr[M16 + k] = 0.f;  // dden, cN, cS, sw
-  for (int64_t c = tid; c < C; c += nth) hdr[3 * M16 + 2 * C + c] = av ? to_f<T>(av[c]) : 0.f;
-  // logits table: rows j < M16: A[:, j] (0 beyond M); row M16: a
+  for (int64_t c = tid; c < C; c += nth)
+    hdr[3 * M16 + 2 * C + c] = av && c < cr ? to_f<T>(av[c]) : 0.f;
+  // logits table: rows j < M16: A[:, j] (0 beyond M); row M16: a (columns
+  // c >= cr: 0)
   const int64_t nL = (int64_t)(M16 + 1) * C;
 #pragma unroll 4
   for (int64_t k = tid; k < nL; k += nth) {
     const int j = (int)(k / C), c = (int)(k - (int64_t)j * C);
     T v;
-    if (j < M16)
+    if (c >= cr)
+      v = from_f<T>(0.f);
+    else if (j < M16)
       v = j < M ? A[(int64_t)c * M + j] : from_f<T>(0.f);
     else
       v = av ? av[c] : from_f<T>(0.f);
@@ -215,6 +221,7 @@ __global__ void __launch_bounds__(256) k_prep(PrepGeo g, PrepArgs p) {
 
 hipError_t launch_prep(const PrepArgs& p, hipStream_t st) {
   if (!p.img || (!p.A && p.pass != kDesliceW)) return hipErrorInvalidValue;
+  if (p.cr < 16 || p.cr > p.C || p.cr % 16) return hipErrorInvalidValue;
   if ((p.pass == kDeslice || p.pass == kDesliceW) && !p.Sp) return hipErrorInvalidValue;
   if (p.pass == kSliceBwd && p.dS && (!p.num || !p.den)) return hipErrorInvalidValue;
   PrepGeo g = prep_geo(p.dtype, p.C, p.M, p.MB);

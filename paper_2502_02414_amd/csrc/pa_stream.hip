@@ -5,11 +5,13 @@
 namespace pa {
 
 template <int SZ>
-static int waves_of(int pass, int C, int MB) {
-  // the block-cooperative slice backward (groups of four waves per block)
-  if (pass == kSliceBwd && SZ == 2 && C == 256 && MB == 4 && coop_slice_bwd<bf16, 256, 4>())
+static int waves_of(int pass, int C, int MB, int cr) {
+  // the block-cooperative slice backward (groups of four waves per block;
+  // rows of exactly 256 channels)
+  const bool coop = pass == kSliceBwd && SZ == 2 && C == 256 && cr == 256;
+  if (coop && MB == 4 && coop_slice_bwd<bf16, 256, 4>())
     return CoopGeo<bf16, 256, 4, coop_groups<bf16, 256, 4>()>::WAVES;
-  if (pass == kSliceBwd && SZ == 2 && C == 256 && MB == 3 && coop_slice_bwd<bf16, 256, 3>())
+  if (coop && MB == 3 && coop_slice_bwd<bf16, 256, 3>())
     return CoopGeo<bf16, 256, 3, coop_groups<bf16, 256, 3>()>::WAVES;
 #define PA_W(CC, BB) \
   if (C == CC && MB == BB) return Geo<SZ, CC, BB>::fits(pass) ? Geo<SZ, CC, BB>::waves(pass) : 0;
@@ -21,8 +23,9 @@ static int waves_of(int pass, int C, int MB) {
   return 0;
 }
 
-int stream_waves(int pass, int dtype, int C, int MB) {
-  return dtype == 1 ? waves_of<2>(pass, C, MB) : waves_of<4>(pass, C, MB);
+int stream_waves(int pass, int dtype, int C, int MB, int cr) {
+  if (cr < 16 || cr > C || cr % 16) return 0;
+  return dtype == 1 ? waves_of<2>(pass, C, MB, cr) : waves_of<4>(pass, C, MB, cr);
 }
 
 hipError_t launch_stream(int pass, int dtype, int C, int MB, const StreamLaunch& L,
@@ -31,7 +34,8 @@ hipError_t launch_stream(int pass, int dtype, int C, int MB, const StreamLaunch&
   // never a device fault)
   // (the stored-weights passes read W, given as G, in place of x and G)
   const bool win = pass == kDesliceW || pass == kDesliceBwdW;
-  if ((win ? !L.G : !L.x) || !L.img || L.N < 1 || L.M < 1 || L.M > 16 * MB || L.P < 1)
+  if ((win ? !L.G : !L.x) || !L.img || L.N < 1 || L.M < 1 || L.M > 16 * MB || L.P < 1 ||
+      L.cr < 16 || L.cr > C || L.cr % 16)
     return hipErrorInvalidValue;
   const bool reduces = agg_fwd(pass) || agg_bwd(pass) || pass == kSliceBwd || pass == kWeightsBwd;
   if (reduces && !L.partials) return hipErrorInvalidValue;
@@ -43,7 +47,8 @@ hipError_t launch_stream(int pass, int dtype, int C, int MB, const StreamLaunch&
   if (pass == kWeightsBwd && !L.dW) return hipErrorInvalidValue;
   StreamArgs a;
   a.x = L.x; a.G = L.G; a.dY = L.dY; a.img = L.img; a.out = L.out; a.tau_out = L.tau_out;
-  a.dW = L.dW; a.dtau = L.dtau; a.partials = L.partials; a.N = L.N; a.M = L.M; a.rec = L.rec;
+  a.dW = L.dW; a.dtau = L.dtau; a.partials = L.partials; a.N = L.N; a.M = L.M; a.cr = L.cr;
+  a.rec = L.rec;
   a.tb = L.tb; a.tb_dev = L.tb_dev; a.tau_min = L.tau_min;
   a.flags = (L.G ? kHasG : 0) | (L.states ? kStatesTerm : 0) | (L.deslice ? kDesliceTerm : 0);
   if (L.heads < 1 || L.heads > kMaxHeads) return hipErrorInvalidValue;

@@ -50,6 +50,7 @@ struct StreamArgs {
   float* partials;       // [P][rec]
   int64_t N;
   int M;
+  int cr;                // channels of the point rows (<= C, a multiple of 16)
   int rec;               // floats per record
   double tb;             // tau0 + b_t (exact sum of the two fp32 values)
   const float* tb_dev;   // nullable: a device scalar added to tb
@@ -241,9 +242,13 @@ __device__ __forceinline__ void stage4(char* tile, int base, int off, const f32x
 
 // ---------------------------------------------------------------------------
 // Point tiles: HBM -> registers -> padded LDS rows, and staged outputs back.
-// Rows [p0, p0+ROWS) of a [N,C] tensor are ROWS*C*SZ contiguous bytes; lane
-// l holds 16-byte chunks q = l + 64k.  Rows >= N re-read row N - 1 (finite
-// data; their points are masked).
+// A tile holds ROWS rows of C channels; lane l holds 16-byte chunks
+// q = l + 64k (row q / RCH, chunk q % RCH).  Rows >= N re-read row N - 1
+// (finite data; their points are masked).  The tensor's rows hold cr <= C
+// channels (cr a multiple of 16, so rows are whole 16-byte chunks): the
+// chunks past a row's end re-read its last chunk (finite data), and the
+// tables hold zeros for those channels, so they contribute nothing; outputs
+// are written for the cr channels only.
 // ---------------------------------------------------------------------------
 template <typename T, int C, int ROWS = 16>
 struct TileRegs {
@@ -260,18 +265,20 @@ __device__ __forceinline__ int last_row(int64_t p0, int64_t N) {
 
 template <typename T, int C, int ROWS = 16, bool NT = true>
 __device__ __forceinline__ void load_tile(TileRegs<T, C, ROWS>& R, const T* base, int64_t p0,
-                                          int64_t N) {
+                                          int64_t N, int cr) {
   // no predicated loads, so the compiler can track these loads exactly
   constexpr int RCH = TileRegs<T, C, ROWS>::RCH;
   const int lane = lane_id();
   const int lim = last_row<ROWS>(p0, N);
-  const char* src = reinterpret_cast<const char*>(base + p0 * C);
+  const int rb = cr * (int)sizeof(T), lc = rb / 16 - 1;  // row bytes, its last chunk
+  const char* src = reinterpret_cast<const char*>(base + p0 * cr);
 #pragma unroll
   for (int k = 0; k < TileRegs<T, C, ROWS>::NCH; ++k) {
     const int q = lane + 64 * k;
     const int row = q / RCH, cc = q - row * RCH;
     const int rr = row < lim ? row : lim;
-    R.c[k] = ld_global16<NT>(src + (uint32_t)(rr * C * (int)sizeof(T) + 16 * cc));
+    const int c = cc < lc ? cc : lc;
+    R.c[k] = ld_global16<NT>(src + (uint32_t)(rr * rb + 16 * c));
   }
 }
 
@@ -288,20 +295,23 @@ __device__ __forceinline__ void store_tile(char* tile, const TileRegs<T, C, ROWS
   }
 }
 
-// Staged output tile (padded LDS rows) -> rows [p0, p0 + nvalid) of dst.
+// Staged output tile (padded LDS rows) -> rows [p0, p0 + nvalid) of dst,
+// their cr channels.
 template <typename T, int C, int ROWS = 16>
-__device__ __forceinline__ void write_tile(T* dst, int64_t p0, const char* tile, int nvalid) {
+__device__ __forceinline__ void write_tile(T* dst, int64_t p0, const char* tile, int nvalid,
+                                           int cr) {
   constexpr int RCH = TileRegs<T, C, ROWS>::RCH;
   constexpr int NCH = TileRegs<T, C, ROWS>::NCH;
   constexpr int ROW = C * (int)sizeof(T) + 32;
   const int lane = lane_id();
-  char* d = reinterpret_cast<char*>(dst + p0 * C);
+  const int rb = cr * (int)sizeof(T);
+  char* d = reinterpret_cast<char*>(dst + p0 * cr);
 #pragma unroll
   for (int k = 0; k < NCH; ++k) {
     const int q = lane + 64 * k;
     const int row = q / RCH, cc = q - row * RCH;
     const uint4 v = *reinterpret_cast<const uint4*>(tile + lds_off(row, 16 * cc, ROW));
-    if (row < nvalid) st_global16(d + (uint32_t)(16 * lane + 1024 * k), v);
+    if (row < nvalid && 16 * cc < rb) st_global16(d + (uint32_t)(row * rb + 16 * cc), v);
   }
 }
 
@@ -958,8 +968,8 @@ k_aggregate(StreamArgs a) {
   auto load = [&](Stage& st, int64_t tile) {
     const int64_t p0 = tile * ROWS;
     constexpr bool NT = !keep_loads<PASS>();
-    if constexpr (!WIN) load_tile<T, C, ROWS, NT>(st.x, X, p0, a.N);
-    if constexpr (BWD) load_tile<T, C, ROWS, NT>(st.y, Y, p0, a.N);
+    if constexpr (!WIN) load_tile<T, C, ROWS, NT>(st.x, X, p0, a.N, a.cr);
+    if constexpr (BWD) load_tile<T, C, ROWS, NT>(st.y, Y, p0, a.N, a.cr);
     // G (or W): streamed either way; `safe` is any readable 16 bytes
     const void* safe = WIN ? a.img : static_cast<const void*>(X);
     load_g<T, MB, ROWS, true>(st.g, Gp, safe, p0, a.N, a.M, hasG);
@@ -1001,8 +1011,9 @@ k_aggregate(StreamArgs a) {
         const int j = 16 * nb + 4 * g + i;
         if (j < a.M) {
 #pragma unroll
-          for (int cb = 0; cb < G_::CB; ++cb) rec[j * C + 16 * cb + r] = acc[nb][cb][i];
-          if (!BWD && r == 0) rec[a.M * C + j] = dacc[nb][i];
+          for (int cb = 0; cb < G_::CB; ++cb)
+            if (16 * cb < a.cr) rec[j * a.cr + 16 * cb + r] = acc[nb][cb][i];
+          if (!BWD && r == 0) rec[a.M * a.cr + j] = dacc[nb][i];
         }
       }
   }
@@ -1063,7 +1074,7 @@ k_deslice(StreamArgs a) {
     if constexpr (WIN) {
       load_g<T, MB, 16, NT>(st.g, Gp, a.img, tile * 16, a.N, a.M, hasG);
     } else {
-      load_tile<T, C, 16, NT>(st.x, X, tile * 16, a.N);
+      load_tile<T, C, 16, NT>(st.x, X, tile * 16, a.N, a.cr);
       load_g<T, MB, 16, NT>(st.g, Gp, X, tile * 16, a.N, a.M, hasG);
     }
   };
@@ -1117,7 +1128,7 @@ k_deslice(StreamArgs a) {
           stage4<T>(xt, stb, 16 * cb * SZ, d);
         });
     wave_sync();
-    write_tile<T, C>(Y, p0, xt, nvalid);
+    write_tile<T, C>(Y, p0, xt, nvalid, a.cr);
   };
   auto tail = [&](int64_t t) {
     Stage st;
@@ -1166,7 +1177,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kWeights)))
   GRegs<T, MB> gr;
   for (int64_t t = t0; t < t1; ++t) {
     const int64_t p0 = t * 16;
-    load_tile<T, C>(xr, X, p0, a.N);
+    load_tile<T, C>(xr, X, p0, a.N, a.cr);
     load_g<T, MB>(gr, Gp, X, p0, a.N, a.M, hasG);
     const int nvalid = (int)(a.N - p0 < 16 ? a.N - p0 : 16);
     wave_sync();
@@ -1292,8 +1303,8 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
     // dY is loaded unconditionally (x stands in without the deslice term),
     // so that the loads are never predicated
     constexpr bool NT = !keep_loads<PASS>();
-    load_tile<T, C, 16, NT>(st.x, X, tile * 16, a.N);
-    load_tile<T, C, 16, NT>(st.y, deslice ? Y : X, tile * 16, a.N);
+    load_tile<T, C, 16, NT>(st.x, X, tile * 16, a.N, a.cr);
+    load_tile<T, C, 16, NT>(st.y, deslice ? Y : X, tile * 16, a.N, a.cr);
     load_g<T, MB, 16, NT>(st.g, Gp, X, tile * 16, a.N, a.M, hasG);
   };
   auto store = [&](const Stage& st) {
@@ -1434,7 +1445,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
       for (int i = 0; i < 4; ++i) scr[r * SROWF + 16 * nb + 4 * g + i] = dl[nb][i];
     if (g == 0) scr_dt[r] = dt;
     wave_sync();
-    write_tile<T, C>(DX, p0, yt, nvalid);
+    write_tile<T, C>(DX, p0, yt, nvalid, a.cr);
     float dlp[MB][4], dtp[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -1512,16 +1523,20 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
       const int j = 16 * nb + r;
       if (j < M) {
 #pragma unroll
-        for (int cb = 0; cb < G_::CB; ++cb)
+        for (int cb = 0; cb < G_::CB; ++cb) {
+          if (16 * cb < a.cr) {
 #pragma unroll
-          for (int i = 0; i < 4; ++i) rec[(16 * cb + 4 * g + i) * M + j] = dA[cb][nb][i];
-        if (g == 0) rec[C * M + j] = scv[nb / 4][nb % 4];
+            for (int i = 0; i < 4; ++i) rec[(16 * cb + 4 * g + i) * M + j] = dA[cb][nb][i];
+          }
+        }
+        if (g == 0) rec[a.cr * M + j] = scv[nb / 4][nb % 4];
       }
     }
     if (g == 0) {
 #pragma unroll
-      for (int cb = 0; cb < G_::CB; ++cb) rec[C * M + M + 16 * cb + r] = dav[cb / 4][cb % 4];
-      if (r == 0) rec[C * M + M + C] = scv[MB / 4][MB % 4];
+      for (int cb = 0; cb < G_::CB; ++cb)
+        if (16 * cb < a.cr) rec[a.cr * M + M + 16 * cb + r] = dav[cb / 4][cb % 4];
+      if (r == 0) rec[a.cr * M + M + a.cr] = scv[MB / 4][MB % 4];
     }
   }
 }

@@ -15,10 +15,9 @@ static hipError_t launch_coop(const StreamArgs& a, int P, hipStream_t st) {
 }
 
 hipError_t launch_slice_bwd_pass(int dtype, int C, int MB, const StreamArgs& a, int P, hipStream_t st) {
-  if (dtype == 1 && C == 256 && MB == 4 && coop_slice_bwd<bf16, 256, 4>())
-    return launch_coop<4>(a, P, st);
-  if (dtype == 1 && C == 256 && MB == 3 && coop_slice_bwd<bf16, 256, 3>())
-    return launch_coop<3>(a, P, st);
+  const bool coop = dtype == 1 && C == 256 && a.cr == 256;  // rows of exactly 256 channels
+  if (coop && MB == 4 && coop_slice_bwd<bf16, 256, 4>()) return launch_coop<4>(a, P, st);
+  if (coop && MB == 3 && coop_slice_bwd<bf16, 256, 3>()) return launch_coop<3>(a, P, st);
   return launch_pass<kSliceBwd>(dtype, C, MB, a, P, st);
 }
 }  // namespace pa

@@ -41,10 +41,11 @@ __device__ __forceinline__ void staged(int n, Ld&& ld, St&& st) {
 
 // ---------------------------------------------------------------------------
 // k_proj: one block per 16 token rows x 32 output columns (of one product,
-// or of the sum over products).  The block's rows of In (transposed to
-// [k][row]) and its 32 columns of op(W) are staged in LDS; the 4 waves split
-// K into quarters, each lane accumulating 2 rows x 4 columns, and the
-// quarters are added in wave order.
+// or of the sum over products; the last block of columns may hold 16).  The
+// block's rows of In (transposed to [k][row]) and its 32 columns of op(W)
+// (zero past Cout) are staged in LDS; the 4 waves split K into quarters,
+// each lane accumulating 2 rows x 4 columns, and the quarters are added in
+// wave order.
 // ---------------------------------------------------------------------------
 __global__ void __launch_bounds__(256) k_proj(Proj q) {
   extern __shared__ __attribute__((aligned(16))) float sm[];
@@ -79,10 +80,14 @@ __global__ void __launch_bounds__(256) k_proj(Proj q) {
       if (e < 8 * Cin) {
         if (!q.transW) {
           const int k = e >> 3, c4 = e & 7;  // W is [Cin][Cout]
-          vw[u] = *reinterpret_cast<const float4*>(W + (int64_t)k * Cout + j0 + 4 * c4);
+          vw[u] = j0 + 4 * c4 < Cout
+                      ? *reinterpret_cast<const float4*>(W + (int64_t)k * Cout + j0 + 4 * c4)
+                      : float4{0.f, 0.f, 0.f, 0.f};
         } else {
           const int c = e & 31, k4 = e >> 5;  // W is [Cout][Cin]
-          vw[u] = *reinterpret_cast<const float4*>(W + (int64_t)(j0 + c) * Cin + 4 * k4);
+          vw[u] = j0 + c < Cout
+                      ? *reinterpret_cast<const float4*>(W + (int64_t)(j0 + c) * Cin + 4 * k4)
+                      : float4{0.f, 0.f, 0.f, 0.f};
         }
       }
     }
@@ -133,7 +138,7 @@ __global__ void __launch_bounds__(256) k_proj(Proj q) {
   const int po = q.sum ? 0 : blockIdx.z;
   for (int e = threadIdx.x; e < 16 * 32; e += 256) {
     const int r = e >> 5, c = e & 31;
-    if (r0 + r >= M) continue;
+    if (r0 + r >= M || j0 + c >= Cout) continue;
     const float v = ((red[e] + red[512 + e]) + red[1024 + e]) + red[1536 + e];
     const float bj = q.b[po] ? q.b[po][j0 + c] : 0.f;
     q.out[po][(int64_t)(r0 + r) * Cout + j0 + c] = v + bj;
@@ -143,14 +148,14 @@ __global__ void __launch_bounds__(256) k_proj(Proj q) {
 hipError_t launch_proj(const Proj& q, hipStream_t st) {
   // (Cin <= 256: the staging loads of k_proj cover 4 Cin and 8 Cin float4)
   if (q.n < 1 || q.n > 3 || q.M < 1 || q.M > 64 || q.Cin < 16 || q.Cin % 16 || q.Cin > 256 ||
-      q.Cout % 32)
+      q.Cout < 16 || q.Cout % 16)
     return hipErrorInvalidValue;
   for (int p = 0; p < q.n; ++p)
     if (!q.in[p] || !q.W[p] || (!q.sum && !q.out[p])) return hipErrorInvalidValue;
   if (q.sum && !q.out[0]) return hipErrorInvalidValue;
   const size_t lds = ((size_t)q.Cin * 48 + 4 * 16 * 32) * sizeof(float);
   if (lds > 160 * 1024) return hipErrorInvalidConfiguration;
-  dim3 grid(q.Cout / 32, (q.M + 15) / 16, q.sum ? 1 : q.n);
+  dim3 grid((q.Cout + 31) / 32, (q.M + 15) / 16, q.sum ? 1 : q.n);
   hipLaunchKernelGGL(k_proj, grid, dim3(256), lds, st, q);
   return hipGetLastError();
 }

@@ -39,7 +39,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version(lib):
-    assert lib.pa_version() == 7
+    assert lib.pa_version() == 8
 
 
 def _dims(**kw):
@@ -63,13 +63,22 @@ def _ws_size(lib, dims):
     (dict(eps=-1.0), B.PA_ERR_INVALID),
     (dict(tau0=float("nan")), B.PA_ERR_INVALID),
     (dict(dtype=7), B.PA_ERR_INVALID),
-    (dict(C=48, H=4), B.PA_ERR_UNSUPPORTED),
+    (dict(C=40, H=4), B.PA_ERR_UNSUPPORTED),
     (dict(C=512, H=8), B.PA_ERR_UNSUPPORTED),
+    (dict(C=272, H=8), B.PA_ERR_UNSUPPORTED),
 ])
 def test_dims_validation(lib, kw, status):
     st, _ = _ws_size(lib, _dims(**kw))
     assert st == status
     assert lib.pa_last_error().decode() != ""
+
+
+@pytest.mark.parametrize("C", list(range(16, 257, 16)))
+def test_every_multiple_of_16_channels_is_served(lib, C):
+    # rows of C channels run on the kernels of the next width up (32, 64, 128
+    # or 256) with zero table columns; the workspace holds that width's tables
+    st, n = _ws_size(lib, _dims(C=C, H=16))
+    assert st == B.PA_OK and n > 0
 
 
 def test_workspace_size_grows_with_shape(lib):

@@ -138,7 +138,14 @@ def compare(w, x, G, p, dY, out, dt):
     elif p.get("a") is not None:
         da = np.concatenate([out["da"].ravel(), out["db_t"].ravel()])
         check("d(a,b_t)", da, np.concatenate([np.ravel(g["da"]), np.ravel(g["db_t"])]), dt)
-        check("dtau0", out["dtau0"].ravel(), np.ravel(g["dtau0"]), dt)
+        # d tau0 sums the heads' d b_t, which can cancel (by a factor of ~80
+        # at H = 4, D = 48): its error is bounded by the bar times the
+        # magnitude of the terms it adds
+        ref = float(np.ravel(g["dtau0"])[0])
+        scale = max(abs(ref), float(np.abs(np.ravel(g["db_t"])).sum()))
+        err = abs(float(out["dtau0"].ravel()[0]) - ref)
+        say(f"  dtau0    |err| = {err:.3e}  (bar {TOL[dt]:.0e} x {scale:.3e})")
+        assert err <= TOL[dt] * scale, ("dtau0", err, scale)
     else:
         db = np.concatenate([out["db"].ravel(), out["db_t"].ravel()])
         check("d(b,b_t)", db, np.concatenate([np.ravel(g["db"]), np.ravel(g["db_t"])]), dt)
@@ -158,6 +165,10 @@ CASES = [
     ("f32", 1000, 2, 32, 12, False, True, False),   # M not a multiple of 8: one call per head
     ("f32", 1, 2, 32, 8, False, True, True),          # one point
     ("bf16", 17, 4, 64, 16, True, True, False),       # one tile and a ragged tail
+    # head widths between the kernels' widths (D = 48, 16, 80)
+    ("bf16", 3001, 4, 48, 32, False, True, True),
+    ("f32", 2000, 3, 16, 24, False, True, False),
+    ("bf16", 1500, 2, 80, 16, True, True, False),
 ]
 
 

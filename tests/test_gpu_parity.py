@@ -37,6 +37,15 @@ SHAPES = [
     # three slice blocks over several tiles; one block with a ragged tile
     (20011, 256, 8, 48, "bf16"),
     (33, 256, 8, 50, "bf16"),
+    # channel counts between the kernels' widths (rows of C channels on the
+    # kernels of the next width up, zero table columns): C = 16, 48, 80, 96,
+    # 160, 208, odd head widths, token projections with a 16-column tail
+    (777, 16, 2, 7, "f32"),
+    (1000, 48, 4, 20, "bf16"),
+    (1203, 80, 5, 12, "f32"),
+    (2049, 96, 8, 64, "f32"),
+    (3001, 160, 8, 40, "bf16"),
+    (5003, 208, 8, 33, "bf16"),
 ]
 IDS = [f"N{n}-C{c}-H{h}-M{m}-{d}" for n, c, h, m, d in SHAPES]
 
