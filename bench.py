@@ -138,6 +138,10 @@ def main():
                          "ns2d_fwd_f32, grid2d_16k_f32, ellipsoid_32k_bf16, aircraft_2p5m_bf16")
     ap.add_argument("--flush", action="store_true",
                     help="with --workload: overwrite 1 GiB between steps (cold last-level cache)")
+    ap.add_argument("--probe", action="store_true",
+                    help="time each streaming kernel of the layer (in the step) beside a probe "
+                         "moving the same tensors the same way with no arithmetic "
+                         "(pa_stream_probe); the headline workload unless --workload")
     ap.add_argument("--graph", action="store_true",
                     help="with --workload: replay the step from a captured HIP graph")
     ap.add_argument("--head-calls", choices=("batched", "per-head"), default=None,
@@ -151,6 +155,9 @@ def main():
         return stack_bench(args)
     if args.heads:
         return heads_bench(args)
+    if args.probe:
+        args.workload = args.workload or WORKLOAD
+        return workload_bench(args)
     if args.workload:
         return workload_bench(args)
 
@@ -276,6 +283,54 @@ def main():
     print(json.dumps(out), flush=True)
 
 
+def probe_report(args, w, dims, step, x, G, dY, out, B, torch):
+    """Each streaming kernel timed inside the layer's step (pa_time_kernel,
+    median of the steps) beside pa_stream_probe for the same call: the same
+    tensors moved by the same blocks, waves, tiles, prefetch, walk direction
+    and cache hints, with no arithmetic (median of as many probes, each after
+    a 1 GiB write so that no input is left in the last-level cache; inside
+    the step a kernel may find part of its input there).  Prints one JSON
+    line."""
+    N, C, M = w.N, w.C, w.M
+    sz = 2 if w.dtype == "bf16" else 4
+    bpp = algo_bytes_per_point(C, M, sz, sz)
+    calls = ["pa_slice_aggregate", "pa_deslice"] + (
+        ["pa_deslice_backward", "pa_slice_aggregate_backward"] if w.backward else [])
+    reps = max(3, args.steps)
+    junk = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+    e0, e1 = B.HipEvent(), B.HipEvent()
+    passes = {}
+    for c in calls:
+        B.pa_time_kernel(c, e0, e1)
+        kt = []
+        for _ in range(reps):
+            step()
+            torch.cuda.synchronize()
+            kt.append(e0.elapsed_ms(e1))
+        B.pa_time_kernel(None)
+        reads_dy = c in ("pa_deslice_backward", "pa_slice_aggregate_backward")
+        writes = c in ("pa_deslice", "pa_slice_aggregate_backward")
+        pt = []
+        for r in range(reps):
+            junk.fill_(float(r))
+            e0.record()
+            B.pa_stream_probe(dims, c, x, dY if reads_dy else None, G, out if writes else None)
+            e1.record()
+            torch.cuda.synchronize()
+            pt.append(e0.elapsed_ms(e1))
+        k_ms, p_ms = sorted(kt)[len(kt) // 2], sorted(pt)[len(pt) // 2]
+        nb = bpp[c] * N
+        passes[c] = {"kernel": STREAM_KERNEL[c], "algo_bytes": nb,
+                     "kernel_us": round(k_ms * 1e3, 1), "probe_us": round(p_ms * 1e3, 1),
+                     "kernel_GBs": round(nb / (k_ms * 1e-3) / 1e9, 1),
+                     "probe_GBs": round(nb / (p_ms * 1e-3) / 1e9, 1),
+                     "kernel_over_probe": round(p_ms / k_ms, 4)}
+    out_line = {"probe": w.name, "N": N, "C": C, "M": M, "dtype": w.dtype, "reps": reps,
+                "kernel_sources_sha": kernel_sources_sha(), "peak_GBs": HBM_PEAK_GBS,
+                "passes": passes}
+    print(json.dumps(out_line), flush=True)
+
+
 def stack_bench(args):
     """The 8-block Transolver++ stack (LN -> Physics-Attention with the folded
     Project step -> MLP 256-1024-256 with GELU, residual adds) at N = 2.5M
@@ -383,6 +438,8 @@ def workload_bench(args):
     junk = torch.empty(1 << 28, dtype=torch.float32, device="cuda") if args.flush else None
     for _ in range(args.warmup):
         step()
+    if args.probe:
+        return probe_report(args, w, dims, step, x, G, dY, y, B, torch)
     if args.graph:
         # capture the step once on a side stream, then time its replays (the
         # library's calls only launch kernels: capturable as they are)

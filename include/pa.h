@@ -259,6 +259,26 @@ pa_status pa_deslice_backward_w(const pa_dims* dims, const void* W, const void* 
  * nothing. */
 pa_status pa_time_kernel(const char* call, void* start, void* stop);
 
+/* Diagnostics: the memory traffic of one streaming pass with none of its
+ * arithmetic, the rate its access pattern reaches on its own (what the
+ * pass would reach if its arithmetic were free; the achievable bandwidth
+ * its roofline fraction is read against).  For call = pa_slice_aggregate,
+ * pa_deslice, pa_deslice_backward or pa_slice_aggregate_backward, it runs
+ * one kernel that moves the point tensors that call's per-wave streaming
+ * kernel reads and writes at these dims exactly as that kernel does: the
+ * same blocks and waves, tile ranges, tile height, register prefetch depth,
+ * walk direction and cache hints of its 16-byte loads, the rows staged in
+ * LDS, and its output rows written back from an LDS tile.  Nothing is
+ * computed: out [N,C] dtype (pa_deslice, pa_slice_aggregate_backward;
+ * otherwise unused, may be NULL) receives the rows of x.  x [N,C] dtype,
+ * dY [N,C] dtype (pa_deslice_backward, pa_slice_aggregate_backward; may be
+ * NULL otherwise), G [N,M] dtype or NULL (no noise); no workspace.  Shapes
+ * whose call runs a block-cooperative kernel (bf16, C = 256, M > 32) are
+ * probed with the per-wave kernel's split.  An unknown call returns
+ * PA_ERR_INVALID. */
+pa_status pa_stream_probe(const pa_dims* dims, const char* call, const void* x,
+                          const void* dY, const void* G, void* out, void* stream);
+
 /* ---------------------------------------------------------------------
  * Block-stack primitives.  A Transolver++ block is the Transformer block
  * with Physics-Attention in place of attention (Section 3; the block

@@ -35,6 +35,7 @@ SYMBOLS = (
     "pa_heads_workspace_size", "pa_heads_slice_aggregate", "pa_heads_deslice",
     "pa_heads_deslice_backward", "pa_heads_slice_aggregate_backward",
     "pa_slice_aggregate_noalloc", "pa_mlp_up", "pa_mlp_up_backward", "pa_gemm_prepare",
+    "pa_stream_probe",
 )
 
 
@@ -105,6 +106,7 @@ def load(path: str = LIB_PATH):
     lib.pa_slice_aggregate_backward.argtypes = [D, P, P, SPp, P, P, P, P, P, P, SGp, P, S, P]
     lib.pa_slice_weights_backward.argtypes = [D, P, P, SPp, P, P, P, SGp, P, S, P]
     lib.pa_time_kernel.argtypes = [ctypes.c_char_p, P, P]
+    lib.pa_stream_probe.argtypes = [D, ctypes.c_char_p, P, P, P, P, P]
     lib.pa_slice_aggregate_w.argtypes = [D, P, P, SPp, P, P, P, P, P, S, P]
     lib.pa_slice_aggregate_noalloc.argtypes = [D, P, P, SPp, P, P, P, P]
     lib.pa_deslice_w.argtypes = [D, P, P, P, P, S, P]
@@ -379,6 +381,17 @@ def pa_time_kernel(call: Optional[str], start=None, stop=None):
     _check(load().pa_time_kernel(call.encode() if call is not None else None,
                                  start.handle if start is not None else None,
                                  stop.handle if stop is not None else None))
+
+
+def pa_stream_probe(dims, call: str, x, dY=None, G=None, out=None, stream=None):
+    """One kernel moving the point tensors of ``call``'s streaming kernel
+    with its loads and stores and no arithmetic (out receives x's rows)."""
+    d = _shapes(dims)
+    _check(load().pa_stream_probe(ctypes.byref(dims), call.encode(), _arg(x, *d["x"], "x"),
+                                  _arg(dY, *d["x"], "dY") if dY is not None else None,
+                                  _arg(G, *d["G"], "G") if G is not None else None,
+                                  _arg(out, *d["x"], "out") if out is not None else None,
+                                  _stream(stream)))
 
 
 # HIP events straight from the HIP runtime (the library times its kernels on

@@ -16,7 +16,7 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 SOURCES = ["pa_stream.hip", "pa_stream_agg.hip", "pa_stream_des.hip", "pa_stream_desbwd.hip",
            "pa_stream_wts.hip", "pa_stream_slbwd.hip", "pa_stream_wtsbwd.hip", "pa_small.hip",
            "pa_stream_aggw.hip", "pa_stream_desw.hip", "pa_stream_desbwdw.hip", "pa_tokens.hip",
-           "pa_tokens64.hip", "pa_block.hip", "pa_mlp.hip", "pa_heads.hip", "pa_api.cpp", "pa_gemm.cpp", "pa_block_api.cpp"]
+           "pa_tokens64.hip", "pa_block.hip", "pa_mlp.hip", "pa_heads.hip", "pa_probe.hip", "pa_api.cpp", "pa_gemm.cpp", "pa_block_api.cpp"]
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-fPIC", "-std=c++17",
     # packed-FP32 VALU forms are kept out of the device code

@@ -250,6 +250,45 @@ pa_status pa_time_kernel(const char* call, void* start, void* stop) {
   return PA_OK;
 }
 
+pa_status pa_stream_probe(const pa_dims* dims, const char* call, const void* x, const void* dY,
+                          const void* G, void* out, void* stream) {
+  PA_TRY(check_dims(dims));
+  static const struct { const char* name; int pass; } kProbed[] = {
+      {"pa_slice_aggregate", pa::kAggregate},
+      {"pa_deslice", pa::kDeslice},
+      {"pa_deslice_backward", pa::kDesliceBwd},
+      {"pa_slice_aggregate_backward", pa::kSliceBwd},
+  };
+  int pass = -1;
+  if (call)
+    for (const auto& c : kProbed)
+      if (std::strcmp(call, c.name) == 0) pass = c.pass;
+  if (pass < 0)
+    return fail(PA_ERR_INVALID, "pa_stream_probe: no probed streaming pass in '%s'",
+                call ? call : "(null)");
+  PA_TRY(check_ptr(x, "x", true));
+  PA_TRY(check_ptr(G, "G", false));
+  PA_TRY(check_ptr(dY, "dY", pass == pa::kDesliceBwd || pass == pa::kSliceBwd));
+  PA_TRY(check_ptr(out, "out", pass == pa::kDeslice || pass == pa::kSliceBwd));
+  const pa_dims& d = *dims;
+  const int waves = pa::probe_waves(pass, d.dtype, cpad(d.C), mblocks(d.M));
+  if (waves <= 0)
+    return fail(PA_ERR_UNSUPPORTED, "pa_stream_probe: shape C=%d M=%d dtype=%d not served", d.C,
+                d.M, d.dtype);
+  pa::StreamLaunch L;
+  L.x = x;
+  L.G = G;
+  L.dY = dY;
+  L.out = out;
+  L.N = d.N;
+  L.M = d.M;
+  L.cr = d.C;
+  L.P = pa::num_chunks(d.N, waves);
+  PA_HIP(pa::launch_probe(pass, d.dtype, cpad(d.C), mblocks(d.M), L, as_stream(stream)),
+         "stream probe");
+  return PA_OK;
+}
+
 pa_status pa_workspace_size(const pa_dims* dims, size_t* bytes) {
   PA_TRY(check_dims(dims));
   if (!bytes) return fail(PA_ERR_INVALID, "bytes is NULL");

@@ -48,6 +48,13 @@ hipError_t launch_stream(int pass, int dtype, int C, int MB, const StreamLaunch&
 // channels of the point rows.
 int stream_waves(int pass, int dtype, int C, int MB, int cr);
 
+// Stream probe (pa_probe.hip): the per-wave kernel of `pass` (kAggregate,
+// kDeslice, kDesliceBwd or kSliceBwd) with its loads and stores and no
+// arithmetic; probe_waves is its block's waves (0 = not served).
+int probe_waves(int pass, int dtype, int C, int MB);
+hipError_t launch_probe(int pass, int dtype, int C, int MB, const StreamLaunch& L,
+                        hipStream_t st);
+
 // Table image for a pass, written into `img` (device).
 struct PrepArgs {
   int pass = 0;

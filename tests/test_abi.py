@@ -32,7 +32,7 @@ def _declared_symbols():
 
 def test_every_declared_symbol_is_exported(lib):
     declared = _declared_symbols()
-    assert len(declared) == 36
+    assert len(declared) == 37
     assert sorted(B.SYMBOLS) == declared
     for name in declared:
         assert hasattr(lib, name), name
@@ -310,3 +310,21 @@ def test_mlp_up_argument_checks(lib):
     st = lib.pa_mlp_up_backward(1000, K, F, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, 2 * F * K,
                                 None)
     assert st == B.PA_ERR_INVALID and "W2" in lib.pa_last_error().decode()
+
+
+@fake_addresses
+def test_stream_probe_argument_checks(lib):
+    d = _dims(C=256, H=8, M=32, dtype=B.PA_BF16)
+    # unknown or missing call names, missing tensors: host errors, nothing launched
+    for call in (b"pa_token_attention", b"nope", None):
+        st = lib.pa_stream_probe(ctypes.byref(d), call, FAKE, FAKE, None, FAKE, None)
+        assert st == B.PA_ERR_INVALID
+    st = lib.pa_stream_probe(ctypes.byref(d), b"pa_slice_aggregate_backward", FAKE, None, None,
+                             FAKE, None)
+    assert st == B.PA_ERR_INVALID  # dY required
+    st = lib.pa_stream_probe(ctypes.byref(d), b"pa_deslice", FAKE, None, None, None, None)
+    assert st == B.PA_ERR_INVALID  # out required
+    st = lib.pa_stream_probe(ctypes.byref(_dims(C=48, H=4)), b"pa_deslice", FAKE + 8, None, None,
+                             FAKE, None)
+    assert st == B.PA_ERR_INVALID  # misaligned x
+    assert lib.pa_last_error().decode() != ""
