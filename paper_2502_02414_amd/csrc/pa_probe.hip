@@ -32,7 +32,7 @@ struct ProbeStage {
   GRegs<T, MB, ROWS> g;
 };
 
-template <typename T, int C, int MB, int PASS>
+template <typename T, int C, int MB, int PASS, bool EX>
 __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_probe(StreamArgs a) {
   using G_ = Geo<sizeof(T), C, MB>;
   constexpr int WAVES = G_::waves(PASS);
@@ -54,8 +54,8 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_p
   using Stage = ProbeStage<T, C, MB, ROWS>;
   auto load = [&](Stage& st, int64_t tile) {
     const int64_t p0 = tile * ROWS;
-    load_tile<T, C, ROWS, NT>(st.x, X, p0, a.N, a.cr);
-    if constexpr (probe_reads_dy<PASS>()) load_tile<T, C, ROWS, true>(st.y, Y, p0, a.N, a.cr);
+    load_tile<T, C, ROWS, NT, EX>(st.x, X, p0, a.N, a.cr);
+    if constexpr (probe_reads_dy<PASS>()) load_tile<T, C, ROWS, true, EX>(st.y, Y, p0, a.N, a.cr);
     load_g<T, MB, ROWS, true>(st.g, Gp, X, p0, a.N, a.M, hasG);
   };
   auto store = [&](const Stage& st) {
@@ -68,7 +68,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_p
       const int64_t p0 = t * ROWS;
       const int nvalid = (int)(a.N - p0 < ROWS ? a.N - p0 : ROWS);
       wave_sync();
-      write_tile<T, C, ROWS>(OUT, p0, xt, nvalid, a.cr);
+      write_tile<T, C, ROWS, EX>(OUT, p0, xt, nvalid, a.cr);
     }
   };
   auto tail = [&](int64_t t) {
@@ -90,7 +90,12 @@ hipError_t launch_probe_t(const StreamArgs& a, int P, hipStream_t st) {
     return hipErrorInvalidConfiguration;
   } else {
     const size_t lds = (size_t)G_::waves(PASS) * G_::wave_bytes(PASS);
-    hipLaunchKernelGGL((k_probe<T, C, MB, PASS>), dim3(P), dim3(64 * G_::waves(PASS)), lds, st, a);
+    if (a.cr == C)
+      hipLaunchKernelGGL((k_probe<T, C, MB, PASS, true>), dim3(P), dim3(64 * G_::waves(PASS)), lds,
+                         st, a);
+    else
+      hipLaunchKernelGGL((k_probe<T, C, MB, PASS, false>), dim3(P), dim3(64 * G_::waves(PASS)), lds,
+                         st, a);
     return hipGetLastError();
   }
 }

@@ -50,7 +50,6 @@ struct StreamArgs {
   float* partials;       // [P][rec]
   int64_t N;
   int M;
-  int cr;                // channels of the point rows (<= C, a multiple of 16)
   int rec;               // floats per record
   double tb;             // tau0 + b_t (exact sum of the two fp32 values)
   const float* tb_dev;   // nullable: a device scalar added to tb
@@ -59,6 +58,7 @@ struct StreamArgs {
   // per-head batch (see StreamLaunch)
   int heads;
   int64_t hs_x, hs_g, hs_dy, hs_out, hs_img, hs_part, hs_tb;
+  int cr;                // channels of the point rows (<= C, a multiple of 16)
 };
 
 enum Flags { kHasG = 1, kStatesTerm = 2, kDesliceTerm = 4 };
@@ -248,7 +248,8 @@ __device__ __forceinline__ void stage4(char* tile, int base, int off, const f32x
 // channels (cr a multiple of 16, so rows are whole 16-byte chunks): the
 // chunks past a row's end re-read its last chunk (finite data), and the
 // tables hold zeros for those channels, so they contribute nothing; outputs
-// are written for the cr channels only.
+// are written for the cr channels only.  EX (cr == C, chosen per launch):
+// the row length is the compile-time C, and the per-chunk addresses fold.
 // ---------------------------------------------------------------------------
 template <typename T, int C, int ROWS = 16>
 struct TileRegs {
@@ -263,21 +264,22 @@ __device__ __forceinline__ int last_row(int64_t p0, int64_t N) {
   return N - 1 - p0 < ROWS - 1 ? (int)(N - 1 - p0) : ROWS - 1;
 }
 
-template <typename T, int C, int ROWS = 16, bool NT = true>
+template <typename T, int C, int ROWS = 16, bool NT = true, bool EX = true>
 __device__ __forceinline__ void load_tile(TileRegs<T, C, ROWS>& R, const T* base, int64_t p0,
                                           int64_t N, int cr) {
   // no predicated loads, so the compiler can track these loads exactly
   constexpr int RCH = TileRegs<T, C, ROWS>::RCH;
   const int lane = lane_id();
   const int lim = last_row<ROWS>(p0, N);
-  const int rb = cr * (int)sizeof(T), lc = rb / 16 - 1;  // row bytes, its last chunk
-  const char* src = reinterpret_cast<const char*>(base + p0 * cr);
+  const int w = EX ? C : cr;                            // channels of a row
+  const int rb = w * (int)sizeof(T), lc = rb / 16 - 1;  // row bytes, its last chunk
+  const char* src = reinterpret_cast<const char*>(base + p0 * w);
 #pragma unroll
   for (int k = 0; k < TileRegs<T, C, ROWS>::NCH; ++k) {
     const int q = lane + 64 * k;
     const int row = q / RCH, cc = q - row * RCH;
     const int rr = row < lim ? row : lim;
-    const int c = cc < lc ? cc : lc;
+    const int c = EX ? cc : (cc < lc ? cc : lc);
     R.c[k] = ld_global16<NT>(src + (uint32_t)(rr * rb + 16 * c));
   }
 }
@@ -297,21 +299,24 @@ __device__ __forceinline__ void store_tile(char* tile, const TileRegs<T, C, ROWS
 
 // Staged output tile (padded LDS rows) -> rows [p0, p0 + nvalid) of dst,
 // their cr channels.
-template <typename T, int C, int ROWS = 16>
+template <typename T, int C, int ROWS = 16, bool EX = true>
 __device__ __forceinline__ void write_tile(T* dst, int64_t p0, const char* tile, int nvalid,
                                            int cr) {
   constexpr int RCH = TileRegs<T, C, ROWS>::RCH;
   constexpr int NCH = TileRegs<T, C, ROWS>::NCH;
   constexpr int ROW = C * (int)sizeof(T) + 32;
   const int lane = lane_id();
-  const int rb = cr * (int)sizeof(T);
-  char* d = reinterpret_cast<char*>(dst + p0 * cr);
+  const int w = EX ? C : cr;
+  const int rb = w * (int)sizeof(T);
+  char* d = reinterpret_cast<char*>(dst + p0 * w);
 #pragma unroll
   for (int k = 0; k < NCH; ++k) {
     const int q = lane + 64 * k;
     const int row = q / RCH, cc = q - row * RCH;
     const uint4 v = *reinterpret_cast<const uint4*>(tile + lds_off(row, 16 * cc, ROW));
-    if (row < nvalid && 16 * cc < rb) st_global16(d + (uint32_t)(row * rb + 16 * cc), v);
+    // (whole rows: chunk q of the tile sits at byte 16 q of the run)
+    const uint32_t off = EX ? (uint32_t)(16 * lane + 1024 * k) : (uint32_t)(row * rb + 16 * cc);
+    if (row < nvalid && (EX || 16 * cc < rb)) st_global16(d + off, v);
   }
 }
 
@@ -820,7 +825,7 @@ constexpr int agg_pass(bool bwd, bool wv) {
   return bwd ? (wv ? kDesliceBwdW : kDesliceBwd) : (wv ? kAggregateW : kAggregate);
 }
 
-template <typename T, int C, int MB, bool BWD, bool WV = false>
+template <typename T, int C, int MB, bool BWD, bool WV = false, bool EX = true>
 __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(agg_pass(BWD, WV))))
 k_aggregate(StreamArgs a) {
   using G_ = Geo<sizeof(T), C, MB>;
@@ -968,8 +973,8 @@ k_aggregate(StreamArgs a) {
   auto load = [&](Stage& st, int64_t tile) {
     const int64_t p0 = tile * ROWS;
     constexpr bool NT = !keep_loads<PASS>();
-    if constexpr (!WIN) load_tile<T, C, ROWS, NT>(st.x, X, p0, a.N, a.cr);
-    if constexpr (BWD) load_tile<T, C, ROWS, NT>(st.y, Y, p0, a.N, a.cr);
+    if constexpr (!WIN) load_tile<T, C, ROWS, NT, EX>(st.x, X, p0, a.N, a.cr);
+    if constexpr (BWD) load_tile<T, C, ROWS, NT, EX>(st.y, Y, p0, a.N, a.cr);
     // G (or W): streamed either way; `safe` is any readable 16 bytes
     const void* safe = WIN ? a.img : static_cast<const void*>(X);
     load_g<T, MB, ROWS, true>(st.g, Gp, safe, p0, a.N, a.M, hasG);
@@ -1004,6 +1009,7 @@ k_aggregate(StreamArgs a) {
   });
   if (wave == 0) {
     float* rec = a.partials + (int64_t)blockIdx.x * a.rec;
+    const int cw = EX ? C : a.cr;  // the record's channels
 #pragma unroll
     for (int nb = 0; nb < MB; ++nb)
 #pragma unroll
@@ -1012,8 +1018,8 @@ k_aggregate(StreamArgs a) {
         if (j < a.M) {
 #pragma unroll
           for (int cb = 0; cb < G_::CB; ++cb)
-            if (16 * cb < a.cr) rec[j * a.cr + 16 * cb + r] = acc[nb][cb][i];
-          if (!BWD && r == 0) rec[a.M * a.cr + j] = dacc[nb][i];
+            if (16 * cb < cw) rec[j * cw + 16 * cb + r] = acc[nb][cb][i];
+          if (!BWD && r == 0) rec[a.M * cw + j] = dacc[nb][i];
         }
       }
   }
@@ -1025,7 +1031,7 @@ k_aggregate(StreamArgs a) {
 // ---------------------------------------------------------------------------
 // WIN (kDesliceW): the weights are read from W (given as a.G, in the Gumbel
 // rows' buffer) instead of recomputed; only the deslice table is in LDS.
-template <typename T, int C, int MB, bool WIN = false>
+template <typename T, int C, int MB, bool WIN = false, bool EX = true>
 __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(WIN ? kDesliceW : kDeslice)))
 k_deslice(StreamArgs a) {
   using G_ = Geo<sizeof(T), C, MB>;
@@ -1074,7 +1080,7 @@ k_deslice(StreamArgs a) {
     if constexpr (WIN) {
       load_g<T, MB, 16, NT>(st.g, Gp, a.img, tile * 16, a.N, a.M, hasG);
     } else {
-      load_tile<T, C, 16, NT>(st.x, X, tile * 16, a.N, a.cr);
+      load_tile<T, C, 16, NT, EX>(st.x, X, tile * 16, a.N, a.cr);
       load_g<T, MB, 16, NT>(st.g, Gp, X, tile * 16, a.N, a.M, hasG);
     }
   };
@@ -1128,7 +1134,7 @@ k_deslice(StreamArgs a) {
           stage4<T>(xt, stb, 16 * cb * SZ, d);
         });
     wave_sync();
-    write_tile<T, C>(Y, p0, xt, nvalid, a.cr);
+    write_tile<T, C, 16, EX>(Y, p0, xt, nvalid, a.cr);
   };
   auto tail = [&](int64_t t) {
     Stage st;
@@ -1146,7 +1152,7 @@ k_deslice(StreamArgs a) {
 // ---------------------------------------------------------------------------
 // kWeights (PS layout): W [N,M] fp32 and tau [N] written out.
 // ---------------------------------------------------------------------------
-template <typename T, int C, int MB>
+template <typename T, int C, int MB, bool EX = true>
 __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kWeights))) k_weights(StreamArgs a) {
   using G_ = Geo<sizeof(T), C, MB>;
   constexpr int WAVES = G_::waves(kWeights);
@@ -1177,7 +1183,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kWeights)))
   GRegs<T, MB> gr;
   for (int64_t t = t0; t < t1; ++t) {
     const int64_t p0 = t * 16;
-    load_tile<T, C>(xr, X, p0, a.N, a.cr);
+    load_tile<T, C, 16, true, EX>(xr, X, p0, a.N, a.cr);
     load_g<T, MB>(gr, Gp, X, p0, a.N, a.M, hasG);
     const int nvalid = (int)(a.N - p0 < 16 ? a.N - p0 : 16);
     wave_sync();
@@ -1223,7 +1229,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kWeights)))
 // term the dY contraction is skipped.  The dx tile is staged in the dY tile
 // (dw is done with it) and written back as whole rows.
 // ---------------------------------------------------------------------------
-template <typename T, int C, int MB, int PASS>
+template <typename T, int C, int MB, int PASS, bool EX = true>
 __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_slice_bwd(StreamArgs a) {
   using G_ = Geo<sizeof(T), C, MB>;
   using V = typename LAcc<T, true>::v;
@@ -1303,8 +1309,8 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
     // dY is loaded unconditionally (x stands in without the deslice term),
     // so that the loads are never predicated
     constexpr bool NT = !keep_loads<PASS>();
-    load_tile<T, C, 16, NT>(st.x, X, tile * 16, a.N, a.cr);
-    load_tile<T, C, 16, NT>(st.y, deslice ? Y : X, tile * 16, a.N, a.cr);
+    load_tile<T, C, 16, NT, EX>(st.x, X, tile * 16, a.N, a.cr);
+    load_tile<T, C, 16, NT, EX>(st.y, deslice ? Y : X, tile * 16, a.N, a.cr);
     load_g<T, MB, 16, NT>(st.g, Gp, X, tile * 16, a.N, a.M, hasG);
   };
   auto store = [&](const Stage& st) {
@@ -1445,7 +1451,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
       for (int i = 0; i < 4; ++i) scr[r * SROWF + 16 * nb + 4 * g + i] = dl[nb][i];
     if (g == 0) scr_dt[r] = dt;
     wave_sync();
-    write_tile<T, C>(DX, p0, yt, nvalid, a.cr);
+    write_tile<T, C, 16, EX>(DX, p0, yt, nvalid, a.cr);
     float dlp[MB][4], dtp[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -1518,25 +1524,26 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
   if (wave == 0) {
     float* rec = a.partials + (int64_t)blockIdx.x * a.rec;
     const int M = a.M;
+    const int cw = EX ? C : a.cr;  // the record's channels
 #pragma unroll
     for (int nb = 0; nb < MB; ++nb) {
       const int j = 16 * nb + r;
       if (j < M) {
 #pragma unroll
         for (int cb = 0; cb < G_::CB; ++cb) {
-          if (16 * cb < a.cr) {
+          if (16 * cb < cw) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) rec[(16 * cb + 4 * g + i) * M + j] = dA[cb][nb][i];
           }
         }
-        if (g == 0) rec[a.cr * M + j] = scv[nb / 4][nb % 4];
+        if (g == 0) rec[cw * M + j] = scv[nb / 4][nb % 4];
       }
     }
     if (g == 0) {
 #pragma unroll
       for (int cb = 0; cb < G_::CB; ++cb)
-        if (16 * cb < a.cr) rec[a.cr * M + M + 16 * cb + r] = dav[cb / 4][cb % 4];
-      if (r == 0) rec[a.cr * M + M + a.cr] = scv[MB / 4][MB % 4];
+        if (16 * cb < cw) rec[cw * M + M + 16 * cb + r] = dav[cb / 4][cb % 4];
+      if (r == 0) rec[cw * M + M + cw] = scv[MB / 4][MB % 4];
     }
   }
 }
@@ -1545,6 +1552,28 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
 // Launch of one pass, dispatched over dtype, C and slice blocks.  Each pass
 // is instantiated in its own translation unit (pa_stream_<pass>.hip).
 // ---------------------------------------------------------------------------
+// EX: rows of exactly C channels (the addresses of the tiles' chunks fold);
+// otherwise rows of a.cr < C channels.
+template <int PASS, typename T, int C, int MB, bool EX>
+static void launch_k(const StreamArgs& a, dim3 grid, int threads, size_t lds, hipStream_t st) {
+  if constexpr (PASS == kAggregate)
+    hipLaunchKernelGGL((k_aggregate<T, C, MB, false, false, EX>), grid, dim3(threads), lds, st, a);
+  else if constexpr (PASS == kAggregateW)
+    hipLaunchKernelGGL((k_aggregate<T, C, MB, false, true, EX>), grid, dim3(threads), lds, st, a);
+  else if constexpr (PASS == kDesliceBwd)
+    hipLaunchKernelGGL((k_aggregate<T, C, MB, true, false, EX>), grid, dim3(threads), lds, st, a);
+  else if constexpr (PASS == kDesliceBwdW)
+    hipLaunchKernelGGL((k_aggregate<T, C, MB, true, true, EX>), grid, dim3(threads), lds, st, a);
+  else if constexpr (PASS == kDeslice)
+    hipLaunchKernelGGL((k_deslice<T, C, MB, false, EX>), grid, dim3(threads), lds, st, a);
+  else if constexpr (PASS == kDesliceW)
+    hipLaunchKernelGGL((k_deslice<T, C, MB, true, EX>), grid, dim3(threads), lds, st, a);
+  else if constexpr (PASS == kWeights)
+    hipLaunchKernelGGL((k_weights<T, C, MB, EX>), grid, dim3(threads), lds, st, a);
+  else
+    hipLaunchKernelGGL((k_slice_bwd<T, C, MB, PASS, EX>), grid, dim3(threads), lds, st, a);
+}
+
 template <int PASS, typename T, int C, int MB>
 static hipError_t launch_t(const StreamArgs& a, int P, hipStream_t st) {
   using G_ = Geo<sizeof(T), C, MB>;
@@ -1554,22 +1583,10 @@ static hipError_t launch_t(const StreamArgs& a, int P, hipStream_t st) {
     const int threads = 64 * G_::waves(PASS);
     const size_t lds = (size_t)G_::lds_bytes(PASS);
     const dim3 grid(P, a.heads);
-    if constexpr (PASS == kAggregate)
-      hipLaunchKernelGGL((k_aggregate<T, C, MB, false>), grid, dim3(threads), lds, st, a);
-    else if constexpr (PASS == kAggregateW)
-      hipLaunchKernelGGL((k_aggregate<T, C, MB, false, true>), grid, dim3(threads), lds, st, a);
-    else if constexpr (PASS == kDesliceBwd)
-      hipLaunchKernelGGL((k_aggregate<T, C, MB, true>), grid, dim3(threads), lds, st, a);
-    else if constexpr (PASS == kDesliceBwdW)
-      hipLaunchKernelGGL((k_aggregate<T, C, MB, true, true>), grid, dim3(threads), lds, st, a);
-    else if constexpr (PASS == kDeslice)
-      hipLaunchKernelGGL((k_deslice<T, C, MB>), grid, dim3(threads), lds, st, a);
-    else if constexpr (PASS == kDesliceW)
-      hipLaunchKernelGGL((k_deslice<T, C, MB, true>), grid, dim3(threads), lds, st, a);
-    else if constexpr (PASS == kWeights)
-      hipLaunchKernelGGL((k_weights<T, C, MB>), grid, dim3(threads), lds, st, a);
+    if (a.cr == C)
+      launch_k<PASS, T, C, MB, true>(a, grid, threads, lds, st);
     else
-      hipLaunchKernelGGL((k_slice_bwd<T, C, MB, PASS>), grid, dim3(threads), lds, st, a);
+      launch_k<PASS, T, C, MB, false>(a, grid, threads, lds, st);
     return hipGetLastError();
   }
 }
