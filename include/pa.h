@@ -444,6 +444,19 @@ pa_status pa_heads_expand(int H, int64_t L, int blockdiag, const float* src, flo
 pa_status pa_heads_sum(int H, int64_t L, int blockdiag, const float* src, float* dst,
                        void* stream);
 
+/* Up to 8 pa_heads_sum in one launch (a layer's shared-parameter gradients
+ * at once): item i sums items[i].src into items[i].dst with its own L and
+ * blockdiag, each exactly as pa_heads_sum does it (same order, same bits).
+ * n in [1, 8]; items is a host array, read before the call returns; every
+ * item is validated as pa_heads_sum validates its arguments. */
+typedef struct {
+  const float* src;
+  float* dst;
+  int64_t L;
+  int blockdiag;
+} pa_heads_sum_item;
+pa_status pa_heads_sum_batch(int H, int n, const pa_heads_sum_item* items, void* stream);
+
 /* ---------------------------------------------------------------------
  * Per-head slicing in one launch per kernel.  The calls below run the
  * layer's aggregate, deslice, deslice backward and slice backward for all

@@ -35,7 +35,7 @@ SYMBOLS = (
     "pa_heads_workspace_size", "pa_heads_slice_aggregate", "pa_heads_deslice",
     "pa_heads_deslice_backward", "pa_heads_slice_aggregate_backward",
     "pa_slice_aggregate_noalloc", "pa_mlp_up", "pa_mlp_up_backward", "pa_gemm_prepare",
-    "pa_stream_probe",
+    "pa_stream_probe", "pa_heads_sum_batch",
 )
 
 
@@ -72,6 +72,11 @@ class pa_heads_params(ctypes.Structure):
 class pa_attn_grads(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p)
                 for n in ("dWq", "dbq", "dWk", "dbk", "dWv", "dbv", "dWo", "dbo")]
+
+
+class pa_heads_sum_item(ctypes.Structure):
+    _fields_ = [("src", ctypes.c_void_p), ("dst", ctypes.c_void_p), ("L", ctypes.c_int64),
+                ("blockdiag", ctypes.c_int)]
 
 
 _lib = None
@@ -127,6 +132,7 @@ def load(path: str = LIB_PATH):
     lib.pa_heads_relayout.argtypes = [I64, I32, I32, I32, I32, P, P, P]
     lib.pa_heads_expand.argtypes = [I32, I64, I32, P, P, P]
     lib.pa_heads_sum.argtypes = [I32, I64, I32, P, P, P]
+    lib.pa_heads_sum_batch.argtypes = [I32, I32, ctypes.POINTER(pa_heads_sum_item), P]
     HPp = ctypes.POINTER(pa_heads_params)
     lib.pa_heads_workspace_size.argtypes = [D, I32, ctypes.POINTER(ctypes.c_size_t)]
     lib.pa_heads_slice_aggregate.argtypes = [D, I32, P, P, HPp, P, P, P, P, S, P]
@@ -571,6 +577,19 @@ def pa_heads_sum(src, dst, H, blockdiag, stream=None):
     L = dst.shape[0] if blockdiag else dst.numel()
     _check(load().pa_heads_sum(H, L, int(bool(blockdiag)), _ptr(src), _ptr(dst),
                                _stream(stream)))
+
+
+def pa_heads_sum_batch(items, H, stream=None):
+    """items: (src, dst, blockdiag) triples, each summed as pa_heads_sum
+    would, all in one launch."""
+    arr = (pa_heads_sum_item * len(items))()
+    for i, (src, dst, bd) in enumerate(items):
+        L = dst.shape[0] if bd else dst.numel()
+        n = H * L * L if bd else H * L
+        _need(src, n, PA_F32, "src")
+        _need(dst, L * L if bd else L, PA_F32, "dst")
+        arr[i] = pa_heads_sum_item(_ptr(src), _ptr(dst), L, int(bool(bd)))
+    _check(load().pa_heads_sum_batch(H, len(items), arr, _stream(stream)))
 
 
 # ---- per-head slicing in one launch per kernel (include/pa.h) ----

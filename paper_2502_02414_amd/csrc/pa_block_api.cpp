@@ -367,4 +367,20 @@ pa_status pa_heads_sum(int H, int64_t L, int blockdiag, const float* src, float*
   return PA_OK;
 }
 
+pa_status pa_heads_sum_batch(int H, int n, const pa_heads_sum_item* items, void* stream) {
+  if (n < 1 || n > pa::kHeadSumMax)
+    return err(PA_ERR_INVALID, "pa_heads_sum_batch: n must be in [1, %d] (got %d)",
+               pa::kHeadSumMax, n);
+  if (!items) return err(PA_ERR_INVALID, "pa_heads_sum_batch: items is NULL");
+  pa::HeadSumBatch b{};
+  b.n = n;
+  for (int i = 0; i < n; ++i) {
+    PB_TRY(heads_small("pa_heads_sum_batch", H, items[i].L, items[i].blockdiag, items[i].src,
+                       items[i].dst));
+    b.it[i] = {items[i].src, items[i].dst, items[i].L, items[i].blockdiag ? 1 : 0};
+  }
+  PB_HIP(pa::launch_heads_sum_batch(H, b, as_stream(stream)), "heads sum batch");
+  return PA_OK;
+}
+
 }  // extern "C"

@@ -53,9 +53,10 @@ __global__ __launch_bounds__(256) void k_expand(int H, int64_t L, int blockdiag,
   }
 }
 
-__global__ __launch_bounds__(256) void k_head_sum(int H, int64_t L, int blockdiag,
-                                                  const float* __restrict__ src,
-                                                  float* __restrict__ dst) {
+// The sum over the heads of one parameter's gradient (grid-stride over its
+// elements), in head order in double precision.
+__device__ __forceinline__ void head_sum(int H, int64_t L, int blockdiag,
+                                         const float* __restrict__ src, float* __restrict__ dst) {
   const int64_t total = blockdiag ? L * L : L;
   const int64_t step = (int64_t)gridDim.x * blockDim.x;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += step) {
@@ -69,6 +70,29 @@ __global__ __launch_bounds__(256) void k_head_sum(int H, int64_t L, int blockdia
     }
     dst[i] = (float)s;
   }
+}
+
+__global__ __launch_bounds__(256) void k_head_sum(int H, int64_t L, int blockdiag,
+                                                  const float* __restrict__ src,
+                                                  float* __restrict__ dst) {
+  head_sum(H, L, blockdiag, src, dst);
+}
+
+// Item blockIdx.y of a batch: selected case by case (a run-time index into
+// the by-value argument array would copy the arguments to scratch memory).
+__global__ __launch_bounds__(256) void k_head_sum_batch(int H, HeadSumBatch b) {
+  HeadSumItem t;
+  switch (blockIdx.y) {
+    case 0: t = b.it[0]; break;
+    case 1: t = b.it[1]; break;
+    case 2: t = b.it[2]; break;
+    case 3: t = b.it[3]; break;
+    case 4: t = b.it[4]; break;
+    case 5: t = b.it[5]; break;
+    case 6: t = b.it[6]; break;
+    default: t = b.it[7]; break;
+  }
+  head_sum(H, t.L, t.blockdiag, t.src, t.dst);
 }
 
 unsigned grid_for(int64_t n) {
@@ -93,6 +117,20 @@ hipError_t launch_heads_expand(int H, int64_t L, int blockdiag, const float* src
   if (H < 1 || L < 1 || !src || !dst) return hipErrorInvalidValue;
   const int64_t n = blockdiag ? (int64_t)H * L * H * L : (int64_t)H * L;
   hipLaunchKernelGGL(k_expand, dim3(grid_for(n)), dim3(256), 0, st, H, L, blockdiag, src, dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_heads_sum_batch(int H, const HeadSumBatch& b, hipStream_t st) {
+  static_assert(kHeadSumMax == 8, "k_head_sum_batch selects among 8 items");
+  if (H < 1 || b.n < 1 || b.n > kHeadSumMax) return hipErrorInvalidValue;
+  unsigned blocks = 1;
+  for (int i = 0; i < b.n; ++i) {
+    const HeadSumItem& t = b.it[i];
+    if (t.L < 1 || !t.src || !t.dst) return hipErrorInvalidValue;
+    const unsigned g = grid_for(t.blockdiag ? t.L * t.L : t.L);
+    blocks = g > blocks ? g : blocks;
+  }
+  hipLaunchKernelGGL(k_head_sum_batch, dim3(blocks, b.n), dim3(256), 0, st, H, b);
   return hipGetLastError();
 }
 

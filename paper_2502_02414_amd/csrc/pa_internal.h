@@ -263,6 +263,19 @@ hipError_t launch_heads_relayout(int64_t R, int H, int D, int dtype, int to_head
                                  const void* src, void* dst, hipStream_t st);
 hipError_t launch_heads_expand(int H, int64_t L, int blockdiag, const float* src, float* dst,
                                hipStream_t st);
+// Up to kHeadSumMax head sums in one launch (item blockIdx.y).
+constexpr int kHeadSumMax = 8;
+struct HeadSumItem {
+  const float* src;
+  float* dst;
+  int64_t L;
+  int blockdiag;
+};
+struct HeadSumBatch {
+  HeadSumItem it[kHeadSumMax];
+  int n;
+};
+hipError_t launch_heads_sum_batch(int H, const HeadSumBatch& b, hipStream_t st);
 hipError_t launch_heads_sum(int H, int64_t L, int blockdiag, const float* src, float* dst,
                             hipStream_t st);
 // Row-major D[m,n] = alpha op(A) op(B) + beta D (+ bias[n]) on hipBLASLt;

@@ -198,22 +198,26 @@ class HeadSlicedLayer:
             self._heads(lambda h, ws, st: B.pa_slice_aggregate_backward(
                 self.dims_h, xh[h], g(h), self.sp[h], c["num"][h], c["den"][h], dS_h[h],
                 c["Sp_h"][h], dYh[h], dxh[h], grs[h], ws, stream=st))
-        grads = {}
+        # the shared parameters' gradients: sums over the heads, up to eight
+        # per launch (pa_heads_sum_batch)
+        grads, sums = {}, []
         for k in ATTN_W:
             if "d" + k in ag:
                 grads["d" + k] = self._f(D, D)
-                B.pa_heads_sum(ag["d" + k], grads["d" + k], H, blockdiag=True)
+                sums.append((ag["d" + k], grads["d" + k], True))
         for k in ATTN_B:
             if "d" + k in ag:
                 grads["d" + k] = self._f(D)
-                B.pa_heads_sum(ag["d" + k], grads["d" + k], H, blockdiag=False)
+                sums.append((ag["d" + k], grads["d" + k], False))
         grads["dtau0"] = self._f(1)
-        B.pa_heads_sum(per["dtau0"], grads["dtau0"], H, blockdiag=False)
+        sums.append((per["dtau0"], grads["dtau0"], False))
         for k in ("dA", "db", "da", "db_t"):
             if self.shared:
                 shape = per[k].shape[1:] or (1,)
                 grads[k] = self._f(*shape)
-                B.pa_heads_sum(per[k], grads[k], H, blockdiag=False)
+                sums.append((per[k], grads[k], False))
             else:
                 grads[k] = per[k]
+        for i in range(0, len(sums), 8):
+            B.pa_heads_sum_batch(sums[i:i + 8], H)
         return dxh, grads

@@ -32,7 +32,7 @@ def _declared_symbols():
 
 def test_every_declared_symbol_is_exported(lib):
     declared = _declared_symbols()
-    assert len(declared) == 37
+    assert len(declared) == 38
     assert sorted(B.SYMBOLS) == declared
     for name in declared:
         assert hasattr(lib, name), name
@@ -328,3 +328,15 @@ def test_stream_probe_argument_checks(lib):
                              FAKE, None)
     assert st == B.PA_ERR_INVALID  # misaligned x
     assert lib.pa_last_error().decode() != ""
+
+
+def test_heads_sum_batch_argument_checks(lib):
+    # host validation only (nothing is launched): item counts outside [1, 8],
+    # NULL items, an item that pa_heads_sum would reject
+    items = (B.pa_heads_sum_item * 9)()
+    assert lib.pa_heads_sum_batch(8, 0, items, None) == B.PA_ERR_INVALID
+    assert lib.pa_heads_sum_batch(8, 9, items, None) == B.PA_ERR_INVALID
+    assert lib.pa_heads_sum_batch(8, 1, None, None) == B.PA_ERR_INVALID
+    items[0] = B.pa_heads_sum_item(None, None, 4, 0)  # NULL src and dst
+    assert lib.pa_heads_sum_batch(8, 1, items, None) == B.PA_ERR_INVALID
+    assert "pa_heads_sum_batch" in lib.pa_last_error().decode()

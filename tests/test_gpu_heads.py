@@ -70,6 +70,16 @@ def test_heads_expand_and_sum(H, D):
     want_bd = sum(F[h * D:(h + 1) * D, h * D:(h + 1) * D].astype(np.float64) for h in range(H))
     np.testing.assert_allclose(host(s_bd), want_bd, rtol=1e-7, atol=1e-7)
     np.testing.assert_allclose(host(s_v), P.astype(np.float64).sum(axis=0), rtol=1e-7, atol=1e-7)
+    # the same sums (and a scalar's) in one batched launch: the same bits
+    S1 = I.normal(5, 13, 0, H, dtype=np.float32)
+    b_bd = torch.empty(D, D, dtype=torch.float32, device="cuda")
+    b_v = torch.empty(3 * D, dtype=torch.float32, device="cuda")
+    b_s = torch.empty(1, dtype=torch.float32, device="cuda")
+    s_s = torch.empty(1, dtype=torch.float32, device="cuda")
+    B.pa_heads_sum(dev(S1), s_s, H, blockdiag=False)
+    B.pa_heads_sum_batch([(dev(F), b_bd, True), (dev(P), b_v, False), (dev(S1), b_s, False)], H)
+    for got, want in ((b_bd, s_bd), (b_v, s_v), (b_s, s_s)):
+        np.testing.assert_array_equal(host(got), host(want))
 
 
 def head_case(N, H, D, M, dt, shared, noise, out_proj, geometry="normal", seed=31, w=None):
