@@ -598,6 +598,33 @@ def heads_bench(args):
         "relayout_ms_per_tensor": round(relayout_ms, 4),
         "relayout_GBs": round(2 * N * C * 2 / (relayout_ms * 1e-3) / 1e9, 1),
     }
+    if args.probe:
+        # each pass's access pattern alone (pa_stream_probe): the head-major
+        # tensors as one head of H N points of D channels, the same bytes in
+        # the same 64-byte rows (one grid over all heads' points instead of
+        # one per head), each probe after a 1 GiB write
+        pdims = B.make_dims(H * N, D, 1, M, w.tau0, w.tau_min, w.eps, B.PA_BF16)
+        pout = torch.empty(H * N, D, dtype=bf, device="cuda")
+        junk = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+        e0, e1 = B.HipEvent(), B.HipEvent()
+        probe = {}
+        for c in ("pa_slice_aggregate", "pa_deslice", "pa_deslice_backward",
+                  "pa_slice_aggregate_backward"):
+            rd = c in ("pa_deslice_backward", "pa_slice_aggregate_backward")
+            wr = c in ("pa_deslice", "pa_slice_aggregate_backward")
+            pt = []
+            for r in range(max(3, steps)):
+                junk.fill_(float(r))
+                e0.record()
+                B.pa_stream_probe(pdims, c, xh, dYh if rd else None, G, pout if wr else None)
+                e1.record()
+                torch.cuda.synchronize()
+                pt.append(e0.elapsed_ms(e1))
+            pm = sorted(pt)[len(pt) // 2]
+            nb = H * N * bpp[c]
+            probe[c] = {"probe_us": round(pm * 1e3, 1),
+                        "probe_GBs": round(nb / (pm * 1e-3) / 1e9, 1)}
+        out["probe"] = probe
     if kernel_ms:
         kb = H * N * bpp["pa_slice_aggregate_backward"]
         ach = kb / (kernel_ms * 1e-3) / 1e9
