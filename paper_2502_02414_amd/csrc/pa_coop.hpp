@@ -145,7 +145,7 @@ k_slice_bwd_coop(StreamArgs a) {
 
   // block set-up: the table image, zeroed Gumbel tiles, the bias and
   // centred dden of the lane's softmax slices
-  copy_image(smem, a.img, CG::IMG);
+  copy_image<CG::IMG, 256 * NG>(smem, a.img);
   for (int q = threadIdx.x & 255; q < G_::GT / 16; q += 256)
     reinterpret_cast<uint4*>(tl + CG::OFF_G)[q] = uint4{0, 0, 0, 0};
   __syncthreads();  // (before any prefetch: a full fence costs nothing here)

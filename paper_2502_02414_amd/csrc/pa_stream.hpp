@@ -759,11 +759,39 @@ __device__ __forceinline__ void zero_lds(char* p, int bytes) {
   for (int q = lane_id(); q < bytes / 16; q += 64) reinterpret_cast<uint4*>(p)[q] = uint4{0, 0, 0, 0};
 }
 
-// Copy the table image from global memory into LDS (all threads).
-__device__ __forceinline__ void copy_image(char* lds, const void* img, int bytes) {
-  const uint4* src = reinterpret_cast<const uint4*>(img);
-  uint4* dst = reinterpret_cast<uint4*>(lds);
-  for (int q = threadIdx.x; q < bytes / 16; q += blockDim.x) dst[q] = src[q];
+// Copy the table image (BYTES, a multiple of 16) from global memory into LDS
+// with the block's THREADS threads: each thread issues the loads of all its
+// 16-byte chunks before it stores any (a copy loop that stores each chunk
+// before loading the next waits one memory round trip per chunk: 10 to 14 of
+// them for the larger images, at the start of every block).  Chunks past the
+// end are the last chunk again, loaded and stored again (the same bytes to
+// the same place), so no lane-dependent branch separates the loads.
+template <int U, int END, int THREADS, int NQ>
+__device__ __forceinline__ void copy_chunks(uint4* dst, const uint4* src, int t) {
+  if constexpr (U < END) {
+    const int q = t + U * THREADS;
+    const int qq = q < NQ ? q : NQ - 1;
+    const uint4 v = src[qq];
+    copy_chunks<U + 1, END, THREADS, NQ>(dst, src, t);  // later chunks' loads first
+    dst[qq] = v;
+  }
+}
+// (batches of at most 16 chunks in registers per thread)
+template <int B0, int PER, int THREADS, int NQ>
+__device__ __forceinline__ void copy_batches(uint4* dst, const uint4* src, int t) {
+  if constexpr (B0 < PER) {
+    constexpr int END = B0 + 16 < PER ? B0 + 16 : PER;
+    copy_chunks<B0, END, THREADS, NQ>(dst, src, t);
+    copy_batches<END, PER, THREADS, NQ>(dst, src, t);
+  }
+}
+template <int BYTES, int THREADS>
+__device__ __forceinline__ void copy_image(char* lds, const void* img) {
+  static_assert(BYTES % 16 == 0, "image bytes must be a multiple of 16");
+  constexpr int NQ = BYTES / 16;
+  constexpr int PER = (NQ + THREADS - 1) / THREADS;  // chunks per thread
+  copy_batches<0, PER, THREADS, NQ>(reinterpret_cast<uint4*>(lds),
+                                    reinterpret_cast<const uint4*>(img), (int)threadIdx.x);
 }
 
 // (wave: the wave's index in its block, uniform, so the range is scalar)
@@ -858,7 +886,7 @@ k_aggregate(StreamArgs a) {
   float bias[MB][4];
   auto init = [&]() {
     if constexpr (!WIN) {
-      copy_image(smem, a.img, G_::img_bytes(PASS));
+      copy_image<G_::img_bytes(PASS), 64 * WAVES>(smem, a.img);
       __syncthreads();
     }
     zero_lds(gbuf, 2 * H * G_::GT);
@@ -1056,9 +1084,9 @@ k_deslice(StreamArgs a) {
   float bias[MB][4];
   auto init = [&]() {
     if constexpr (WIN)  // the deslice table part of the image only
-      copy_image(smem, reinterpret_cast<const char*>(a.img) + G_::OFF_2, G_::SZ_S);
+      copy_image<G_::SZ_S, 64 * WAVES>(smem, reinterpret_cast<const char*>(a.img) + G_::OFF_2);
     else
-      copy_image(smem, a.img, G_::img_bytes(kDeslice));
+      copy_image<G_::img_bytes(kDeslice), 64 * WAVES>(smem, a.img);
     __syncthreads();
     zero_lds(gt, G_::GT);
 #pragma unroll
@@ -1163,7 +1191,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(kWeights)))
   const int r = lane_id() & 15, g = lane_id() >> 4;
   const bool hasG = a.flags & kHasG;
 
-  copy_image(smem, a.img, G_::img_bytes(kWeights));
+  copy_image<G_::img_bytes(kWeights), 64 * WAVES>(smem, a.img);
   __syncthreads();
   const char* tabL = smem + G_::OFF_L;
   char* xt = smem + G_::img_bytes(kWeights) + wave * G_::wave_bytes(kWeights);
@@ -1267,7 +1295,7 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
 
   float bias[MB][4], dden[MB][4];
   auto init = [&]() {
-    copy_image(smem, a.img, G_::img_bytes(PASS));
+    copy_image<G_::img_bytes(PASS), 64 * WAVES>(smem, a.img);
     __syncthreads();
     zero_lds(gt, G_::GT);
     // dden_j centred by its den-weighted mean (a shift common to all slices)
