@@ -336,10 +336,11 @@ k_slice_bwd_coop(StreamArgs a) {
       for (int i = 0; i < 4; ++i) {
         const float d = w[i] * (dw[i] - wdw);
         res += d;
-        if (w[i] != 0.f) {
-          q1 += d * zs[i];
-          q2 += w[i] * zs[i];
-        }
+        // a padded slice: exponent -inf, w = d = 0; the exponent clamped to
+        // a finite value keeps the products 0
+        const float zc = __builtin_amdgcn_fmed3f(zs[i], -__FLT_MAX__, __FLT_MAX__);
+        q1 = fmaf(d, zc, q1);
+        q2 = fmaf(w[i], zc, q2);
       }
       res = row16_sum(res);
       q1 = row16_sum(q1);

@@ -456,16 +456,20 @@ __device__ __forceinline__ LogitsBases<T, C, MB> logits_bases() {
           row_base<T>(0, G_::TROW)};
 }
 
+// init (nullable): starting values of the slice blocks' accumulators (the
+// biases, so that the contraction adds them); the temperature block starts
+// at zero.
 template <typename T, int C, int MB, bool SP, bool KEEP_X = true>
 __device__ __forceinline__ void logits(typename LAcc<T, SP>::v (&acc)[MB + 1],
                                        K32<T> (&xa)[C / 32], const char* xt, const char* tabL,
-                                       const LogitsBases<T, C, MB>& lb) {
+                                       const LogitsBases<T, C, MB>& lb,
+                                       const typename LAcc<T, SP>::v* init = nullptr) {
   using G_ = Geo<sizeof(T), C, MB>;
   using V = typename LAcc<T, SP>::v;
   constexpr int NT = sizeof(T) == 2 ? MB + 1 : MB;
   constexpr int SZ = (int)sizeof(T);
 #pragma unroll
-  for (int nb = 0; nb <= MB; ++nb) acc[nb] = zero_acc<V>();
+  for (int nb = 0; nb <= MB; ++nb) acc[nb] = (init && nb < MB) ? init[nb] : zero_acc<V>();
   // KEEP_X: all point fragments are read up front and returned in xa (for
   // reuse by the caller); otherwise each is read with its step's table
   // fragments and dropped after use (fewer live registers).
@@ -1353,17 +1357,42 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
 
     V lg[MB + 1];
     K32<T> xa[G_::XF];
-    logits<T, C, MB, true>(lg, xa, xt, tabL, lb);
-    float w[MB][4], zs[MB][4], tau;
-    const float tt = temperature_own<T, C, MB>(lg, xa, tabL, lb.a, a.tb);
-    softmax_sp<T, MB>(lg, gt, a.M, bias, tt, a.tau_min, nvalid, w, zs, tau);
+    float w[MB][4], zs[MB][4], tau, tt;
+    // narrow rows (a pass bound by instruction issue): the logit contraction
+    // starts at the biases and the dw contraction below at dden (no
+    // separate adds per slice); the softmax then adds -0, which the
+    // compiler drops.  (On wide rows, bound by memory, the separate adds
+    // measured slightly faster.)
+    constexpr bool NARROW = narrow_rows<T, C>() && SZ == 2;
+    if constexpr (NARROW) {
+      V bi[MB];
+      float nob[MB][4];
+#pragma unroll
+      for (int nb = 0; nb < MB; ++nb) {
+        bi[nb] = V{bias[nb][0], bias[nb][1], bias[nb][2], bias[nb][3]};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) nob[nb][i] = -0.f;
+      }
+      logits<T, C, MB, true>(lg, xa, xt, tabL, lb, bi);
+      tt = temperature_own<T, C, MB>(lg, xa, tabL, lb.a, a.tb);
+      softmax_sp<T, MB>(lg, gt, a.M, nob, tt, a.tau_min, nvalid, w, zs, tau);
+    } else {
+      logits<T, C, MB, true>(lg, xa, xt, tabL, lb);
+      tt = temperature_own<T, C, MB>(lg, xa, tabL, lb.a, a.tb);
+      softmax_sp<T, MB>(lg, gt, a.M, bias, tt, a.tau_min, nvalid, w, zs, tau);
+    }
 
     // dw in the SP layout
     float dw[MB][4];
     if constexpr (PASS == kSliceBwd) {
       V acc[MB];
 #pragma unroll
-      for (int nb = 0; nb < MB; ++nb) acc[nb] = zero_acc<V>();
+      for (int nb = 0; nb < MB; ++nb) {
+        if constexpr (NARROW)
+          acc[nb] = V{dden[nb][0], dden[nb][1], dden[nb][2], dden[nb][3]};
+        else
+          acc[nb] = zero_acc<V>();
+      }
       // states term: x . (dnum_j - cN)  (zero rows without the states term)
       struct FS { K32<T> tw[MB]; };
       pipelined<G_::XF, 2, FS>(
@@ -1394,7 +1423,8 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
 #pragma unroll
       for (int nb = 0; nb < MB; ++nb)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) dw[nb][i] = (float)(acc[nb][i] + dden[nb][i]);
+        for (int i = 0; i < 4; ++i)
+          dw[nb][i] = NARROW ? (float)acc[nb][i] : (float)(acc[nb][i] + dden[nb][i]);
     } else {
 #pragma unroll
       for (int nb = 0; nb < MB; ++nb)
@@ -1431,7 +1461,14 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
       for (int i = 0; i < 4; ++i) {
         const float dz = w[nb][i] * ((dw[nb][i] - wdw) - res);
         dl[nb][i] = dz * rtau;
-        if (w[nb][i] != 0.f) zdz += dz * zs[nb][i];
+        // a padded slice has the exponent -inf and dz exactly 0 (w = 0):
+        // narrow rows clamp the exponent to a finite value (one
+        // median-of-three, not a compare and select), which keeps their
+        // product 0
+        if constexpr (NARROW)
+          zdz = fmaf(dz, __builtin_amdgcn_fmed3f(zs[nb][i], -__FLT_MAX__, __FLT_MAX__), zdz);
+        else if (w[nb][i] != 0.f)
+          zdz += dz * zs[nb][i];
       }
     zdz = groups_sum(zdz);
     float dtau = -kLn2 * zdz * rtau;
@@ -1463,12 +1500,20 @@ __global__ void __launch_bounds__((64 * Geo<sizeof(T), C, MB>::waves(PASS))) k_s
           // the 2 MB products [A^T | dnum - cN] x [dl ; w], two per MFMA
           auto fa = [&](int q) -> const K16<T>& { return q < MB ? f.ta[q] : f.tn[q - MB]; };
           auto fb = [&](int q) -> const K16<T>& { return q < MB ? lbk[q] : wb[q - MB]; };
-          f32x4 d = zero4();
+          // + a dt, + cN (the table rows hold dnum_j - cN, and sum_j w_j =
+          // 1): on narrow rows, whose pass is bound by instruction issue, as
+          // the products' starting value (one fma per element); on wider
+          // rows added after them (as a starting value the accumulators
+          // would move into AGPRs first)
+          f32x4 d;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) d[i] = NARROW ? fmaf(f.av[i], dt, f.cn[i]) : 0.f;
 #pragma unroll
           for (int q = 0; q < 2 * MB; q += 2) d = mma16x2(fa(q), fb(q), fa(q + 1), fb(q + 1), d);
-          // + a dt, + cN: the table rows hold dnum_j - cN, and sum_j w_j = 1
+          if constexpr (!NARROW) {
 #pragma unroll
-          for (int i = 0; i < 4; ++i) d[i] += f.av[i] * dt + f.cn[i];
+            for (int i = 0; i < 4; ++i) d[i] += f.av[i] * dt + f.cn[i];
+          }
           stage4<T>(yt, stb, 16 * cb * SZ, d);
         });
 
