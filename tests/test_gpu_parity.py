@@ -46,6 +46,11 @@ SHAPES = [
     (2049, 96, 8, 64, "f32"),
     (3001, 160, 8, 40, "bf16"),
     (5003, 208, 8, 33, "bf16"),
+    # narrow rows (bf16 rows of 64 bytes or less: the pass bound by
+    # instruction issue, with the biases and dden as the contractions'
+    # starting values) with padded slices (M not a multiple of 16)
+    (3001, 32, 2, 20, "bf16"),
+    (777, 16, 1, 7, "bf16"),
 ]
 IDS = [f"N{n}-C{c}-H{h}-M{m}-{d}" for n, c, h, m, d in SHAPES]
 
